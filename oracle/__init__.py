@@ -1,0 +1,229 @@
+"""SGD-KV CPU oracle -- test infrastructure only.
+
+A thin ctypes wrapper over ``sgdkv_oracle.c``: plain fp64 C that computes
+what the SGD-KV hot path computes, step by step, straight from the paper's
+definitions (Sec. 3.3 with Eq. 2, Appendix A.1 Algorithm 1, Appendix A.2 and
+A.7, Sec. 5). Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU
+baseline leg of ``bench.py`` may import this package. It shares no code with
+the HIP product path and never imports it.
+
+End-to-end outputs are *parity unpinned* against the paper, which prints no
+numeric worked example of the hot path; each step is pinned separately by
+the ``-m "not gpu"`` tests (closed forms, invariants, brute force, library
+routines).
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(_HERE, "sgdkv_oracle.c")
+DEFAULT_LIB_PATH = os.path.join(_HERE, "libsgdkv_oracle.so")
+# The mutation test points this at deliberately broken builds of the oracle.
+LIB_PATH = os.environ.get("SGDKV_ORACLE_LIB", DEFAULT_LIB_PATH)
+
+_lib = None
+
+
+GCC_FLAGS = ["-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-std=c11", "-Wall",
+             "-shared", "-fPIC"]
+
+
+def build(force: bool = True, src: str = SRC, out: str = DEFAULT_LIB_PATH) -> str:
+    """Compile the oracle with gcc (fp64, OpenMP, no FP contraction)."""
+    if force or not os.path.exists(out):
+        tmp = out + ".tmp"
+        subprocess.run(["gcc", *GCC_FLAGS, src, "-o", tmp, "-lm"], check=True)
+        os.replace(tmp, out)
+    return out
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        build(force=False)
+    lib = ctypes.CDLL(LIB_PATH)
+    i32, i64, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_double
+    P = ctypes.c_void_p
+    lib.orc_reduce_group_max.argtypes = [P, i32, i32, i32, P]
+    lib.orc_total_from_ratio.argtypes = [f64, i32, i32, i64, i64, i64, i32, P]
+    lib.orc_allocate_budgets.argtypes = [P, i32, i32, i64, i64, i64, i64, i32, P]
+    lib.orc_window_lse.argtypes = [P, P, i32, i32, i32, i32, i64, i32, f64, P]
+    lib.orc_window_colsum.argtypes = [P, P, P, i32, i32, i32, i32, i64, i32, f64, P]
+    lib.orc_pool.argtypes = [P, i64, i64, i32, P]
+    lib.orc_select.argtypes = [P, i64, i32, i64, i64, i64, P]
+    lib.orc_decode.argtypes = [P, P, P, P, i32, i32, i32, i32, f64, P, P]
+    lib.orc_num_threads.argtypes = []
+    for f in ("orc_reduce_group_max", "orc_total_from_ratio", "orc_allocate_budgets",
+              "orc_window_lse", "orc_window_colsum", "orc_pool", "orc_select", "orc_decode",
+              "orc_num_threads"):
+        getattr(lib, f).restype = i32
+    _lib = lib
+    return lib
+
+
+class OracleError(ValueError):
+    pass
+
+
+def _f64(a) -> np.ndarray:
+    """Exact fp64 copy of a numpy array or a CPU torch tensor (bf16/fp32 upcast exactly)."""
+    if hasattr(a, "detach"):
+        a = a.detach().cpu().double().numpy()
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        raise OracleError(f"oracle {what}: invalid arguments")
+
+
+def num_threads() -> int:
+    return int(_load().orc_num_threads())
+
+
+# --------------------------------------------------------------- allocation
+def reduce_group_max(per_q, num_kv_heads: int) -> np.ndarray:
+    """[L, Hq] per-query-head scores -> [L, Hkv], max over each group (Appendix A.7)."""
+    a = _f64(per_q)
+    L, Hq = a.shape
+    out = np.zeros((L, num_kv_heads), dtype=np.float64)
+    _check(_load().orc_reduce_group_max(_ptr(a), L, Hq, num_kv_heads, _ptr(out)), "reduce_group_max")
+    return out
+
+
+def total_from_ratio(R: float, L: int, H: int, C: int, s: int, W: int, of_middle: int = 0) -> int:
+    """Total kept rows for ratio R (of all rows, or of the middle as in Eq. 2)."""
+    t = ctypes.c_int64(0)
+    _check(_load().orc_total_from_ratio(float(R), L, H, C, s, W, int(of_middle), ctypes.byref(t)),
+           "total_from_ratio")
+    return int(t.value)
+
+
+def allocate_budgets(scores, L: int, H: int, C: int, s: int, W: int, total: int,
+                     mode: int = 0) -> np.ndarray:
+    """Per-KV-head budgets b_h (Eq. 2 + Algorithm 1), int64 [L*H], layer-major."""
+    sc = _f64(scores).reshape(-1)
+    if sc.size != L * H:
+        raise OracleError("scores must hold L*H values")
+    out = np.zeros(L * H, dtype=np.int64)
+    _check(_load().orc_allocate_budgets(_ptr(sc), L, H, C, s, W, int(total), int(mode), _ptr(out)),
+           "allocate_budgets")
+    return out
+
+
+# ------------------------------------------------------------------ scores
+def _scale(d: int, scale):
+    return 1.0 / math.sqrt(d) if scale is None or scale == 0 else float(scale)
+
+
+def window_lse(q_win, k, num_kv_heads: int | None = None, scale=None) -> np.ndarray:
+    """LSE of each observation-window row over its causal keys; [B, Hq, w]."""
+    q = _f64(q_win)
+    kk = _f64(k)
+    B, Hq, w, d = q.shape
+    _, Hkv, C, _ = kk.shape
+    out = np.zeros((B, Hq, w), dtype=np.float64)
+    _check(_load().orc_window_lse(_ptr(q), _ptr(kk), B, Hq, Hkv, d, C, w, _scale(d, scale), _ptr(out)),
+           "window_lse")
+    return out
+
+
+def window_colsum(q_win, k, lse, scale=None) -> np.ndarray:
+    """Group-mean cumulative window attention of each scored key; [B, Hkv, C-w]."""
+    q = _f64(q_win)
+    kk = _f64(k)
+    ls = _f64(lse)
+    B, Hq, w, d = q.shape
+    _, Hkv, C, _ = kk.shape
+    out = np.zeros((B, Hkv, C - w), dtype=np.float64)
+    _check(_load().orc_window_colsum(_ptr(q), _ptr(kk), _ptr(ls), B, Hq, Hkv, d, C, w,
+                                     _scale(d, scale), _ptr(out)), "window_colsum")
+    return out
+
+
+def pool(a, kp: int) -> np.ndarray:
+    """Average pooling along the last axis (odd kernel, stride 1, zero padding)."""
+    x = _f64(a)
+    n = x.shape[-1]
+    rows = int(np.prod(x.shape[:-1])) if x.ndim > 1 else 1
+    out = np.zeros_like(x)
+    _check(_load().orc_pool(_ptr(x), rows, n, kp, _ptr(out)), "pool")
+    return out
+
+
+def select(pooled_row, C: int, w: int, s: int, W: int, m: int) -> np.ndarray:
+    """Kept positions of one head, ascending: sink, top-m candidates, window."""
+    p = _f64(pooled_row).reshape(-1)
+    if p.size != C - w:
+        raise OracleError("pooled row must hold C-w scores")
+    out = np.zeros(s + m + W, dtype=np.int32)
+    _check(_load().orc_select(_ptr(p), C, w, s, W, m, _ptr(out)), "select")
+    return out
+
+
+# -------------------------------------------------------------- full steps
+def compress(q_win, k, v, budgets, *, w: int, kp: int, s: int, W: int, scale=None,
+             lse=None) -> dict:
+    """One layer's compression: scores, pooling, per-head selection and gather.
+
+    budgets: [Hkv] int (the layer's rows per KV head, shared by every sequence).
+    Returns kept_pos [B*T] int32, offsets [B*Hkv+1] int64, k_c/v_c [B*T, d] fp64
+    (exact copies of the input rows), colsum/pooled [B, Hkv, C-w], lse [B, Hq, w].
+    """
+    q = _f64(q_win)
+    kk = _f64(k)
+    vv = _f64(v)
+    B, Hq, w_, d = q.shape
+    _, Hkv, C, _ = kk.shape
+    assert w_ == w
+    budgets = np.asarray(budgets, dtype=np.int64).reshape(-1)
+    assert budgets.size == Hkv
+    if lse is None:
+        lse = window_lse(q, kk, scale=scale)
+    colsum = window_colsum(q, kk, lse, scale=scale)
+    pooled = pool(colsum, kp)
+    T = int(budgets.sum())
+    kept = np.zeros(B * T, dtype=np.int32)
+    offsets = np.zeros(B * Hkv + 1, dtype=np.int64)
+    k_c = np.zeros((B * T, d), dtype=np.float64)
+    v_c = np.zeros((B * T, d), dtype=np.float64)
+    row = 0
+    for b in range(B):
+        for h in range(Hkv):
+            offsets[b * Hkv + h] = row
+            m = int(budgets[h]) - s - W
+            pos = select(pooled[b, h], C, w, s, W, m)
+            n = pos.size
+            kept[row:row + n] = pos
+            k_c[row:row + n] = kk[b, h, pos]
+            v_c[row:row + n] = vv[b, h, pos]
+            row += n
+    offsets[B * Hkv] = row
+    return dict(kept_pos=kept, offsets=offsets, k_c=k_c, v_c=v_c, colsum=colsum, pooled=pooled,
+                lse=lse)
+
+
+def decode(q, k_c, v_c, offsets, num_kv_heads: int, scale=None):
+    """Decode attention over the ragged per-KV-head cache: (out [B,Hq,d], lse [B,Hq])."""
+    qq = _f64(q)
+    kc = _f64(k_c)
+    vc = _f64(v_c)
+    off = np.ascontiguousarray(np.asarray(offsets, dtype=np.int64))
+    B, Hq, d = qq.shape
+    out = np.zeros((B, Hq, d), dtype=np.float64)
+    lse = np.zeros((B, Hq), dtype=np.float64)
+    _check(_load().orc_decode(_ptr(qq), _ptr(kc), _ptr(vc), _ptr(off), B, Hq, num_kv_heads, d,
+                              _scale(d, scale), _ptr(out), _ptr(lse)), "decode")
+    return out, lse

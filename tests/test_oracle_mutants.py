@@ -1,0 +1,59 @@
+"""The oracle's pins must catch plausible mistakes.
+
+Each case plants one mistake (a dropped term, an off-by-one, a wrong sign,
+index or operand order) in a temporary copy of the oracle's C source, builds
+it, and runs the oracle pin tests against that build in a subprocess: at
+least one pin must fail. Everything runs on the CPU.
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+ALLOC = "tests/test_oracle_alloc.py"
+SCORES = "tests/test_oracle_scores.py"
+SELDEC = "tests/test_oracle_select_decode.py"
+
+MUTANTS = {
+    "lse_not_causal": ("int64_t last = C - w + i; /* causal: keys 0..last */",
+                       "int64_t last = C - 1;", SCORES),
+    "lse_off_by_one": ("for (int64_t j = 0; j <= last; ++j) z +=", "for (int64_t j = 0; j < last; ++j) z +=", SCORES),
+    "colsum_no_group_mean": ("colsum[c] = acc / (double)G;", "colsum[c] = acc;", SCORES),
+    "colsum_lse_sign": ("orc_dot(q_win + r * d, kj, d) - lse[r]", "orc_dot(q_win + r * d, kj, d) + lse[r] - 2.0 * lse[r] * (i == 0)", SCORES),
+    "colsum_no_scale": ("acc += exp(scale * orc_dot(q_win + r * d, kj, d)", "acc += exp(orc_dot(q_win + r * d, kj, d)", SCORES),
+    "lse_wrong_group": ("int64_t h = q / G;\n    const double* qi", "int64_t h = q % Hkv;\n    const double* qi", SCORES),
+    "pool_divisor": ("pooled[row * n + j] = s / (double)kp;", "pooled[row * n + j] = s / (double)(kp - 1);", SCORES),
+    "pool_window": ("for (int64_t t = j - r; t <= j + r; ++t)", "for (int64_t t = j - r; t < j + r; ++t)", SCORES),
+    "select_tie_high": ("return (a->j < b->j) ? -1 : (a->j > b->j);\n}\n\nstatic int orc_cmp_i32",
+                        "return (a->j > b->j) ? -1 : (a->j < b->j);\n}\n\nstatic int orc_cmp_i32", SELDEC),
+    "alloc_no_reserve": ("for (int64_t h = 0; h < n; ++h) x[h] = (sg[h] * (double)T) / sgsum;",
+                         "for (int64_t h = 0; h < n; ++h) x[h] = (sg[h] * (double)(T + n)) / sgsum;", ALLOC),
+    "alloc_greedy_ascending": ("if (a->sigma > b->sigma) return -1;\n  if (a->sigma < b->sigma) return 1;\n  return (a->idx < b->idx) ? -1 : (a->idx > b->idx);\n}\n\nint orc_allocate",
+                               "if (a->sigma < b->sigma) return -1;\n  if (a->sigma > b->sigma) return 1;\n  return (a->idx < b->idx) ? -1 : (a->idx > b->idx);\n}\n\nint orc_allocate", ALLOC),
+    "alloc_round_smallest": ("if (a->frac > b->frac) return -1;\n  if (a->frac < b->frac) return 1;",
+                             "if (a->frac < b->frac) return -1;\n  if (a->frac > b->frac) return 1;", ALLOC),
+    "decode_no_normalise": ("for (int t = 0; t < d; ++t) o[t] /= z;", "", SELDEC),
+    "decode_wrong_group": ("int64_t b = bq / Hq, qh = bq % Hq, h = qh / G;", "int64_t b = bq / Hq, qh = bq % Hq, h = qh % Hkv;", SELDEC),
+}
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(name, tmp_path):
+    old, new, pins = MUTANTS[name]
+    src = open(oracle.SRC).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not unique"
+    mutated = tmp_path / "mutant.c"
+    mutated.write_text(src.replace(old, new))
+    lib = str(tmp_path / "libmutant.so")
+    oracle.build(force=True, src=str(mutated), out=lib)
+    env = dict(os.environ, SGDKV_ORACLE_LIB=lib, OMP_NUM_THREADS="2")
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:randomly",
+                        "--hypothesis-seed=0", pins], cwd=ROOT, env=env,
+                       capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
+    assert "failed" in r.stdout or "error" in r.stdout.lower()
