@@ -1,0 +1,196 @@
+/*
+ * sgdkv.h -- C ABI of the SGD-KV hot path for AMD Instinct MI355X (gfx950).
+ *
+ * SGD-KV (Liu et al., "SGD-KV: Summarization Guided KV Cache Compression")
+ * compresses a long prompt's KV cache per KV head: each head gets a budget
+ * from its summarization score (Sec. 3.3, Eq. 2, redistributed by Appendix
+ * A.1, Algorithm 1), and inside that budget it keeps the tokens with the
+ * largest cumulative attention of a final observation window (Sec. 3.3, last
+ * paragraph; Sec. 5), always keeping an initial sink and a recent window.
+ * Budgets apply per KV head, before the heads are repeated for GQA
+ * (Appendix A.2). Decode attention then reads the ragged compressed cache.
+ *
+ * Conventions shared by every entry point:
+ *   - Every function returns an sgdkv_status; no exception crosses the ABI.
+ *     On any error nothing has been written to any output and nothing has
+ *     been enqueued; sgdkv_last_error() describes the failure.
+ *   - The caller owns all memory. The library never allocates device memory;
+ *     scratch space comes from a caller buffer sized by *_workspace_size.
+ *   - Device work is enqueued on `stream` (a hipStream_t passed as void*;
+ *     NULL = the null stream) and is asynchronous. Device faults surface at
+ *     the caller's next synchronisation.
+ *   - Device pointers must be 16-byte aligned. Tensors are dense, row-major,
+ *     in the layouts given below.
+ *   - Outputs are bitwise reproducible run to run. The only atomics are
+ *     integer histogram counts.
+ *   - Calls on different streams are independent given distinct workspaces.
+ */
+#ifndef SGDKV_H
+#define SGDKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t sgdkv_status;
+#define SGDKV_OK 0
+#define SGDKV_ERR_INVALID_ARG 1 /* a size, pointer, alignment or value is out of range */
+#define SGDKV_ERR_UNSUPPORTED 2 /* valid, but not built: head_dim, group size, ... */
+#define SGDKV_ERR_WORKSPACE 3   /* workspace too small or misaligned */
+#define SGDKV_ERR_HIP 4         /* the HIP runtime refused a call (no device, launch failure) */
+
+#define SGDKV_DTYPE_F32 0
+#define SGDKV_DTYPE_BF16 1
+
+/* Thread-local description of the last failure on this thread; valid until
+ * the next sgdkv_* call on the same thread. Never NULL. */
+const char* sgdkv_last_error(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int32_t sgdkv_version(void);
+
+/* ------------------------------------------------------------------ */
+/* Head budgets (host only; never touches the device).                */
+
+/* GQA reduction of per-attention-head summarization scores to one score per
+ * KV head: the maximum over the G = Hq/Hkv query heads of each group
+ * (Appendix A.7, where max beats mean). Query head q belongs to KV head q/G.
+ * per_qhead: host [L][Hq] fp64. per_kvhead_out: host [L][Hkv] fp64.
+ * Errors: L, Hq, Hkv < 1; Hq not a multiple of Hkv; NULL pointers. */
+sgdkv_status sgdkv_reduce_query_head_scores(const double* per_qhead, int32_t L, int32_t Hq,
+                                            int32_t Hkv, double* per_kvhead_out);
+
+/* Total number of kept rows over all L*H KV heads for a budget ratio R.
+ * of_middle = 0: R of all rows, floor(R*L*H*C) -- the "KV memory reduced by
+ *                up to 75 %" reading at R = 25 % (abstract, Sec. 1).
+ * of_middle = 1: Eq. 2 summed over heads, R applied to the compressible
+ *                middle only: L*H*(s+W) + floor(R*L*H*(C-s-W)) (Sec. 3.3).
+ * Errors: R outside [0,1]; L, H, C < 1; s, W < 0; s+W > C; a total that
+ * cannot cover every head's sink and window (of_middle = 0). */
+sgdkv_status sgdkv_total_from_ratio(double R, int32_t L, int32_t H, int64_t C, int64_t b_sink,
+                                    int64_t b_window, int32_t of_middle, int64_t* total_out);
+
+/* Per-KV-head budgets b_h for all L*H heads (Sec. 3.3, Eq. 2; Appendix A.1,
+ * Algorithm 1). head_scores: host [L][H] fp64 raw summarization scores
+ * (>= 0, finite), normalised internally over all L*H heads. Every head keeps
+ * b_sink initial and b_window recent rows; the rest of total_budget,
+ * T = total_budget - L*H*(b_sink+b_window), is shared over the middles of
+ * length M = C - b_sink - b_window in proportion to the score:
+ *   x_h = (sigma_h * T) / sum(sigma)   (all-zero scores: uniform shares).
+ * mode 0 (default, Algorithm 1): x_h rounded by largest remainder (ties:
+ *   larger score, then lower flat index); every middle capped at M; the
+ *   excess handed to the remaining heads in descending score order (ties:
+ *   lower index), each filled up to M before the next.
+ * mode 1 (proportional water level): x_h = min(lambda*sigma_h, M) with the
+ *   exact level lambda making the sum T, then rounded as above.
+ * budgets_out: host [L][H] int64, b_h = b_sink + b_window + m_h, summing to
+ * total_budget, each in [b_sink + b_window, C].
+ * Errors: sizes as for sgdkv_total_from_ratio; a score < 0, NaN or Inf;
+ * total_budget outside [L*H*(s+W), L*H*C]; mode not 0/1; NULL pointers. */
+sgdkv_status sgdkv_allocate_budgets(const double* head_scores, int32_t L, int32_t H, int64_t C,
+                                    int64_t b_sink, int64_t b_window, int64_t total_budget,
+                                    int32_t mode, int64_t* budgets_out);
+
+/* ------------------------------------------------------------------ */
+/* One layer's compression (device).                                   */
+
+typedef struct sgdkv_compress_desc {
+  int32_t batch;        /* B >= 1 sequences */
+  int32_t num_q_heads;  /* Hq */
+  int32_t num_kv_heads; /* Hkv, Hq % Hkv == 0, Hkv <= 64 */
+  int32_t head_dim;     /* d: 64 or 128 */
+  int32_t obs_window;   /* w >= 1: the last w prompt positions are the window rows */
+  int32_t pool_kernel;  /* odd k_p >= 1: average pooling, stride 1, zero padding */
+  int64_t seq_len;      /* C: prompt length */
+  int64_t b_sink;       /* s >= 0 initial rows always kept */
+  int64_t b_window;     /* W >= w recent rows always kept (so every candidate has a score) */
+  int32_t dtype;        /* SGDKV_DTYPE_F32 or SGDKV_DTYPE_BF16 for q_win, k, v, k_out, v_out */
+  float scale;          /* logit scale; 0 selects 1/sqrt(head_dim) */
+} sgdkv_compress_desc;
+
+/* Bytes of device workspace sgdkv_compress_layer needs for `desc`
+ * (the same for every budget vector). */
+sgdkv_status sgdkv_compress_workspace_size(const sgdkv_compress_desc* desc, size_t* bytes);
+
+/* Compress one layer: score, pool, select per KV head and gather.
+ *
+ * Window scores (Sec. 3.3 last paragraph, SnapKV-style; Sec. 5 Query-Aware
+ * window): window row i of query head q sits at prompt position C-w+i and
+ * attends causally to keys 0..C-w+i, logits l = scale*<q_i, k_j>. For every
+ * scored key j in [0, C-w) the group mean over the G query heads of the
+ * KV head of the window-summed softmax probabilities is
+ *   a_j = (1/G) sum_q sum_i exp(l_{q,i,j} - lse_{q,i}),
+ * then pooled_j = (1/k_p) sum_{|t-j| <= (k_p-1)/2} a_t (a_t = 0 outside).
+ * Selection: for KV head h with budget b_h (m_h = b_h - s - W), the kept
+ * positions are [0,s), the m_h candidates in [s, C-W) with the largest
+ * pooled score (ties to the lower position) and [C-W, C), in ascending order.
+ *
+ * layer_budgets: HOST [Hkv] int64, each in [s+W, C] (one layer's slice of
+ *   sgdkv_allocate_budgets); T_layer = sum_h layer_budgets[h].
+ * q_win:   device [B][Hq][w][d]  window queries (post-RoPE), dtype.
+ * k, v:    device [B][Hkv][C][d] the layer's full cache, dtype.
+ * window_lse: optional device [B][Hq][w] fp32 natural-log LSE of each window
+ *   row over its causal keys (prefill attention produces it); NULL = the
+ *   library computes it (one extra pass over K).
+ * k_out, v_out: device [B*T_layer][d] dtype; segment (b,h) occupies rows
+ *   offsets_out[b*Hkv+h] .. offsets_out[b*Hkv+h+1]-1 in kept order.
+ * kept_pos_out: device [B*T_layer] int32 prompt positions of the kept rows.
+ * offsets_out: device [B*Hkv+1] int64, offsets[b*Hkv+h] = b*T_layer +
+ *   sum_{h'<h} layer_budgets[h'].
+ * k_out, v_out, kept_pos_out and offsets_out are either all non-NULL, or
+ *   all NULL (scores-only mode: only scores_out is produced).
+ * scores_out: optional device [B][Hkv][C-w] fp32 pooled scores (the values
+ *   the selection used); required in scores-only mode.
+ * workspace: device, 256-byte aligned, >= sgdkv_compress_workspace_size.
+ * Errors (nothing enqueued): sizes < 1; Hq % Hkv; Hkv > 64; d not 64/128
+ *   (UNSUPPORTED); G*w > 512 (UNSUPPORTED); k_p even; s+W > C; W < w;
+ *   a budget outside [s+W, C]; C > 2^31-1; misaligned or missing pointers;
+ *   small workspace (WORKSPACE); no usable device (HIP). */
+sgdkv_status sgdkv_compress_layer(const sgdkv_compress_desc* desc, const int64_t* layer_budgets,
+                                  const void* q_win, const void* k, const void* v,
+                                  const float* window_lse, void* k_out, void* v_out,
+                                  int32_t* kept_pos_out, int64_t* offsets_out, float* scores_out,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------ */
+/* Decode attention over the ragged compressed cache (device).         */
+
+typedef struct sgdkv_decode_desc {
+  int32_t batch;        /* B */
+  int32_t num_q_heads;  /* Hq */
+  int32_t num_kv_heads; /* Hkv, Hq % Hkv == 0 */
+  int32_t head_dim;     /* d: 64 or 128 */
+  int32_t kv_dtype;     /* dtype of q, k_c, v_c */
+  int32_t out_dtype;    /* dtype of out */
+  float scale;          /* 0 selects 1/sqrt(head_dim) */
+} sgdkv_decode_desc;
+
+/* Bytes of device workspace sgdkv_decode_attention needs for these segment
+ * lengths (offsets_host: host [B*Hkv+1] int64, non-decreasing from 0). */
+sgdkv_status sgdkv_decode_workspace_size(const sgdkv_decode_desc* desc, const int64_t* offsets_host,
+                                         size_t* bytes);
+
+/* One decode step: query head q of sequence b attends to the rows of its
+ * KV head's segment (b, q/G) of the compressed cache -- the cache is kept
+ * per KV head, before GQA repetition (Appendix A.2):
+ *   out = sum_r softmax_r(scale*<q, k_r>) v_r,  lse = log sum_r exp(scale*<q,k_r>).
+ * An empty segment gives out = 0 and lse = -inf.
+ * q: device [B][Hq][d] kv_dtype. k_c, v_c: device [rows][d] kv_dtype with
+ * rows = offsets[B*Hkv]. offsets: device [B*Hkv+1] int64; offsets_host: the
+ * same values on the host, used to plan the split without a device sync.
+ * out: device [B][Hq][d] out_dtype. lse_out: optional device [B][Hq] fp32.
+ * Errors: sizes < 1; Hq % Hkv; d not 64/128 (UNSUPPORTED); decreasing or
+ * negative offsets; misaligned or missing pointers; small workspace. */
+sgdkv_status sgdkv_decode_attention(const sgdkv_decode_desc* desc, const void* q, const void* k_c,
+                                    const void* v_c, const int64_t* offsets,
+                                    const int64_t* offsets_host, void* out, float* lse_out,
+                                    void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SGDKV_H */

@@ -1,0 +1,291 @@
+// Decode attention over the ragged compressed KV cache (gfx950).
+//
+// SGD-KV keeps its compressed cache per KV head, before the heads are repeated
+// for GQA (Appendix A.2), so one segment of rows serves the G query heads of
+// its group. Decode reads each segment once for all G heads:
+//
+//   decode_split: workgroup = (chunk of a segment's rows, segment). Logits of
+//     the G heads against 16 keys at a time are one 16x16 MFMA (the G query
+//     rows padded to 16 form the A operand). Each wave keeps an online
+//     softmax (running max m and sum s per head, base-2 units) over its
+//     quarter of the chunk and accumulates P.V in fp32 on the vector ALU
+//     (bf16 V rows are widened exactly). The four waves are merged in a fixed
+//     order and one partial (m, s, o[d]) per head and chunk is written.
+//   decode_combine: per (sequence, query head), a fixed-order log-sum-exp
+//     merge of the chunk partials; out = o/s, lse = (m + log2 s) * ln 2.
+//
+// Work is a flattened (chunk, segment) grid, so unequal budgets (one head
+// with most of the rows, others with few) still spread over the whole chip.
+#include "device_common.h"
+#include "mfma_frag.h"
+#include "sgdkv_internal.h"
+
+namespace sgdkv {
+
+namespace {
+constexpr int kKeysPerStep = 32;  // keys per wave per step (two 16-key MFMA tiles)
+constexpr int kWaves = kBlock / 64;
+
+__device__ __forceinline__ void clamp_segment(const DecodeArgs& a, int seg, int64_t& r0, int64_t& r1) {
+  const int nseg = a.B * a.Hkv;
+  const rsrc_t orr = make_rsrc(a.offsets, (uint64_t)(nseg + 1) * 8);
+  r0 = (int64_t)ld64(orr, (uint32_t)seg * 8);
+  r1 = (int64_t)ld64(orr, (uint32_t)(seg + 1) * 8);
+  r0 = r0 < 0 ? 0 : (r0 > a.total_rows ? a.total_rows : r0);
+  r1 = r1 < r0 ? r0 : (r1 > a.total_rows ? a.total_rows : r1);
+}
+}  // namespace
+
+// GM = compile-time bound on the group size (8 or 16).
+template <typename T, int D, int GM>
+__global__ __launch_bounds__(kBlock, 2) void decode_split_kernel(DecodeArgs a) {
+  constexpr int EB = sizeof(T);
+  constexpr int RB = D * EB;
+  constexpr int NC = D / 32;
+  constexpr int LPR = D / 8;     // lanes sharing one value row (8 columns each)
+  constexpr int KG = 64 / LPR;   // key groups per wave
+  constexpr int KB = kKeysPerStep;
+  __shared__ float lg[kWaves][16][KB];  // logits in base-2 units
+  __shared__ float pl[kWaves][16][KB];  // probabilities
+  __shared__ float al[kWaves][16];      // per-head rescale factor of this step
+  __shared__ float wm[kWaves][16], ws[kWaves][16];
+  __shared__ float wo[kWaves][GM][D];
+
+  const int seg = blockIdx.y;
+  const int b = seg / a.Hkv, h = seg % a.Hkv;
+  int64_t r0, r1;
+  clamp_segment(a, seg, r0, r1);
+  const int64_t len = r1 - r0;
+  const int chunk = blockIdx.x;
+  const int64_t c0 = (int64_t)chunk * a.chunk;
+  if (c0 >= len) return;  // this segment has fewer chunks
+  const int64_t c1 = c0 + a.chunk < len ? c0 + a.chunk : len;
+
+  const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
+  const int lr = lane & 15, lgp = lane >> 4;
+  const int G = a.G;
+
+  const rsrc_t kr = make_rsrc(static_cast<const char*>(a.k_c) + r0 * RB, (uint64_t)len * RB);
+  const rsrc_t vr = make_rsrc(static_cast<const char*>(a.v_c) + r0 * RB, (uint64_t)len * RB);
+  const rsrc_t qr = make_rsrc(static_cast<const char*>(a.q) + ((int64_t)b * a.Hq + (int64_t)h * G) * RB,
+                              (uint64_t)G * RB);
+  // query fragments: row lr = head (rows >= G read as zeros)
+  Frag<T> qa[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) qa[c] = gload_frag<T>(qr, (uint32_t)(lr * RB + (32 * c + 8 * lgp) * EB));
+
+  // this wave's rows [w0, w1) of the chunk
+  const int64_t per = a.chunk / kWaves;
+  const int64_t w0 = c0 + wid * per;
+  const int64_t w1 = w0 + per < c1 ? w0 + per : c1;
+  const int nsteps = (int)(per / KB);
+
+  // softmax state of head lane/4, replicated over its 4 lanes; s is this lane's share
+  const int sh_head = lane >> 2, sh_part = lane & 3;
+  float m_run = -INFINITY, s_run = 0.f;
+  const int kg = lane / LPR, col0 = 8 * (lane % LPR);
+  float o[GM][8];
+#pragma unroll
+  for (int g = 0; g < GM; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
+
+  for (int it = 0; it < nsteps; ++it) {
+    const int64_t k0 = w0 + (int64_t)it * KB;  // first key of this step (chunk-relative rows)
+    // 1. logits of the (padded) 16 heads against 32 keys
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int64_t key = k0 + 16 * t + lr;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const Frag<T> kb = gload_frag<T>(kr, (uint32_t)(key * RB + (32 * c + 8 * lgp) * EB));
+        acc = mma(qa[c], kb, acc);
+      }
+      const bool valid = key < w1;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) lg[wid][4 * lgp + i][16 * t + lr] = valid ? acc[i] * a.c2 : -INFINITY;
+    }
+    __syncthreads();
+    // 2. online softmax: lane handles head lane/4, keys 8*(lane%4) .. +7
+    {
+      float y[8];
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        y[u] = lg[wid][sh_head][8 * sh_part + u];
+        tmax = fmaxf(tmax, y[u]);
+      }
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 1, 64));
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 2, 64));
+      const float m_new = fmaxf(m_run, tmax);
+      const float alpha = (m_run == -INFINITY) ? (m_new == -INFINITY ? 1.f : 0.f) : fast_exp2(m_run - m_new);
+      float ps = 0.f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float p = (y[u] == -INFINITY) ? 0.f : fast_exp2(y[u] - m_new);
+        pl[wid][sh_head][8 * sh_part + u] = p;
+        ps += p;
+      }
+      s_run = s_run * alpha + ps;
+      m_run = m_new;
+      if (sh_part == 0) al[wid][sh_head] = alpha;
+    }
+    __syncthreads();
+    // 3. rescale and accumulate P.V for this lane's keys and columns
+#pragma unroll
+    for (int g = 0; g < GM; ++g) {
+      if (g < G) {
+        const float alpha = al[wid][g];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[g][e] *= alpha;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < KB / KG; ++u) {
+      const int kk = kg + KG * u;
+      const int64_t key = k0 + kk;
+      float v[8];
+      if (EB == 2) {
+        const u32x4 x = ld128(vr, (uint32_t)(key * RB + col0 * EB));
+        v[0] = bf16_lo(x.x); v[1] = bf16_hi(x.x); v[2] = bf16_lo(x.y); v[3] = bf16_hi(x.y);
+        v[4] = bf16_lo(x.z); v[5] = bf16_hi(x.z); v[6] = bf16_lo(x.w); v[7] = bf16_hi(x.w);
+      } else {
+        const u32x4 x0 = ld128(vr, (uint32_t)(key * RB + col0 * EB));
+        const u32x4 x1 = ld128(vr, (uint32_t)(key * RB + col0 * EB + 16));
+        v[0] = __uint_as_float(x0.x); v[1] = __uint_as_float(x0.y); v[2] = __uint_as_float(x0.z);
+        v[3] = __uint_as_float(x0.w); v[4] = __uint_as_float(x1.x); v[5] = __uint_as_float(x1.y);
+        v[6] = __uint_as_float(x1.z); v[7] = __uint_as_float(x1.w);
+      }
+#pragma unroll
+      for (int g = 0; g < GM; ++g) {
+        if (g < G) {
+          const float p = pl[wid][g][kk];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[g][e] = fmaf(p, v[e], o[g][e]);
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  // Reduce within the wave: the 4 lanes of each head's sum, the KG key groups of o.
+  s_run += __shfl_xor(s_run, 1, 64);
+  s_run += __shfl_xor(s_run, 2, 64);
+#pragma unroll
+  for (int g = 0; g < GM; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float x = o[g][e];
+#pragma unroll
+      for (int sft = LPR; sft < 64; sft <<= 1) x += __shfl_xor(x, sft, 64);
+      o[g][e] = x;
+    }
+  if (sh_part == 0 && sh_head < 16) {
+    wm[wid][sh_head] = m_run;
+    ws[wid][sh_head] = s_run;
+  }
+  if (kg == 0) {
+#pragma unroll
+    for (int g = 0; g < GM; ++g)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) wo[wid][g][col0 + e] = o[g][e];
+  }
+  __syncthreads();
+
+  // Merge the 4 waves in order and write this chunk's partial for each head.
+  const int stride = D + 2;
+  for (int x = tid; x < G * D; x += kBlock) {
+    const int g = x / D, col = x % D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kWaves; ++u) M = fmaxf(M, wm[u][g]);
+    float S = 0.f, O = 0.f;
+#pragma unroll
+    for (int u = 0; u < kWaves; ++u) {
+      const float sc = (wm[u][g] == -INFINITY) ? 0.f : fast_exp2(wm[u][g] - M);
+      S += ws[u][g] * sc;
+      O += wo[u][g][col] * sc;
+    }
+    const int64_t bq = (int64_t)b * a.Hq + (int64_t)h * G + g;
+    const rsrc_t pr = make_rsrc(a.part + (bq * a.n_chunk_max + chunk) * stride, (uint64_t)stride * 4);
+    if (col == 0) {
+      stf(pr, 0, M);
+      stf(pr, 4, S);
+    }
+    stf(pr, (uint32_t)(8 + col * 4), O);
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(128) void decode_combine_kernel(DecodeArgs a) {
+  const int bq = blockIdx.x;
+  const int b = bq / a.Hq, qh = bq % a.Hq, h = qh / a.G;
+  const int seg = b * a.Hkv + h;
+  int64_t r0, r1;
+  clamp_segment(a, seg, r0, r1);
+  const int64_t len = r1 - r0;
+  int64_t nch = (len + a.chunk - 1) / a.chunk;
+  if (nch > a.n_chunk_max) nch = a.n_chunk_max;
+  const int col = threadIdx.x;
+  const int stride = D + 2;
+  const rsrc_t pr = make_rsrc(a.part + (int64_t)bq * a.n_chunk_max * stride,
+                              (uint64_t)a.n_chunk_max * stride * 4);
+  float M = -INFINITY;
+  for (int64_t c = 0; c < nch; ++c) M = fmaxf(M, ldf(pr, (uint32_t)(c * stride * 4)));
+  float S = 0.f, O = 0.f;
+  if (M != -INFINITY) {
+    for (int64_t c = 0; c < nch; ++c) {
+      const float mc = ldf(pr, (uint32_t)(c * stride * 4));
+      const float sc = (mc == -INFINITY) ? 0.f : fast_exp2(mc - M);
+      S += ldf(pr, (uint32_t)(c * stride * 4 + 4)) * sc;
+      if (col < D) O += ldf(pr, (uint32_t)((c * stride + 2 + col) * 4)) * sc;
+    }
+  }
+  const bool empty = !(S > 0.f);
+  const float res = empty ? 0.f : O / S;
+  if (col < D) {
+    if (a.out_dtype == 1) {
+      const rsrc_t orr = make_rsrc(static_cast<char*>(a.out) + (int64_t)bq * D * 2, (uint64_t)D * 2);
+      // two columns per 32-bit store
+      const float other = __shfl_xor(res, 1, 64);
+      if ((col & 1) == 0) st32(orr, (uint32_t)col * 2, f32_to_bf16_bits(res) | (f32_to_bf16_bits(other) << 16));
+    } else {
+      const rsrc_t orr = make_rsrc(static_cast<char*>(a.out) + (int64_t)bq * D * 4, (uint64_t)D * 4);
+      stf(orr, (uint32_t)col * 4, res);
+    }
+  }
+  if (a.lse_out != nullptr && col == 0) {
+    const rsrc_t lr = make_rsrc(a.lse_out, (uint64_t)a.B * a.Hq * 4);
+    const float lse = empty ? -INFINITY : (M + fast_log2(S)) * 0.69314718055994530942f;
+    stf(lr, (uint32_t)bq * 4, lse);
+  }
+}
+
+template <typename T, int D>
+static void launch_decode_t(const DecodeArgs& a, hipStream_t st) {
+  const dim3 grid(a.n_chunk_max, a.B * a.Hkv);
+  if (a.G <= 8)
+    hipLaunchKernelGGL((decode_split_kernel<T, D, 8>), grid, dim3(kBlock), 0, st, a);
+  else
+    hipLaunchKernelGGL((decode_split_kernel<T, D, 16>), grid, dim3(kBlock), 0, st, a);
+}
+
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {
+  if (a.n_chunk_max > 0) {
+    if (a.kv_dtype == 1) {
+      if (a.D == 128) launch_decode_t<__bf16, 128>(a, st);
+      else launch_decode_t<__bf16, 64>(a, st);
+    } else {
+      if (a.D == 128) launch_decode_t<float, 128>(a, st);
+      else launch_decode_t<float, 64>(a, st);
+    }
+  }
+  if (a.D == 128)
+    hipLaunchKernelGGL(decode_combine_kernel<128>, dim3(a.B * a.Hq), dim3(128), 0, st, a);
+  else
+    hipLaunchKernelGGL(decode_combine_kernel<64>, dim3(a.B * a.Hq), dim3(128), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace sgdkv

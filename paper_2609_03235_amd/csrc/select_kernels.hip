@@ -1,0 +1,326 @@
+// Pooling, per-head top-k selection and gather for SGD-KV (gfx950).
+//
+// For KV head h with budget b_h, SGD-KV keeps the b_sink initial rows, the
+// b_window most recent rows (Sec. 3.3) and, in between, the m_h = b_h -
+// b_sink - b_window candidates with the largest pooled window score
+// (Sec. 3.3, last paragraph). The kept rows are copied, per KV head and
+// before GQA repetition (Appendix A.2), into a ragged cache.
+//
+// Selection is an exact, deterministic top-k with ties to the lower
+// position. Scores are non-negative fp32, so their bit patterns order like
+// the values. An MSB-first radix select (four 8-bit digits) finds the k-th
+// largest pattern tau and how many of the rows equal to tau are kept (q);
+// the compaction then keeps every candidate above tau and the first q equal
+// to tau in position order. Histograms use integer atomics only; everything
+// else is fixed-order, so results are bitwise reproducible.
+//
+// Kernels (grid y = segment b*Hkv + h):
+//   select_init    zero histograms, seed the radix state, write offsets
+//   pool           pooled_j = (1/k_p) sum_{|t-j|<=r} a_t (zero outside)
+//   radix_hist<p>  digit-p histogram of candidates matching the prefix
+//   radix_digit<p> pick digit p of tau; clear the histogram
+//   sel_count      per chunk: sink/window rows, candidates > tau, == tau
+//   gather         ordered compaction of a chunk + 16-byte row copies
+#include "device_common.h"
+#include "sgdkv_internal.h"
+
+namespace sgdkv {
+
+namespace {
+
+struct SegState {
+  uint32_t prefix, mask, rem;
+};
+
+__device__ __forceinline__ SegState load_state(const CompressArgs& a, int seg) {
+  const rsrc_t r = make_rsrc(a.state + (int64_t)seg * 4, 16);
+  SegState st;
+  st.prefix = ld32(r, 0);
+  st.mask = ld32(r, 4);
+  st.rem = ld32(r, 8);
+  return st;
+}
+
+// Exclusive rank of `flag` among the threads of a 256-thread block, and the
+// block total. Uses wave ballots plus one LDS exchange; `wtot` holds 4 words.
+__device__ __forceinline__ uint32_t block_rank(bool flag, uint32_t* wtot, uint32_t& total) {
+  const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
+  const unsigned long long bal = __ballot(flag);
+  const uint32_t below = (uint32_t)__popcll(bal & ((1ull << lane) - 1ull));
+  if (lane == 0) wtot[wid] = (uint32_t)__popcll(bal);
+  __syncthreads();
+  uint32_t before = 0, tot = 0;
+#pragma unroll
+  for (int u = 0; u < kBlock / 64; ++u) {
+    const uint32_t t = wtot[u];
+    before += (u < wid) ? t : 0u;
+    tot += t;
+  }
+  __syncthreads();
+  total = tot;
+  return before + below;
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(kBlock) void select_init_kernel(CompressArgs a, int write_offsets) {
+  const int seg = blockIdx.x;
+  const int b = seg / a.Hkv, h = seg % a.Hkv;
+  const int nseg = a.B * a.Hkv;
+  const rsrc_t hr = make_rsrc(a.hist + (int64_t)seg * 256, 256 * 4);
+  st32(hr, threadIdx.x * 4, 0u);
+  if (threadIdx.x == 0) {
+    const rsrc_t sr = make_rsrc(a.state + (int64_t)seg * 4, 16);
+    st32(sr, 0, 0u);
+    st32(sr, 4, 0u);
+    st32(sr, 8, (uint32_t)a.m[h]);
+    st32(sr, 12, 0u);
+    if (write_offsets) {
+      const rsrc_t orr = make_rsrc(a.offsets, (uint64_t)(nseg + 1) * 8);
+      st64(orr, (uint32_t)seg * 8, (uint64_t)((int64_t)b * a.T_layer + a.prefix[h]));
+      if (seg == nseg - 1) st64(orr, (uint32_t)nseg * 8, (uint64_t)((int64_t)a.B * a.T_layer));
+    }
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void pool_kernel(CompressArgs a) {
+  const int seg = blockIdx.y;
+  const int64_t j0 = (int64_t)blockIdx.x * a.sel_chunk;
+  const int64_t j1 = j0 + a.sel_chunk < a.n_scored ? j0 + a.sel_chunk : a.n_scored;
+  const rsrc_t cr = make_rsrc(a.colsum + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
+  const rsrc_t pr = make_rsrc(a.pooled + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
+  const int r = (a.kp - 1) / 2;
+  const float fk = (float)a.kp;
+  for (int64_t j = j0 + threadIdx.x; j < j1; j += kBlock) {
+    float s = 0.f;
+    // neighbours outside [0, n_scored) fall outside the descriptor and read as 0
+    for (int t = -r; t <= r; ++t) s += ldf(cr, (uint32_t)((j + t) * 4));
+    stf(pr, (uint32_t)(j * 4), s / fk);
+  }
+}
+
+template <int PASS>
+__global__ __launch_bounds__(kBlock) void radix_hist_kernel(CompressArgs a) {
+  __shared__ uint32_t lh[256];
+  const int seg = blockIdx.y;
+  const SegState st = load_state(a, seg);
+  if (st.rem == 0) return;  // nothing (left) to choose in this segment
+  constexpr int shift = 24 - 8 * PASS;
+  lh[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t cend = a.C - a.W;
+  const int64_t j0 = a.s + (int64_t)blockIdx.x * a.sel_chunk;
+  const int64_t j1 = j0 + a.sel_chunk < cend ? j0 + a.sel_chunk : cend;
+  const rsrc_t pr = make_rsrc(a.pooled + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
+  for (int64_t j = j0 + threadIdx.x; j < j1; j += kBlock) {
+    const uint32_t bits = ld32(pr, (uint32_t)(j * 4));
+    if ((bits & st.mask) == st.prefix) atomicAdd(&lh[(bits >> shift) & 255u], 1u);
+  }
+  __syncthreads();
+  const uint32_t v = lh[threadIdx.x];
+  if (v) atomicAdd(a.hist + (int64_t)seg * 256 + threadIdx.x, v);
+}
+
+template <int PASS>
+__global__ __launch_bounds__(kBlock) void radix_digit_kernel(CompressArgs a) {
+  __shared__ uint32_t sh[256];
+  const int seg = blockIdx.x;
+  const int tid = threadIdx.x;
+  constexpr int shift = 24 - 8 * PASS;
+  const rsrc_t hr = make_rsrc(a.hist + (int64_t)seg * 256, 256 * 4);
+  const uint32_t hv = ld32(hr, tid * 4);
+  const SegState st = load_state(a, seg);
+  sh[tid] = hv;
+  __syncthreads();
+  st32(hr, tid * 4, 0u);  // ready for the next pass
+  if (st.rem == 0) return;
+  // inclusive suffix sums S[t] = sum_{u >= t} hist[u]
+  for (int off = 1; off < 256; off <<= 1) {
+    const uint32_t add = tid + off < 256 ? sh[tid + off] : 0u;
+    __syncthreads();
+    sh[tid] += add;
+    __syncthreads();
+  }
+  const uint32_t S = sh[tid];
+  const uint32_t Sn = tid < 255 ? sh[tid + 1] : 0u;
+  if (S >= st.rem && Sn < st.rem) {  // exactly one digit satisfies this
+    const rsrc_t sr = make_rsrc(a.state + (int64_t)seg * 4, 16);
+    st32(sr, 0, st.prefix | ((uint32_t)tid << shift));
+    st32(sr, 4, st.mask | (0xFFu << shift));
+    st32(sr, 8, st.rem - Sn);
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void sel_count_kernel(CompressArgs a) {
+  __shared__ uint32_t red[3][kBlock / 64];
+  const int seg = blockIdx.y, h = seg % a.Hkv;
+  const SegState st = load_state(a, seg);
+  const bool active = a.m[h] > 0;
+  const uint32_t tau = st.prefix;
+  const int64_t j0 = (int64_t)blockIdx.x * a.sel_chunk;
+  const int64_t j1 = j0 + a.sel_chunk < a.C ? j0 + a.sel_chunk : a.C;
+  const int64_t cend = a.C - a.W;
+  const rsrc_t pr = make_rsrc(a.pooled + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
+  uint32_t nf = 0, ng = 0, ne = 0;
+  for (int64_t j = j0 + threadIdx.x; j < j1; j += kBlock) {
+    if (j < a.s || j >= cend) {
+      ++nf;
+    } else if (active) {
+      const uint32_t bits = ld32(pr, (uint32_t)(j * 4));
+      ng += bits > tau;
+      ne += bits == tau;
+    }
+  }
+  // fixed-order block reduction
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    nf += __shfl_xor(nf, o, 64);
+    ng += __shfl_xor(ng, o, 64);
+    ne += __shfl_xor(ne, o, 64);
+  }
+  const int wid = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    red[0][wid] = nf;
+    red[1][wid] = ng;
+    red[2][wid] = ne;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t f = 0, g = 0, e = 0;
+    for (int u = 0; u < kBlock / 64; ++u) {
+      f += red[0][u];
+      g += red[1][u];
+      e += red[2][u];
+    }
+    const rsrc_t cr = make_rsrc(a.counts + (int64_t)seg * a.n_sel_chunks * 4,
+                                (uint64_t)a.n_sel_chunks * 16);
+    const uint32_t base = blockIdx.x * 16u;
+    st32(cr, base + 0, f);
+    st32(cr, base + 4, g);
+    st32(cr, base + 8, e);
+  }
+}
+
+// Ordered compaction of one chunk of positions plus the K/V row copies.
+// RB = bytes per row (head_dim * element size).
+template <int RB>
+__global__ __launch_bounds__(kBlock) void gather_kernel(CompressArgs a) {
+  constexpr int V16 = RB / 16;
+  __shared__ int32_t list[kBlock];
+  __shared__ uint32_t wt0[kBlock / 64], wt1[kBlock / 64];
+  __shared__ uint32_t pre[3][kBlock / 64];
+  const int seg = blockIdx.y, b = seg / a.Hkv, h = seg % a.Hkv;
+  const int chunk = blockIdx.x;
+  const int tid = threadIdx.x;
+  const SegState st = load_state(a, seg);
+  const bool active = a.m[h] > 0;
+  const uint32_t tau = st.prefix;
+  const uint32_t q = active ? st.rem : 0u;
+
+  // totals of the chunks before this one: sink/window rows, > tau, == tau
+  const rsrc_t cr = make_rsrc(a.counts + (int64_t)seg * a.n_sel_chunks * 4, (uint64_t)a.n_sel_chunks * 16);
+  uint32_t f = 0, g = 0, e = 0;
+  for (int c = tid; c < chunk; c += kBlock) {
+    f += ld32(cr, c * 16u + 0);
+    g += ld32(cr, c * 16u + 4);
+    e += ld32(cr, c * 16u + 8);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    f += __shfl_xor(f, o, 64);
+    g += __shfl_xor(g, o, 64);
+    e += __shfl_xor(e, o, 64);
+  }
+  if ((tid & 63) == 0) {
+    pre[0][tid >> 6] = f;
+    pre[1][tid >> 6] = g;
+    pre[2][tid >> 6] = e;
+  }
+  __syncthreads();
+  uint32_t F = 0, Gt = 0, E = 0;
+#pragma unroll
+  for (int u = 0; u < kBlock / 64; ++u) {
+    F += pre[0][u];
+    Gt += pre[1][u];
+    E += pre[2][u];
+  }
+  uint32_t run_keep = F + Gt + (E < q ? E : q);
+  uint32_t run_eq = E;
+
+  const int64_t seg_off = (int64_t)b * a.T_layer + a.prefix[h];
+  const int64_t seg_len = a.prefix[h + 1] - a.prefix[h];
+  const rsrc_t kp = make_rsrc(a.kept_pos + seg_off, (uint64_t)seg_len * 4);
+  const rsrc_t ko = make_rsrc(static_cast<char*>(a.k_out) + seg_off * RB, (uint64_t)seg_len * RB);
+  const rsrc_t vo = make_rsrc(static_cast<char*>(a.v_out) + seg_off * RB, (uint64_t)seg_len * RB);
+  const rsrc_t ki = make_rsrc(static_cast<const char*>(a.k) + (int64_t)seg * a.C * RB, (uint64_t)a.C * RB);
+  const rsrc_t vi = make_rsrc(static_cast<const char*>(a.v) + (int64_t)seg * a.C * RB, (uint64_t)a.C * RB);
+  const rsrc_t pr = make_rsrc(a.pooled + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
+
+  const int64_t j0 = (int64_t)chunk * a.sel_chunk;
+  const int64_t j1 = j0 + a.sel_chunk < a.C ? j0 + a.sel_chunk : a.C;
+  const int64_t cend = a.C - a.W;
+  for (int64_t base = j0; base < j1; base += kBlock) {
+    const int64_t j = base + tid;
+    const bool inr = j < j1;
+    const bool fixed = inr && (j < a.s || j >= cend);
+    const bool cand = inr && !fixed && active;
+    const uint32_t bits = cand ? ld32(pr, (uint32_t)(j * 4)) : 0u;
+    const bool gt = cand && bits > tau;
+    const bool eq = cand && bits == tau;
+    uint32_t n_eq, n_keep;
+    const uint32_t eq_rank = run_eq + block_rank(eq, wt0, n_eq);
+    const bool keep = fixed || gt || (eq && eq_rank < q);
+    const uint32_t r = block_rank(keep, wt1, n_keep);
+    const uint32_t slot = run_keep + r;
+    if (keep) {
+      st32(kp, slot * 4u, (uint32_t)j);
+      list[r] = (int32_t)j;
+    }
+    __syncthreads();
+    // copy the chunk's kept rows, 16 bytes per thread per step
+    for (uint32_t x = tid; x < n_keep * V16; x += kBlock) {
+      const uint32_t rr = x / V16, c16 = x % V16;
+      const uint32_t src = (uint32_t)list[rr] * RB + c16 * 16;
+      const uint32_t dst = (run_keep + rr) * RB + c16 * 16;
+      st128(ko, dst, ld128(ki, src));
+      st128(vo, dst, ld128(vi, src));
+    }
+    __syncthreads();
+    run_eq += n_eq;
+    run_keep += n_keep;
+  }
+}
+
+template <int RB>
+static void launch_gather(const CompressArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((gather_kernel<RB>), dim3(a.n_sel_chunks, a.B * a.Hkv), dim3(kBlock), 0, st, a);
+}
+
+hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t st) {
+  const int nseg = a.B * a.Hkv;
+  const dim3 blk(kBlock);
+  hipLaunchKernelGGL(select_init_kernel, dim3(nseg), blk, 0, st, a, scores_only ? 0 : 1);
+  if (a.n_pool_chunks > 0) hipLaunchKernelGGL(pool_kernel, dim3(a.n_pool_chunks, nseg), blk, 0, st, a);
+  if (scores_only) return hipGetLastError();
+  if (a.n_cand_chunks > 0) {
+    hipLaunchKernelGGL(radix_hist_kernel<0>, dim3(a.n_cand_chunks, nseg), blk, 0, st, a);
+    hipLaunchKernelGGL(radix_digit_kernel<0>, dim3(nseg), blk, 0, st, a);
+    hipLaunchKernelGGL(radix_hist_kernel<1>, dim3(a.n_cand_chunks, nseg), blk, 0, st, a);
+    hipLaunchKernelGGL(radix_digit_kernel<1>, dim3(nseg), blk, 0, st, a);
+    hipLaunchKernelGGL(radix_hist_kernel<2>, dim3(a.n_cand_chunks, nseg), blk, 0, st, a);
+    hipLaunchKernelGGL(radix_digit_kernel<2>, dim3(nseg), blk, 0, st, a);
+    hipLaunchKernelGGL(radix_hist_kernel<3>, dim3(a.n_cand_chunks, nseg), blk, 0, st, a);
+    hipLaunchKernelGGL(radix_digit_kernel<3>, dim3(nseg), blk, 0, st, a);
+  }
+  hipLaunchKernelGGL(sel_count_kernel, dim3(a.n_sel_chunks, nseg), blk, 0, st, a);
+  const int rb = a.D * (a.dtype == 1 ? 2 : 4);
+  switch (rb) {
+    case 128: launch_gather<128>(a, st); break;
+    case 256: launch_gather<256>(a, st); break;
+    case 512: launch_gather<512>(a, st); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace sgdkv

@@ -1,0 +1,543 @@
+// C ABI of the SGD-KV hot path: argument validation, head budget allocation
+// (host), work planning and kernel launches. See include/sgdkv.h for the
+// contract of every entry point.
+//
+// Compiled with -ffp-contract=off: the allocation's fp64 arithmetic decides
+// integers, so every operation happens exactly in the order written.
+#include "sgdkv.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "sgdkv_internal.h"
+
+namespace {
+
+thread_local std::string g_error;
+
+sgdkv_status fail(sgdkv_status code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return code;
+}
+
+sgdkv_status ok() {
+  g_error.clear();
+  return SGDKV_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// The kernels are built for gfx950 only; check the current device once per device.
+sgdkv_status check_device() {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "no HIP device: %s", hipGetErrorString(e));
+  static std::mutex mu;
+  static std::vector<int> verdict;  // -1 unknown, 0 unsupported, 1 gfx950
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)verdict.size() <= dev) verdict.resize(dev + 1, -1);
+  if (verdict[dev] < 0) {
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
+    verdict[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 0;
+    if (!verdict[dev]) return fail(SGDKV_ERR_UNSUPPORTED, "device %d is %s; kernels are built for gfx950",
+                                   dev, prop.gcnArchName);
+  }
+  if (!verdict[dev]) return fail(SGDKV_ERR_UNSUPPORTED, "device %d is not gfx950", dev);
+  return SGDKV_OK;
+}
+
+// ----------------------------------------------------------------- budgets
+struct Ranked {
+  double frac;
+  double score;
+  int64_t index;
+};
+
+// Largest-remainder rounding of real shares that sum to T. Ties: larger
+// score, then lower index. Fp residue (never seen on well-posed inputs) is
+// absorbed round-robin in the same order.
+void round_shares(const std::vector<double>& x, const std::vector<double>& score, int64_t T,
+                  std::vector<int64_t>& out) {
+  const int64_t n = (int64_t)x.size();
+  std::vector<Ranked> r(n);
+  int64_t floors = 0, fractional = 0;
+  for (int64_t h = 0; h < n; ++h) {
+    const double f = std::floor(x[h]);
+    out[h] = (int64_t)f;
+    floors += out[h];
+    r[h] = Ranked{x[h] - f, score[h], h};
+    if (r[h].frac > 0.0) ++fractional;
+  }
+  std::sort(r.begin(), r.end(), [](const Ranked& a, const Ranked& b) {
+    if (a.frac != b.frac) return a.frac > b.frac;
+    if (a.score != b.score) return a.score > b.score;
+    return a.index < b.index;
+  });
+  int64_t left = T - floors;
+  const int64_t ones = left <= 0 ? 0 : std::min(left, fractional);
+  for (int64_t k = 0; k < ones; ++k) out[r[k].index] += 1;
+  left -= ones;
+  for (int64_t k = 0; left > 0; k = (k + 1) % n, --left) out[r[k].index] += 1;
+  for (int64_t k = 0; left < 0; k = (k + 1) % n) {
+    const int64_t h = r[n - 1 - k].index;
+    if (out[h] > 0) {
+      out[h] -= 1;
+      ++left;
+    }
+  }
+}
+
+// Heads in descending score order, ties to the lower index.
+std::vector<int64_t> score_order(const std::vector<double>& score) {
+  std::vector<int64_t> idx(score.size());
+  for (size_t h = 0; h < idx.size(); ++h) idx[h] = (int64_t)h;
+  std::sort(idx.begin(), idx.end(), [&](int64_t a, int64_t b) {
+    if (score[a] != score[b]) return score[a] > score[b];
+    return a < b;
+  });
+  return idx;
+}
+
+sgdkv_status check_sizes(int32_t L, int32_t H, int64_t C, int64_t s, int64_t W) {
+  if (L < 1 || H < 1) return fail(SGDKV_ERR_INVALID_ARG, "L=%d and H=%d must be >= 1", L, H);
+  if (C < 1) return fail(SGDKV_ERR_INVALID_ARG, "C=%lld must be >= 1", (long long)C);
+  if (s < 0 || W < 0) return fail(SGDKV_ERR_INVALID_ARG, "b_sink and b_window must be >= 0");
+  if (s + W > C) return fail(SGDKV_ERR_INVALID_ARG, "b_sink + b_window = %lld exceeds C = %lld",
+                             (long long)(s + W), (long long)C);
+  return SGDKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sgdkv_last_error(void) { return g_error.c_str(); }
+
+int32_t sgdkv_version(void) { return 100; }
+
+sgdkv_status sgdkv_reduce_query_head_scores(const double* per_qhead, int32_t L, int32_t Hq, int32_t Hkv,
+                                            double* per_kvhead_out) {
+  if (!per_qhead || !per_kvhead_out) return fail(SGDKV_ERR_INVALID_ARG, "NULL score pointer");
+  if (L < 1 || Hq < 1 || Hkv < 1) return fail(SGDKV_ERR_INVALID_ARG, "L, Hq, Hkv must be >= 1");
+  if (Hq % Hkv) return fail(SGDKV_ERR_INVALID_ARG, "Hq=%d is not a multiple of Hkv=%d", Hq, Hkv);
+  const int32_t G = Hq / Hkv;
+  for (int32_t l = 0; l < L; ++l)
+    for (int32_t h = 0; h < Hkv; ++h) {
+      const double* grp = per_qhead + (int64_t)l * Hq + (int64_t)h * G;
+      per_kvhead_out[(int64_t)l * Hkv + h] = *std::max_element(grp, grp + G);
+    }
+  return ok();
+}
+
+sgdkv_status sgdkv_total_from_ratio(double R, int32_t L, int32_t H, int64_t C, int64_t b_sink,
+                                    int64_t b_window, int32_t of_middle, int64_t* total_out) {
+  if (!total_out) return fail(SGDKV_ERR_INVALID_ARG, "NULL total_out");
+  if (!(R >= 0.0 && R <= 1.0)) return fail(SGDKV_ERR_INVALID_ARG, "ratio %g outside [0, 1]", R);
+  if (sgdkv_status st = check_sizes(L, H, C, b_sink, b_window)) return st;
+  const double LH = (double)L * (double)H;
+  const int64_t reserved = (int64_t)L * H * (b_sink + b_window);
+  int64_t total;
+  if (of_middle) {
+    total = reserved + (int64_t)std::floor(R * LH * (double)(C - b_sink - b_window));
+  } else {
+    total = (int64_t)std::floor(R * LH * (double)C);
+    if (total < reserved)
+      return fail(SGDKV_ERR_INVALID_ARG, "ratio %g gives %lld rows, fewer than the %lld sink+window rows",
+                  R, (long long)total, (long long)reserved);
+  }
+  *total_out = total;
+  return ok();
+}
+
+sgdkv_status sgdkv_allocate_budgets(const double* head_scores, int32_t L, int32_t H, int64_t C,
+                                    int64_t b_sink, int64_t b_window, int64_t total_budget, int32_t mode,
+                                    int64_t* budgets_out) {
+  if (!head_scores || !budgets_out) return fail(SGDKV_ERR_INVALID_ARG, "NULL pointer");
+  if (sgdkv_status st = check_sizes(L, H, C, b_sink, b_window)) return st;
+  if (mode != 0 && mode != 1) return fail(SGDKV_ERR_INVALID_ARG, "mode %d is not 0 or 1", mode);
+  const int64_t n = (int64_t)L * H;
+  const int64_t reserve = b_sink + b_window;
+  const int64_t M = C - reserve;
+  if (total_budget < n * reserve || total_budget > n * C)
+    return fail(SGDKV_ERR_INVALID_ARG, "total_budget %lld outside [%lld, %lld]", (long long)total_budget,
+                (long long)(n * reserve), (long long)(n * C));
+  double sum = 0.0;
+  for (int64_t h = 0; h < n; ++h) {
+    const double v = head_scores[h];
+    if (!(v >= 0.0) || std::isinf(v)) return fail(SGDKV_ERR_INVALID_ARG, "score %lld is %g", (long long)h, v);
+    sum += v;
+  }
+  if (std::isinf(sum)) return fail(SGDKV_ERR_INVALID_ARG, "scores sum to infinity");
+  const int64_t T = total_budget - n * reserve;
+
+  // Normalisation over all L*H heads (Sec. 3.3); all-zero scores mean uniform shares.
+  std::vector<double> score(n);
+  for (int64_t h = 0; h < n; ++h) score[h] = sum > 0.0 ? head_scores[h] : 1.0;
+  const double denom = sum > 0.0 ? sum : (double)n;
+
+  std::vector<double> share(n);
+  std::vector<int64_t> mid(n);
+  const std::vector<int64_t> order = score_order(score);
+  if (mode == 0) {
+    // Eq. 2 without the reserved rows, rounded; then Algorithm 1.
+    for (int64_t h = 0; h < n; ++h) share[h] = (score[h] * (double)T) / denom;
+    round_shares(share, score, T, mid);
+    int64_t excess = 0;
+    for (int64_t h = 0; h < n; ++h)
+      if (mid[h] > M) {
+        excess += mid[h] - M;
+        mid[h] = M;
+      }
+    for (int64_t h : order) {
+      if (excess == 0) break;
+      const int64_t give = std::min(M - mid[h], excess);
+      if (give > 0) {
+        mid[h] += give;
+        excess -= give;
+      }
+    }
+  } else {
+    // Water level: share = min(lambda*score, M), summing to T.
+    std::vector<double> tail(n + 1, 0.0);  // score sums over order[k..n-1], smallest first
+    for (int64_t k = n - 1; k >= 0; --k) tail[k] = tail[k + 1] + score[order[k]];
+    int64_t capped = 0;
+    double lambda = 0.0;
+    bool flat = false;
+    for (capped = 0; capped < n; ++capped) {
+      const double left = (double)T - (double)capped * (double)M;
+      if (tail[capped] <= 0.0) {
+        flat = true;  // only zero-score heads remain: they share the rest evenly
+        lambda = left / (double)(n - capped);
+        break;
+      }
+      lambda = left / tail[capped];
+      if (lambda * score[order[capped]] <= (double)M) break;
+    }
+    for (int64_t k = 0; k < n; ++k) {
+      const int64_t h = order[k];
+      double v = k < capped ? (double)M : (flat ? lambda : lambda * score[h]);
+      share[h] = v > (double)M ? (double)M : v;
+    }
+    round_shares(share, score, T, mid);
+    int64_t excess = 0;
+    for (int64_t h = 0; h < n; ++h)
+      if (mid[h] > M) {
+        excess += mid[h] - M;
+        mid[h] = M;
+      }
+    for (int64_t h : order) {
+      if (excess == 0) break;
+      const int64_t give = std::min(M - mid[h], excess);
+      if (give > 0) {
+        mid[h] += give;
+        excess -= give;
+      }
+    }
+  }
+  for (int64_t h = 0; h < n; ++h) budgets_out[h] = reserve + mid[h];
+  return ok();
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------ compress plan
+namespace {
+
+struct CompressPlan {
+  sgdkv::CompressArgs a;
+  size_t off_lse_part, off_lse2, off_colsum, off_pooled, off_hist, off_state, off_counts, bytes;
+};
+
+sgdkv_status plan_compress(const sgdkv_compress_desc* d, CompressPlan& p) {
+  if (!d) return fail(SGDKV_ERR_INVALID_ARG, "NULL descriptor");
+  if (d->batch < 1 || d->num_q_heads < 1 || d->num_kv_heads < 1)
+    return fail(SGDKV_ERR_INVALID_ARG, "batch, num_q_heads, num_kv_heads must be >= 1");
+  if (d->num_q_heads % d->num_kv_heads)
+    return fail(SGDKV_ERR_INVALID_ARG, "num_q_heads %d is not a multiple of num_kv_heads %d", d->num_q_heads,
+                d->num_kv_heads);
+  if (d->num_kv_heads > sgdkv::kMaxKvHeads)
+    return fail(SGDKV_ERR_UNSUPPORTED, "num_kv_heads %d > %d", d->num_kv_heads, sgdkv::kMaxKvHeads);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(SGDKV_ERR_UNSUPPORTED, "head_dim %d (built: 64, 128)", d->head_dim);
+  if (d->dtype != SGDKV_DTYPE_F32 && d->dtype != SGDKV_DTYPE_BF16)
+    return fail(SGDKV_ERR_INVALID_ARG, "dtype %d", d->dtype);
+  if (d->obs_window < 1) return fail(SGDKV_ERR_INVALID_ARG, "obs_window must be >= 1");
+  if (d->pool_kernel < 1 || d->pool_kernel % 2 == 0)
+    return fail(SGDKV_ERR_INVALID_ARG, "pool_kernel %d must be odd and >= 1", d->pool_kernel);
+  if (d->seq_len < 1 || d->seq_len > 0x7FFFFFFFll)
+    return fail(SGDKV_ERR_INVALID_ARG, "seq_len %lld outside [1, 2^31-1]", (long long)d->seq_len);
+  if (d->b_sink < 0 || d->b_window < 0) return fail(SGDKV_ERR_INVALID_ARG, "b_sink, b_window must be >= 0");
+  if (d->b_sink + d->b_window > d->seq_len) return fail(SGDKV_ERR_INVALID_ARG, "b_sink + b_window > seq_len");
+  if (d->b_window < d->obs_window)
+    return fail(SGDKV_ERR_INVALID_ARG, "b_window %lld < obs_window %d: recent candidates would have no score",
+                (long long)d->b_window, d->obs_window);
+  if (!(d->scale >= 0.f) || std::isinf(d->scale)) return fail(SGDKV_ERR_INVALID_ARG, "scale %g", d->scale);
+  const int G = d->num_q_heads / d->num_kv_heads;
+  const int64_t R = (int64_t)G * d->obs_window;
+  if (R > sgdkv::kMaxGroupRows)
+    return fail(SGDKV_ERR_UNSUPPORTED, "group rows G*w = %lld > %d", (long long)R, sgdkv::kMaxGroupRows);
+  if ((int64_t)d->batch * d->num_kv_heads > 65535)
+    return fail(SGDKV_ERR_UNSUPPORTED, "batch * num_kv_heads = %lld > 65535",
+                (long long)d->batch * d->num_kv_heads);
+  const int eb = d->dtype == SGDKV_DTYPE_BF16 ? 2 : 4;
+  const int64_t rb = (int64_t)d->head_dim * eb;
+  if (d->seq_len * rb > 0xFFFFFFFFll)
+    return fail(SGDKV_ERR_UNSUPPORTED, "one head's keys (%lld bytes) exceed 4 GiB", (long long)(d->seq_len * rb));
+
+  sgdkv::CompressArgs& a = p.a;
+  std::memset(&a, 0, sizeof a);
+  a.B = d->batch;
+  a.Hq = d->num_q_heads;
+  a.Hkv = d->num_kv_heads;
+  a.G = G;
+  a.D = d->head_dim;
+  a.w = d->obs_window;
+  a.kp = d->pool_kernel;
+  a.R = (int)R;
+  a.dtype = d->dtype;
+  a.C = d->seq_len;
+  a.s = d->b_sink;
+  a.W = d->b_window;
+  a.n_scored = a.C - a.w;
+  const double scale = d->scale > 0.f ? (double)d->scale : 1.0 / std::sqrt((double)d->head_dim);
+  a.c2 = (float)(scale * 1.4426950408889634074);
+  a.inv_G = 1.0f / (float)G;
+
+  const int64_t nseg = (int64_t)a.B * a.Hkv;
+  // score workgroups: about 2048 in total, whole 64-key tiles
+  a.score_chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(nseg * a.C, 2048), 64), 256), 1 << 16);
+  a.n_lse_chunks = (int)ceil_div(a.C, a.score_chunk);
+  a.n_col_chunks = (int)ceil_div(a.n_scored, a.score_chunk);
+  // selection workgroups: about 4096 in total
+  a.sel_chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(nseg * a.C, 4096), 256), 1024), 1 << 20);
+  a.n_pool_chunks = (int)ceil_div(a.n_scored, a.sel_chunk);
+  a.n_cand_chunks = (int)ceil_div(a.C - a.s - a.W, a.sel_chunk);
+  a.n_sel_chunks = (int)ceil_div(a.C, a.sel_chunk);
+
+  size_t off = 0;
+  p.off_lse_part = off;
+  off += align256((size_t)nseg * a.n_lse_chunks * R * 2 * sizeof(float));
+  p.off_lse2 = off;
+  off += align256((size_t)nseg * R * sizeof(float));
+  p.off_colsum = off;
+  off += align256((size_t)nseg * a.n_scored * sizeof(float));
+  p.off_pooled = off;
+  off += align256((size_t)nseg * a.n_scored * sizeof(float));
+  p.off_hist = off;
+  off += align256((size_t)nseg * 256 * sizeof(uint32_t));
+  p.off_state = off;
+  off += align256((size_t)nseg * 4 * sizeof(uint32_t));
+  p.off_counts = off;
+  off += align256((size_t)nseg * a.n_sel_chunks * 4 * sizeof(uint32_t));
+  p.bytes = off;
+  return SGDKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sgdkv_status sgdkv_compress_workspace_size(const sgdkv_compress_desc* desc, size_t* bytes) {
+  if (!bytes) return fail(SGDKV_ERR_INVALID_ARG, "NULL bytes");
+  CompressPlan p;
+  if (sgdkv_status st = plan_compress(desc, p)) return st;
+  *bytes = p.bytes;
+  return ok();
+}
+
+sgdkv_status sgdkv_compress_layer(const sgdkv_compress_desc* desc, const int64_t* layer_budgets,
+                                  const void* q_win, const void* k, const void* v, const float* window_lse,
+                                  void* k_out, void* v_out, int32_t* kept_pos_out, int64_t* offsets_out,
+                                  float* scores_out, void* workspace, size_t workspace_bytes, void* stream) {
+  CompressPlan p;
+  if (sgdkv_status st = plan_compress(desc, p)) return st;
+  sgdkv::CompressArgs& a = p.a;
+  const int n_out = (k_out != nullptr) + (v_out != nullptr) + (kept_pos_out != nullptr) + (offsets_out != nullptr);
+  if (n_out != 0 && n_out != 4)
+    return fail(SGDKV_ERR_INVALID_ARG, "k_out, v_out, kept_pos_out, offsets_out must be all set or all NULL");
+  const bool scores_only = n_out == 0;
+  if (scores_only && !scores_out) return fail(SGDKV_ERR_INVALID_ARG, "scores-only mode needs scores_out");
+  if (!q_win || !k) return fail(SGDKV_ERR_INVALID_ARG, "NULL q_win or k");
+  if (!scores_only && !v) return fail(SGDKV_ERR_INVALID_ARG, "NULL v");
+  const void* ptrs[] = {q_win, k, v, window_lse, k_out, v_out, kept_pos_out, offsets_out, scores_out};
+  const char* names[] = {"q_win", "k", "v", "window_lse", "k_out", "v_out", "kept_pos_out", "offsets_out",
+                         "scores_out"};
+  for (int i = 0; i < 9; ++i)
+    if (ptrs[i] && !aligned16(ptrs[i])) return fail(SGDKV_ERR_INVALID_ARG, "%s is not 16-byte aligned", names[i]);
+  if (!scores_only || layer_budgets) {
+    if (!layer_budgets) return fail(SGDKV_ERR_INVALID_ARG, "NULL layer_budgets");
+    int64_t run = 0;
+    for (int h = 0; h < a.Hkv; ++h) {
+      const int64_t bh = layer_budgets[h];
+      if (bh < a.s + a.W || bh > a.C)
+        return fail(SGDKV_ERR_INVALID_ARG, "layer_budgets[%d] = %lld outside [%lld, %lld]", h, (long long)bh,
+                    (long long)(a.s + a.W), (long long)a.C);
+      a.m[h] = bh - a.s - a.W;
+      a.prefix[h] = run;
+      run += bh;
+    }
+    a.prefix[a.Hkv] = run;
+    a.T_layer = run;
+  }
+  if (p.bytes > 0) {
+    if (!workspace) return fail(SGDKV_ERR_WORKSPACE, "NULL workspace (%zu bytes needed)", p.bytes);
+    if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+      return fail(SGDKV_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+    if (workspace_bytes < p.bytes)
+      return fail(SGDKV_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.bytes);
+  }
+  if (sgdkv_status st = check_device()) return st;
+
+  char* ws = static_cast<char*>(workspace);
+  a.q_win = q_win;
+  a.k = k;
+  a.v = v;
+  a.window_lse = window_lse;
+  a.k_out = k_out;
+  a.v_out = v_out;
+  a.kept_pos = kept_pos_out;
+  a.offsets = offsets_out;
+  a.pooled = scores_out ? scores_out : reinterpret_cast<float*>(ws + p.off_pooled);
+  a.lse_part = reinterpret_cast<float*>(ws + p.off_lse_part);
+  a.lse2 = reinterpret_cast<float*>(ws + p.off_lse2);
+  a.colsum = reinterpret_cast<float*>(ws + p.off_colsum);
+  a.hist = reinterpret_cast<uint32_t*>(ws + p.off_hist);
+  a.state = reinterpret_cast<uint32_t*>(ws + p.off_state);
+  a.counts = reinterpret_cast<uint32_t*>(ws + p.off_counts);
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = hipGetLastError();  // clear a stale error left by earlier, unrelated work
+  (void)e;
+  e = sgdkv::launch_scores(a, st);
+  if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "score kernels: %s", hipGetErrorString(e));
+  e = sgdkv::launch_select(a, scores_only, st);
+  if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "selection kernels: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"
+
+// -------------------------------------------------------------- decode plan
+namespace {
+
+struct DecodePlan {
+  sgdkv::DecodeArgs a;
+  size_t bytes;
+};
+
+sgdkv_status plan_decode(const sgdkv_decode_desc* d, const int64_t* offsets_host, DecodePlan& p) {
+  if (!d) return fail(SGDKV_ERR_INVALID_ARG, "NULL descriptor");
+  if (!offsets_host) return fail(SGDKV_ERR_INVALID_ARG, "NULL offsets_host");
+  if (d->batch < 1 || d->num_q_heads < 1 || d->num_kv_heads < 1)
+    return fail(SGDKV_ERR_INVALID_ARG, "batch, num_q_heads, num_kv_heads must be >= 1");
+  if (d->num_q_heads % d->num_kv_heads)
+    return fail(SGDKV_ERR_INVALID_ARG, "num_q_heads %d is not a multiple of num_kv_heads %d", d->num_q_heads,
+                d->num_kv_heads);
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(SGDKV_ERR_UNSUPPORTED, "head_dim %d (built: 64, 128)", d->head_dim);
+  if ((d->kv_dtype != 0 && d->kv_dtype != 1) || (d->out_dtype != 0 && d->out_dtype != 1))
+    return fail(SGDKV_ERR_INVALID_ARG, "dtype");
+  const int G = d->num_q_heads / d->num_kv_heads;
+  if (G > sgdkv::kMaxDecodeGroup) return fail(SGDKV_ERR_UNSUPPORTED, "group size %d > %d", G, sgdkv::kMaxDecodeGroup);
+  if (!(d->scale >= 0.f) || std::isinf(d->scale)) return fail(SGDKV_ERR_INVALID_ARG, "scale %g", d->scale);
+  const int64_t nseg = (int64_t)d->batch * d->num_kv_heads;
+  if (nseg > 65535) return fail(SGDKV_ERR_UNSUPPORTED, "batch * num_kv_heads = %lld > 65535", (long long)nseg);
+  if ((int64_t)d->batch * d->num_q_heads > 0x7FFFFFFFll) return fail(SGDKV_ERR_UNSUPPORTED, "batch * num_q_heads");
+  const int64_t rb = (int64_t)d->head_dim * (d->kv_dtype == 1 ? 2 : 4);
+  if (offsets_host[0] < 0) return fail(SGDKV_ERR_INVALID_ARG, "offsets[0] < 0");
+  int64_t longest = 0;
+  for (int64_t i = 0; i < nseg; ++i) {
+    const int64_t len = offsets_host[i + 1] - offsets_host[i];
+    if (len < 0) return fail(SGDKV_ERR_INVALID_ARG, "offsets decrease at %lld", (long long)i);
+    longest = std::max(longest, len);
+  }
+  if (longest * rb > 0xFFFFFFFFll) return fail(SGDKV_ERR_UNSUPPORTED, "a segment exceeds 4 GiB");
+  const int64_t total = offsets_host[nseg];
+
+  sgdkv::DecodeArgs& a = p.a;
+  std::memset(&a, 0, sizeof a);
+  a.B = d->batch;
+  a.Hq = d->num_q_heads;
+  a.Hkv = d->num_kv_heads;
+  a.G = G;
+  a.D = d->head_dim;
+  a.kv_dtype = d->kv_dtype;
+  a.out_dtype = d->out_dtype;
+  const double scale = d->scale > 0.f ? (double)d->scale : 1.0 / std::sqrt((double)d->head_dim);
+  a.c2 = (float)(scale * 1.4426950408889634074);
+  a.total_rows = total;
+  // rows per split: about 4096 splits over the whole batch, at least 256
+  a.chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(total - offsets_host[0], 4096), 128), 256), 1 << 24);
+  a.n_chunk_max = (int)ceil_div(longest, a.chunk);
+  p.bytes = align256((size_t)a.B * a.Hq * a.n_chunk_max * (a.D + 2) * sizeof(float));
+  return SGDKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sgdkv_status sgdkv_decode_workspace_size(const sgdkv_decode_desc* desc, const int64_t* offsets_host,
+                                         size_t* bytes) {
+  if (!bytes) return fail(SGDKV_ERR_INVALID_ARG, "NULL bytes");
+  DecodePlan p;
+  if (sgdkv_status st = plan_decode(desc, offsets_host, p)) return st;
+  *bytes = p.bytes;
+  return ok();
+}
+
+sgdkv_status sgdkv_decode_attention(const sgdkv_decode_desc* desc, const void* q, const void* k_c,
+                                    const void* v_c, const int64_t* offsets, const int64_t* offsets_host,
+                                    void* out, float* lse_out, void* workspace, size_t workspace_bytes,
+                                    void* stream) {
+  DecodePlan p;
+  if (sgdkv_status st = plan_decode(desc, offsets_host, p)) return st;
+  sgdkv::DecodeArgs& a = p.a;
+  if (!q || !offsets || !out) return fail(SGDKV_ERR_INVALID_ARG, "NULL q, offsets or out");
+  if (a.total_rows > 0 && (!k_c || !v_c)) return fail(SGDKV_ERR_INVALID_ARG, "NULL k_c or v_c");
+  const void* ptrs[] = {q, k_c, v_c, offsets, out, lse_out};
+  const char* names[] = {"q", "k_c", "v_c", "offsets", "out", "lse_out"};
+  for (int i = 0; i < 6; ++i)
+    if (ptrs[i] && !aligned16(ptrs[i])) return fail(SGDKV_ERR_INVALID_ARG, "%s is not 16-byte aligned", names[i]);
+  if (p.bytes > 0) {
+    if (!workspace) return fail(SGDKV_ERR_WORKSPACE, "NULL workspace (%zu bytes needed)", p.bytes);
+    if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+      return fail(SGDKV_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+    if (workspace_bytes < p.bytes)
+      return fail(SGDKV_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.bytes);
+  }
+  if (sgdkv_status st = check_device()) return st;
+  a.q = q;
+  a.k_c = k_c;
+  a.v_c = v_c;
+  a.offsets = offsets;
+  a.out = out;
+  a.lse_out = lse_out;
+  a.part = static_cast<float*>(workspace);
+  hipError_t e = hipGetLastError();
+  (void)e;
+  e = sgdkv::launch_decode(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "decode kernels: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,79 @@
+// Internal interface between the C-ABI host layer (sgdkv_host.cpp) and the
+// HIP kernels. Not installed; not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sgdkv {
+
+constexpr int kMaxKvHeads = 64;    // per-head tables travel by value in kernel arguments
+constexpr int kMaxGroupRows = 512; // G*w rows of one KV head's window queries
+constexpr int kMaxDecodeGroup = 16;
+constexpr int kBlock = 256;        // threads per workgroup in every kernel
+constexpr int kScoreTile = 64;     // keys staged in LDS per step of the score kernels
+constexpr int kScoreWaves = 8;     // waves per score workgroup
+constexpr int kScoreBlock = 64 * kScoreWaves;
+
+// ---------------------------------------------------------------- compress
+struct CompressArgs {
+  // shapes
+  int B, Hq, Hkv, G, D, w, kp, R, dtype;
+  int64_t C, s, W, n_scored;  // n_scored = C - w
+  float c2;                   // logit scale * log2(e): scores work in base-2 units
+  float inv_G;
+  // inputs
+  const void* q_win;
+  const void* k;
+  const void* v;
+  const float* window_lse;  // natural log, optional
+  // outputs
+  void* k_out;
+  void* v_out;
+  int32_t* kept_pos;
+  int64_t* offsets;
+  float* pooled;  // caller's scores_out or workspace
+  // workspace regions
+  float* lse_part;  // [B*Hkv][n_lse_chunks][R][2]  (m, s) in base-2 units
+  float* lse2;      // [B*Hkv][R]                   base-2 LSE of each window row
+  float* colsum;    // [B*Hkv][n_scored]
+  uint32_t* hist;   // [B*Hkv][256]
+  uint32_t* state;  // [B*Hkv][4]: prefix, mask, rows still to place, unused
+  uint32_t* counts; // [B*Hkv][n_sel_chunks][4]: fixed, greater, equal, unused
+  // chunking
+  int64_t score_chunk;  // keys per score workgroup (multiple of kScoreTile)
+  int n_lse_chunks;     // ceil(C / score_chunk)
+  int n_col_chunks;     // ceil(n_scored / score_chunk)
+  int64_t sel_chunk;    // positions per selection workgroup
+  int n_pool_chunks;    // ceil(n_scored / sel_chunk)
+  int n_cand_chunks;    // ceil(M / sel_chunk), M = C - s - W candidates
+  int n_sel_chunks;     // ceil(C / sel_chunk)
+  // per KV head of this layer (shared by every sequence)
+  int64_t T_layer;
+  int64_t m[kMaxKvHeads];           // middle rows kept per head
+  int64_t prefix[kMaxKvHeads + 1];  // exclusive prefix sums of the budgets
+};
+
+hipError_t launch_scores(const CompressArgs& a, hipStream_t stream);      // passes 1 and 2
+hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t stream);
+
+// ------------------------------------------------------------------ decode
+struct DecodeArgs {
+  int B, Hq, Hkv, G, D, kv_dtype, out_dtype;
+  float c2;  // scale * log2(e)
+  const void* q;
+  const void* k_c;
+  const void* v_c;
+  const int64_t* offsets;
+  int64_t total_rows;  // offsets_host[B*Hkv]: device offsets are clamped to it
+  void* out;
+  float* lse_out;
+  float* part;        // [B*Hq][n_chunk_max][D+2]: (m, s, o[D]) per split
+  int64_t chunk;      // rows per split (multiple of 128)
+  int n_chunk_max;    // max over segments of ceil(len / chunk)
+};
+
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
+
+}  // namespace sgdkv

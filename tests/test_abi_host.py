@@ -1,0 +1,200 @@
+"""Host-side tests of the C ABI (no GPU needed).
+
+* the library loads and exports every function include/sgdkv.h declares;
+* budget allocation (host code) is bit-exact against the oracle;
+* every validation error returns its status before any device work, and
+  leaves host outputs untouched;
+* without a usable GPU, well-formed compress/decode calls fail with
+  SGDKV_ERR_HIP only after validation passed.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+from hypothesis import HealthCheck, given, settings
+from hypothesis import strategies as st
+
+import oracle
+import paper_2609_03235_amd as sg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _gpu():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False
+
+
+def test_exports_every_declared_symbol():
+    header = open(os.path.join(ROOT, "include", "sgdkv.h")).read()
+    declared = set(re.findall(r"^\s*(?:sgdkv_status|const char\*|int32_t)\s+(sgdkv_\w+)\(", header, re.M))
+    assert declared == set(sg.SYMBOLS)
+    lib = sg.load_library()
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert sg.version() == 100
+
+
+problem = st.integers(min_value=1, max_value=4).flatmap(
+    lambda L: st.integers(min_value=1, max_value=8).flatmap(
+        lambda H: st.tuples(
+            st.just(L), st.just(H),
+            st.lists(st.one_of(st.floats(0.0, 1.0), st.floats(0.0, 1e6), st.sampled_from([0.0, 0.5, 1.0])),
+                     min_size=L * H, max_size=L * H),
+            st.integers(1, 5000), st.integers(0, 64), st.integers(0, 64), st.floats(0.0, 1.0))))
+
+
+@settings(max_examples=400, deadline=None, suppress_health_check=[HealthCheck.too_slow])
+@given(problem, st.sampled_from([0, 1]))
+def test_allocation_bit_exact_vs_oracle(p, mode):
+    L, H, scores, C, s, W, frac = p
+    if s + W > C:
+        return
+    n = L * H
+    total = n * (s + W) + int(frac * n * (C - s - W))
+    got = sg.allocate_budgets(scores, L, H, C, s, W, total, mode)
+    ref = oracle.allocate_budgets(np.array(scores), L, H, C, s, W, total, mode)
+    assert np.array_equal(got, ref)
+
+
+def test_allocation_workload_tables_bit_exact():
+    import workloads
+    for wl in workloads.WORKLOADS.values():
+        sc = workloads.head_scores(wl)
+        for R in wl.ratios:
+            for of_middle in (0, 1):
+                t_lib = sg.total_from_ratio(R, wl.layers, wl.num_kv_heads, wl.seq_len, wl.b_sink, wl.b_window,
+                                            of_middle)
+                t_orc = oracle.total_from_ratio(R, wl.layers, wl.num_kv_heads, wl.seq_len, wl.b_sink,
+                                                wl.b_window, of_middle)
+                assert t_lib == t_orc
+                for mode in (0, 1):
+                    got = sg.allocate_budgets(sc, wl.layers, wl.num_kv_heads, wl.seq_len, wl.b_sink,
+                                              wl.b_window, t_lib, mode)
+                    ref = oracle.allocate_budgets(sc, wl.layers, wl.num_kv_heads, wl.seq_len, wl.b_sink,
+                                                  wl.b_window, t_orc, mode)
+                    assert np.array_equal(got, ref), (wl.key, R, mode)
+
+
+def test_reduce_query_head_scores_matches_oracle():
+    rng = np.random.Generator(np.random.PCG64(4))
+    per_q = rng.random((28, 28))
+    assert np.array_equal(sg.reduce_query_head_scores(per_q, 4), oracle.reduce_group_max(per_q, 4))
+
+
+def test_allocation_errors_leave_output_untouched():
+    lib = sg.load_library()
+    out = np.full(4, -7, dtype=np.int64)
+    P = sg._np_ptr
+    bad = [
+        (np.array([0.1, -1.0, 0.2, 0.3]), 1, 4, 100, 2, 2, 50, 0),
+        (np.array([0.1, np.inf, 0.2, 0.3]), 1, 4, 100, 2, 2, 50, 0),
+        (np.array([0.1, np.nan, 0.2, 0.3]), 1, 4, 100, 2, 2, 50, 0),
+        (np.array([0.1, 0.1, 0.2, 0.3]), 1, 4, 100, 2, 2, 15, 0),   # below 4*(2+2)
+        (np.array([0.1, 0.1, 0.2, 0.3]), 1, 4, 100, 2, 2, 401, 0),  # above 4*100
+        (np.array([0.1, 0.1, 0.2, 0.3]), 1, 4, 100, 60, 60, 300, 0),  # s+W > C
+        (np.array([0.1, 0.1, 0.2, 0.3]), 1, 4, 100, 2, 2, 50, 2),   # mode
+        (np.array([0.1, 0.1, 0.2, 0.3]), 0, 4, 100, 2, 2, 50, 0),   # L
+    ]
+    for sc, L, H, C, s, W, total, mode in bad:
+        rc = lib.sgdkv_allocate_budgets(P(np.ascontiguousarray(sc)), L, H, C, s, W, total, mode, P(out))
+        assert rc == sg.ERR_INVALID_ARG, (sc, L, H, C, s, W, total, mode)
+        assert lib.sgdkv_last_error()
+        assert np.all(out == -7)
+    assert lib.sgdkv_allocate_budgets(None, 1, 4, 100, 2, 2, 50, 0, P(out)) == sg.ERR_INVALID_ARG
+    with pytest.raises(sg.SgdkvError):
+        sg.total_from_ratio(1.5, 1, 4, 100, 2, 2)
+
+
+FAKE = 0x7F0000000000  # 256-aligned stand-in device address; validation never dereferences it
+
+
+def _desc(**kw):
+    base = dict(batch=1, num_q_heads=4, num_kv_heads=2, head_dim=64, obs_window=32, pool_kernel=7,
+                seq_len=2048, b_sink=4, b_window=32, dtype=sg.DTYPE_F32, scale=0.0)
+    base.update(kw)
+    return sg.CompressDesc(**base)
+
+
+def _compress(desc, budgets, ptrs=None, ws_bytes=None, ws=FAKE):
+    lib = sg.load_library()
+    ptrs = {**dict(q_win=FAKE, k=FAKE, v=FAKE, lse=None, k_out=FAKE, v_out=FAKE, kept=FAKE, offsets=FAKE,
+                   scores=FAKE), **(ptrs or {})}
+    need = ctypes.c_size_t(0)
+    lib.sgdkv_compress_workspace_size(ctypes.byref(desc), ctypes.byref(need))
+    b = None if budgets is None else np.ascontiguousarray(np.asarray(budgets, dtype=np.int64))
+    return lib.sgdkv_compress_layer(
+        ctypes.byref(desc), None if b is None else sg._np_ptr(b), ptrs["q_win"], ptrs["k"], ptrs["v"],
+        ptrs["lse"], ptrs["k_out"], ptrs["v_out"], ptrs["kept"], ptrs["offsets"], ptrs["scores"], ws,
+        need.value if ws_bytes is None else ws_bytes, None)
+
+
+def test_compress_validation():
+    good = [512, 512]
+    cases = [
+        (_desc(batch=0), good, None, None, sg.ERR_INVALID_ARG),
+        (_desc(num_q_heads=5), good, None, None, sg.ERR_INVALID_ARG),
+        (_desc(head_dim=96), good, None, None, sg.ERR_UNSUPPORTED),
+        (_desc(pool_kernel=4), good, None, None, sg.ERR_INVALID_ARG),
+        (_desc(b_window=16), good, None, None, sg.ERR_INVALID_ARG),          # W < w
+        (_desc(b_sink=2000, b_window=100), good, None, None, sg.ERR_INVALID_ARG),
+        (_desc(num_q_heads=64, num_kv_heads=2, obs_window=32), good, None, None, sg.ERR_UNSUPPORTED),  # G*w
+        (_desc(num_kv_heads=65, num_q_heads=65), [512] * 65, None, None, sg.ERR_UNSUPPORTED),
+        (_desc(dtype=5), good, None, None, sg.ERR_INVALID_ARG),
+        (_desc(scale=-1.0), good, None, None, sg.ERR_INVALID_ARG),
+        (_desc(), [35, 512], None, None, sg.ERR_INVALID_ARG),                  # budget < s+W
+        (_desc(), [512, 2049], None, None, sg.ERR_INVALID_ARG),                # budget > C
+        (_desc(), None, None, None, sg.ERR_INVALID_ARG),                       # budgets needed
+        (_desc(), good, dict(k_out=None), None, sg.ERR_INVALID_ARG),           # partial outputs
+        (_desc(), good, dict(k_out=None, v_out=None, kept=None, offsets=None, scores=None), None,
+         sg.ERR_INVALID_ARG),                                                  # scores-only needs scores
+        (_desc(), good, dict(q_win=FAKE + 4), None, sg.ERR_INVALID_ARG),       # misaligned
+        (_desc(), good, dict(k=None), None, sg.ERR_INVALID_ARG),
+        (_desc(), good, None, 16, sg.ERR_WORKSPACE),                            # small workspace
+    ]
+    for desc, budgets, ptrs, ws_bytes, want in cases:
+        assert _compress(desc, budgets, ptrs, ws_bytes) == want, (desc.__dict__ if hasattr(desc, "__dict__") else desc)
+        assert sg.load_library().sgdkv_last_error()
+    assert _compress(_desc(), good, ws=FAKE + 16) == sg.ERR_WORKSPACE  # misaligned workspace
+    assert _compress(_desc(), good, ws=None) == sg.ERR_WORKSPACE
+
+
+def test_workspace_size_independent_of_budgets():
+    n = sg.compress_workspace_size(_desc())
+    assert n > 0 and n % 256 == 0
+    assert sg.compress_workspace_size(_desc(batch=2)) > n
+
+
+def _decode(desc, offsets_host, ptrs=None, ws_bytes=None, ws=FAKE):
+    lib = sg.load_library()
+    ptrs = {**dict(q=FAKE, k=FAKE, v=FAKE, off=FAKE, out=FAKE, lse=FAKE), **(ptrs or {})}
+    oh = np.ascontiguousarray(np.asarray(offsets_host, dtype=np.int64))
+    need = ctypes.c_size_t(0)
+    lib.sgdkv_decode_workspace_size(ctypes.byref(desc), sg._np_ptr(oh), ctypes.byref(need))
+    return lib.sgdkv_decode_attention(ctypes.byref(desc), ptrs["q"], ptrs["k"], ptrs["v"], ptrs["off"],
+                                      sg._np_ptr(oh), ptrs["out"], ptrs["lse"], ws,
+                                      need.value if ws_bytes is None else ws_bytes, None)
+
+
+def test_decode_validation():
+    d = sg.DecodeDesc(2, 4, 2, 64, 1, 0, 0.0)
+    oh = [0, 10, 10, 30, 31]
+    assert _decode(sg.DecodeDesc(2, 4, 3, 64, 1, 0, 0.0), oh) == sg.ERR_INVALID_ARG
+    assert _decode(sg.DecodeDesc(2, 4, 2, 80, 1, 0, 0.0), oh) == sg.ERR_UNSUPPORTED
+    assert _decode(sg.DecodeDesc(1, 34, 2, 64, 1, 0, 0.0), [0, 1, 2]) == sg.ERR_UNSUPPORTED  # G = 17
+    assert _decode(d, [0, 10, 9, 30, 31]) == sg.ERR_INVALID_ARG  # decreasing
+    assert _decode(d, [-1, 10, 10, 30, 31]) == sg.ERR_INVALID_ARG
+    assert _decode(d, oh, dict(out=None)) == sg.ERR_INVALID_ARG
+    assert _decode(d, oh, dict(k=FAKE + 8)) == sg.ERR_INVALID_ARG
+    assert _decode(d, oh, ws_bytes=8) == sg.ERR_WORKSPACE
+
+
+@pytest.mark.skipif(_gpu(), reason="checks the no-device path")
+def test_no_device_fails_after_validation():
+    assert _compress(_desc(), [512, 512]) == sg.ERR_HIP
+    assert _decode(sg.DecodeDesc(2, 4, 2, 64, 1, 0, 0.0), [0, 10, 10, 30, 31]) == sg.ERR_HIP

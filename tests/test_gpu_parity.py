@@ -1,0 +1,274 @@
+"""GPU parity of the HIP path against the CPU oracle (MI355X).
+
+Every check calls the library through the C ABI (paper_2609_03235_amd) and
+compares with the oracle on the same seeded inputs:
+
+* budgets, offsets and the gathered K/V rows: bit-exact;
+* pooled window scores: |gpu - oracle| <= 1e-5 * max(|oracle|, 1e-12 * max);
+* kept positions: bit-exact against the oracle's selection applied to the
+  GPU's own fp32 scores (both sides decide in the kernel's precision), and
+  against the oracle's fp64 selection except inside the near-tie band
+  (|score - tau| <= 1e-5 * tau);
+* decode: the oracle's compressed cache fed to the GPU decode, within 1e-5
+  absolute for fp32 inputs and 2e-2 absolute (fp32 output) for bf16 inputs.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_03235_amd as sg
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+SCORE_RTOL = 1e-5
+DEV = "cuda"
+
+
+def _announce(msg):
+    print(f"[gpu case] {msg}", flush=True)
+
+
+def _f64(t):
+    return t.detach().cpu().double().numpy()
+
+
+def _check_scores(g, o, tag=""):
+    g = np.asarray(g, dtype=np.float64)
+    floor = 1e-12 * np.max(np.abs(o), axis=-1, keepdims=True)
+    tol = SCORE_RTOL * np.maximum(np.abs(o), floor)
+    bad = np.abs(g - o) > tol
+    if bad.any():
+        idx = np.argwhere(bad)[:5]
+        rel = (np.abs(g - o) / np.maximum(np.abs(o), 1e-300))[bad]
+        raise AssertionError(f"{tag} {bad.sum()} scores outside rtol {SCORE_RTOL}; worst rel {rel.max():.3e}; "
+                             f"first {idx.tolist()}")
+
+
+def _check_kept(res, orc, q_shape, C, w, s, W, budgets, tag=""):
+    """Selection checks for every segment; returns True if GPU and oracle kept sets are identical."""
+    B, Hq = q_shape[0], q_shape[1]
+    Hkv = len(budgets)
+    kept = res["kept_pos"].cpu().numpy()
+    offs = res["offsets"].cpu().numpy()
+    assert np.array_equal(offs, res["offsets_host"]), f"{tag} offsets"
+    assert np.array_equal(offs, orc["offsets"]), f"{tag} offsets vs oracle"
+    scores = res["scores"].cpu().numpy().astype(np.float64)
+    identical = True
+    for b in range(B):
+        for h in range(Hkv):
+            seg = kept[offs[b * Hkv + h]:offs[b * Hkv + h + 1]]
+            m = int(budgets[h]) - s - W
+            # same decision in the kernel's precision: the oracle's top-k of the GPU's scores
+            ref_same = oracle.select(scores[b, h], C, w, s, W, m)
+            assert np.array_equal(seg, ref_same), f"{tag} b={b} h={h}: kept set differs from top-k of GPU scores"
+            ref = orc["kept_pos"][orc["offsets"][b * Hkv + h]:orc["offsets"][b * Hkv + h + 1]]
+            if not np.array_equal(seg, ref):
+                identical = False
+                po = orc["pooled"][b, h]
+                cand = np.sort(po[s:C - W])[::-1]
+                tau = cand[m - 1]
+                diff = np.setxor1d(seg, ref)
+                assert np.all(np.abs(po[diff] - tau) <= SCORE_RTOL * tau), \
+                    f"{tag} b={b} h={h}: kept sets differ outside the near-tie band"
+    return identical
+
+
+def _check_gather(res, k, v, budgets):
+    B, Hkv = k.shape[0], k.shape[1]
+    kept = res["kept_pos"].long()
+    offs = res["offsets_host"]
+    for b in range(B):
+        for h in range(Hkv):
+            lo, hi = offs[b * Hkv + h], offs[b * Hkv + h + 1]
+            pos = kept[lo:hi]
+            assert torch.equal(res["k_c"][lo:hi], k[b, h][pos]), f"K gather b={b} h={h}"
+            assert torch.equal(res["v_c"][lo:hi], v[b, h][pos]), f"V gather b={b} h={h}"
+
+
+def _compress_both(q_win, k, v, budgets, *, kp, s, W, window_lse=None, orc_lse=None):
+    w = q_win.shape[2]
+    res = sg.compress_layer(q_win, k, v, budgets, pool_kernel=kp, b_sink=s, b_window=W, window_lse=window_lse)
+    torch.cuda.synchronize()
+    orc = oracle.compress(_f64(q_win), _f64(k), _f64(v), budgets, w=w, kp=kp, s=s, W=W, lse=orc_lse)
+    return res, orc
+
+
+def _decode_on_oracle_cache(orc, q, Hkv, dtype, atol, tag):
+    """Upload the oracle's compressed cache, decode on the GPU, compare with the oracle's decode."""
+    kc = torch.from_numpy(orc["k_c"]).to(dtype).to(DEV)
+    vc = torch.from_numpy(orc["v_c"]).to(dtype).to(DEV)
+    offs = torch.from_numpy(orc["offsets"]).to(DEV)
+    out, lse = sg.decode_attention(q, kc, vc, offs, orc["offsets"], Hkv, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref_out, ref_lse = oracle.decode(_f64(q), _f64(kc), _f64(vc), orc["offsets"], Hkv)
+    err = np.abs(out.cpu().numpy() - ref_out).max()
+    assert err <= atol, f"{tag} decode max abs err {err:.3e} > {atol}"
+    fin = np.isfinite(ref_lse)
+    assert np.array_equal(np.isfinite(lse.cpu().numpy()), fin)
+    assert np.abs(lse.cpu().numpy()[fin] - ref_lse[fin]).max() <= max(atol, 1e-5)
+    return out
+
+
+# ---------------------------------------------------------------------- cases
+def _tiny_inputs(B=1, C=None, seed=None):
+    wl = workloads.WORKLOADS["tiny"]
+    t = workloads.numpy_tensors(wl, batch=B, seq_len=C, seed=seed)
+    return wl, {k: torch.from_numpy(x).to(DEV) for k, x in t.items()}
+
+
+def test_tiny_end_to_end():
+    """The tiny fp32 workload: 4 query / 2 KV heads, d 64, C 2048, w 32, k_p 7, 25 % of all rows."""
+    wl, t = _tiny_inputs()
+    _announce("tiny fp32 end-to-end")
+    sc = workloads.head_scores(wl)
+    total = sg.total_from_ratio(0.25, 1, 2, wl.seq_len, wl.b_sink, wl.b_window)
+    assert total == 1024
+    budgets = sg.allocate_budgets(sc, 1, 2, wl.seq_len, wl.b_sink, wl.b_window, total)
+    assert np.array_equal(budgets, oracle.allocate_budgets(sc, 1, 2, wl.seq_len, wl.b_sink, wl.b_window, total))
+    res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=wl.pool_kernel, s=wl.b_sink, W=wl.b_window)
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "tiny")
+    _check_kept(res, orc, t["q_win"].shape, wl.seq_len, wl.obs_window, wl.b_sink, wl.b_window, budgets, "tiny")
+    _check_gather(res, t["k"], t["v"], budgets)
+    _decode_on_oracle_cache(orc, t["q"], 2, torch.float32, 1e-5, "tiny")
+    # end to end on the GPU's own cache
+    out, _ = sg.decode_attention(t["q"], res["k_c"], res["v_c"], res["offsets"], res["offsets_host"], 2)
+    ref, _ = oracle.decode(_f64(t["q"]), orc["k_c"], orc["v_c"], orc["offsets"], 2)
+    assert np.abs(out.cpu().numpy() - ref).max() <= 1e-5
+
+
+@pytest.mark.parametrize("B,C,budget_kind", [(2, 1000, "edges"), (3, 777, "random"), (1, 64 * 20 + 13, "random")])
+def test_tiny_ragged_batches(B, C, budget_kind):
+    """Ragged C (not a multiple of any tile), several sequences, empty and full middles."""
+    wl, t = _tiny_inputs(B=B, C=C, seed=B * 7 + C)
+    s, W, w = 4, 32, wl.obs_window
+    if budget_kind == "edges":
+        budgets = np.array([s + W, C])  # one head keeps no middle row, the other keeps everything
+    else:
+        rng = np.random.Generator(np.random.PCG64(C))
+        budgets = rng.integers(s + W, C + 1, size=2)
+    _announce(f"tiny ragged B={B} C={C} budgets={budgets.tolist()}")
+    res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=7, s=s, W=W)
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "ragged")
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "ragged")
+    _check_gather(res, t["k"], t["v"], budgets)
+    _decode_on_oracle_cache(orc, t["q"], 2, torch.float32, 1e-5, "ragged")
+
+
+def _qwen_small(B, C, seed_layer=0, Hq=28, Hkv=4, d=128, w=64):
+    wl = workloads.WORKLOADS["qwen25_32k"]
+    wl = workloads.Workload(wl.key, wl.name, 1, Hq, Hkv, d, C, w, 7, 64, 128, B, "bf16", 11, "beta")
+    return wl, workloads.torch_layer_tensors(wl, seed_layer, DEV)
+
+
+@pytest.mark.parametrize("B,C,Hq,Hkv,d", [(2, 3000, 28, 4, 128), (1, 2500, 8, 8, 64), (1, 1800, 16, 2, 128)])
+def test_bf16_qwen_shaped(B, C, Hq, Hkv, d):
+    """bf16, heavy-hitter and sink rows, GQA groups of 7, 1 and 8 (48 window rows..512)."""
+    w = 64 if Hq // Hkv <= 8 else 32
+    wl, t = _qwen_small(B, C, Hq=Hq, Hkv=Hkv, d=d, w=w)
+    s, W = wl.b_sink, wl.b_window
+    sc = workloads.head_scores(wl)
+    total = sg.total_from_ratio(0.25, 1, Hkv, C, s, W)
+    budgets = sg.allocate_budgets(sc, 1, Hkv, C, s, W, total)
+    _announce(f"bf16 B={B} C={C} Hq={Hq} Hkv={Hkv} d={d} budgets={budgets.tolist()}")
+    res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=7, s=s, W=W)
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "bf16")
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "bf16")
+    _check_gather(res, t["k"], t["v"], budgets)
+    _decode_on_oracle_cache(orc, t["q"], Hkv, torch.bfloat16, 2e-2, "bf16")
+
+
+def test_caller_supplied_lse_and_scores_only():
+    wl, t = _qwen_small(1, 2100)
+    s, W = wl.b_sink, wl.b_window
+    budgets = np.array([600, 300, 900, 2100])
+    lse = oracle.window_lse(_f64(t["q_win"]), _f64(t["k"]))
+    lse_t = torch.from_numpy(lse).float().to(DEV)
+    _announce("caller-supplied window LSE")
+    res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=7, s=s, W=W, window_lse=lse_t,
+                              orc_lse=lse_t.cpu().double().numpy())
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "lse-in")
+    _check_kept(res, orc, t["q_win"].shape, 2100, 64, s, W, budgets, "lse-in")
+    _check_gather(res, t["k"], t["v"], budgets)
+    _announce("scores-only mode")
+    only = sg.compress_layer(t["q_win"], t["k"], None, None, pool_kernel=7, b_sink=s, b_window=W,
+                             scores_only=True)
+    torch.cuda.synchronize()
+    full = sg.compress_layer(t["q_win"], t["k"], t["v"], budgets, pool_kernel=7, b_sink=s, b_window=W)
+    torch.cuda.synchronize()
+    assert torch.equal(only["scores"], full["scores"])
+    assert "k_c" not in only
+
+
+def test_identical_keys_exact_ties():
+    """Equal keys: every interior pooled score ties exactly; ties go to the lower positions."""
+    C, w, s, W = 2048, 32, 4, 32
+    wl, t = _tiny_inputs()
+    k = t["k"][:, :, :1, :].expand(-1, -1, C, -1).contiguous()
+    budgets = np.array([s + W + 700, s + W + 2009])
+    _announce("identical keys")
+    res = sg.compress_layer(t["q_win"], k, t["v"], budgets, pool_kernel=7, b_sink=s, b_window=W)
+    torch.cuda.synchronize()
+    kept = res["kept_pos"].cpu().numpy()
+    offs = res["offsets_host"]
+    for h, m in enumerate([700, 2009]):
+        seg = kept[offs[h]:offs[h + 1]]
+        assert seg.tolist() == list(range(s + m)) + list(range(C - W, C))
+
+
+def test_full_budget_is_full_attention():
+    """100 % budget: the cache is the whole prompt and decode equals full attention (torch, fp64)."""
+    wl, t = _tiny_inputs(B=2, C=700, seed=3)
+    C = 700
+    _announce("full budget")
+    res = sg.compress_layer(t["q_win"], t["k"], t["v"], [C, C], pool_kernel=7, b_sink=4, b_window=32)
+    torch.cuda.synchronize()
+    assert res["kept_pos"].cpu().numpy().tolist() == list(range(C)) * 4
+    assert torch.equal(res["k_c"], t["k"].reshape(-1, 64)) and torch.equal(res["v_c"], t["v"].reshape(-1, 64))
+    out, lse = sg.decode_attention(t["q"], res["k_c"], res["v_c"], res["offsets"], res["offsets_host"], 2)
+    torch.cuda.synchronize()
+    q = t["q"].double().cpu()[:, :, None, :]
+    kk = t["k"].double().cpu().repeat_interleave(2, dim=1)
+    vv = t["v"].double().cpu().repeat_interleave(2, dim=1)
+    ref = torch.nn.functional.scaled_dot_product_attention(q, kk, vv)[:, :, 0, :]
+    assert (out.cpu().double() - ref).abs().max().item() <= 1e-5
+
+
+def test_decode_edge_segments_and_bf16_output():
+    rng = np.random.Generator(np.random.PCG64(9))
+    d, Hq, Hkv = 128, 8, 4
+    lens = [0, 1, 17, 300, 5, 0, 1000, 129]  # B=2 x 4 heads
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    kc = torch.from_numpy(rng.standard_normal((offs[-1], d)) * 3).to(torch.bfloat16).to(DEV)
+    vc = torch.from_numpy(rng.standard_normal((offs[-1], d))).to(torch.bfloat16).to(DEV)
+    q = torch.from_numpy(rng.standard_normal((2, Hq, d))).to(torch.bfloat16).to(DEV)
+    _announce("decode edge segments")
+    out, lse = sg.decode_attention(q, kc, vc, torch.from_numpy(offs).to(DEV), offs, Hkv, out_dtype=torch.float32)
+    outb, _ = sg.decode_attention(q, kc, vc, torch.from_numpy(offs).to(DEV), offs, Hkv, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    ref, ref_lse = oracle.decode(_f64(q), _f64(kc), _f64(vc), offs, Hkv)
+    assert np.abs(out.cpu().numpy() - ref).max() <= 2e-2
+    o = out.cpu().numpy()
+    assert np.all(o[0, 0:2] == 0) and np.all(np.isneginf(lse.cpu().numpy()[0, 0:2]))  # empty segment
+    # one row: exactly that V row
+    assert torch.equal(out[0, 2:4].cpu(), vc[0].float().cpu().expand(2, -1))
+    ob = outb.float().cpu().numpy()
+    ulp = np.abs(ref) * 2.0 ** -8
+    assert np.all(np.abs(ob - ref) <= 2e-2 + ulp)
+
+
+def test_run_twice_bitwise():
+    wl, t = _qwen_small(2, 2222)
+    budgets = np.array([700, 500, 1500, 400])
+    _announce("determinism")
+    a = sg.compress_layer(t["q_win"], t["k"], t["v"], budgets, pool_kernel=7, b_sink=64, b_window=128)
+    b = sg.compress_layer(t["q_win"], t["k"], t["v"], budgets, pool_kernel=7, b_sink=64, b_window=128)
+    oa, la = sg.decode_attention(t["q"], a["k_c"], a["v_c"], a["offsets"], a["offsets_host"], 4)
+    ob, lb = sg.decode_attention(t["q"], b["k_c"], b["v_c"], b["offsets"], b["offsets_host"], 4)
+    torch.cuda.synchronize()
+    for key in ("scores", "kept_pos", "offsets", "k_c", "v_c"):
+        assert torch.equal(a[key], b[key]), key
+    assert torch.equal(oa, ob) and torch.equal(la, lb)
