@@ -1,0 +1,245 @@
+#!/usr/bin/env python3
+"""Benchmark of the SGD-KV hot path on one MI355X.
+
+One step is the whole path over one batch of synthetic, HBM-resident input:
+  S0  per-KV-head budgets for every head of the stack (host, Eq. 2 + Algorithm 1)
+  S1-S6  sgdkv_compress_layer for every layer (window scores, pooling, top-k,
+         gather into the ragged per-head cache)
+  S7-S8  sgdkv_decode_attention for every layer (one decode query per
+         sequence and query head over that layer's compressed cache)
+Layers are compressed first and decoded afterwards, so no decode reads a
+cache still warm in the 256 MB last-level cache from its own compression.
+
+Default workload: the 28-layer Qwen2.5-7B-shaped stack (28 query / 4 KV
+heads, head dim 128) at a 131072-token prompt, batch 8, bf16, 25 % budget,
+observation window 64, pool kernel 7, sink/window 1024/1024.
+
+Prints one JSON line: throughput in prompt tokens per second per layer for
+the whole step, the decode HBM bandwidth, the roofline of the kernel that
+takes the most time (per-kernel durations from HIP events recorded on the
+launch stream during a timed run), and the CPU oracle timed on a bounded
+sample of the same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen25_128k",
+                    help="qwen25_128k (default), qwen25_32k, qwen3_256k, qwen25_1m, tiny")
+    ap.add_argument("--ratio", type=float, default=0.25, help="budget as a fraction of all rows")
+    ap.add_argument("--caller-lse", action="store_true",
+                    help="hand each layer its window-row LSE (as prefill attention would), skipping pass 1")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        log(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
+            "this build has no multi-GPU path.")
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2609_03235_amd as sg
+    import workloads
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(int(os.environ.get("LOCAL_RANK", "0")))
+    dev = torch.device("cuda")
+    wl = workloads.WORKLOADS[args.workload]
+    L, B, Hq, Hkv, d = wl.layers, wl.batch, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+    C, w, s, W, kp = wl.seq_len, wl.obs_window, wl.b_sink, wl.b_window, wl.pool_kernel
+    eb = 2 if wl.dtype == "bf16" else 4
+    stream = torch.cuda.current_stream()
+
+    # ------------------------------------------------------------ inputs (HBM-resident)
+    t0 = time.perf_counter()
+    scores = workloads.head_scores(wl)
+    total = sg.total_from_ratio(args.ratio, L, Hkv, C, s, W)
+    budgets = sg.allocate_budgets(scores, L, Hkv, C, s, W, total).reshape(L, Hkv)
+    layers = [workloads.torch_layer_tensors(wl, l, dev) for l in range(L)]
+    lse_in = [None] * L
+    if args.caller_lse:
+        # Stand-in for the LSE prefill attention already produced: fp32 logits of each window
+        # row over its causal keys, one (sequence, KV head) block at a time, outside the timed region.
+        G = Hq // Hkv
+        scale = 1.0 / math.sqrt(d)
+        pos = torch.arange(C - w, C, device=dev)[:, None]
+        for l in range(L):
+            out = torch.empty((B, Hq, w), dtype=torch.float32, device=dev)
+            for b in range(B):
+                for h in range(Hkv):
+                    qg = layers[l]["q_win"][b, h * G:(h + 1) * G].float().reshape(G * w, d)
+                    kt = layers[l]["k"][b, h].float().t().contiguous()
+                    lg = (qg @ kt) * scale
+                    lg = lg.reshape(G, w, C).masked_fill(torch.arange(C, device=dev)[None, :] > pos, float("-inf"))
+                    out[b, h * G:(h + 1) * G] = torch.logsumexp(lg, dim=-1)
+                    del lg, kt
+            lse_in[l] = out
+    outs = []
+    for l in range(L):
+        T = int(budgets[l].sum())
+        outs.append(dict(k_c=torch.empty((B * T, d), dtype=layers[l]["k"].dtype, device=dev),
+                         v_c=torch.empty((B * T, d), dtype=layers[l]["k"].dtype, device=dev),
+                         kept_pos=torch.empty(B * T, dtype=torch.int32, device=dev),
+                         offsets=torch.empty(B * Hkv + 1, dtype=torch.int64, device=dev),
+                         scores=torch.empty((B, Hkv, C - w), dtype=torch.float32, device=dev)))
+    dec_out = [torch.empty((B, Hq, d), dtype=torch.float32, device=dev) for _ in range(L)]
+    dec_lse = [torch.empty((B, Hq), dtype=torch.float32, device=dev) for _ in range(L)]
+    cdesc = sg.compress_desc(layers[0]["q_win"], layers[0]["k"], pool_kernel=kp, b_sink=s, b_window=W)
+    ws_c = sg.alloc_workspace(sg.compress_workspace_size(cdesc), dev)
+    offsets_host = []
+    for l in range(L):
+        pre = np.concatenate([[0], np.cumsum(budgets[l])])
+        T = int(budgets[l].sum())
+        offsets_host.append(np.array([b * T + pre[h] for b in range(B) for h in range(Hkv)] + [B * T],
+                                     dtype=np.int64))
+    ddesc = sg.decode_desc(layers[0]["q"], Hkv, torch.float32)
+    ws_d = sg.alloc_workspace(max(sg.decode_workspace_size(ddesc, oh) for oh in offsets_host), dev)
+    torch.cuda.synchronize()
+    log(f"[bench] inputs ready in {time.perf_counter() - t0:.1f}s: {wl.name}, total budget {total} rows "
+        f"({args.ratio:.0%}), {L} layers x {B} sequences")
+
+    def step():
+        # S0 on the host, then every layer's compression, then every layer's decode
+        sg.allocate_budgets(scores, L, Hkv, C, s, W, total)
+        for l in range(L):
+            t = layers[l]
+            sg.compress_layer(t["q_win"], t["k"], t["v"], budgets[l], pool_kernel=kp, b_sink=s, b_window=W,
+                              window_lse=lse_in[l], out=outs[l], workspace=ws_c, stream=stream)
+        for l in range(L):
+            o = outs[l]
+            sg.decode_attention(layers[l]["q"], o["k_c"], o["v_c"], o["offsets"], offsets_host[l], Hkv,
+                                out_dtype=torch.float32, workspace=ws_d, out=dec_out[l], lse=dec_lse[l],
+                                stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # ------------------------------------------------------------ timed region (headline)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    t_wall0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_wall0) * 1e3 / args.steps
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+
+    # ------------------------------------------------------------ timed region with kernel events
+    sg.profile_reset()
+    sg.profile_enable(True)
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    sg.profile_enable(False)
+    prof_ms_per_step = ev0.elapsed_time(ev1) / args.steps
+    kern = sg.profile_read()
+
+    # ------------------------------------------------------------ algorithmic work per launch
+    T_layers = budgets.sum(axis=1)
+    T_mean = float(T_layers.mean())
+    flops_tok = 2.0 * Hq * w * d                      # window x key GEMM, counted once
+    work = {
+        "score_lse": ("mfma", flops_tok * B * C, "TFLOP/s"),
+        "score_colsum": ("mfma", flops_tok * B * (C - w), "TFLOP/s"),
+        # read kept K and V rows, write them, write positions, read pooled scores of the candidates
+        "gather": ("hbm", B * T_mean * (4 * d * eb + 4) + B * Hkv * C * 4.0, "GB/s"),
+        # read every kept K and V row once, plus the queries and outputs
+        "decode_split": ("hbm", B * T_mean * 2 * d * eb + B * Hq * d * (eb + 4.0), "GB/s"),
+    }
+    kernels = {}
+    for name, (count, ms) in sorted(kern.items(), key=lambda kv: -kv[1][1]):
+        kernels[name] = dict(launches_per_step=count / args.steps, ms_per_step=ms / args.steps,
+                             avg_us=1e3 * ms / count, share=ms / max(1e-9, sum(v[1] for v in kern.values())))
+    dominant = max(kern.items(), key=lambda kv: kv[1][1])[0]
+
+    def roof(name):
+        count, ms = kern[name]
+        bound, amount, unit = work[name]
+        avg_s = ms / count / 1e3
+        if bound == "mfma":
+            achieved, peak = amount / avg_s / 1e12, PEAK_TFLOPS[wl.dtype]
+        else:
+            achieved, peak = amount / avg_s / 1e9, PEAK_HBM_GBS
+        return dict(kernel=name, bound=bound, achieved=round(achieved, 2), peak=peak, unit=unit,
+                    frac=round(achieved / peak, 4), traffic=None, avg_us=round(avg_s * 1e6, 2),
+                    work_per_launch=amount)
+
+    roofline = roof(dominant) if dominant in work else None
+    decode = roof("decode_split") if "decode_split" in kern else None
+    dec_ms = (kern.get("decode_split", (0, 0))[1] + kern.get("decode_combine", (0, 0))[1]) / args.steps
+    dec_bytes = work["decode_split"][1] * L
+    comp_ms = sum(ms for n, (c, ms) in kern.items() if not n.startswith("decode")) / args.steps
+
+    tokens = float(B) * C * L  # prompt tokens per step, over all layers
+    value = tokens / (ms_per_step / 1e3)
+
+    # ------------------------------------------------------------ CPU oracle on a bounded sample
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        t = layers[0]
+        q_win = t["q_win"][:1].cpu().double().numpy()
+        kk = t["k"][:1].cpu().double().numpy()
+        vv = t["v"][:1].cpu().double().numpy()
+        qq = t["q"][:1].cpu().double().numpy()
+        tc0 = time.perf_counter()
+        res = oracle.compress(q_win, kk, vv, budgets[0], w=w, kp=kp, s=s, W=W)
+        oracle.decode(qq, res["k_c"], res["v_c"], res["offsets"], Hkv)
+        cpu_s = time.perf_counter() - tc0
+        cpu = dict(value=round(C / cpu_s, 1), unit="tokens/s per layer", cores=oracle.num_threads(), kind="oracle",
+                   sample=f"sequence 0 of layer 0 ({Hkv} KV heads, C={C}): compress + decode, {cpu_s:.1f} s")
+        del res
+
+    line = dict(
+        metric="compressed K/V tokens/s per layer + ragged decode-attn HBM GB/s (% of peak), 1 GPU",
+        value=round(value, 1), unit="tokens/s per layer", n_gpus=1, steps=args.steps, warmup=args.warmup,
+        ms_per_step=round(ms_per_step, 4), higher_is_better=True, scaling="weak", vs_baseline=None,
+        dtype=wl.dtype, data="synthetic",
+        config=dict(workload=wl.name, layers=L, batch=B, prompt=C, q_heads=Hq, kv_heads=Hkv, head_dim=d,
+                    obs_window=w, pool_kernel=kp, b_sink=s, b_window=W, budget_ratio=args.ratio,
+                    total_budget_rows=int(total), window_lse="caller" if args.caller_lse else "computed"),
+        compress_tokens_per_s=round(tokens / (comp_ms / 1e3), 1) if comp_ms > 0 else None,
+        decode=dict(gbps=round(dec_bytes / (dec_ms / 1e3) / 1e9, 1) if dec_ms > 0 else None,
+                    frac_of_peak=round(dec_bytes / (dec_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4) if dec_ms > 0 else None,
+                    ms_per_step=round(dec_ms, 4), split_kernel=decode),
+        roofline=roofline, kernels=kernels, profiled_ms_per_step=round(prof_ms_per_step, 4),
+        wall_ms_per_step=round(wall_ms, 4), cpu_baseline=cpu,
+    )
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

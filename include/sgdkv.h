@@ -189,6 +189,26 @@ sgdkv_status sgdkv_decode_attention(const sgdkv_decode_desc* desc, const void* q
                                     const int64_t* offsets_host, void* out, float* lse_out,
                                     void* workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------ */
+/* Kernel timing for benchmarks (not part of the method).             */
+
+/* While enabled (on != 0), every kernel the library launches is bracketed by
+ * a pair of HIP events recorded on the launch stream. Costs two event
+ * records per kernel; off by default. Thread-safe. */
+sgdkv_status sgdkv_profile_enable(int32_t on);
+
+/* Drops every recorded duration (waiting for pending events first). */
+sgdkv_status sgdkv_profile_reset(void);
+
+/* Waits for the recorded events and reports, per kernel name, the number of
+ * launches and their total duration in milliseconds since the last reset.
+ * names: host buffer of max_entries * 64 chars (NUL-terminated names);
+ * counts, total_ms: host [max_entries]. *n_out receives the number of
+ * kernels seen (entries beyond max_entries are not written).
+ * Errors: negative max_entries; NULL buffers with max_entries > 0. */
+sgdkv_status sgdkv_profile_read(int32_t max_entries, char* names, int64_t* counts, double* total_ms,
+                                int32_t* n_out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -26,7 +26,8 @@ OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, 1, 2, 3, 4
 DTYPE_F32, DTYPE_BF16 = 0, 1
 SYMBOLS = ("sgdkv_last_error", "sgdkv_version", "sgdkv_reduce_query_head_scores", "sgdkv_total_from_ratio",
            "sgdkv_allocate_budgets", "sgdkv_compress_workspace_size", "sgdkv_compress_layer",
-           "sgdkv_decode_workspace_size", "sgdkv_decode_attention")
+           "sgdkv_decode_workspace_size", "sgdkv_decode_attention", "sgdkv_profile_enable",
+           "sgdkv_profile_reset", "sgdkv_profile_read")
 
 
 class SgdkvError(RuntimeError):
@@ -78,6 +79,9 @@ def load_library():
         "sgdkv_compress_layer": [P, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
         "sgdkv_decode_workspace_size": [P, P, P],
         "sgdkv_decode_attention": [P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
+        "sgdkv_profile_enable": [i32],
+        "sgdkv_profile_reset": [],
+        "sgdkv_profile_read": [i32, P, P, P, P],
     }
     for name, args in sigs.items():
         fn = getattr(lib, name)
@@ -243,3 +247,26 @@ def decode_attention(q, k_c, v_c, offsets, offsets_host, num_kv_heads: int, *, o
         _ptr(lse) if with_lse else None, _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st)
     return out, (lse if with_lse else None)
+
+
+# ------------------------------------------------------- kernel timing
+def profile_enable(on: bool = True):
+    _check(load_library().sgdkv_profile_enable(1 if on else 0))
+
+
+def profile_reset():
+    _check(load_library().sgdkv_profile_reset())
+
+
+def profile_read(max_entries: int = 64) -> dict:
+    """{kernel name: (launches, total ms)} since the last reset (waits for pending events)."""
+    names = ctypes.create_string_buffer(max_entries * 64)
+    counts = np.zeros(max_entries, dtype=np.int64)
+    ms = np.zeros(max_entries, dtype=np.float64)
+    n = ctypes.c_int32(0)
+    _check(load_library().sgdkv_profile_read(max_entries, names, _np_ptr(counts), _np_ptr(ms), ctypes.byref(n)))
+    out = {}
+    for i in range(min(n.value, max_entries)):
+        name = names.raw[i * 64:(i + 1) * 64].split(b"\0", 1)[0].decode()
+        out[name] = (int(counts[i]), float(ms[i]))
+    return out

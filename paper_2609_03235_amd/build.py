@@ -23,7 +23,7 @@ ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-command-line-argument"]
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 KERNEL_SOURCES = ["score_kernels.hip", "select_kernels.hip", "decode_kernels.hip"]
-HOST_SOURCES = ["sgdkv_host.cpp"]
+HOST_SOURCES = ["sgdkv_host.cpp", "profile.cpp"]
 
 
 def _run(cmd):

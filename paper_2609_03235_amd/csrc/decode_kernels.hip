@@ -266,9 +266,9 @@ template <typename T, int D>
 static void launch_decode_t(const DecodeArgs& a, hipStream_t st) {
   const dim3 grid(a.n_chunk_max, a.B * a.Hkv);
   if (a.G <= 8)
-    hipLaunchKernelGGL((decode_split_kernel<T, D, 8>), grid, dim3(kBlock), 0, st, a);
+    SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, 8>), grid, dim3(kBlock), st, a);
   else
-    hipLaunchKernelGGL((decode_split_kernel<T, D, 16>), grid, dim3(kBlock), 0, st, a);
+    SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, 16>), grid, dim3(kBlock), st, a);
 }
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {
@@ -282,9 +282,9 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {
     }
   }
   if (a.D == 128)
-    hipLaunchKernelGGL(decode_combine_kernel<128>, dim3(a.B * a.Hq), dim3(128), 0, st, a);
+    SGDKV_LAUNCH("decode_combine", decode_combine_kernel<128>, dim3(a.B * a.Hq), dim3(128), st, a);
   else
-    hipLaunchKernelGGL(decode_combine_kernel<64>, dim3(a.B * a.Hq), dim3(128), 0, st, a);
+    SGDKV_LAUNCH("decode_combine", decode_combine_kernel<64>, dim3(a.B * a.Hq), dim3(128), st, a);
   return hipGetLastError();
 }
 

@@ -323,13 +323,12 @@ template <typename T, int D, int RBW>
 static hipError_t launch_scores_t(const CompressArgs& a, hipStream_t st) {
   const dim3 sblk(kScoreBlock);
   if (a.window_lse == nullptr) {
-    hipLaunchKernelGGL((lse_kernel<T, D, RBW>), dim3(a.n_lse_chunks, a.B * a.Hkv), sblk, 0, st, a);
+    SGDKV_LAUNCH("score_lse", (lse_kernel<T, D, RBW>), dim3(a.n_lse_chunks, a.B * a.Hkv), sblk, st, a);
     const int64_t nrows = (int64_t)a.B * a.Hkv * a.R;
-    hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)((nrows + kBlock - 1) / kBlock)), dim3(kBlock),
-                       0, st, a);
+    SGDKV_LAUNCH("lse_merge", lse_merge_kernel, dim3((unsigned)((nrows + kBlock - 1) / kBlock)), dim3(kBlock), st, a);
   }
   if (a.n_col_chunks > 0)
-    hipLaunchKernelGGL((colsum_kernel<T, D, RBW>), dim3(a.n_col_chunks, a.B * a.Hkv), sblk, 0, st, a);
+    SGDKV_LAUNCH("score_colsum", (colsum_kernel<T, D, RBW>), dim3(a.n_col_chunks, a.B * a.Hkv), sblk, st, a);
   return hipGetLastError();
 }
 

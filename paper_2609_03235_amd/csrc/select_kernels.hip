@@ -293,26 +293,26 @@ __global__ __launch_bounds__(kBlock) void gather_kernel(CompressArgs a) {
 
 template <int RB>
 static void launch_gather(const CompressArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((gather_kernel<RB>), dim3(a.n_sel_chunks, a.B * a.Hkv), dim3(kBlock), 0, st, a);
+  SGDKV_LAUNCH("gather", (gather_kernel<RB>), dim3(a.n_sel_chunks, a.B * a.Hkv), dim3(kBlock), st, a);
 }
 
 hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t st) {
   const int nseg = a.B * a.Hkv;
   const dim3 blk(kBlock);
-  hipLaunchKernelGGL(select_init_kernel, dim3(nseg), blk, 0, st, a, scores_only ? 0 : 1);
-  if (a.n_pool_chunks > 0) hipLaunchKernelGGL(pool_kernel, dim3(a.n_pool_chunks, nseg), blk, 0, st, a);
+  SGDKV_LAUNCH("select_init", select_init_kernel, dim3(nseg), blk, st, a, scores_only ? 0 : 1);
+  if (a.n_pool_chunks > 0) SGDKV_LAUNCH("pool", pool_kernel, dim3(a.n_pool_chunks, nseg), blk, st, a);
   if (scores_only) return hipGetLastError();
   if (a.n_cand_chunks > 0) {
-    hipLaunchKernelGGL(radix_hist_kernel<0>, dim3(a.n_cand_chunks, nseg), blk, 0, st, a);
-    hipLaunchKernelGGL(radix_digit_kernel<0>, dim3(nseg), blk, 0, st, a);
-    hipLaunchKernelGGL(radix_hist_kernel<1>, dim3(a.n_cand_chunks, nseg), blk, 0, st, a);
-    hipLaunchKernelGGL(radix_digit_kernel<1>, dim3(nseg), blk, 0, st, a);
-    hipLaunchKernelGGL(radix_hist_kernel<2>, dim3(a.n_cand_chunks, nseg), blk, 0, st, a);
-    hipLaunchKernelGGL(radix_digit_kernel<2>, dim3(nseg), blk, 0, st, a);
-    hipLaunchKernelGGL(radix_hist_kernel<3>, dim3(a.n_cand_chunks, nseg), blk, 0, st, a);
-    hipLaunchKernelGGL(radix_digit_kernel<3>, dim3(nseg), blk, 0, st, a);
+    SGDKV_LAUNCH("radix_hist", radix_hist_kernel<0>, dim3(a.n_cand_chunks, nseg), blk, st, a);
+    SGDKV_LAUNCH("radix_digit", radix_digit_kernel<0>, dim3(nseg), blk, st, a);
+    SGDKV_LAUNCH("radix_hist", radix_hist_kernel<1>, dim3(a.n_cand_chunks, nseg), blk, st, a);
+    SGDKV_LAUNCH("radix_digit", radix_digit_kernel<1>, dim3(nseg), blk, st, a);
+    SGDKV_LAUNCH("radix_hist", radix_hist_kernel<2>, dim3(a.n_cand_chunks, nseg), blk, st, a);
+    SGDKV_LAUNCH("radix_digit", radix_digit_kernel<2>, dim3(nseg), blk, st, a);
+    SGDKV_LAUNCH("radix_hist", radix_hist_kernel<3>, dim3(a.n_cand_chunks, nseg), blk, st, a);
+    SGDKV_LAUNCH("radix_digit", radix_digit_kernel<3>, dim3(nseg), blk, st, a);
   }
-  hipLaunchKernelGGL(sel_count_kernel, dim3(a.n_sel_chunks, nseg), blk, 0, st, a);
+  SGDKV_LAUNCH("sel_count", sel_count_kernel, dim3(a.n_sel_chunks, nseg), blk, st, a);
   const int rb = a.D * (a.dtype == 1 ? 2 : 4);
   switch (rb) {
     case 128: launch_gather<128>(a, st); break;

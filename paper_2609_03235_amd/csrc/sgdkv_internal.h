@@ -16,6 +16,16 @@ constexpr int kScoreTile = 64;     // keys staged in LDS per step of the score k
 constexpr int kScoreWaves = 8;     // waves per score workgroup
 constexpr int kScoreBlock = 64 * kScoreWaves;
 
+// Opt-in per-kernel timing (see sgdkv_profile_*): brackets a launch with events.
+void prof_begin(const char* name, hipStream_t stream);
+void prof_end(hipStream_t stream);
+#define SGDKV_LAUNCH(name, kernel, grid, block, stream, ...)                  \
+  do {                                                                        \
+    ::sgdkv::prof_begin(name, stream);                                        \
+    hipLaunchKernelGGL(kernel, grid, block, 0, stream, __VA_ARGS__);          \
+    ::sgdkv::prof_end(stream);                                                \
+  } while (0)
+
 // ---------------------------------------------------------------- compress
 struct CompressArgs {
   // shapes
