@@ -92,8 +92,9 @@ int orc_total_from_ratio(double R, int L, int H, int64_t C, int64_t s, int64_t W
  * sigma[L*H]  raw per-KV-head summarization scores, layer-major, >= 0.
  * Normalisation S_h = sigma_h / sum(sigma) over all L*H heads (Sec. 3.3).
  * Eq. 2 without the reserved rows gives the middle share
- *   x_h = S_h * L*H*R*M = sigma_h * T / sum(sigma),  T = total - L*H*(s+W),
- * computed here as (sigma_h * T) / sum(sigma).
+ *   x_h = S_h * L*H*R*M = S_h * T,  T = total - L*H*(s+W),
+ * computed as (sigma_h / sum(sigma)) * T: the normalised score first, so no
+ * intermediate exceeds T whatever the scale of the raw scores.
  * mode 0: integerise, cap every m_h at M, give the excess to the remaining
  *         heads in descending score order, each up to M (Algorithm 1).
  * mode 1: x_h = min(lambda*sigma_h, M) with the exact water level lambda,
@@ -182,7 +183,7 @@ int orc_allocate_budgets(const double* sigma, int L, int H, int64_t C, int64_t s
 
   if (mode == 0) {
     /* Eq. 2 shares, integerised */
-    for (int64_t h = 0; h < n; ++h) x[h] = (sg[h] * (double)T) / sgsum;
+    for (int64_t h = 0; h < n; ++h) x[h] = (sg[h] / sgsum) * (double)T;
     orc_integerise(x, sg, n, T, m);
     /* Algorithm 1: excess over the cap, cap, greedy redistribution */
     int64_t E = 0;
@@ -205,6 +206,8 @@ int orc_allocate_budgets(const double* sigma, int L, int H, int64_t C, int64_t s
      * Heads sorted by sigma descending; the first c are capped at M. Take
      * the smallest c with lambda_c*sigma_(c) <= M, where
      * lambda_c = (T - c*M) / (sum of the sigmas not capped).
+     * lambda*sigma_h is evaluated as (sigma_h / rest) * left, a fraction of
+     * at most 1 times the rows left, so tiny scores cannot overflow it.
      * If every uncapped head has sigma 0, the rows left after the capped
      * heads are split evenly over those heads (a flat water level).       */
     orc_head_t* order = (orc_head_t*)malloc(sizeof(orc_head_t) * (size_t)n);
@@ -217,15 +220,15 @@ int orc_allocate_budgets(const double* sigma, int L, int H, int64_t C, int64_t s
     int64_t c = 0;
     double lambda = 0.0;
     int flat = 0;
+    double left = (double)T;
     for (c = 0; c < n; ++c) {
-      double left = (double)T - (double)c * (double)M;
+      left = (double)T - (double)c * (double)M;
       if (rest[c] <= 0.0) { flat = 1; lambda = left / (double)(n - c); break; }
-      lambda = left / rest[c];
-      if (lambda * order[c].sigma <= (double)M) break;
+      if ((order[c].sigma / rest[c]) * left <= (double)M) break;
     }
     for (int64_t k = 0; k < n; ++k) {
       int64_t h = order[k].idx;
-      double v = (k < c) ? (double)M : (flat ? lambda : lambda * order[k].sigma);
+      double v = (k < c) ? (double)M : (flat ? lambda : (order[k].sigma / rest[c]) * left);
       x[h] = v > (double)M ? (double)M : v;
     }
     orc_integerise(x, sg, n, T, m);

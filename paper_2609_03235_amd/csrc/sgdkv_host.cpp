@@ -198,8 +198,8 @@ sgdkv_status sgdkv_allocate_budgets(const double* head_scores, int32_t L, int32_
   std::vector<int64_t> mid(n);
   const std::vector<int64_t> order = score_order(score);
   if (mode == 0) {
-    // Eq. 2 without the reserved rows, rounded; then Algorithm 1.
-    for (int64_t h = 0; h < n; ++h) share[h] = (score[h] * (double)T) / denom;
+    // Eq. 2 without the reserved rows (normalised score times T), rounded; then Algorithm 1.
+    for (int64_t h = 0; h < n; ++h) share[h] = (score[h] / denom) * (double)T;
     round_shares(share, score, T, mid);
     int64_t excess = 0;
     for (int64_t h = 0; h < n; ++h)
@@ -216,25 +216,26 @@ sgdkv_status sgdkv_allocate_budgets(const double* head_scores, int32_t L, int32_
       }
     }
   } else {
-    // Water level: share = min(lambda*score, M), summing to T.
+    // Water level: share = min(lambda*score, M), summing to T. lambda*score is
+    // evaluated as (score / uncapped score sum) * rows left, a fraction <= 1 of
+    // the rows left, so tiny scores cannot overflow it.
     std::vector<double> tail(n + 1, 0.0);  // score sums over order[k..n-1], smallest first
     for (int64_t k = n - 1; k >= 0; --k) tail[k] = tail[k + 1] + score[order[k]];
     int64_t capped = 0;
-    double lambda = 0.0;
+    double left = (double)T, level = 0.0;
     bool flat = false;
     for (capped = 0; capped < n; ++capped) {
-      const double left = (double)T - (double)capped * (double)M;
+      left = (double)T - (double)capped * (double)M;
       if (tail[capped] <= 0.0) {
         flat = true;  // only zero-score heads remain: they share the rest evenly
-        lambda = left / (double)(n - capped);
+        level = left / (double)(n - capped);
         break;
       }
-      lambda = left / tail[capped];
-      if (lambda * score[order[capped]] <= (double)M) break;
+      if ((score[order[capped]] / tail[capped]) * left <= (double)M) break;
     }
     for (int64_t k = 0; k < n; ++k) {
       const int64_t h = order[k];
-      double v = k < capped ? (double)M : (flat ? lambda : lambda * score[h]);
+      double v = k < capped ? (double)M : (flat ? level : (score[h] / tail[capped]) * left);
       share[h] = v > (double)M ? (double)M : v;
     }
     round_shares(share, score, T, mid);
@@ -485,8 +486,8 @@ sgdkv_status plan_decode(const sgdkv_decode_desc* d, const int64_t* offsets_host
   const double scale = d->scale > 0.f ? (double)d->scale : 1.0 / std::sqrt((double)d->head_dim);
   a.c2 = (float)(scale * 1.4426950408889634074);
   a.total_rows = total;
-  // rows per split: about 4096 splits over the whole batch, at least 256
-  a.chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(total - offsets_host[0], 4096), 128), 256), 1 << 24);
+  // rows per split: about 2048 splits over the whole batch, at least 512 rows
+  a.chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(total - offsets_host[0], 2048), 128), 512), 1 << 24);
   a.n_chunk_max = (int)ceil_div(longest, a.chunk);
   p.bytes = align256((size_t)a.B * a.Hq * a.n_chunk_max * (a.D + 2) * sizeof(float));
   return SGDKV_OK;

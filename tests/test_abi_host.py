@@ -198,3 +198,14 @@ def test_decode_validation():
 def test_no_device_fails_after_validation():
     assert _compress(_desc(), [512, 512]) == sg.ERR_HIP
     assert _decode(sg.DecodeDesc(2, 4, 2, 64, 1, 0, 0.0), [0, 10, 10, 30, 31]) == sg.ERR_HIP
+
+
+def test_allocation_extreme_scales_bit_exact():
+    for sc, L, H, C, total in [([0.0, 0.0, 0.0, 1.0, 1.0, 2.225073858507203e-309], 2, 3, 8, 18),
+                               ([1e300, 1e299, 3e298, 0.0], 1, 4, 1000, 1500),
+                               ([5e-324, 5e-324, 0.0], 1, 3, 10, 17)]:
+        for mode in (0, 1):
+            got = sg.allocate_budgets(sc, L, H, C, 0, 0, total, mode)
+            ref = oracle.allocate_budgets(np.array(sc), L, H, C, 0, 0, total, mode)
+            assert np.array_equal(got, ref), (sc, mode, got, ref)
+            assert np.all(got >= 0) and int(got.sum()) == total

@@ -224,3 +224,17 @@ def test_invalid_inputs():
         oracle.allocate_budgets(sc, 1, 2, 100, 1, 1, 201)  # above 2*100
     with pytest.raises(oracle.OracleError):
         oracle.allocate_budgets(sc, 1, 2, 100, 60, 60, 150)  # s + W > C
+
+
+def test_extreme_score_scales():
+    """Denormal and huge scores: shares are formed from normalised scores, so nothing overflows.
+    Heads 3 and 4 exceed M = 8 and are capped; the 2 rows left go to the denormal head."""
+    sc = np.array([0.0, 0.0, 0.0, 1.0, 1.0, 2.225073858507203e-309])
+    for mode in (0, 1):
+        b = oracle.allocate_budgets(sc, 2, 3, 8, 0, 0, 18, mode)
+        assert b.tolist() == [0, 0, 0, 8, 8, 2], (mode, b)
+    big = np.array([1e300, 1e299, 3e298, 0.0])
+    for mode in (0, 1):
+        b = oracle.allocate_budgets(big, 1, 4, 1000, 0, 0, 1500, mode)
+        assert int(b.sum()) == 1500 and np.all(b >= 0) and np.all(b <= 1000)
+        assert b[0] == 1000 and b[1] >= b[2] >= b[3]

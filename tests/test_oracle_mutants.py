@@ -30,8 +30,8 @@ MUTANTS = {
     "pool_window": ("for (int64_t t = j - r; t <= j + r; ++t)", "for (int64_t t = j - r; t < j + r; ++t)", SCORES),
     "select_tie_high": ("return (a->j < b->j) ? -1 : (a->j > b->j);\n}\n\nstatic int orc_cmp_i32",
                         "return (a->j > b->j) ? -1 : (a->j < b->j);\n}\n\nstatic int orc_cmp_i32", SELDEC),
-    "alloc_no_reserve": ("for (int64_t h = 0; h < n; ++h) x[h] = (sg[h] * (double)T) / sgsum;",
-                         "for (int64_t h = 0; h < n; ++h) x[h] = (sg[h] * (double)(T + n)) / sgsum;", ALLOC),
+    "alloc_no_reserve": ("for (int64_t h = 0; h < n; ++h) x[h] = (sg[h] / sgsum) * (double)T;",
+                         "for (int64_t h = 0; h < n; ++h) x[h] = (sg[h] / sgsum) * (double)(T + n);", ALLOC),
     "alloc_greedy_ascending": ("if (a->sigma > b->sigma) return -1;\n  if (a->sigma < b->sigma) return 1;\n  return (a->idx < b->idx) ? -1 : (a->idx > b->idx);\n}\n\nint orc_allocate",
                                "if (a->sigma < b->sigma) return -1;\n  if (a->sigma > b->sigma) return 1;\n  return (a->idx < b->idx) ? -1 : (a->idx > b->idx);\n}\n\nint orc_allocate", ALLOC),
     "alloc_round_smallest": ("if (a->frac > b->frac) return -1;\n  if (a->frac < b->frac) return 1;",
