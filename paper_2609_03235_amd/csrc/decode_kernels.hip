@@ -217,8 +217,15 @@ __global__ __launch_bounds__(kBlock, 2) void decode_split_kernel(DecodeArgs a) {
   }
 }
 
+// One workgroup per (sequence, query head). Thread = (chunk group, column):
+// groups stride over the chunk partials with independent loads, then merge
+// in group order through LDS.
 template <int D>
-__global__ __launch_bounds__(128) void decode_combine_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kBlock) void decode_combine_kernel(DecodeArgs a) {
+  constexpr int NG = kBlock / D;  // chunk groups
+  __shared__ float red_m[kBlock / 64];
+  __shared__ float red_o[NG][D];
+  __shared__ float red_s[NG];
   const int bq = blockIdx.x;
   const int b = bq / a.Hq, qh = bq % a.Hq, h = qh / a.G;
   const int seg = b * a.Hkv + h;
@@ -227,33 +234,65 @@ __global__ __launch_bounds__(128) void decode_combine_kernel(DecodeArgs a) {
   const int64_t len = r1 - r0;
   int64_t nch = (len + a.chunk - 1) / a.chunk;
   if (nch > a.n_chunk_max) nch = a.n_chunk_max;
-  const int col = threadIdx.x;
+  const int tid = threadIdx.x, col = tid % D, grp = tid / D;
   const int stride = D + 2;
-  const rsrc_t pr = make_rsrc(a.part + (int64_t)bq * a.n_chunk_max * stride,
-                              (uint64_t)a.n_chunk_max * stride * 4);
+  const rsrc_t pr = make_rsrc(a.part + (int64_t)bq * a.n_chunk_max * stride, (uint64_t)a.n_chunk_max * stride * 4);
+  // global max over the chunks
   float M = -INFINITY;
-  for (int64_t c = 0; c < nch; ++c) M = fmaxf(M, ldf(pr, (uint32_t)(c * stride * 4)));
+  for (int64_t c = tid; c < nch; c += kBlock) M = fmaxf(M, ldf(pr, (uint32_t)(c * stride * 4)));
+  M = wave_max(M);
+  if ((tid & 63) == 0) red_m[tid >> 6] = M;
+  __syncthreads();
+  M = red_m[0];
+#pragma unroll
+  for (int u = 1; u < kBlock / 64; ++u) M = fmaxf(M, red_m[u]);
   float S = 0.f, O = 0.f;
   if (M != -INFINITY) {
-    for (int64_t c = 0; c < nch; ++c) {
-      const float mc = ldf(pr, (uint32_t)(c * stride * 4));
-      const float sc = (mc == -INFINITY) ? 0.f : fast_exp2(mc - M);
-      S += ldf(pr, (uint32_t)(c * stride * 4 + 4)) * sc;
-      if (col < D) O += ldf(pr, (uint32_t)((c * stride + 2 + col) * 4)) * sc;
+    int64_t c = grp;
+    for (; c + 3 * NG < nch; c += 4 * NG) {
+      float mc[4], sc[4], oc[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t base = (uint32_t)((c + u * NG) * stride * 4);
+        mc[u] = ldf(pr, base);
+        sc[u] = ldf(pr, base + 4);
+        oc[u] = ldf(pr, base + 8 + col * 4);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float e = (mc[u] == -INFINITY) ? 0.f : fast_exp2(mc[u] - M);
+        S += sc[u] * e;
+        O += oc[u] * e;
+      }
     }
+    for (; c < nch; c += NG) {
+      const uint32_t base = (uint32_t)(c * stride * 4);
+      const float mc = ldf(pr, base);
+      const float e = (mc == -INFINITY) ? 0.f : fast_exp2(mc - M);
+      S += ldf(pr, base + 4) * e;
+      O += ldf(pr, base + 8 + col * 4) * e;
+    }
+  }
+  red_o[grp][col] = O;
+  if (col == 0) red_s[grp] = S;
+  __syncthreads();
+  if (grp != 0) return;
+  S = red_s[0];
+  O = red_o[0][col];
+#pragma unroll
+  for (int g = 1; g < NG; ++g) {
+    S += red_s[g];
+    O += red_o[g][col];
   }
   const bool empty = !(S > 0.f);
   const float res = empty ? 0.f : O / S;
-  if (col < D) {
-    if (a.out_dtype == 1) {
-      const rsrc_t orr = make_rsrc(static_cast<char*>(a.out) + (int64_t)bq * D * 2, (uint64_t)D * 2);
-      // two columns per 32-bit store
-      const float other = __shfl_xor(res, 1, 64);
-      if ((col & 1) == 0) st32(orr, (uint32_t)col * 2, f32_to_bf16_bits(res) | (f32_to_bf16_bits(other) << 16));
-    } else {
-      const rsrc_t orr = make_rsrc(static_cast<char*>(a.out) + (int64_t)bq * D * 4, (uint64_t)D * 4);
-      stf(orr, (uint32_t)col * 4, res);
-    }
+  if (a.out_dtype == 1) {
+    const rsrc_t orr = make_rsrc(static_cast<char*>(a.out) + (int64_t)bq * D * 2, (uint64_t)D * 2);
+    const float other = __shfl_xor(res, 1, 64);  // two columns per 32-bit store
+    if ((col & 1) == 0) st32(orr, (uint32_t)col * 2, f32_to_bf16_bits(res) | (f32_to_bf16_bits(other) << 16));
+  } else {
+    const rsrc_t orr = make_rsrc(static_cast<char*>(a.out) + (int64_t)bq * D * 4, (uint64_t)D * 4);
+    stf(orr, (uint32_t)col * 4, res);
   }
   if (a.lse_out != nullptr && col == 0) {
     const rsrc_t lr = make_rsrc(a.lse_out, (uint64_t)a.B * a.Hq * 4);
@@ -282,9 +321,9 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {
     }
   }
   if (a.D == 128)
-    SGDKV_LAUNCH("decode_combine", decode_combine_kernel<128>, dim3(a.B * a.Hq), dim3(128), st, a);
+    SGDKV_LAUNCH("decode_combine", decode_combine_kernel<128>, dim3(a.B * a.Hq), dim3(kBlock), st, a);
   else
-    SGDKV_LAUNCH("decode_combine", decode_combine_kernel<64>, dim3(a.B * a.Hq), dim3(128), st, a);
+    SGDKV_LAUNCH("decode_combine", decode_combine_kernel<64>, dim3(a.B * a.Hq), dim3(kBlock), st, a);
   return hipGetLastError();
 }
 

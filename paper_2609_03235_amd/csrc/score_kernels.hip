@@ -27,6 +27,10 @@
 #include "mfma_frag.h"
 #include "sgdkv_internal.h"
 
+// Row blocks per wave the dispatch instantiates: at most 512 rows over all waves.
+#define SGDKV_SCORE_WAVES_MAX_RBW (kMaxGroupRowsMacro / (16 * SGDKV_SCORE_WAVES))
+#define kMaxGroupRowsMacro 512
+
 namespace sgdkv {
 
 // Shared pieces of both passes ------------------------------------------------
@@ -81,47 +85,152 @@ __device__ __forceinline__ void load_group_queries(const CompressArgs& a, int b,
   }
 }
 
+// Per-tile compute -----------------------------------------------------------
+//
+// A 64-key tile is four 16-key subtiles, processed as one branch-free rolling
+// pipeline: while subtile t's logits go through the vector ALU (one fma, one
+// exp2, one add per logit), the MFMAs of subtile t+1 run on the matrix core and
+// the key fragments of subtile t+2 are read from LDS. The MFMAs of each
+// subtile are independent accumulator chains, one per row block.
+template <typename T, int D, int NB>
+__device__ __forceinline__ void subtile_mfma(const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
+                                             const Frag<T> (&kb)[D / 32], f32x4 (&acc)[NB > 0 ? NB : 1]) {
+#pragma unroll
+  for (int c = 0; c < D / 32; ++c)
+#pragma unroll
+    for (int j = 0; j < NB; ++j) acc[j] = mma(qa[j][c], kb[c], c == 0 ? f32x4{0.f, 0.f, 0.f, 0.f} : acc[j]);
+}
+
+template <typename T, int D>
+__device__ __forceinline__ void subtile_frags(const char* ktile, int t, int lr, int lg, Frag<T> (&kb)[D / 32]) {
+  using G = TileGeom<T, D>;
+#pragma unroll
+  for (int c = 0; c < G::NC; ++c)
+    kb[c] = lds_frag<T>(ktile, (uint32_t)((16 * t + lr) * G::LDS_STRIDE + (32 * c + 8 * lg) * G::EB));
+}
+
+// Runs op(t, acc_of_subtile_t) for the four subtiles of the staged tile.
+template <typename T, int D, int NB, typename Op>
+__device__ __forceinline__ void tile_pipeline(const char* ktile, int lr, int lg,
+                                              const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], Op&& op) {
+  constexpr int NBX = NB > 0 ? NB : 1;
+  constexpr int NT = kScoreTile / 16;
+  Frag<T> kb[2][D / 32];
+  f32x4 acc[2][NBX];
+  subtile_frags<T, D>(ktile, 0, lr, lg, kb[0]);
+  subtile_frags<T, D>(ktile, 1, lr, lg, kb[1]);
+  subtile_mfma<T, D, NB>(qa, kb[0], acc[0]);
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    if (t + 1 < NT) subtile_mfma<T, D, NB>(qa, kb[(t + 1) & 1], acc[(t + 1) & 1]);
+    if (t + 2 < NT) subtile_frags<T, D>(ktile, t + 2, lr, lg, kb[t & 1]);
+    op(t, acc[t & 1]);
+  }
+  // schedule: subtile 0's MFMAs, then the later MFMAs spread one per 3 vector instructions
+#pragma unroll
+  for (int i = 0; i < NB * (D / 32); ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+#pragma unroll
+  for (int i = 0; i < (NT - 1) * NB * (D / 32); ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+  }
+}
+
 // Pass 1: per-chunk partial log-sum-exp of every window row -------------------
 //
-// Each lane keeps, for each of its 4*RBW row slots, a reference m and a sum
-// s = sum 2^(y - m) over the keys it has seen (y = logit*log2 e). m only
-// moves when a value exceeds it by more than 64 (then the slot is updated
-// exactly); otherwise s += 2^(y-m) costs one fma + one exp2 + one add.
-// The sum stays below 2^64 * keys, far from fp32 overflow.
-template <typename T, int D, int RBW>
-__global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
-  using G = TileGeom<T, D>;
-  __shared__ __attribute__((aligned(16))) char ktile[kScoreTile * G::LDS_STRIDE];
-  const int seg = blockIdx.y;
-  const int b = seg / a.Hkv, h = seg % a.Hkv;
-  const int64_t key0 = (int64_t)blockIdx.x * a.score_chunk;
-  if (key0 >= a.C) return;
-  const int64_t key_end = key0 + a.score_chunk < a.C ? key0 + a.score_chunk : a.C;
-  const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
-  const int lr = lane & 15, lg = lane >> 4;
-  const int nrb = (a.R + 15) / 16;
-
-  Frag<T> qa[RBW][G::NC];
-  load_group_queries<T, D, RBW>(a, b, h, wid, lane, qa);
-  const rsrc_t kr = make_rsrc(static_cast<const T*>(a.k) + (int64_t)seg * a.C * D,
-                              (uint64_t)a.C * G::RB);
-
-  // Causality: the row with window index i sees key j iff j - (C-w) <= i.
-  // Rows past R see nothing.
-  const int64_t vis0 = a.C - a.w;
-  int wi[RBW][4];
-  float m[RBW][4], s[RBW][4];
+// Each lane keeps, for each of its 4*NB row slots, a reference m and a sum
+// s = sum 2^(y - m) over the keys it has seen (y = logit * log2 e). Within a
+// tile m is fixed, so each logit costs one fma, one exp2 and one add. After
+// the tile, if any slot's sum left [0, 2^96] (a logit more than ~96 above its
+// reference, +inf, or the +inf that m = -inf produces on a slot's first
+// tile), the tile is redone for the whole wave from the saved sums with the
+// exact online update (two exp2 per logit, m = running max). This happens on
+// the first tile of a chunk, on tiles of the causal window block, and after
+// rare large jumps. Padded rows (past R) start at m = 0 and are never stored.
+template <typename T, int D, int NB>
+__device__ __forceinline__ void lse_exact_tile(const char* ktile, int lr, int lg, int wid, int w, int64_t tile0,
+                                               int64_t vis0, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
+                                               float c2, float (&m)[NB > 0 ? NB : 1][4],
+                                               float (&s)[NB > 0 ? NB : 1][4]) {
+  constexpr int NBX = NB > 0 ? NB : 1;
+  const bool masked = tile0 + kScoreTile > vis0;
+#pragma unroll 1
+  for (int t = 0; t < kScoreTile / 16; ++t) {
+    Frag<T> kb[D / 32];
+    subtile_frags<T, D>(ktile, t, lr, lg, kb);
+    f32x4 acc[NBX];
+    subtile_mfma<T, D, NB>(qa, kb, acc);
+    const int64_t dk64 = tile0 + 16 * t + lr - vis0;
+    const int dk = dk64 < -(1 << 30) ? -(1 << 30) : (int)dk64;
 #pragma unroll
-  for (int j = 0; j < RBW; ++j)
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int wi = ((wid + kScoreWaves * j) * 16 + 4 * lg + i) % w;  // window index of the row
+        const float y = (masked && dk > wi) ? -INFINITY : acc[j][i] * c2;
+        const float mn = fmaxf(m[j][i], y);
+        if (mn != -INFINITY) {
+          s[j][i] = s[j][i] * fast_exp2(m[j][i] - mn) + fast_exp2(y - mn);
+          m[j][i] = mn;
+        }
+      }
+  }
+}
+
+template <typename T, int D, int NB>
+__device__ __forceinline__ void lse_tile(const char* ktile, int lr, int lg, int wid, int w, int64_t tile0,
+                                         int64_t vis0, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], float c2,
+                                         float (&m)[NB > 0 ? NB : 1][4], float (&s)[NB > 0 ? NB : 1][4]) {
+  constexpr int NBX = NB > 0 ? NB : 1;
+  if (tile0 + kScoreTile > vis0) {  // uniform: the tile reaches the causal window block
+    lse_exact_tile<T, D, NB>(ktile, lr, lg, wid, w, tile0, vis0, qa, c2, m, s);
+    return;
+  }
+  float s0[NBX][4], nm[NBX][4];
+#pragma unroll
+  for (int j = 0; j < NBX; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      s0[j][i] = s[j][i];
+      nm[j][i] = -m[j][i];
+    }
+  tile_pipeline<T, D, NB>(ktile, lr, lg, qa, [&](int, const f32x4(&acc)[NBX]) {
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s[j][i] += fast_exp2(fmaf(acc[j][i], c2, nm[j][i]));
+  });
+  bool bad = false;
+#pragma unroll
+  for (int j = 0; j < NB; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) bad |= !(s[j][i] <= 7.9228162514264338e28f);  // 2^96; catches inf and NaN
+  if (__any(bad)) {
+#pragma unroll
+    for (int j = 0; j < NBX; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s[j][i] = s0[j][i];
+    lse_exact_tile<T, D, NB>(ktile, lr, lg, wid, w, tile0, vis0, qa, c2, m, s);
+  }
+}
+
+template <typename T, int D, int NB>
+__device__ void lse_chunk(const CompressArgs& a, char* ktile, int seg, int wid, int lane,
+                          const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], const rsrc_t& kr, int64_t key0,
+                          int64_t key_end) {
+  constexpr int NBX = NB > 0 ? NB : 1;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int64_t vis0 = a.C - a.w;  // the row with window index i sees key j iff j - vis0 <= i
+  float m[NBX][4], s[NBX][4];
+#pragma unroll
+  for (int j = 0; j < NBX; ++j)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = (wid + kScoreWaves * j) * 16 + 4 * lg + i;
-      wi[j][i] = row < a.R ? row % a.w : -(1 << 30);
-      m[j][i] = -INFINITY;
+      m[j][i] = row < a.R ? -INFINITY : 0.f;  // a padded row must not force the exact path
       s[j][i] = 0.f;
     }
   const float c2 = a.c2;
-
   KeyStage<T, D> stage;
   stage.load(kr, key0);
   for (int64_t tile0 = key0; tile0 < key_end; tile0 += kScoreTile) {
@@ -129,71 +238,14 @@ __global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
     stage.store(ktile);
     __syncthreads();
     if (tile0 + kScoreTile < key_end) stage.load(kr, tile0 + kScoreTile);
-    const bool masked = tile0 + kScoreTile > vis0;  // uniform: tile reaches the window block
-#pragma unroll 1
-    for (int t = 0; t < kScoreTile / 16; ++t) {
-      Frag<T> kb[G::NC];
-#pragma unroll
-      for (int c = 0; c < G::NC; ++c)
-        kb[c] = lds_frag<T>(ktile, (uint32_t)((16 * t + lr) * G::LDS_STRIDE + (32 * c + 8 * lg) * G::EB));
-      // key offset past the start of the window block, clamped into int range
-      const int64_t dk64 = tile0 + 16 * t + lr - vis0;
-      const int dk = dk64 < -(1 << 30) ? -(1 << 30) : (int)dk64;
-      f32x4 acc[RBW];
-      float tmax = -INFINITY;
-#pragma unroll
-      for (int j = 0; j < RBW; ++j) {
-        if (wid + kScoreWaves * j < nrb) {
-          acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int c = 0; c < G::NC; ++c) acc[j] = mma(qa[j][c], kb[c], acc[j]);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            float tv = fmaf(acc[j][i], c2, -m[j][i]);
-            if (wi[j][i] < 0 || (masked && dk > wi[j][i])) tv = -INFINITY;  // padding / causal
-            acc[j][i] = tv;
-            tmax = fmaxf(tmax, tv);
-          }
-        } else {
-          acc[j] = f32x4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-        }
-      }
-      if (__any(tmax > 64.f)) {
-        // Exact online update for this key: taken for the first key a slot sees
-        // (m = -inf) and after jumps of more than 2^64. acc now holds t = y - m,
-        // which is +inf while m is -inf, so the logits are recomputed.
-#pragma unroll
-        for (int j = 0; j < RBW; ++j) {
-          if (wid + kScoreWaves * j >= nrb) continue;
-          f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int c = 0; c < G::NC; ++c) z = mma(qa[j][c], kb[c], z);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const bool vis = !(masked && dk > wi[j][i]) && wi[j][i] >= 0;
-            const float y = vis ? z[i] * c2 : -INFINITY;
-            const float mn = fmaxf(m[j][i], y);
-            if (mn != -INFINITY) {
-              s[j][i] = s[j][i] * fast_exp2(m[j][i] - mn) + fast_exp2(y - mn);
-              m[j][i] = mn;
-            }
-          }
-        }
-      } else {
-#pragma unroll
-        for (int j = 0; j < RBW; ++j)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) s[j][i] += fast_exp2(acc[j][i]);
-      }
-    }
+    lse_tile<T, D, NB>(ktile, lr, lg, wid, a.w, tile0, vis0, qa, c2, m, s);
   }
-
   // Combine the 16 lanes (keys) of each row, then store (m, s) for the row.
   const int chunk = blockIdx.x;
   float* part = a.lse_part + ((int64_t)seg * a.n_lse_chunks + chunk) * a.R * 2;
   const rsrc_t pr = make_rsrc(part, (uint64_t)a.R * 2 * sizeof(float));
 #pragma unroll
-  for (int j = 0; j < RBW; ++j)
+  for (int j = 0; j < NB; ++j)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       float mm = m[j][i], ss = s[j][i];
@@ -215,58 +267,79 @@ __global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
     }
 }
 
-// Merge the per-chunk partials of every window row, in chunk order, in fp64.
+template <typename T, int D, int RBW>
+__global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
+  using G = TileGeom<T, D>;
+  __shared__ __attribute__((aligned(16))) char ktile[kScoreTile * G::LDS_STRIDE];
+  const int seg = blockIdx.y;
+  const int b = seg / a.Hkv, h = seg % a.Hkv;
+  const int64_t key0 = (int64_t)blockIdx.x * a.score_chunk;
+  if (key0 >= a.C) return;
+  const int64_t key_end = key0 + a.score_chunk < a.C ? key0 + a.score_chunk : a.C;
+  const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
+  const rsrc_t kr = make_rsrc(static_cast<const T*>(a.k) + (int64_t)seg * a.C * D, (uint64_t)a.C * G::RB);
+  Frag<T> qa[RBW][G::NC];
+  load_group_queries<T, D, RBW>(a, b, h, wid, lane, qa);
+  // blocks this wave owns: RBW or RBW-1 (uniform per wave)
+  const int nrb = (a.R + 15) / 16;
+  if (wid + kScoreWaves * (RBW - 1) < nrb) {
+    lse_chunk<T, D, RBW>(a, ktile, seg, wid, lane, qa, kr, key0, key_end);
+  } else {
+    Frag<T> qb[RBW > 1 ? RBW - 1 : 1][G::NC];
+#pragma unroll
+    for (int j = 0; j < RBW - 1; ++j)
+#pragma unroll
+      for (int c = 0; c < G::NC; ++c) qb[j][c] = qa[j][c];
+    lse_chunk<T, D, RBW - 1>(a, ktile, seg, wid, lane, qb, kr, key0, key_end);
+  }
+}
+
+// Merge the per-chunk partials of every window row in fp64: one wave per row,
+// lanes stride over the chunks, fixed-order shuffle trees for max and sum.
 __global__ __launch_bounds__(kBlock) void lse_merge_kernel(CompressArgs a) {
-  const int64_t idx = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int64_t idx = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
   const int64_t nrows = (int64_t)a.B * a.Hkv * a.R;
-  if (idx >= nrows) return;
+  if (idx >= nrows) return;  // uniform per wave
   const int64_t seg = idx / a.R, row = idx % a.R;
   const float* part = a.lse_part + (seg * a.n_lse_chunks) * a.R * 2;
   const rsrc_t pr = make_rsrc(part, (uint64_t)a.n_lse_chunks * a.R * 2 * sizeof(float));
   float mx = -INFINITY;
-  for (int c = 0; c < a.n_lse_chunks; ++c)
+  for (int c = lane; c < a.n_lse_chunks; c += 64)
     mx = fmaxf(mx, ldf(pr, (uint32_t)(((int64_t)c * a.R + row) * 8)));
+  mx = wave_max(mx);
   double sum = 0.0;
   if (mx != -INFINITY) {
-    for (int c = 0; c < a.n_lse_chunks; ++c) {
+    for (int c = lane; c < a.n_lse_chunks; c += 64) {
       const float mc = ldf(pr, (uint32_t)(((int64_t)c * a.R + row) * 8));
       const float sc = ldf(pr, (uint32_t)(((int64_t)c * a.R + row) * 8 + 4));
       if (mc != -INFINITY) sum += (double)sc * exp2((double)mc - (double)mx);
     }
   }
-  const float lse2 = (mx == -INFINITY || !(sum > 0.0)) ? -INFINITY : (float)((double)mx + log2(sum));
-  const rsrc_t lr = make_rsrc(a.lse2, (uint64_t)nrows * sizeof(float));
-  stf(lr, (uint32_t)(idx * 4), lse2);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o, 64);
+  if (lane == 0) {
+    const float lse2 = (mx == -INFINITY || !(sum > 0.0)) ? -INFINITY : (float)((double)mx + log2(sum));
+    const rsrc_t lr = make_rsrc(a.lse2, (uint64_t)nrows * sizeof(float));
+    stf(lr, (uint32_t)(idx * 4), lse2);
+  }
 }
 
 // Pass 2: window-summed probabilities of every scored key --------------------
-template <typename T, int D, int RBW>
-__global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) {
-  using G = TileGeom<T, D>;
-  __shared__ __attribute__((aligned(16))) char ktile[kScoreTile * G::LDS_STRIDE];
-  __shared__ float red[kScoreWaves][kScoreTile];
-  const int seg = blockIdx.y;
-  const int b = seg / a.Hkv, h = seg % a.Hkv;
-  const int64_t key0 = (int64_t)blockIdx.x * a.score_chunk;
-  if (key0 >= a.n_scored) return;
-  const int64_t key_end = key0 + a.score_chunk < a.n_scored ? key0 + a.score_chunk : a.n_scored;
-  const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
+template <typename T, int D, int NB>
+__device__ void colsum_chunk(const CompressArgs& a, char* ktile, float (*red)[kScoreTile], int seg, int wid,
+                             int lane, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], const rsrc_t& kr,
+                             int64_t key0, int64_t key_end) {
+  constexpr int NBX = NB > 0 ? NB : 1;
+  const int tid = threadIdx.x;
   const int lr = lane & 15, lg = lane >> 4;
-  const int nrb = (a.R + 15) / 16;
-
-  Frag<T> qa[RBW][G::NC];
-  load_group_queries<T, D, RBW>(a, b, h, wid, lane, qa);
-  const rsrc_t kr = make_rsrc(static_cast<const T*>(a.k) + (int64_t)seg * a.C * D,
-                              (uint64_t)a.C * G::RB);
-
   // -lse2 of this lane's row slots; rows past R get -inf so they add exp2(-inf) = 0
   const uint64_t nl = (uint64_t)a.B * a.Hkv * a.R;
   const bool natural = a.window_lse != nullptr;
-  const rsrc_t lr2 = make_rsrc(natural ? (const void*)a.window_lse : (const void*)a.lse2,
-                               nl * sizeof(float));
-  float nlse[RBW][4];
+  const rsrc_t lr2 = make_rsrc(natural ? (const void*)a.window_lse : (const void*)a.lse2, nl * sizeof(float));
+  float nlse[NBX][4];
 #pragma unroll
-  for (int j = 0; j < RBW; ++j)
+  for (int j = 0; j < NBX; ++j)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = (wid + kScoreWaves * j) * 16 + 4 * lg + i;
@@ -284,27 +357,16 @@ __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) 
     stage.store(ktile);
     __syncthreads();
     if (tile0 + kScoreTile < key_end) stage.load(kr, tile0 + kScoreTile);
-#pragma unroll 1
-    for (int t = 0; t < kScoreTile / 16; ++t) {
-      Frag<T> kb[G::NC];
-#pragma unroll
-      for (int c = 0; c < G::NC; ++c)
-        kb[c] = lds_frag<T>(ktile, (uint32_t)((16 * t + lr) * G::LDS_STRIDE + (32 * c + 8 * lg) * G::EB));
+    tile_pipeline<T, D, NB>(ktile, lr, lg, qa, [&](int t, const f32x4(&acc)[NBX]) {
       float p = 0.f;
 #pragma unroll
-      for (int j = 0; j < RBW; ++j) {
-        if (wid + kScoreWaves * j < nrb) {
-          f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < NB; ++j)
 #pragma unroll
-          for (int c = 0; c < G::NC; ++c) acc = mma(qa[j][c], kb[c], acc);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) p += fast_exp2(fmaf(acc[i], c2, nlse[j][i]));
-        }
-      }
+        for (int i = 0; i < 4; ++i) p += fast_exp2(fmaf(acc[j][i], c2, nlse[j][i]));
       p += __shfl_xor(p, 16, 64);
       p += __shfl_xor(p, 32, 64);
-      if (lane < 16) red[wid][16 * t + lane] = p;
-    }
+      red[wid][16 * t + lr] = p;  // all four lane groups hold the same value
+    });
     __syncthreads();
     if (tid < kScoreTile) {
       const int64_t key = tile0 + tid;
@@ -318,6 +380,33 @@ __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) 
   }
 }
 
+template <typename T, int D, int RBW>
+__global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) {
+  using G = TileGeom<T, D>;
+  __shared__ __attribute__((aligned(16))) char ktile[kScoreTile * G::LDS_STRIDE];
+  __shared__ float red[kScoreWaves][kScoreTile];
+  const int seg = blockIdx.y;
+  const int b = seg / a.Hkv, h = seg % a.Hkv;
+  const int64_t key0 = (int64_t)blockIdx.x * a.score_chunk;
+  if (key0 >= a.n_scored) return;
+  const int64_t key_end = key0 + a.score_chunk < a.n_scored ? key0 + a.score_chunk : a.n_scored;
+  const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
+  const rsrc_t kr = make_rsrc(static_cast<const T*>(a.k) + (int64_t)seg * a.C * D, (uint64_t)a.C * G::RB);
+  Frag<T> qa[RBW][G::NC];
+  load_group_queries<T, D, RBW>(a, b, h, wid, lane, qa);
+  const int nrb = (a.R + 15) / 16;
+  if (wid + kScoreWaves * (RBW - 1) < nrb) {
+    colsum_chunk<T, D, RBW>(a, ktile, red, seg, wid, lane, qa, kr, key0, key_end);
+  } else {
+    Frag<T> qb[RBW > 1 ? RBW - 1 : 1][G::NC];
+#pragma unroll
+    for (int j = 0; j < RBW - 1; ++j)
+#pragma unroll
+      for (int c = 0; c < G::NC; ++c) qb[j][c] = qa[j][c];
+    colsum_chunk<T, D, RBW - 1>(a, ktile, red, seg, wid, lane, qb, kr, key0, key_end);
+  }
+}
+
 // Host-side dispatch ----------------------------------------------------------
 template <typename T, int D, int RBW>
 static hipError_t launch_scores_t(const CompressArgs& a, hipStream_t st) {
@@ -325,7 +414,9 @@ static hipError_t launch_scores_t(const CompressArgs& a, hipStream_t st) {
   if (a.window_lse == nullptr) {
     SGDKV_LAUNCH("score_lse", (lse_kernel<T, D, RBW>), dim3(a.n_lse_chunks, a.B * a.Hkv), sblk, st, a);
     const int64_t nrows = (int64_t)a.B * a.Hkv * a.R;
-    SGDKV_LAUNCH("lse_merge", lse_merge_kernel, dim3((unsigned)((nrows + kBlock - 1) / kBlock)), dim3(kBlock), st, a);
+    const int64_t rows_per_block = kBlock / 64;
+    SGDKV_LAUNCH("lse_merge", lse_merge_kernel, dim3((unsigned)((nrows + rows_per_block - 1) / rows_per_block)),
+                 dim3(kBlock), st, a);
   }
   if (a.n_col_chunks > 0)
     SGDKV_LAUNCH("score_colsum", (colsum_kernel<T, D, RBW>), dim3(a.n_col_chunks, a.B * a.Hkv), sblk, st, a);
@@ -341,6 +432,12 @@ static hipError_t launch_scores_d(const CompressArgs& a, hipStream_t st) {
     case 2: return launch_scores_t<T, D, 2>(a, st);
     case 3: return launch_scores_t<T, D, 3>(a, st);
     case 4: return launch_scores_t<T, D, 4>(a, st);
+#if SGDKV_SCORE_WAVES_MAX_RBW > 4
+    case 5: return launch_scores_t<T, D, 5>(a, st);
+    case 6: return launch_scores_t<T, D, 6>(a, st);
+    case 7: return launch_scores_t<T, D, 7>(a, st);
+    case 8: return launch_scores_t<T, D, 8>(a, st);
+#endif
     default: return hipErrorInvalidValue;
   }
 }

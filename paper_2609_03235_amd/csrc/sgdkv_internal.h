@@ -13,7 +13,10 @@ constexpr int kMaxGroupRows = 512; // G*w rows of one KV head's window queries
 constexpr int kMaxDecodeGroup = 16;
 constexpr int kBlock = 256;        // threads per workgroup in every kernel
 constexpr int kScoreTile = 64;     // keys staged in LDS per step of the score kernels
-constexpr int kScoreWaves = 8;     // waves per score workgroup
+#ifndef SGDKV_SCORE_WAVES
+#define SGDKV_SCORE_WAVES 8
+#endif
+constexpr int kScoreWaves = SGDKV_SCORE_WAVES;  // waves per score workgroup
 constexpr int kScoreBlock = 64 * kScoreWaves;
 
 // Opt-in per-kernel timing (see sgdkv_profile_*): brackets a launch with events.

@@ -272,3 +272,41 @@ def test_run_twice_bitwise():
     for key in ("scores", "kept_pos", "offsets", "k_c", "v_c"):
         assert torch.equal(a[key], b[key]), key
     assert torch.equal(oa, ob) and torch.equal(la, lb)
+
+
+def test_lse_exact_redo_paths():
+    """Pass 1 keeps a per-slot reference fixed within a tile and redoes a tile exactly when a sum
+    leaves [0, 2^96]. Every 16th key is strongly anti-aligned with the window queries (logit about
+    -120) and three keys inside later chunks are strongly aligned (logit about +70, i.e. ~101 in
+    base 2), which forces the exact redo after the reference was set by ordinary keys."""
+    rng = np.random.Generator(np.random.PCG64(31))
+    B, Hq, Hkv, d, C, w, s, W = 1, 4, 2, 64, 3000, 32, 4, 32
+    common = rng.standard_normal((Hkv, d))
+    common *= 8.0 / np.linalg.norm(common, axis=1, keepdims=True)
+    q_win = rng.standard_normal((B, Hq, w, d)) * 0.5 + np.repeat(common, Hq // Hkv, axis=0)[None, :, None, :]
+    k = rng.standard_normal((B, Hkv, C, d))
+    k[:, :, ::16, :] = -15.0 * common[None, :, None, :]  # <common, key>/sqrt(d) = -120
+    for pos in (700, 1500, 2300):
+        k[:, :, pos, :] = 8.75 * common  # <common, key>/sqrt(d) = +70
+    v = rng.standard_normal((B, Hkv, C, d))
+    t = {n: torch.from_numpy(x.astype(np.float32)).to(DEV) for n, x in dict(q_win=q_win, k=k, v=v).items()}
+    budgets = np.array([s + W + 15, s + W + 5])  # selection stays among the keys near the spikes
+    _announce("pass-1 exact redo paths")
+    res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=7, s=s, W=W)
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "redo")
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "redo")
+
+
+@pytest.mark.parametrize("w,W", [(100, 128), (200, 200)])
+def test_long_window_spans_masked_tiles(w, W):
+    """Window rows spanning several 64-key tiles of the causal block."""
+    rng = np.random.Generator(np.random.PCG64(w))
+    B, Hq, Hkv, d, C, s = 2, 4, 2, 64, 1500, 8
+    t = {n: torch.from_numpy(rng.standard_normal(shape).astype(np.float32)).to(DEV)
+         for n, shape in dict(q_win=(B, Hq, w, d), k=(B, Hkv, C, d), v=(B, Hkv, C, d)).items()}
+    budgets = np.array([s + W + 300, s + W + 17])
+    _announce(f"long window w={w} W={W}")
+    res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=5, s=s, W=W)
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "longwin")
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "longwin")
+    _check_gather(res, t["k"], t["v"], budgets)
