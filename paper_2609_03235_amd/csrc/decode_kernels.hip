@@ -4,13 +4,13 @@
 // for GQA (Appendix A.2), so one segment of rows serves the G query heads of
 // its group. Decode reads each segment once for all G heads:
 //
-//   decode_split: workgroup = (chunk of a segment's rows, segment). Logits of
-//     the G heads against 16 keys at a time are one 16x16 MFMA (the G query
-//     rows padded to 16 form the A operand). Each wave keeps an online
-//     softmax (running max m and sum s per head, base-2 units) over its
-//     quarter of the chunk and accumulates P.V in fp32 on the vector ALU
-//     (bf16 V rows are widened exactly). The four waves are merged in a fixed
-//     order and one partial (m, s, o[d]) per head and chunk is written.
+//   decode_split: each wave owns one chunk of a segment's rows. Logits of the
+//     G heads against 16 keys at a time are one 16x16 MFMA (the G query rows
+//     padded to 16 form the A operand). The wave keeps an online softmax
+//     (running max m and sum s per head, base-2 units) and accumulates P.V in
+//     fp32 on the vector ALU (bf16 V rows are widened exactly); the next
+//     step's K and V are already in flight. One partial (m, s, o[d]) per head
+//     and chunk is written; waves never synchronise with each other.
 //   decode_combine: per (sequence, query head), a fixed-order log-sum-exp
 //     merge of the chunk partials; out = o/s, lse = (m + log2 s) * ln 2.
 //
@@ -23,7 +23,6 @@
 namespace sgdkv {
 
 namespace {
-constexpr int kKeysPerStep = 32;  // keys per wave per step (two 16-key MFMA tiles)
 constexpr int kWaves = kBlock / 64;
 
 __device__ __forceinline__ void clamp_segment(const DecodeArgs& a, int seg, int64_t& r0, int64_t& r1) {
@@ -36,84 +35,98 @@ __device__ __forceinline__ void clamp_segment(const DecodeArgs& a, int seg, int6
 }
 }  // namespace
 
-// GM = compile-time bound on the group size (8 or 16).
+// Loads of one 16-key step: the K fragments of the MFMA (key lr, k = 32c + 8*lg)
+// and this lane's V rows (keys kg + KG*u, columns col0 .. col0+7).
+template <typename T, int D>
+struct DecodeStep {
+  static constexpr int EB = sizeof(T);
+  static constexpr int RB = D * EB;
+  static constexpr int NC = D / 32;
+  static constexpr int LPR = D / 8;        // lanes sharing one value row (8 columns each)
+  static constexpr int KG = 64 / LPR;      // key groups per wave
+  static constexpr int VPL = 16 / KG;      // value rows per lane per step
+  static constexpr int VW = EB == 2 ? 1 : 2;  // 16-byte pieces per 8 columns
+  Frag<T> kb[NC];
+  u32x4 vv[VPL][VW];
+  __device__ __forceinline__ void load(const rsrc_t& kr, const rsrc_t& vr, int64_t k0, int lr, int lgp, int kg,
+                                       int col0) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c) kb[c] = gload_frag<T>(kr, (uint32_t)((k0 + lr) * RB + (32 * c + 8 * lgp) * EB));
+#pragma unroll
+    for (int u = 0; u < VPL; ++u)
+#pragma unroll
+      for (int x = 0; x < VW; ++x) vv[u][x] = ld128(vr, (uint32_t)((k0 + kg + KG * u) * RB + col0 * EB + 16 * x));
+  }
+};
+
+__device__ __forceinline__ void wave_sync() {
+  // order this wave's LDS writes before its following LDS reads (other lanes read them)
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// GM = compile-time bound on the group size (8 or 16). Each wave owns one
+// chunk of a segment: chunk index = 4*blockIdx.x + wave.
 template <typename T, int D, int GM>
 __global__ __launch_bounds__(kBlock, 2) void decode_split_kernel(DecodeArgs a) {
-  constexpr int EB = sizeof(T);
-  constexpr int RB = D * EB;
-  constexpr int NC = D / 32;
-  constexpr int LPR = D / 8;     // lanes sharing one value row (8 columns each)
-  constexpr int KG = 64 / LPR;   // key groups per wave
-  constexpr int KB = kKeysPerStep;
-  __shared__ float lg[kWaves][16][KB];  // logits in base-2 units
-  __shared__ float pl[kWaves][16][KB];  // probabilities
-  __shared__ float al[kWaves][16];      // per-head rescale factor of this step
-  __shared__ float wm[kWaves][16], ws[kWaves][16];
-  __shared__ float wo[kWaves][GM][D];
+  using S = DecodeStep<T, D>;
+  constexpr int KS = 16;  // keys per step
+  __shared__ float lgs[kWaves][16][KS];  // logits (base-2 units), per wave
+  __shared__ float pls[kWaves][16][KS];  // probabilities, per wave
+  __shared__ float als[kWaves][16];      // per-head rescale factor of the step, per wave
 
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
+  const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
   int64_t r0, r1;
   clamp_segment(a, seg, r0, r1);
   const int64_t len = r1 - r0;
-  const int chunk = blockIdx.x;
-  const int64_t c0 = (int64_t)chunk * a.chunk;
-  if (c0 >= len) return;  // this segment has fewer chunks
+  const int64_t chunk = (int64_t)blockIdx.x * kWaves + wid;
+  const int64_t c0 = chunk * a.chunk;
+  if (c0 >= len) return;  // this wave's chunk is past the segment (waves never synchronise)
   const int64_t c1 = c0 + a.chunk < len ? c0 + a.chunk : len;
 
-  const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
   const int lr = lane & 15, lgp = lane >> 4;
   const int G = a.G;
-
-  const rsrc_t kr = make_rsrc(static_cast<const char*>(a.k_c) + r0 * RB, (uint64_t)len * RB);
-  const rsrc_t vr = make_rsrc(static_cast<const char*>(a.v_c) + r0 * RB, (uint64_t)len * RB);
-  const rsrc_t qr = make_rsrc(static_cast<const char*>(a.q) + ((int64_t)b * a.Hq + (int64_t)h * G) * RB,
-                              (uint64_t)G * RB);
-  // query fragments: row lr = head (rows >= G read as zeros)
-  Frag<T> qa[NC];
+  const rsrc_t kr = make_rsrc(static_cast<const char*>(a.k_c) + r0 * S::RB, (uint64_t)len * S::RB);
+  const rsrc_t vr = make_rsrc(static_cast<const char*>(a.v_c) + r0 * S::RB, (uint64_t)len * S::RB);
+  const rsrc_t qr = make_rsrc(static_cast<const char*>(a.q) + ((int64_t)b * a.Hq + (int64_t)h * G) * S::RB,
+                              (uint64_t)G * S::RB);
+  Frag<T> qa[S::NC];  // row lr = head; rows >= G read as zeros
 #pragma unroll
-  for (int c = 0; c < NC; ++c) qa[c] = gload_frag<T>(qr, (uint32_t)(lr * RB + (32 * c + 8 * lgp) * EB));
+  for (int c = 0; c < S::NC; ++c) qa[c] = gload_frag<T>(qr, (uint32_t)(lr * S::RB + (32 * c + 8 * lgp) * S::EB));
 
-  // this wave's rows [w0, w1) of the chunk
-  const int64_t per = a.chunk / kWaves;
-  const int64_t w0 = c0 + wid * per;
-  const int64_t w1 = w0 + per < c1 ? w0 + per : c1;
-  const int nsteps = (int)(per / KB);
-
-  // softmax state of head lane/4, replicated over its 4 lanes; s is this lane's share
-  const int sh_head = lane >> 2, sh_part = lane & 3;
+  const int sh_head = lane >> 2, sh_part = lane & 3;  // softmax: head lane/4, keys 4*(lane%4)..+3
+  const int kg = lane / S::LPR, col0 = 8 * (lane % S::LPR);
   float m_run = -INFINITY, s_run = 0.f;
-  const int kg = lane / LPR, col0 = 8 * (lane % LPR);
   float o[GM][8];
 #pragma unroll
   for (int g = 0; g < GM; ++g)
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
 
+  const int nsteps = (int)((c1 - c0 + KS - 1) / KS);
+  S cur, nxt;
+  cur.load(kr, vr, c0, lr, lgp, kg, col0);
   for (int it = 0; it < nsteps; ++it) {
-    const int64_t k0 = w0 + (int64_t)it * KB;  // first key of this step (chunk-relative rows)
-    // 1. logits of the (padded) 16 heads against 32 keys
+    const int64_t k0 = c0 + (int64_t)it * KS;
+    if (it + 1 < nsteps) nxt.load(kr, vr, k0 + KS, lr, lgp, kg, col0);
+    // 1. logits of the (padded) 16 heads against 16 keys
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int64_t key = k0 + 16 * t + lr;
+    for (int c = 0; c < S::NC; ++c) acc = mma(qa[c], cur.kb[c], acc);
+    const bool valid = k0 + lr < c1;
 #pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        const Frag<T> kb = gload_frag<T>(kr, (uint32_t)(key * RB + (32 * c + 8 * lgp) * EB));
-        acc = mma(qa[c], kb, acc);
-      }
-      const bool valid = key < w1;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) lg[wid][4 * lgp + i][16 * t + lr] = valid ? acc[i] * a.c2 : -INFINITY;
-    }
-    __syncthreads();
-    // 2. online softmax: lane handles head lane/4, keys 8*(lane%4) .. +7
+    for (int i = 0; i < 4; ++i) lgs[wid][4 * lgp + i][lr] = valid ? acc[i] * a.c2 : -INFINITY;
+    wave_sync();
+    // 2. online softmax per head
     {
-      float y[8];
+      float y[4];
       float tmax = -INFINITY;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        y[u] = lg[wid][sh_head][8 * sh_part + u];
+      for (int u = 0; u < 4; ++u) {
+        y[u] = lgs[wid][sh_head][4 * sh_part + u];
         tmax = fmaxf(tmax, y[u]);
       }
       tmax = fmaxf(tmax, __shfl_xor(tmax, 1, 64));
@@ -122,37 +135,39 @@ __global__ __launch_bounds__(kBlock, 2) void decode_split_kernel(DecodeArgs a) {
       const float alpha = (m_run == -INFINITY) ? (m_new == -INFINITY ? 1.f : 0.f) : fast_exp2(m_run - m_new);
       float ps = 0.f;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < 4; ++u) {
         const float p = (y[u] == -INFINITY) ? 0.f : fast_exp2(y[u] - m_new);
-        pl[wid][sh_head][8 * sh_part + u] = p;
+        pls[wid][sh_head][4 * sh_part + u] = p;
         ps += p;
       }
       s_run = s_run * alpha + ps;
       m_run = m_new;
-      if (sh_part == 0) al[wid][sh_head] = alpha;
-    }
-    __syncthreads();
-    // 3. rescale and accumulate P.V for this lane's keys and columns
+      if (sh_part == 0) als[wid][sh_head] = alpha;
+      // the accumulators need rescaling only when some head's running max moved
+      const bool moved = __any(alpha != 1.f);
+      wave_sync();
+      if (moved) {
 #pragma unroll
-    for (int g = 0; g < GM; ++g) {
-      if (g < G) {
-        const float alpha = al[wid][g];
+        for (int g = 0; g < GM; ++g) {
+          if (g < G) {
+            const float al = als[wid][g];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[g][e] *= alpha;
+            for (int e = 0; e < 8; ++e) o[g][e] *= al;
+          }
+        }
       }
     }
+    // 3. P.V for this lane's value rows and columns
 #pragma unroll
-    for (int u = 0; u < KB / KG; ++u) {
-      const int kk = kg + KG * u;
-      const int64_t key = k0 + kk;
+    for (int u = 0; u < S::VPL; ++u) {
+      const int kk = kg + S::KG * u;
       float v[8];
-      if (EB == 2) {
-        const u32x4 x = ld128(vr, (uint32_t)(key * RB + col0 * EB));
+      if (S::EB == 2) {
+        const u32x4 x = cur.vv[u][0];
         v[0] = bf16_lo(x.x); v[1] = bf16_hi(x.x); v[2] = bf16_lo(x.y); v[3] = bf16_hi(x.y);
         v[4] = bf16_lo(x.z); v[5] = bf16_hi(x.z); v[6] = bf16_lo(x.w); v[7] = bf16_hi(x.w);
       } else {
-        const u32x4 x0 = ld128(vr, (uint32_t)(key * RB + col0 * EB));
-        const u32x4 x1 = ld128(vr, (uint32_t)(key * RB + col0 * EB + 16));
+        const u32x4 x0 = cur.vv[u][0], x1 = cur.vv[u][S::VW - 1];
         v[0] = __uint_as_float(x0.x); v[1] = __uint_as_float(x0.y); v[2] = __uint_as_float(x0.z);
         v[3] = __uint_as_float(x0.w); v[4] = __uint_as_float(x1.x); v[5] = __uint_as_float(x1.y);
         v[6] = __uint_as_float(x1.z); v[7] = __uint_as_float(x1.w);
@@ -160,13 +175,14 @@ __global__ __launch_bounds__(kBlock, 2) void decode_split_kernel(DecodeArgs a) {
 #pragma unroll
       for (int g = 0; g < GM; ++g) {
         if (g < G) {
-          const float p = pl[wid][g][kk];
+          const float p = pls[wid][g][kk];
 #pragma unroll
           for (int e = 0; e < 8; ++e) o[g][e] = fmaf(p, v[e], o[g][e]);
         }
       }
     }
-    __syncthreads();
+    wave_sync();  // this step's LDS values are consumed before the next step overwrites them
+    cur = nxt;
   }
 
   // Reduce within the wave: the 4 lanes of each head's sum, the KG key groups of o.
@@ -178,42 +194,26 @@ __global__ __launch_bounds__(kBlock, 2) void decode_split_kernel(DecodeArgs a) {
     for (int e = 0; e < 8; ++e) {
       float x = o[g][e];
 #pragma unroll
-      for (int sft = LPR; sft < 64; sft <<= 1) x += __shfl_xor(x, sft, 64);
+      for (int sft = S::LPR; sft < 64; sft <<= 1) x += __shfl_xor(x, sft, 64);
       o[g][e] = x;
     }
-  if (sh_part == 0 && sh_head < 16) {
-    wm[wid][sh_head] = m_run;
-    ws[wid][sh_head] = s_run;
+  // write this chunk's partial (m, s, o[D]) for each of the G heads
+  const int stride = D + 2;
+  const int64_t bq0 = (int64_t)b * a.Hq + (int64_t)h * G;
+  if (sh_part == 0 && sh_head < G) {
+    const rsrc_t pr = make_rsrc(a.part + ((bq0 + sh_head) * a.n_chunk_max + chunk) * stride, (uint64_t)stride * 4);
+    stf(pr, 0, m_run);
+    stf(pr, 4, s_run);
   }
   if (kg == 0) {
 #pragma unroll
-    for (int g = 0; g < GM; ++g)
+    for (int g = 0; g < GM; ++g) {
+      if (g < G) {
+        const rsrc_t pr = make_rsrc(a.part + ((bq0 + g) * a.n_chunk_max + chunk) * stride, (uint64_t)stride * 4);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) wo[wid][g][col0 + e] = o[g][e];
-  }
-  __syncthreads();
-
-  // Merge the 4 waves in order and write this chunk's partial for each head.
-  const int stride = D + 2;
-  for (int x = tid; x < G * D; x += kBlock) {
-    const int g = x / D, col = x % D;
-    float M = -INFINITY;
-#pragma unroll
-    for (int u = 0; u < kWaves; ++u) M = fmaxf(M, wm[u][g]);
-    float S = 0.f, O = 0.f;
-#pragma unroll
-    for (int u = 0; u < kWaves; ++u) {
-      const float sc = (wm[u][g] == -INFINITY) ? 0.f : fast_exp2(wm[u][g] - M);
-      S += ws[u][g] * sc;
-      O += wo[u][g][col] * sc;
+        for (int e = 0; e < 8; ++e) stf(pr, (uint32_t)(8 + (col0 + e) * 4), o[g][e]);
+      }
     }
-    const int64_t bq = (int64_t)b * a.Hq + (int64_t)h * G + g;
-    const rsrc_t pr = make_rsrc(a.part + (bq * a.n_chunk_max + chunk) * stride, (uint64_t)stride * 4);
-    if (col == 0) {
-      stf(pr, 0, M);
-      stf(pr, 4, S);
-    }
-    stf(pr, (uint32_t)(8 + col * 4), O);
   }
 }
 
@@ -303,7 +303,7 @@ __global__ __launch_bounds__(kBlock) void decode_combine_kernel(DecodeArgs a) {
 
 template <typename T, int D>
 static void launch_decode_t(const DecodeArgs& a, hipStream_t st) {
-  const dim3 grid(a.n_chunk_max, a.B * a.Hkv);
+  const dim3 grid((a.n_chunk_max + kWaves - 1) / kWaves, a.B * a.Hkv);
   if (a.G <= 8)
     SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, 8>), grid, dim3(kBlock), st, a);
   else

@@ -20,7 +20,10 @@
 //   radix_hist<p>  digit-p histogram of candidates matching the prefix
 //   radix_digit<p> pick digit p of tau; clear the histogram
 //   sel_count      per chunk: sink/window rows, candidates > tau, == tau
-//   gather         ordered compaction of a chunk + 16-byte row copies
+//   compact        ordered ballot/prefix compaction of a chunk -> kept_pos
+//   copy_rows      K and V rows of the kept positions -> the ragged cache
+#include <algorithm>
+
 #include "device_common.h"
 #include "sgdkv_internal.h"
 
@@ -201,12 +204,9 @@ __global__ __launch_bounds__(kBlock) void sel_count_kernel(CompressArgs a) {
   }
 }
 
-// Ordered compaction of one chunk of positions plus the K/V row copies.
-// RB = bytes per row (head_dim * element size).
-template <int RB>
-__global__ __launch_bounds__(kBlock) void gather_kernel(CompressArgs a) {
-  constexpr int V16 = RB / 16;
-  __shared__ int32_t list[kBlock];
+// Ordered compaction of one chunk of positions: writes the prompt positions of
+// the kept rows (ascending) into the segment's slice of kept_pos.
+__global__ __launch_bounds__(kBlock) void compact_kernel(CompressArgs a) {
   __shared__ uint32_t wt0[kBlock / 64], wt1[kBlock / 64];
   __shared__ uint32_t pre[3][kBlock / 64];
   const int seg = blockIdx.y, b = seg / a.Hkv, h = seg % a.Hkv;
@@ -250,10 +250,6 @@ __global__ __launch_bounds__(kBlock) void gather_kernel(CompressArgs a) {
   const int64_t seg_off = (int64_t)b * a.T_layer + a.prefix[h];
   const int64_t seg_len = a.prefix[h + 1] - a.prefix[h];
   const rsrc_t kp = make_rsrc(a.kept_pos + seg_off, (uint64_t)seg_len * 4);
-  const rsrc_t ko = make_rsrc(static_cast<char*>(a.k_out) + seg_off * RB, (uint64_t)seg_len * RB);
-  const rsrc_t vo = make_rsrc(static_cast<char*>(a.v_out) + seg_off * RB, (uint64_t)seg_len * RB);
-  const rsrc_t ki = make_rsrc(static_cast<const char*>(a.k) + (int64_t)seg * a.C * RB, (uint64_t)a.C * RB);
-  const rsrc_t vi = make_rsrc(static_cast<const char*>(a.v) + (int64_t)seg * a.C * RB, (uint64_t)a.C * RB);
   const rsrc_t pr = make_rsrc(a.pooled + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
 
   const int64_t j0 = (int64_t)chunk * a.sel_chunk;
@@ -271,29 +267,49 @@ __global__ __launch_bounds__(kBlock) void gather_kernel(CompressArgs a) {
     const uint32_t eq_rank = run_eq + block_rank(eq, wt0, n_eq);
     const bool keep = fixed || gt || (eq && eq_rank < q);
     const uint32_t r = block_rank(keep, wt1, n_keep);
-    const uint32_t slot = run_keep + r;
-    if (keep) {
-      st32(kp, slot * 4u, (uint32_t)j);
-      list[r] = (int32_t)j;
-    }
-    __syncthreads();
-    // copy the chunk's kept rows, 16 bytes per thread per step
-    for (uint32_t x = tid; x < n_keep * V16; x += kBlock) {
-      const uint32_t rr = x / V16, c16 = x % V16;
-      const uint32_t src = (uint32_t)list[rr] * RB + c16 * 16;
-      const uint32_t dst = (run_keep + rr) * RB + c16 * 16;
-      st128(ko, dst, ld128(ki, src));
-      st128(vo, dst, ld128(vi, src));
-    }
-    __syncthreads();
+    if (keep) st32(kp, (run_keep + r) * 4u, (uint32_t)j);
     run_eq += n_eq;
     run_keep += n_keep;
   }
 }
 
+// Copies the kept K and V rows of one segment into the ragged cache. Each
+// workgroup moves kCopyRows output rows; every thread keeps several 16-byte
+// loads in flight before storing. RB = bytes per row.
+constexpr int kCopyRows = 64;
 template <int RB>
-static void launch_gather(const CompressArgs& a, hipStream_t st) {
-  SGDKV_LAUNCH("gather", (gather_kernel<RB>), dim3(a.n_sel_chunks, a.B * a.Hkv), dim3(kBlock), st, a);
+__global__ __launch_bounds__(kBlock) void copy_rows_kernel(CompressArgs a) {
+  constexpr int V16 = RB / 16;                        // 16-byte pieces per row
+  constexpr int PER = kCopyRows * V16 / kBlock;       // pieces per thread per tensor
+  static_assert(PER >= 1 && (kCopyRows * V16) % kBlock == 0, "copy tile must split evenly");
+  const int seg = blockIdx.y, b = seg / a.Hkv, h = seg % a.Hkv;
+  const int64_t seg_len = a.prefix[h + 1] - a.prefix[h];
+  const int64_t row0 = (int64_t)blockIdx.x * kCopyRows;
+  if (row0 >= seg_len) return;
+  const int64_t seg_off = (int64_t)b * a.T_layer + a.prefix[h];
+  const rsrc_t kp = make_rsrc(a.kept_pos + seg_off, (uint64_t)seg_len * 4);
+  const rsrc_t ko = make_rsrc(static_cast<char*>(a.k_out) + seg_off * RB, (uint64_t)seg_len * RB);
+  const rsrc_t vo = make_rsrc(static_cast<char*>(a.v_out) + seg_off * RB, (uint64_t)seg_len * RB);
+  const rsrc_t ki = make_rsrc(static_cast<const char*>(a.k) + (int64_t)seg * a.C * RB, (uint64_t)a.C * RB);
+  const rsrc_t vi = make_rsrc(static_cast<const char*>(a.v) + (int64_t)seg * a.C * RB, (uint64_t)a.C * RB);
+  u32x4 kx[PER], vx[PER];
+  uint32_t dst[PER];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int x = threadIdx.x + u * kBlock;
+    const int r = x / V16, c16 = x % V16;
+    const int64_t row = row0 + r;  // rows past the segment read position 0 and store out of range
+    const uint32_t pos = ld32(kp, (uint32_t)(row * 4));
+    const uint32_t src = pos * RB + c16 * 16;
+    dst[u] = (uint32_t)(row * RB + c16 * 16);
+    kx[u] = ld128(ki, src);
+    vx[u] = ld128(vi, src);
+  }
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    st128(ko, dst[u], kx[u]);
+    st128(vo, dst[u], vx[u]);
+  }
 }
 
 hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t st) {
@@ -313,12 +329,18 @@ hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t st
     SGDKV_LAUNCH("radix_digit", radix_digit_kernel<3>, dim3(nseg), blk, st, a);
   }
   SGDKV_LAUNCH("sel_count", sel_count_kernel, dim3(a.n_sel_chunks, nseg), blk, st, a);
-  const int rb = a.D * (a.dtype == 1 ? 2 : 4);
-  switch (rb) {
-    case 128: launch_gather<128>(a, st); break;
-    case 256: launch_gather<256>(a, st); break;
-    case 512: launch_gather<512>(a, st); break;
-    default: return hipErrorInvalidValue;
+  SGDKV_LAUNCH("compact", compact_kernel, dim3(a.n_sel_chunks, nseg), blk, st, a);
+  int64_t longest = 0;
+  for (int hh = 0; hh < a.Hkv; ++hh) longest = std::max<int64_t>(longest, a.prefix[hh + 1] - a.prefix[hh]);
+  const unsigned copy_blocks = (unsigned)((longest + kCopyRows - 1) / kCopyRows);
+  if (copy_blocks > 0) {
+    const int rb = a.D * (a.dtype == 1 ? 2 : 4);
+    switch (rb) {
+      case 128: SGDKV_LAUNCH("gather", copy_rows_kernel<128>, dim3(copy_blocks, nseg), blk, st, a); break;
+      case 256: SGDKV_LAUNCH("gather", copy_rows_kernel<256>, dim3(copy_blocks, nseg), blk, st, a); break;
+      case 512: SGDKV_LAUNCH("gather", copy_rows_kernel<512>, dim3(copy_blocks, nseg), blk, st, a); break;
+      default: return hipErrorInvalidValue;
+    }
   }
   return hipGetLastError();
 }
