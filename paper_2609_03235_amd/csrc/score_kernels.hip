@@ -43,13 +43,13 @@ struct TileGeom {
   static constexpr int V16 = RB / 16;         // 16-byte vectors per row
 };
 
-// K tile staging: keys [tile0, tile0+64) of this head travel global -> registers
+// K tile staging: keys [tile0, tile0+TILE) of this head travel global -> registers
 // (issued one tile ahead) -> LDS. Keys past the end of the head read as zeros.
-template <typename T, int D>
+template <typename T, int D, int TILE>
 struct KeyStage {
   using G = TileGeom<T, D>;
-  static constexpr int N = (kScoreTile * G::V16) / kScoreBlock;  // 16-byte vectors per thread
-  static_assert(N >= 1 && (kScoreTile * G::V16) % kScoreBlock == 0, "tile must split evenly");
+  static constexpr int N = (TILE * G::V16) / kScoreBlock;  // 16-byte vectors per thread
+  static_assert(N >= 1 && (TILE * G::V16) % kScoreBlock == 0, "tile must split evenly");
   u32x4 r[N];
   __device__ __forceinline__ void load(rsrc_t kr, int64_t tile0) {
 #pragma unroll
@@ -87,7 +87,7 @@ __device__ __forceinline__ void load_group_queries(const CompressArgs& a, int b,
 
 // Per-tile compute -----------------------------------------------------------
 //
-// A 64-key tile is four 16-key subtiles, processed as one branch-free rolling
+// A tile of 16-key subtiles (64 keys for pass 2, 128 for pass 1) is one branch-free rolling
 // pipeline: while subtile t's logits go through the vector ALU (one fma, one
 // exp2, one add per logit), the MFMAs of subtile t+1 run on the matrix core and
 // the key fragments of subtile t+2 are read from LDS. The MFMAs of each
@@ -109,12 +109,12 @@ __device__ __forceinline__ void subtile_frags(const char* ktile, int t, int lr, 
     kb[c] = lds_frag<T>(ktile, (uint32_t)((16 * t + lr) * G::LDS_STRIDE + (32 * c + 8 * lg) * G::EB));
 }
 
-// Runs op(t, acc_of_subtile_t) for the four subtiles of the staged tile.
-template <typename T, int D, int NB, typename Op>
+// Runs op(t, acc_of_subtile_t) for the TILE/16 subtiles of the staged tile.
+template <typename T, int D, int NB, int TILE, typename Op>
 __device__ __forceinline__ void tile_pipeline(const char* ktile, int lr, int lg,
                                               const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], Op&& op) {
   constexpr int NBX = NB > 0 ? NB : 1;
-  constexpr int NT = kScoreTile / 16;
+  constexpr int NT = TILE / 16;
   Frag<T> kb[2][D / 32];
   f32x4 acc[2][NBX];
   subtile_frags<T, D>(ktile, 0, lr, lg, kb[0]);
@@ -147,15 +147,15 @@ __device__ __forceinline__ void tile_pipeline(const char* ktile, int lr, int lg,
 // exact online update (two exp2 per logit, m = running max). This happens on
 // the first tile of a chunk, on tiles of the causal window block, and after
 // rare large jumps. Padded rows (past R) start at m = 0 and are never stored.
-template <typename T, int D, int NB>
+template <typename T, int D, int NB, int TILE>
 __device__ __forceinline__ void lse_exact_tile(const char* ktile, int lr, int lg, int wid, int w, int64_t tile0,
                                                int64_t vis0, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
                                                float c2, float (&m)[NB > 0 ? NB : 1][4],
                                                float (&s)[NB > 0 ? NB : 1][4]) {
   constexpr int NBX = NB > 0 ? NB : 1;
-  const bool masked = tile0 + kScoreTile > vis0;
+  const bool masked = tile0 + TILE > vis0;
 #pragma unroll 1
-  for (int t = 0; t < kScoreTile / 16; ++t) {
+  for (int t = 0; t < TILE / 16; ++t) {
     Frag<T> kb[D / 32];
     subtile_frags<T, D>(ktile, t, lr, lg, kb);
     f32x4 acc[NBX];
@@ -177,28 +177,25 @@ __device__ __forceinline__ void lse_exact_tile(const char* ktile, int lr, int lg
   }
 }
 
-template <typename T, int D, int NB>
+template <typename T, int D, int NB, int TILE>
 __device__ __forceinline__ void lse_tile(const char* ktile, int lr, int lg, int wid, int w, int64_t tile0,
                                          int64_t vis0, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], float c2,
                                          float (&m)[NB > 0 ? NB : 1][4], float (&s)[NB > 0 ? NB : 1][4]) {
   constexpr int NBX = NB > 0 ? NB : 1;
-  if (tile0 + kScoreTile > vis0) {  // uniform: the tile reaches the causal window block
-    lse_exact_tile<T, D, NB>(ktile, lr, lg, wid, w, tile0, vis0, qa, c2, m, s);
+  if (tile0 + TILE > vis0) {  // uniform: the tile reaches the causal window block
+    lse_exact_tile<T, D, NB, TILE>(ktile, lr, lg, wid, w, tile0, vis0, qa, c2, m, s);
     return;
   }
-  float s0[NBX][4], nm[NBX][4];
+  float s0[NBX][4];
 #pragma unroll
   for (int j = 0; j < NBX; ++j)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      s0[j][i] = s[j][i];
-      nm[j][i] = -m[j][i];
-    }
-  tile_pipeline<T, D, NB>(ktile, lr, lg, qa, [&](int, const f32x4(&acc)[NBX]) {
+    for (int i = 0; i < 4; ++i) s0[j][i] = s[j][i];
+  tile_pipeline<T, D, NB, TILE>(ktile, lr, lg, qa, [&](int, const f32x4(&acc)[NBX]) {
 #pragma unroll
     for (int j = 0; j < NB; ++j)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) s[j][i] += fast_exp2(fmaf(acc[j][i], c2, nm[j][i]));
+      for (int i = 0; i < 4; ++i) s[j][i] += fast_exp2(fmaf(acc[j][i], c2, -m[j][i]));
   });
   bool bad = false;
 #pragma unroll
@@ -210,7 +207,7 @@ __device__ __forceinline__ void lse_tile(const char* ktile, int lr, int lg, int 
     for (int j = 0; j < NBX; ++j)
 #pragma unroll
       for (int i = 0; i < 4; ++i) s[j][i] = s0[j][i];
-    lse_exact_tile<T, D, NB>(ktile, lr, lg, wid, w, tile0, vis0, qa, c2, m, s);
+    lse_exact_tile<T, D, NB, TILE>(ktile, lr, lg, wid, w, tile0, vis0, qa, c2, m, s);
   }
 }
 
@@ -231,14 +228,14 @@ __device__ void lse_chunk(const CompressArgs& a, char* ktile, int seg, int wid, 
       s[j][i] = 0.f;
     }
   const float c2 = a.c2;
-  KeyStage<T, D> stage;
+  KeyStage<T, D, kLseTile> stage;
   stage.load(kr, key0);
-  for (int64_t tile0 = key0; tile0 < key_end; tile0 += kScoreTile) {
+  for (int64_t tile0 = key0; tile0 < key_end; tile0 += kLseTile) {
     __syncthreads();
     stage.store(ktile);
     __syncthreads();
-    if (tile0 + kScoreTile < key_end) stage.load(kr, tile0 + kScoreTile);
-    lse_tile<T, D, NB>(ktile, lr, lg, wid, a.w, tile0, vis0, qa, c2, m, s);
+    if (tile0 + kLseTile < key_end) stage.load(kr, tile0 + kLseTile);
+    lse_tile<T, D, NB, kLseTile>(ktile, lr, lg, wid, a.w, tile0, vis0, qa, c2, m, s);
   }
   // Combine the 16 lanes (keys) of each row, then store (m, s) for the row.
   const int chunk = blockIdx.x;
@@ -270,7 +267,7 @@ __device__ void lse_chunk(const CompressArgs& a, char* ktile, int seg, int wid, 
 template <typename T, int D, int RBW>
 __global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
   using G = TileGeom<T, D>;
-  __shared__ __attribute__((aligned(16))) char ktile[kScoreTile * G::LDS_STRIDE];
+  __shared__ __attribute__((aligned(16))) char ktile[kLseTile * G::LDS_STRIDE];
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
   const int64_t key0 = (int64_t)blockIdx.x * a.score_chunk;
@@ -327,7 +324,7 @@ __global__ __launch_bounds__(kBlock) void lse_merge_kernel(CompressArgs a) {
 
 // Pass 2: window-summed probabilities of every scored key --------------------
 template <typename T, int D, int NB>
-__device__ void colsum_chunk(const CompressArgs& a, char* ktile, float (*red)[kScoreTile], int seg, int wid,
+__device__ void colsum_chunk(const CompressArgs& a, char* ktile, float (*red)[kColTile], int seg, int wid,
                              int lane, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], const rsrc_t& kr,
                              int64_t key0, int64_t key_end) {
   constexpr int NBX = NB > 0 ? NB : 1;
@@ -350,25 +347,27 @@ __device__ void colsum_chunk(const CompressArgs& a, char* ktile, float (*red)[kS
   const float c2 = a.c2;
   const rsrc_t cr = make_rsrc(a.colsum + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
 
-  KeyStage<T, D> stage;
+  KeyStage<T, D, kColTile> stage;
   stage.load(kr, key0);
-  for (int64_t tile0 = key0; tile0 < key_end; tile0 += kScoreTile) {
+  for (int64_t tile0 = key0; tile0 < key_end; tile0 += kColTile) {
     __syncthreads();
     stage.store(ktile);
     __syncthreads();
-    if (tile0 + kScoreTile < key_end) stage.load(kr, tile0 + kScoreTile);
-    tile_pipeline<T, D, NB>(ktile, lr, lg, qa, [&](int t, const f32x4(&acc)[NBX]) {
-      float p = 0.f;
+    if (tile0 + kColTile < key_end) stage.load(kr, tile0 + kColTile);
+    tile_pipeline<T, D, NB, kColTile>(ktile, lr, lg, qa, [&](int t, const f32x4(&acc)[NBX]) {
+      // four independent partial sums (one per row slot) keep the add chains short
+      float pp[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int j = 0; j < NB; ++j)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) p += fast_exp2(fmaf(acc[j][i], c2, nlse[j][i]));
+        for (int i = 0; i < 4; ++i) pp[i] += fast_exp2(fmaf(acc[j][i], c2, nlse[j][i]));
+      float p = (pp[0] + pp[1]) + (pp[2] + pp[3]);
       p += __shfl_xor(p, 16, 64);
       p += __shfl_xor(p, 32, 64);
       red[wid][16 * t + lr] = p;  // all four lane groups hold the same value
     });
     __syncthreads();
-    if (tid < kScoreTile) {
+    if (tid < kColTile) {
       const int64_t key = tile0 + tid;
       if (key < key_end) {
         float v = red[0][tid];
@@ -383,8 +382,8 @@ __device__ void colsum_chunk(const CompressArgs& a, char* ktile, float (*red)[kS
 template <typename T, int D, int RBW>
 __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) {
   using G = TileGeom<T, D>;
-  __shared__ __attribute__((aligned(16))) char ktile[kScoreTile * G::LDS_STRIDE];
-  __shared__ float red[kScoreWaves][kScoreTile];
+  __shared__ __attribute__((aligned(16))) char ktile[kColTile * G::LDS_STRIDE];
+  __shared__ float red[kScoreWaves][kColTile];
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
   const int64_t key0 = (int64_t)blockIdx.x * a.score_chunk;

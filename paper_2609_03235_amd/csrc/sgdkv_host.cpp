@@ -327,7 +327,9 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, CompressPlan& p) {
   // score workgroups: about 2048 in total; a chunk is a whole number of key tiles, so no
   // tile of pass 1 reaches into the next chunk (which would count those keys twice)
   a.score_chunk = std::min<int64_t>(
-      std::max<int64_t>(round_up(ceil_div(nseg * a.C, 2048), sgdkv::kScoreTile), 4 * sgdkv::kScoreTile), 1 << 16);
+      std::max<int64_t>(round_up(ceil_div(nseg * a.C, 2048), sgdkv::kScoreChunkQuantum),
+                        2 * sgdkv::kScoreChunkQuantum),
+      1 << 16);
   a.n_lse_chunks = (int)ceil_div(a.C, a.score_chunk);
   a.n_col_chunks = (int)ceil_div(a.n_scored, a.score_chunk);
   // selection workgroups: about 4096 in total

@@ -12,7 +12,9 @@ constexpr int kMaxKvHeads = 64;    // per-head tables travel by value in kernel 
 constexpr int kMaxGroupRows = 512; // G*w rows of one KV head's window queries
 constexpr int kMaxDecodeGroup = 16;
 constexpr int kBlock = 256;        // threads per workgroup in every kernel
-constexpr int kScoreTile = 64;     // keys staged in LDS per step of the score kernels
+constexpr int kLseTile = 128;      // keys staged in LDS per step of score pass 1
+constexpr int kColTile = 64;       // keys staged in LDS per step of score pass 2
+constexpr int kScoreChunkQuantum = 128;  // score chunks are whole tiles of both passes
 #ifndef SGDKV_SCORE_WAVES
 #define SGDKV_SCORE_WAVES 8
 #endif
@@ -55,7 +57,7 @@ struct CompressArgs {
   uint32_t* state;  // [B*Hkv][4]: prefix, mask, rows still to place, unused
   uint32_t* counts; // [B*Hkv][n_sel_chunks][4]: fixed, greater, equal, unused
   // chunking
-  int64_t score_chunk;  // keys per score workgroup (multiple of kScoreTile)
+  int64_t score_chunk;  // keys per score workgroup (multiple of kScoreChunkQuantum)
   int n_lse_chunks;     // ceil(C / score_chunk)
   int n_col_chunks;     // ceil(n_scored / score_chunk)
   int64_t sel_chunk;    // positions per selection workgroup
