@@ -17,10 +17,10 @@
 //
 // Work split: workgroup = 8 waves; wave v holds row blocks v, v+8, v+16, ...
 // (16 rows each) as MFMA A-fragments in registers, so a SIMD (waves v and
-// v+4) covers a quarter of the rows. Each 64-key tile of K is staged once in
-// LDS (the next tile is already in flight in registers) and read by all eight
-// waves as B-fragments; blocks past the last row are skipped. MFMA
-// 16x16x32 bf16 (or 8 x 16x16x4 f32 for fp32 inputs) accumulates in fp32.
+// v+4) covers a quarter of the rows. Each key tile (128 keys in pass 1, 64 in
+// pass 2) is staged once in LDS and read by all eight waves as B-fragments;
+// blocks past the last row are skipped. MFMA 16x16x32 bf16 (or 8 x 16x16x4
+// f32 for fp32 inputs) accumulates in fp32.
 // Output layout of a 16x16 MFMA: lane l holds rows 4*(l/16)+0..3 of key
 // column l%16.
 #include "device_common.h"
@@ -85,13 +85,20 @@ __device__ __forceinline__ void load_group_queries(const CompressArgs& a, int b,
   }
 }
 
-// Per-tile compute -----------------------------------------------------------
+// Chunk pipeline --------------------------------------------------------------
 //
-// A tile of 16-key subtiles (64 keys for pass 2, 128 for pass 1) is one branch-free rolling
-// pipeline: while subtile t's logits go through the vector ALU (one fma, one
-// exp2, one add per logit), the MFMAs of subtile t+1 run on the matrix core and
-// the key fragments of subtile t+2 are read from LDS. The MFMAs of each
-// subtile are independent accumulator chains, one per row block.
+// A workgroup streams the key tiles of its chunk through two LDS buffers and
+// the MFMAs as one rolling pipeline. In step s of tile t a wave issues the
+// MFMAs of the next subtile (16 keys), reads the key fragments of the subtile
+// after that from LDS, and hands the logits of subtile s to the vector ALU.
+// Tile t+1 goes into the other buffer at the start of tile t (its global loads
+// were issued one tile earlier), and the tile's single barrier, two subtiles
+// before its end, makes that buffer readable; the buffer written at the start
+// of tile t was last read before the barrier of tile t-1. The MFMAs of the
+// subtile after the chunk's last one run on whatever keys follow (zeros past
+// the head) and are discarded. On gfx950 MFMA and vector instructions of one
+// SIMD issue one after the other, so the two waves of a SIMD hide each
+// other's latencies rather than overlapping the two units.
 template <typename T, int D, int NB>
 __device__ __forceinline__ void subtile_mfma(const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
                                              const Frag<T> (&kb)[D / 32], f32x4 (&acc)[NB > 0 ? NB : 1]) {
@@ -109,55 +116,83 @@ __device__ __forceinline__ void subtile_frags(const char* ktile, int t, int lr, 
     kb[c] = lds_frag<T>(ktile, (uint32_t)((16 * t + lr) * G::LDS_STRIDE + (32 * c + 8 * lg) * G::EB));
 }
 
-// Runs op(t, acc_of_subtile_t) for the TILE/16 subtiles of the staged tile.
-template <typename T, int D, int NB, int TILE, typename Op>
-__device__ __forceinline__ void tile_pipeline(const char* ktile, int lr, int lg,
-                                              const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], Op&& op) {
+// Hooks: begin(acc) once with the logits of the chunk's first subtile (before
+// any sub call); sub(t, s, acc) per subtile; at_barrier(t) right after tile t's
+// barrier; end_tile(t) after tile t's last subtile.
+template <typename T, int D, int NB, int TILE, typename Begin, typename Sub, typename AtBarrier, typename EndTile>
+__device__ __forceinline__ void chunk_pipeline(char* kbuf, const rsrc_t& kr, int64_t key0, int64_t C, int64_t ntiles,
+                                               int lr, int lg, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
+                                               Begin&& begin, Sub&& sub, AtBarrier&& at_barrier, EndTile&& end_tile) {
+  using G = TileGeom<T, D>;
   constexpr int NBX = NB > 0 ? NB : 1;
-  constexpr int NT = TILE / 16;
+  constexpr int S = TILE / 16;
+  constexpr int BUF = TILE * G::LDS_STRIDE;
+  static_assert(S >= 4 && S % 2 == 0, "tile geometry");
+  // keys past the head read as zeros; the clamp keeps byte offsets below 4 GiB
+  auto tile_key = [&](int64_t t) {
+    const int64_t k = key0 + t * TILE;
+    return k < C ? k : C;
+  };
+  KeyStage<T, D, TILE> stage;
+  stage.load(kr, tile_key(0));
+  stage.store(kbuf);
+  stage.load(kr, tile_key(1));
+  __syncthreads();
   Frag<T> kb[2][D / 32];
   f32x4 acc[2][NBX];
-  subtile_frags<T, D>(ktile, 0, lr, lg, kb[0]);
-  subtile_frags<T, D>(ktile, 1, lr, lg, kb[1]);
+  subtile_frags<T, D>(kbuf, 0, lr, lg, kb[0]);
+  subtile_frags<T, D>(kbuf, 1, lr, lg, kb[1]);
   subtile_mfma<T, D, NB>(qa, kb[0], acc[0]);
+  begin(acc[0]);
+  for (int64_t t = 0; t < ntiles; ++t) {
+    const char* buf = kbuf + (t & 1) * BUF;
+    char* nbuf = kbuf + ((t + 1) & 1) * BUF;
 #pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    if (t + 1 < NT) subtile_mfma<T, D, NB>(qa, kb[(t + 1) & 1], acc[(t + 1) & 1]);
-    if (t + 2 < NT) subtile_frags<T, D>(ktile, t + 2, lr, lg, kb[t & 1]);
-    op(t, acc[t & 1]);
-  }
-  // schedule: subtile 0's MFMAs, then the later MFMAs spread one per 3 vector instructions
-#pragma unroll
-  for (int i = 0; i < NB * (D / 32); ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-#pragma unroll
-  for (int i = 0; i < (NT - 1) * NB * (D / 32); ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+    for (int s = 0; s < S; ++s) {
+      if (s == 0) {
+        stage.store(nbuf);
+        stage.load(kr, tile_key(t + 2));
+      }
+      if (s == S - 2) {
+        __syncthreads();
+        at_barrier(t);
+      }
+      subtile_mfma<T, D, NB>(qa, kb[(s + 1) & 1], acc[(s + 1) & 1]);
+      if (s + 2 < S)
+        subtile_frags<T, D>(buf, s + 2, lr, lg, kb[s & 1]);
+      else
+        subtile_frags<T, D>(nbuf, s + 2 - S, lr, lg, kb[s & 1]);
+      sub(t, s, acc[s & 1]);
+    }
+    end_tile(t);
   }
 }
 
 // Pass 1: per-chunk partial log-sum-exp of every window row -------------------
 //
 // Each lane keeps, for each of its 4*NB row slots, a reference m and a sum
-// s = sum 2^(y - m) over the keys it has seen (y = logit * log2 e). Within a
-// tile m is fixed, so each logit costs one fma, one exp2 and one add. After
-// the tile, if any slot's sum left [0, 2^96] (a logit more than ~96 above its
-// reference, +inf, or the +inf that m = -inf produces on a slot's first
-// tile), the tile is redone for the whole wave from the saved sums with the
-// exact online update (two exp2 per logit, m = running max). This happens on
-// the first tile of a chunk, on tiles of the causal window block, and after
-// rare large jumps. Padded rows (past R) start at m = 0 and are never stored.
+// s = sum 2^(y - m) over the keys it has seen (y = logit * log2 e). m is fixed
+// within a tile, so each logit costs one fma, one exp2 and one add; it starts
+// at the lane's own logit of the chunk's first key. After each tile, if any
+// slot's sum left [0, 2^96] (a logit more than ~96 above its reference, or
+// inf/NaN), and on every tile that reaches the causal window block, the wave
+// restores the sums and redoes the tile with the exact online update (two
+// exp2 per logit, m = running max), reading the keys from global memory so
+// that the LDS buffers are free to move on. Padded rows (past R) keep m = 0.
 template <typename T, int D, int NB, int TILE>
-__device__ __forceinline__ void lse_exact_tile(const char* ktile, int lr, int lg, int wid, int w, int64_t tile0,
-                                               int64_t vis0, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
-                                               float c2, float (&m)[NB > 0 ? NB : 1][4],
-                                               float (&s)[NB > 0 ? NB : 1][4]) {
+__device__ __forceinline__ void lse_exact_tile(const rsrc_t& kr, int lr, int lg, int wid, int w, int64_t tile0,
+                                            int64_t vis0, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
+                                            float c2, float (&m)[NB > 0 ? NB : 1][4],
+                                            float (&s)[NB > 0 ? NB : 1][4]) {
+  using G = TileGeom<T, D>;
   constexpr int NBX = NB > 0 ? NB : 1;
   const bool masked = tile0 + TILE > vis0;
 #pragma unroll 1
   for (int t = 0; t < TILE / 16; ++t) {
     Frag<T> kb[D / 32];
-    subtile_frags<T, D>(ktile, t, lr, lg, kb);
+#pragma unroll
+    for (int c = 0; c < G::NC; ++c)
+      kb[c] = gload_frag<T>(kr, (uint32_t)((tile0 + 16 * t + lr) * G::RB + (32 * c + 8 * lg) * G::EB));
     f32x4 acc[NBX];
     subtile_mfma<T, D, NB>(qa, kb, acc);
     const int64_t dk64 = tile0 + 16 * t + lr - vis0;
@@ -177,66 +212,65 @@ __device__ __forceinline__ void lse_exact_tile(const char* ktile, int lr, int lg
   }
 }
 
-template <typename T, int D, int NB, int TILE>
-__device__ __forceinline__ void lse_tile(const char* ktile, int lr, int lg, int wid, int w, int64_t tile0,
-                                         int64_t vis0, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], float c2,
-                                         float (&m)[NB > 0 ? NB : 1][4], float (&s)[NB > 0 ? NB : 1][4]) {
-  constexpr int NBX = NB > 0 ? NB : 1;
-  if (tile0 + TILE > vis0) {  // uniform: the tile reaches the causal window block
-    lse_exact_tile<T, D, NB, TILE>(ktile, lr, lg, wid, w, tile0, vis0, qa, c2, m, s);
-    return;
-  }
-  float s0[NBX][4];
-#pragma unroll
-  for (int j = 0; j < NBX; ++j)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) s0[j][i] = s[j][i];
-  tile_pipeline<T, D, NB, TILE>(ktile, lr, lg, qa, [&](int, const f32x4(&acc)[NBX]) {
-#pragma unroll
-    for (int j = 0; j < NB; ++j)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) s[j][i] += fast_exp2(fmaf(acc[j][i], c2, -m[j][i]));
-  });
-  bool bad = false;
-#pragma unroll
-  for (int j = 0; j < NB; ++j)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) bad |= !(s[j][i] <= 7.9228162514264338e28f);  // 2^96; catches inf and NaN
-  if (__any(bad)) {
-#pragma unroll
-    for (int j = 0; j < NBX; ++j)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) s[j][i] = s0[j][i];
-    lse_exact_tile<T, D, NB, TILE>(ktile, lr, lg, wid, w, tile0, vis0, qa, c2, m, s);
-  }
-}
-
 template <typename T, int D, int NB>
-__device__ void lse_chunk(const CompressArgs& a, char* ktile, int seg, int wid, int lane,
+__device__ void lse_chunk(const CompressArgs& a, char* kbuf, int seg, int wid, int lane,
                           const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], const rsrc_t& kr, int64_t key0,
                           int64_t key_end) {
   constexpr int NBX = NB > 0 ? NB : 1;
+  constexpr int TILE = kLseTile;
   const int lr = lane & 15, lg = lane >> 4;
   const int64_t vis0 = a.C - a.w;  // the row with window index i sees key j iff j - vis0 <= i
-  float m[NBX][4], s[NBX][4];
+  const float c2 = a.c2;
+  float m[NBX][4], s[NBX][4], s0[NBX][4];
+  bool real[NBX][4];
 #pragma unroll
   for (int j = 0; j < NBX; ++j)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int row = (wid + kScoreWaves * j) * 16 + 4 * lg + i;
-      m[j][i] = row < a.R ? -INFINITY : 0.f;  // a padded row must not force the exact path
+      real[j][i] = (wid + kScoreWaves * j) * 16 + 4 * lg + i < a.R;
+      m[j][i] = real[j][i] ? -INFINITY : 0.f;  // a padded row must not force the exact path
       s[j][i] = 0.f;
     }
-  const float c2 = a.c2;
-  KeyStage<T, D, kLseTile> stage;
-  stage.load(kr, key0);
-  for (int64_t tile0 = key0; tile0 < key_end; tile0 += kLseTile) {
-    __syncthreads();
-    stage.store(ktile);
-    __syncthreads();
-    if (tile0 + kLseTile < key_end) stage.load(kr, tile0 + kLseTile);
-    lse_tile<T, D, NB, kLseTile>(ktile, lr, lg, wid, a.w, tile0, vis0, qa, c2, m, s);
-  }
+  const int64_t ntiles = (key_end - key0 + TILE - 1) / TILE;
+  chunk_pipeline<T, D, NB, TILE>(
+      kbuf, kr, key0, a.C, ntiles, lr, lg, qa,
+      [&](const f32x4(&acc)[NBX]) {
+        if (key0 + TILE <= vis0) {  // uniform: every row sees every key of the first tile
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (real[j][i]) m[j][i] = acc[j][i] * c2;
+        }
+      },
+      [&](int64_t, int sub, const f32x4(&acc)[NBX]) {
+        if (sub == 0) {
+#pragma unroll
+          for (int j = 0; j < NBX; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) s0[j][i] = s[j][i];
+        }
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) s[j][i] += fast_exp2(fmaf(acc[j][i], c2, -m[j][i]));
+      },
+      [&](int64_t) {},
+      [&](int64_t t) {
+        const int64_t tile0 = key0 + t * TILE;
+        bool bad = tile0 + TILE > vis0;
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) bad |= !(s[j][i] <= 7.9228162514264338e28f);  // 2^96; catches inf and NaN
+        if (__any(bad)) {
+#pragma unroll
+          for (int j = 0; j < NBX; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) s[j][i] = s0[j][i];
+          lse_exact_tile<T, D, NB, TILE>(kr, lr, lg, wid, a.w, tile0, vis0, qa, c2, m, s);
+        }
+      });
   // Combine the 16 lanes (keys) of each row, then store (m, s) for the row.
   const int chunk = blockIdx.x;
   float* part = a.lse_part + ((int64_t)seg * a.n_lse_chunks + chunk) * a.R * 2;
@@ -267,7 +301,7 @@ __device__ void lse_chunk(const CompressArgs& a, char* ktile, int seg, int wid, 
 template <typename T, int D, int RBW>
 __global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
   using G = TileGeom<T, D>;
-  __shared__ __attribute__((aligned(16))) char ktile[kLseTile * G::LDS_STRIDE];
+  __shared__ __attribute__((aligned(16))) char ktile[2 * kLseTile * G::LDS_STRIDE];
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
   const int64_t key0 = (int64_t)blockIdx.x * a.score_chunk;
@@ -324,11 +358,11 @@ __global__ __launch_bounds__(kBlock) void lse_merge_kernel(CompressArgs a) {
 
 // Pass 2: window-summed probabilities of every scored key --------------------
 template <typename T, int D, int NB>
-__device__ void colsum_chunk(const CompressArgs& a, char* ktile, float (*red)[kColTile], int seg, int wid,
-                             int lane, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], const rsrc_t& kr,
-                             int64_t key0, int64_t key_end) {
+__device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float (*red)[kScoreWaves][kColTile], int seg,
+                             int wid, int lane, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
+                             const rsrc_t& kr, int64_t key0, int64_t key_end) {
   constexpr int NBX = NB > 0 ? NB : 1;
-  const int tid = threadIdx.x;
+  constexpr int TILE = kColTile;
   const int lr = lane & 15, lg = lane >> 4;
   // -lse2 of this lane's row slots; rows past R get -inf so they add exp2(-inf) = 0
   const uint64_t nl = (uint64_t)a.B * a.Hkv * a.R;
@@ -346,44 +380,50 @@ __device__ void colsum_chunk(const CompressArgs& a, char* ktile, float (*red)[kC
     }
   const float c2 = a.c2;
   const rsrc_t cr = make_rsrc(a.colsum + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
-
-  KeyStage<T, D, kColTile> stage;
-  stage.load(kr, key0);
-  for (int64_t tile0 = key0; tile0 < key_end; tile0 += kColTile) {
-    __syncthreads();
-    stage.store(ktile);
-    __syncthreads();
-    if (tile0 + kColTile < key_end) stage.load(kr, tile0 + kColTile);
-    tile_pipeline<T, D, NB, kColTile>(ktile, lr, lg, qa, [&](int t, const f32x4(&acc)[NBX]) {
-      // four independent partial sums (one per row slot) keep the add chains short
-      float pp[4] = {0.f, 0.f, 0.f, 0.f};
+  // Partials of tile t sit in red[t % 3]: written during tile t, complete at the barrier of
+  // tile t+1, summed right after it, rewritten only after the barrier of tile t+2. Each
+  // wave sums 8 columns: lane l reads the partial of wave l/8 for column 8*wid + l%8,
+  // three swaps add the eight, and lanes 0-7 store. Branch-free: a store that must not
+  // happen gets an offset past the buffer, which the hardware drops.
+  static_assert(kScoreWaves * 8 == TILE, "reduction layout");
+  const int rcol = 8 * wid + (lane & 7), rwave = lane >> 3;
+  auto reduce = [&](int64_t t) {  // t may be -1: nothing is stored
+    const float(*r)[TILE] = red[(t + 3) % 3];
+    float v = r[rwave][rcol];
+    v += __shfl_xor(v, 8, 64);
+    v = sum_lane_groups(v);
+    const int64_t key = key0 + t * TILE + rcol;
+    const bool store = t >= 0 && lane < 8 && key < key_end;
+    stf(cr, store ? (uint32_t)(key * 4) : (uint32_t)(a.n_scored * 4), v * a.inv_G);
+  };
+  const int64_t ntiles = (key_end - key0 + TILE - 1) / TILE;
+  chunk_pipeline<T, D, NB, TILE>(
+      kbuf, kr, key0, a.C, ntiles, lr, lg, qa, [](const f32x4(&)[NBX]) {},
+      [&](int64_t t, int sub, const f32x4(&acc)[NBX]) {
+        float p = 0.f;
+        if constexpr (NB > 0) {
+          // four independent partial sums (one per row slot) keep the add chains short
+          float pp[4];
 #pragma unroll
-      for (int j = 0; j < NB; ++j)
+          for (int i = 0; i < 4; ++i) pp[i] = fast_exp2(fmaf(acc[0][i], c2, nlse[0][i]));
 #pragma unroll
-        for (int i = 0; i < 4; ++i) pp[i] += fast_exp2(fmaf(acc[j][i], c2, nlse[j][i]));
-      float p = (pp[0] + pp[1]) + (pp[2] + pp[3]);
-      p += __shfl_xor(p, 16, 64);
-      p += __shfl_xor(p, 32, 64);
-      red[wid][16 * t + lr] = p;  // all four lane groups hold the same value
-    });
-    __syncthreads();
-    if (tid < kColTile) {
-      const int64_t key = tile0 + tid;
-      if (key < key_end) {
-        float v = red[0][tid];
+          for (int j = 1; j < NB; ++j)
 #pragma unroll
-        for (int u = 1; u < kScoreWaves; ++u) v += red[u][tid];
-        stf(cr, (uint32_t)(key * 4), v * a.inv_G);
-      }
-    }
-  }
+            for (int i = 0; i < 4; ++i) pp[i] += fast_exp2(fmaf(acc[j][i], c2, nlse[j][i]));
+          p = sum_lane_groups((pp[0] + pp[1]) + (pp[2] + pp[3]));
+        }
+        red[t % 3][wid][16 * sub + lr] = p;  // all four lane groups hold the same value
+      },
+      [&](int64_t t) { reduce(t - 1); }, [](int64_t) {});
+  __syncthreads();
+  reduce(ntiles - 1);
 }
 
 template <typename T, int D, int RBW>
 __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) {
   using G = TileGeom<T, D>;
-  __shared__ __attribute__((aligned(16))) char ktile[kColTile * G::LDS_STRIDE];
-  __shared__ float red[kScoreWaves][kColTile];
+  __shared__ __attribute__((aligned(16))) char ktile[2 * kColTile * G::LDS_STRIDE];
+  __shared__ float red[3][kScoreWaves][kColTile];
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
   const int64_t key0 = (int64_t)blockIdx.x * a.score_chunk;

@@ -301,8 +301,10 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, CompressPlan& p) {
                 (long long)d->batch * d->num_kv_heads);
   const int eb = d->dtype == SGDKV_DTYPE_BF16 ? 2 : 4;
   const int64_t rb = (int64_t)d->head_dim * eb;
-  if (d->seq_len * rb > 0xFFFFFFFFll)
-    return fail(SGDKV_ERR_UNSUPPORTED, "one head's keys (%lld bytes) exceed 4 GiB", (long long)(d->seq_len * rb));
+  // kernels address one head's keys, plus a margin of 256 key rows read past its end, in 32 bits
+  if ((d->seq_len + 256) * rb > 0xFFFFFFFFll)
+    return fail(SGDKV_ERR_UNSUPPORTED, "one head's keys (%lld bytes) exceed 4 GiB less 256 rows",
+                (long long)(d->seq_len * rb));
 
   sgdkv::CompressArgs& a = p.a;
   std::memset(&a, 0, sizeof a);
