@@ -48,23 +48,29 @@ struct TileGeom {
 template <typename T, int D, int TILE>
 struct KeyStage {
   using G = TileGeom<T, D>;
-  static constexpr int N = (TILE * G::V16) / kScoreBlock;  // 16-byte vectors per thread
-  static_assert(N >= 1 && (TILE * G::V16) % kScoreBlock == 0, "tile must split evenly");
+  static constexpr int TOT = TILE * G::V16;                        // 16-byte vectors per tile
+  static constexpr int N = (TOT + kScoreBlock - 1) / kScoreBlock;  // per thread
+  static constexpr bool ALL = TOT >= kScoreBlock;                  // every thread moves N vectors
+  static_assert(TOT % kScoreBlock == 0 || !ALL, "tile must split evenly");
   u32x4 r[N];
   __device__ __forceinline__ void load(rsrc_t kr, int64_t tile0) {
+    if (ALL || (int)threadIdx.x < TOT) {
 #pragma unroll
-    for (int u = 0; u < N; ++u) {
-      const int vi = threadIdx.x + u * kScoreBlock;
-      const int row = vi / G::V16, c16 = vi % G::V16;
-      r[u] = ld128(kr, (uint32_t)((tile0 + row) * G::RB + c16 * 16));
+      for (int u = 0; u < N; ++u) {
+        const int vi = threadIdx.x + u * kScoreBlock;
+        const int row = vi / G::V16, c16 = vi % G::V16;
+        r[u] = ld128(kr, (uint32_t)((tile0 + row) * G::RB + c16 * 16));
+      }
     }
   }
   __device__ __forceinline__ void store(char* ktile) const {
+    if (ALL || (int)threadIdx.x < TOT) {
 #pragma unroll
-    for (int u = 0; u < N; ++u) {
-      const int vi = threadIdx.x + u * kScoreBlock;
-      const int row = vi / G::V16, c16 = vi % G::V16;
-      *reinterpret_cast<u32x4*>(ktile + row * G::LDS_STRIDE + c16 * 16) = r[u];
+      for (int u = 0; u < N; ++u) {
+        const int vi = threadIdx.x + u * kScoreBlock;
+        const int row = vi / G::V16, c16 = vi % G::V16;
+        *reinterpret_cast<u32x4*>(ktile + row * G::LDS_STRIDE + c16 * 16) = r[u];
+      }
     }
   }
 };
@@ -382,18 +388,22 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float (*red)[kSc
   const rsrc_t cr = make_rsrc(a.colsum + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
   // Partials of tile t sit in red[t % 3]: written during tile t, complete at the barrier of
   // tile t+1, summed right after it, rewritten only after the barrier of tile t+2. Each
-  // wave sums 8 columns: lane l reads the partial of wave l/8 for column 8*wid + l%8,
-  // three swaps add the eight, and lanes 0-7 store. Branch-free: a store that must not
-  // happen gets an offset past the buffer, which the hardware drops.
-  static_assert(kScoreWaves * 8 == TILE, "reduction layout");
-  const int rcol = 8 * wid + (lane & 7), rwave = lane >> 3;
+  // wave sums CPW columns: the LPC lanes of a column read PPL partials each, shuffles add
+  // them, and the first CPW lanes store. Branch-free: a store that must not happen gets an
+  // offset past the buffer, which the hardware drops.
+  constexpr int CPW = TILE / kScoreWaves, LPC = 64 / CPW, PPL = kScoreWaves / LPC;
+  static_assert(CPW <= 16 && 64 % CPW == 0 && PPL >= 1 && PPL * LPC == kScoreWaves, "reduction layout");
+  const int rcol = CPW * wid + lane % CPW, rgrp = lane / CPW;
   auto reduce = [&](int64_t t) {  // t may be -1: nothing is stored
     const float(*r)[TILE] = red[(t + 3) % 3];
-    float v = r[rwave][rcol];
-    v += __shfl_xor(v, 8, 64);
+    float v = r[rgrp][rcol];
+#pragma unroll
+    for (int k = 1; k < PPL; ++k) v += r[rgrp + LPC * k][rcol];
+#pragma unroll
+    for (int o = CPW; o < 16; o <<= 1) v += __shfl_xor(v, o, 64);
     v = sum_lane_groups(v);
     const int64_t key = key0 + t * TILE + rcol;
-    const bool store = t >= 0 && lane < 8 && key < key_end;
+    const bool store = t >= 0 && lane < CPW && key < key_end;
     stf(cr, store ? (uint32_t)(key * 4) : (uint32_t)(a.n_scored * 4), v * a.inv_G);
   };
   const int64_t ntiles = (key_end - key0 + TILE - 1) / TILE;
