@@ -57,6 +57,18 @@ struct DecodeStep {
 #pragma unroll
       for (int x = 0; x < VW; ++x) vv[u][x] = ld128(vr, (uint32_t)((k0 + kg + KG * u) * RB + col0 * EB + 16 * x));
   }
+  __device__ __forceinline__ void value_row(int u, float (&v)[8]) const {
+    if constexpr (EB == 2) {
+      const u32x4 x = vv[u][0];
+      v[0] = bf16_lo(x.x); v[1] = bf16_hi(x.x); v[2] = bf16_lo(x.y); v[3] = bf16_hi(x.y);
+      v[4] = bf16_lo(x.z); v[5] = bf16_hi(x.z); v[6] = bf16_lo(x.w); v[7] = bf16_hi(x.w);
+    } else {
+      const u32x4 x0 = vv[u][0], x1 = vv[u][VW - 1];
+      v[0] = __uint_as_float(x0.x); v[1] = __uint_as_float(x0.y); v[2] = __uint_as_float(x0.z);
+      v[3] = __uint_as_float(x0.w); v[4] = __uint_as_float(x1.x); v[5] = __uint_as_float(x1.y);
+      v[6] = __uint_as_float(x1.z); v[7] = __uint_as_float(x1.w);
+    }
+  }
 };
 
 __device__ __forceinline__ void wave_sync() {
@@ -66,15 +78,139 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// GM = compile-time bound on the group size (8 or 16). Each wave owns one
-// chunk of a segment: chunk index = 4*blockIdx.x + wave.
-template <typename T, int D, int GM>
+// Maximum over the 16 lanes of a row (lanes 16r .. 16r+15), by DPP rotations.
+__device__ __forceinline__ float row16_max(float x) {
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x128, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x124, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x122, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x121, 0xF, 0xF, false)));
+  return x;
+}
+__device__ __forceinline__ float row16_sum(float x) {
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x128, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x124, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x122, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x121, 0xF, 0xF, false));
+  return x;
+}
+
+// One wave's pass over its chunk. Lane (lr, lg) of the logit MFMA holds key lr
+// of the step for heads 4*lg+i. Every head keeps a reference m (base-2 units)
+// and the lane-local sums s = sum 2^(y - m) and o = sum 2^(y - m) v.
+//   EXACT = false: m is the head's largest logit of the chunk's first step and
+//     stays fixed, so a logit costs one fma and one exp2 and nothing rescales.
+//     The caller checks the result for overflow and then reruns the chunk
+//     with EXACT = true.
+//   EXACT = true: m is the running maximum; s and o are rescaled when it moves.
+// The probabilities of a step reach the P.V lanes through LDS (double
+// buffered by step parity, so one wave-local sync per step orders both the
+// writes before the reads and the reads before the writes two steps later).
+template <typename T, int D, int GM, int PF, bool EXACT>
+__device__ __forceinline__ void decode_chunk(const DecodeArgs& a, float (*pls)[16][16], float (*als)[16],
+                                             const rsrc_t& kr, const rsrc_t& vr, int64_t c0, int64_t c1,
+                                             const Frag<T> (&qa)[D / 32], int lane, float (&m)[4], float (&s)[4],
+                                             float (&o)[GM][8]) {
+  using S = DecodeStep<T, D>;
+  constexpr int KS = 16;
+  constexpr int NBUF = PF + 1;
+  const int lr = lane & 15, lgp = lane >> 4;
+  const int kg = lane / S::LPR, col0 = 8 * (lane % S::LPR);
+  const int G = a.G;
+  const float c2 = a.c2;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    m[i] = -INFINITY;
+    s[i] = 0.f;
+  }
+#pragma unroll
+  for (int g = 0; g < GM; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
+  const int nsteps = (int)((c1 - c0 + KS - 1) / KS);
+  S buf[NBUF];
+#pragma unroll
+  for (int p = 0; p < PF; ++p)
+    if (p < nsteps) buf[p].load(kr, vr, c0 + p * KS, lr, lgp, kg, col0);
+  for (int it0 = 0; it0 < nsteps; it0 += NBUF) {
+#pragma unroll
+    for (int u = 0; u < NBUF; ++u) {
+      const int it = it0 + u;
+      if (it >= nsteps) break;
+      const int64_t k0 = c0 + (int64_t)it * KS;
+      if (it + PF < nsteps) buf[(u + PF) % NBUF].load(kr, vr, k0 + PF * KS, lr, lgp, kg, col0);
+      const S& cur = buf[u];
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < S::NC; ++c) acc = mma(qa[c], cur.kb[c], acc);
+      const bool valid = k0 + lr < c1;
+      float alpha[4] = {1.f, 1.f, 1.f, 1.f};
+      if (EXACT || it == 0) {
+        // running (or first-step) maximum per head over the 16 keys
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float mx = row16_max(valid ? acc[i] * c2 : -INFINITY);
+          const float mn = fmaxf(m[i], mx);
+          if (EXACT) alpha[i] = (m[i] == -INFINITY) ? (mn == -INFINITY ? 1.f : 0.f) : fast_exp2(m[i] - mn);
+          m[i] = mn;
+        }
+      }
+      float p[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        p[i] = (valid && m[i] != -INFINITY) ? fast_exp2(fmaf(acc[i], c2, -m[i])) : 0.f;
+        s[i] = EXACT ? fmaf(s[i], alpha[i], p[i]) : s[i] + p[i];
+      }
+      float(*pw)[16] = pls[it & 1];
+      *reinterpret_cast<f32x4*>(&pw[lr][4 * lgp]) = f32x4{p[0], p[1], p[2], p[3]};
+      bool moved = false;
+      if (EXACT) {
+        if (lr == 0) *reinterpret_cast<f32x4*>(&als[it & 1][4 * lgp]) = f32x4{alpha[0], alpha[1], alpha[2], alpha[3]};
+        moved = __any(alpha[0] != 1.f || alpha[1] != 1.f || alpha[2] != 1.f || alpha[3] != 1.f);
+      }
+      wave_sync();
+      if (EXACT && moved) {
+#pragma unroll
+        for (int g = 0; g < GM; ++g)
+          if (g < G) {
+            const float al = als[it & 1][g];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[g][e] *= al;
+          }
+      }
+      // P.V for this lane's value rows and columns
+#pragma unroll
+      for (int u2 = 0; u2 < S::VPL; ++u2) {
+        const int kk = kg + S::KG * u2;
+        float v[8];
+        cur.value_row(u2, v);
+        float pk[GM];
+#pragma unroll
+        for (int g4 = 0; g4 < GM; g4 += 4) {
+          const f32x4 q4 = *reinterpret_cast<const f32x4*>(&pw[kk][g4]);
+          pk[g4] = q4[0];
+          if (g4 + 1 < GM) pk[g4 + 1] = q4[1];
+          if (g4 + 2 < GM) pk[g4 + 2] = q4[2];
+          if (g4 + 3 < GM) pk[g4 + 3] = q4[3];
+        }
+#pragma unroll
+        for (int g = 0; g < GM; ++g)
+          if (g < G) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[g][e] = fmaf(pk[g], v[e], o[g][e]);
+          }
+      }
+    }
+  }
+}
+
+// GM = compile-time bound on the group size (8 or 16); PF = steps of K/V in
+// flight ahead of the one being computed. Each wave owns one chunk of a
+// segment: chunk index = 4*blockIdx.x + wave.
+template <typename T, int D, int GM, int PF>
 __global__ __launch_bounds__(kBlock, 2) void decode_split_kernel(DecodeArgs a) {
   using S = DecodeStep<T, D>;
-  constexpr int KS = 16;  // keys per step
-  __shared__ float lgs[kWaves][16][KS];  // logits (base-2 units), per wave
-  __shared__ float pls[kWaves][16][KS];  // probabilities, per wave
-  __shared__ float als[kWaves][16];      // per-head rescale factor of the step, per wave
+  __shared__ __attribute__((aligned(16))) float pls[kWaves][2][16][16];  // probabilities [key][head]
+  __shared__ __attribute__((aligned(16))) float als[kWaves][2][16];      // per-head rescale (exact pass)
 
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
@@ -97,97 +233,22 @@ __global__ __launch_bounds__(kBlock, 2) void decode_split_kernel(DecodeArgs a) {
 #pragma unroll
   for (int c = 0; c < S::NC; ++c) qa[c] = gload_frag<T>(qr, (uint32_t)(lr * S::RB + (32 * c + 8 * lgp) * S::EB));
 
-  const int sh_head = lane >> 2, sh_part = lane & 3;  // softmax: head lane/4, keys 4*(lane%4)..+3
-  const int kg = lane / S::LPR, col0 = 8 * (lane % S::LPR);
-  float m_run = -INFINITY, s_run = 0.f;
-  float o[GM][8];
+  float m[4], s[4], o[GM][8];
+  decode_chunk<T, D, GM, PF, false>(a, pls[wid], als[wid], kr, vr, c0, c1, qa, lane, m, s, o);
+  // 2^64 bounds every probability, so s and o stay finite unless V is huge or the
+  // first step's maximum sat far below a later logit: then redo with rescaling
+  bool bad = false;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) bad |= !(s[i] <= 1.8446744073709552e19f);
 #pragma unroll
   for (int g = 0; g < GM; ++g)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
+    for (int e = 0; e < 8; ++e) bad |= !(fabsf(o[g][e]) < INFINITY);
+  if (__any(bad)) decode_chunk<T, D, GM, PF, true>(a, pls[wid], als[wid], kr, vr, c0, c1, qa, lane, m, s, o);
 
-  const int nsteps = (int)((c1 - c0 + KS - 1) / KS);
-  S cur, nxt;
-  cur.load(kr, vr, c0, lr, lgp, kg, col0);
-  for (int it = 0; it < nsteps; ++it) {
-    const int64_t k0 = c0 + (int64_t)it * KS;
-    if (it + 1 < nsteps) nxt.load(kr, vr, k0 + KS, lr, lgp, kg, col0);
-    // 1. logits of the (padded) 16 heads against 16 keys
-    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  // Reduce within the wave: the 16 lanes of each head's sum, the KG key groups of o.
 #pragma unroll
-    for (int c = 0; c < S::NC; ++c) acc = mma(qa[c], cur.kb[c], acc);
-    const bool valid = k0 + lr < c1;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) lgs[wid][4 * lgp + i][lr] = valid ? acc[i] * a.c2 : -INFINITY;
-    wave_sync();
-    // 2. online softmax per head
-    {
-      float y[4];
-      float tmax = -INFINITY;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        y[u] = lgs[wid][sh_head][4 * sh_part + u];
-        tmax = fmaxf(tmax, y[u]);
-      }
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 1, 64));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 2, 64));
-      const float m_new = fmaxf(m_run, tmax);
-      const float alpha = (m_run == -INFINITY) ? (m_new == -INFINITY ? 1.f : 0.f) : fast_exp2(m_run - m_new);
-      float ps = 0.f;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float p = (y[u] == -INFINITY) ? 0.f : fast_exp2(y[u] - m_new);
-        pls[wid][sh_head][4 * sh_part + u] = p;
-        ps += p;
-      }
-      s_run = s_run * alpha + ps;
-      m_run = m_new;
-      if (sh_part == 0) als[wid][sh_head] = alpha;
-      // the accumulators need rescaling only when some head's running max moved
-      const bool moved = __any(alpha != 1.f);
-      wave_sync();
-      if (moved) {
-#pragma unroll
-        for (int g = 0; g < GM; ++g) {
-          if (g < G) {
-            const float al = als[wid][g];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) o[g][e] *= al;
-          }
-        }
-      }
-    }
-    // 3. P.V for this lane's value rows and columns
-#pragma unroll
-    for (int u = 0; u < S::VPL; ++u) {
-      const int kk = kg + S::KG * u;
-      float v[8];
-      if (S::EB == 2) {
-        const u32x4 x = cur.vv[u][0];
-        v[0] = bf16_lo(x.x); v[1] = bf16_hi(x.x); v[2] = bf16_lo(x.y); v[3] = bf16_hi(x.y);
-        v[4] = bf16_lo(x.z); v[5] = bf16_hi(x.z); v[6] = bf16_lo(x.w); v[7] = bf16_hi(x.w);
-      } else {
-        const u32x4 x0 = cur.vv[u][0], x1 = cur.vv[u][S::VW - 1];
-        v[0] = __uint_as_float(x0.x); v[1] = __uint_as_float(x0.y); v[2] = __uint_as_float(x0.z);
-        v[3] = __uint_as_float(x0.w); v[4] = __uint_as_float(x1.x); v[5] = __uint_as_float(x1.y);
-        v[6] = __uint_as_float(x1.z); v[7] = __uint_as_float(x1.w);
-      }
-#pragma unroll
-      for (int g = 0; g < GM; ++g) {
-        if (g < G) {
-          const float p = pls[wid][g][kk];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) o[g][e] = fmaf(p, v[e], o[g][e]);
-        }
-      }
-    }
-    wave_sync();  // this step's LDS values are consumed before the next step overwrites them
-    cur = nxt;
-  }
-
-  // Reduce within the wave: the 4 lanes of each head's sum, the KG key groups of o.
-  s_run += __shfl_xor(s_run, 1, 64);
-  s_run += __shfl_xor(s_run, 2, 64);
+  for (int i = 0; i < 4; ++i) s[i] = row16_sum(s[i]);
 #pragma unroll
   for (int g = 0; g < GM; ++g)
 #pragma unroll
@@ -200,11 +261,18 @@ __global__ __launch_bounds__(kBlock, 2) void decode_split_kernel(DecodeArgs a) {
   // write this chunk's partial (m, s, o[D]) for each of the G heads
   const int stride = D + 2;
   const int64_t bq0 = (int64_t)b * a.Hq + (int64_t)h * G;
-  if (sh_part == 0 && sh_head < G) {
-    const rsrc_t pr = make_rsrc(a.part + ((bq0 + sh_head) * a.n_chunk_max + chunk) * stride, (uint64_t)stride * 4);
-    stf(pr, 0, m_run);
-    stf(pr, 4, s_run);
+  if (lr == 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int hd = 4 * lgp + i;
+      if (hd < G) {
+        const rsrc_t pr = make_rsrc(a.part + ((bq0 + hd) * a.n_chunk_max + chunk) * stride, (uint64_t)stride * 4);
+        stf(pr, 0, m[i]);
+        stf(pr, 4, s[i]);
+      }
+    }
   }
+  const int kg = lane / S::LPR, col0 = 8 * (lane % S::LPR);
   if (kg == 0) {
 #pragma unroll
     for (int g = 0; g < GM; ++g) {
@@ -301,13 +369,19 @@ __global__ __launch_bounds__(kBlock) void decode_combine_kernel(DecodeArgs a) {
   }
 }
 
+#ifndef SGDKV_DECODE_PF
+#define SGDKV_DECODE_PF 2
+#endif
+
+// Two steps in flight where the registers allow it (bf16, groups up to 8), else one.
 template <typename T, int D>
 static void launch_decode_t(const DecodeArgs& a, hipStream_t st) {
   const dim3 grid((a.n_chunk_max + kWaves - 1) / kWaves, a.B * a.Hkv);
+  constexpr int PF = sizeof(T) == 2 ? SGDKV_DECODE_PF : 1;
   if (a.G <= 8)
-    SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, 8>), grid, dim3(kBlock), st, a);
+    SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, 8, PF>), grid, dim3(kBlock), st, a);
   else
-    SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, 16>), grid, dim3(kBlock), st, a);
+    SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, 16, 1>), grid, dim3(kBlock), st, a);
 }
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {

@@ -260,6 +260,36 @@ def test_decode_edge_segments_and_bf16_output():
     assert np.all(np.abs(ob - ref) <= 2e-2 + ulp)
 
 
+def test_decode_fixed_reference_redo():
+    """Decode keeps each head's reference fixed at the largest logit of a chunk's first 16 keys and
+    reruns the chunk with a running maximum when a sum could overflow. Keys planted later in three
+    chunks have logits 80-160 (base 2) above anything in their chunk's first step (past the 2^64
+    bound on s; 2^160 overflows fp32 outright); in another segment a key 38 above carries a V row of 1e30, so the unrescaled o
+    overflows while s does not. Both must match the oracle."""
+    rng = np.random.Generator(np.random.PCG64(21))
+    d, Hq, Hkv = 128, 8, 4
+    lens = [600, 300, 900, 40]  # B=1; 256-row chunks
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    q = rng.standard_normal((1, Hq, d))
+    kc = rng.standard_normal((offs[-1], d))
+    vc = rng.standard_normal((offs[-1], d))
+    for seg, pos, f in ((0, 20, 6.0), (0, 356, 6.0), (2, 700, 9.0)):
+        kc[offs[seg] + pos] = f * q[0, 2 * seg]  # far above the first step of its chunk
+    kc[offs[1] + 40] = 3.0 * q[0, 2]  # ~38 above the first step's maximum: s stays below 2^64 ...
+    vc[offs[1] + 40] = 1e30  # ... but 2^38 * 1e30 overflows o
+    qt = torch.from_numpy(q).to(torch.bfloat16).to(DEV)
+    kt = torch.from_numpy(kc).to(torch.bfloat16).to(DEV)
+    vt = torch.from_numpy(vc).to(torch.bfloat16).to(DEV)
+    _announce("decode reference redo")
+    out, lse = sg.decode_attention(qt, kt, vt, torch.from_numpy(offs).to(DEV), offs, Hkv, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref, ref_lse = oracle.decode(_f64(qt), _f64(kt), _f64(vt), offs, Hkv)
+    o = out.cpu().numpy()
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(lse.cpu().numpy()))
+    assert np.all(np.abs(o - ref) <= 2e-2 + 1e-5 * np.abs(ref))
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() <= 2e-2
+
+
 def test_run_twice_bitwise():
     wl, t = _qwen_small(2, 2222)
     budgets = np.array([700, 500, 1500, 400])
