@@ -35,6 +35,18 @@ if ROOT not in sys.path:
 
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+# MI355X unit rates (256 CUs x 4 SIMDs at 2.4 GHz): fp32 vector ops issue 32 lanes per
+# cycle per SIMD (78.6 T op/s, 157.3 TFLOP/s counting an fma as two), exp2 at a quarter of
+# that (19.66 T/s). On a SIMD, MFMA and vector instructions issue one after the other (a
+# wave's MFMAs do not overlap vector work of any wave of that SIMD), so a score logit costs
+# the sum of its MFMA time (2*d flops), one exp2 and two plain ops (fma, add).
+VALU_OPS = 256 * 4 * 32 * 2.4e9
+EXP2_OPS = VALU_OPS / 4
+
+
+def score_logit_seconds(d, dtype):
+    """Chip-wide issue time of one window-row x key logit of either score pass."""
+    return 2.0 * d / (PEAK_TFLOPS[dtype] * 1e12) + 1.0 / EXP2_OPS + 2.0 / VALU_OPS
 
 
 def log(*a):
@@ -52,11 +64,109 @@ def parse():
     ap.add_argument("--caller-lse", action="store_true",
                     help="hand each layer its window-row LSE (as prefill attention would), skipping pass 1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0, metavar="MIB",
+                    help="first run three elementwise copies of MIB MiB (fp32 x 1.0), untimed: under "
+                         "rocprofv3 --pmc they calibrate FETCH_SIZE / WRITE_SIZE")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="no GPU work: turn the counter CSVs of two rocprofv3 --pmc runs (FETCH_SIZE, "
+                         "then WRITE_SIZE) of this script with --calibrate-copy-mib into "
+                         "profiles/traffic_<workload>.json")
     return ap.parse_args()
+
+
+# ------------------------------------------------------------------ HBM traffic from counters
+KERNEL_OF = {"score_lse": "lse_kernel", "score_colsum": "colsum_kernel", "gather": "copy_rows_kernel",
+             "decode_split": "decode_split_kernel"}
+SOURCE_OF = {"score_lse": "score_kernels.hip", "score_colsum": "score_kernels.hip",
+             "gather": "select_kernels.hip", "decode_split": "decode_kernels.hip"}
+SHARED_SOURCES = ("device_common.h", "mfma_frag.h", "sgdkv_internal.h")
+
+
+def source_sha(name):
+    """Hash of the source a kernel is built from: counters taken before a change do not apply."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in (SOURCE_OF[name],) + SHARED_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_03235_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_path(workload, ratio):
+    return os.path.join(ROOT, "profiles", f"traffic_{workload}_r{int(round(ratio * 100))}.json")
+
+
+_TRAFFIC = {}
+
+
+def traffic_of(name, workload=None, ratio=None):
+    """HBM bytes per launch of a kernel from the committed counter summary, or None when there is
+    none or the kernel's source changed since the counters were taken."""
+    if workload is not None:
+        _TRAFFIC.clear()
+        try:
+            with open(traffic_path(workload, ratio)) as fh:
+                _TRAFFIC.update(json.load(fh))
+        except (OSError, ValueError):
+            pass
+        return None
+    rec = _TRAFFIC.get("kernels", {}).get(name)
+    if not rec or rec.get("source_sha") != source_sha(name):
+        return None
+    return rec["hbm_bytes_per_launch"]
+
+
+def summarize_traffic(fetch_csv, write_csv, args):
+    import csv
+    import statistics
+
+    def per_kernel(path, counter):
+        vals = {}
+        with open(path, newline="") as fh:
+            for row in csv.DictReader(fh):
+                if row["Counter_Name"] == counter:
+                    vals.setdefault(row["Kernel_Name"], []).append(float(row["Counter_Value"]))
+        return vals
+
+    fetch, write = per_kernel(fetch_csv, "FETCH_SIZE"), per_kernel(write_csv, "WRITE_SIZE")
+    kib = args.calibrate_copy_mib * 1024.0
+
+    def copy_median(vals):
+        xs = [v for n, vs in vals.items() if "elementwise_kernel" in n for v in vs if v > 0.5 * kib]
+        return statistics.median(xs) if xs else None
+
+    cf, cw = copy_median(fetch), copy_median(write)
+    if not kib or cf is None or cw is None:
+        sys.exit("no calibration copy found: run the counter passes with --calibrate-copy-mib")
+    out = dict(workload=args.workload, ratio=args.ratio, unit="KiB per dispatch",
+               commands=[f"rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pmc_{c.split('_')[0].lower()} "
+                         f"-o pmc -- python3 bench.py --workload {args.workload} --ratio {args.ratio} --steps 1 "
+                         f"--warmup 0 --no-cpu-baseline --calibrate-copy-mib {args.calibrate_copy_mib}"
+                         for c in ("FETCH_SIZE", "WRITE_SIZE")],
+               note="hbm_bytes_per_launch = 1024 * (fetch_kib * fetch_factor + write_kib * write_factor); "
+                    "the factors make a plain elementwise copy of copy_kib read and write exactly copy_kib",
+               calibration=dict(copy_kib=kib, fetch_kib=cf, write_kib=cw, fetch_factor=kib / cf,
+                                write_factor=kib / cw),
+               kernels={})
+    for name, pat in KERNEL_OF.items():
+        fv = [v for n, vs in fetch.items() if pat in n for v in vs]
+        wv = [v for n, vs in write.items() if pat in n for v in vs]
+        if not fv or not wv:
+            continue
+        f, w_ = statistics.mean(fv), statistics.mean(wv)
+        out["kernels"][name] = dict(dispatches=len(fv), fetch_kib=f, write_kib=w_, source_sha=source_sha(name),
+                                    hbm_bytes_per_launch=round(1024.0 * (f * kib / cf + w_ * kib / cw)))
+    path = traffic_path(args.workload, args.ratio)
+    with open(path, "w") as fh:
+        json.dump(out, fh, indent=1)
+    print(f"wrote {path}")
 
 
 def main():
     args = parse()
+    if args.summarize_traffic:
+        summarize_traffic(*args.summarize_traffic, args)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         log(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
@@ -77,6 +187,14 @@ def main():
     C, w, s, W, kp = wl.seq_len, wl.obs_window, wl.b_sink, wl.b_window, wl.pool_kernel
     eb = 2 if wl.dtype == "bf16" else 4
     stream = torch.cuda.current_stream()
+    traffic_of(None, wl.name, args.ratio)
+    if args.calibrate_copy_mib:
+        src = torch.ones(args.calibrate_copy_mib << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     # ------------------------------------------------------------ inputs (HBM-resident)
     t0 = time.perf_counter()
@@ -172,8 +290,9 @@ def main():
     T_mean = float(T_layers.mean())
     flops_tok = 2.0 * Hq * w * d                      # window x key GEMM, counted once
     work = {
-        "score_lse": ("mfma", flops_tok * B * C, "TFLOP/s"),
-        "score_colsum": ("mfma", flops_tok * B * (C - w), "TFLOP/s"),
+        # MFMA flops of the logits; bound by MFMA + vector issue, see score_logit_seconds
+        "score_lse": ("alu", flops_tok * B * C, "TFLOP/s"),
+        "score_colsum": ("alu", flops_tok * B * (C - w), "TFLOP/s"),
         # read kept K and V rows, write them, write positions, read pooled scores of the candidates
         "gather": ("hbm", B * T_mean * (4 * d * eb + 4) + B * Hkv * C * 4.0, "GB/s"),
         # read every kept K and V row once, plus the queries and outputs
@@ -189,13 +308,19 @@ def main():
         count, ms = kern[name]
         bound, amount, unit = work[name]
         avg_s = ms / count / 1e3
-        if bound == "mfma":
+        extra = {}
+        if bound == "alu":
+            # peak: MFMA flops per second when every logit also pays its exp2, fma and add
+            achieved = amount / avg_s / 1e12
+            peak = 2.0 * d / score_logit_seconds(d, wl.dtype) / 1e12
+            extra = dict(mfma_peak=PEAK_TFLOPS[wl.dtype], mfma_frac=round(achieved / PEAK_TFLOPS[wl.dtype], 4))
+        elif bound == "mfma":
             achieved, peak = amount / avg_s / 1e12, PEAK_TFLOPS[wl.dtype]
         else:
             achieved, peak = amount / avg_s / 1e9, PEAK_HBM_GBS
-        return dict(kernel=name, bound=bound, achieved=round(achieved, 2), peak=peak, unit=unit,
-                    frac=round(achieved / peak, 4), traffic=None, avg_us=round(avg_s * 1e6, 2),
-                    work_per_launch=amount)
+        return dict(kernel=name, bound=bound, achieved=round(achieved, 2), peak=round(peak, 1), unit=unit,
+                    frac=round(achieved / peak, 4), traffic=traffic_of(name), avg_us=round(avg_s * 1e6, 2),
+                    work_per_launch=amount, **extra)
 
     roofline = roof(dominant) if dominant in work else None
     decode = roof("decode_split") if "decode_split" in kern else None
