@@ -25,48 +25,72 @@ namespace sgdkv {
 namespace {
 constexpr int kWaves = kBlock / 64;
 
+// The segment bounds are the same for every lane: taking them from lane 0 lets the
+// compiler keep them, and every buffer descriptor built from them, in scalar
+// registers (a descriptor in vector registers costs a waterfall loop per load).
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 __device__ __forceinline__ void clamp_segment(const DecodeArgs& a, int seg, int64_t& r0, int64_t& r1) {
   const int nseg = a.B * a.Hkv;
   const rsrc_t orr = make_rsrc(a.offsets, (uint64_t)(nseg + 1) * 8);
-  r0 = (int64_t)ld64(orr, (uint32_t)seg * 8);
-  r1 = (int64_t)ld64(orr, (uint32_t)(seg + 1) * 8);
+  r0 = uniform64((int64_t)ld64(orr, (uint32_t)seg * 8));
+  r1 = uniform64((int64_t)ld64(orr, (uint32_t)(seg + 1) * 8));
   r0 = r0 < 0 ? 0 : (r0 > a.total_rows ? a.total_rows : r0);
   r1 = r1 < r0 ? r0 : (r1 > a.total_rows ? a.total_rows : r1);
 }
 }  // namespace
 
 // Loads of one 16-key step: the K fragments of the MFMA (key lr, k = 32c + 8*lg)
-// and this lane's V rows (keys kg + KG*u, columns col0 .. col0+7).
-template <typename T, int D>
+// and this lane's V rows (keys kg + KG*u, columns col0 .. col0+CPL-1).
+template <typename T, int D, int CPL>
 struct DecodeStep {
   static constexpr int EB = sizeof(T);
   static constexpr int RB = D * EB;
   static constexpr int NC = D / 32;
-  static constexpr int LPR = D / 8;        // lanes sharing one value row (8 columns each)
+  static constexpr int LPR = D / CPL;      // lanes sharing one value row
   static constexpr int KG = 64 / LPR;      // key groups per wave
   static constexpr int VPL = 16 / KG;      // value rows per lane per step
-  static constexpr int VW = EB == 2 ? 1 : 2;  // 16-byte pieces per 8 columns
+  static constexpr int NW = CPL * EB / 4;  // 32-bit words per lane per value row
+  static_assert(NW == 2 || NW % 4 == 0, "value piece");
   Frag<T> kb[NC];
-  u32x4 vv[VPL][VW];
+  uint32_t vv[VPL][NW];
   __device__ __forceinline__ void load(const rsrc_t& kr, const rsrc_t& vr, int64_t k0, int lr, int lgp, int kg,
                                        int col0) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) kb[c] = gload_frag<T>(kr, (uint32_t)((k0 + lr) * RB + (32 * c + 8 * lgp) * EB));
 #pragma unroll
-    for (int u = 0; u < VPL; ++u)
+    for (int u = 0; u < VPL; ++u) {
+      const uint32_t off = (uint32_t)((k0 + kg + KG * u) * RB + col0 * EB);
+      if constexpr (NW == 2) {
+        const uint64_t x = ld64(vr, off);
+        vv[u][0] = (uint32_t)x;
+        vv[u][1] = (uint32_t)(x >> 32);
+      } else {
 #pragma unroll
-      for (int x = 0; x < VW; ++x) vv[u][x] = ld128(vr, (uint32_t)((k0 + kg + KG * u) * RB + col0 * EB + 16 * x));
+        for (int x = 0; x < NW / 4; ++x) {
+          const u32x4 y = ld128(vr, off + 16 * x);
+          vv[u][4 * x] = y.x;
+          vv[u][4 * x + 1] = y.y;
+          vv[u][4 * x + 2] = y.z;
+          vv[u][4 * x + 3] = y.w;
+        }
+      }
+    }
   }
-  __device__ __forceinline__ void value_row(int u, float (&v)[8]) const {
+  __device__ __forceinline__ void value_row(int u, float (&v)[CPL]) const {
     if constexpr (EB == 2) {
-      const u32x4 x = vv[u][0];
-      v[0] = bf16_lo(x.x); v[1] = bf16_hi(x.x); v[2] = bf16_lo(x.y); v[3] = bf16_hi(x.y);
-      v[4] = bf16_lo(x.z); v[5] = bf16_hi(x.z); v[6] = bf16_lo(x.w); v[7] = bf16_hi(x.w);
+#pragma unroll
+      for (int x = 0; x < NW; ++x) {
+        v[2 * x] = bf16_lo(vv[u][x]);
+        v[2 * x + 1] = bf16_hi(vv[u][x]);
+      }
     } else {
-      const u32x4 x0 = vv[u][0], x1 = vv[u][VW - 1];
-      v[0] = __uint_as_float(x0.x); v[1] = __uint_as_float(x0.y); v[2] = __uint_as_float(x0.z);
-      v[3] = __uint_as_float(x0.w); v[4] = __uint_as_float(x1.x); v[5] = __uint_as_float(x1.y);
-      v[6] = __uint_as_float(x1.z); v[7] = __uint_as_float(x1.w);
+#pragma unroll
+      for (int x = 0; x < NW; ++x) v[x] = __uint_as_float(vv[u][x]);
     }
   }
 };
@@ -105,17 +129,16 @@ __device__ __forceinline__ float row16_sum(float x) {
 // The probabilities of a step reach the P.V lanes through LDS (double
 // buffered by step parity, so one wave-local sync per step orders both the
 // writes before the reads and the reads before the writes two steps later).
-template <typename T, int D, int GM, int PF, bool EXACT>
+template <typename T, int D, int CPL, int GM, int PF, bool EXACT>
 __device__ __forceinline__ void decode_chunk(const DecodeArgs& a, float (*pls)[16][16], float (*als)[16],
                                              const rsrc_t& kr, const rsrc_t& vr, int64_t c0, int64_t c1,
                                              const Frag<T> (&qa)[D / 32], int lane, float (&m)[4], float (&s)[4],
-                                             float (&o)[GM][8]) {
-  using S = DecodeStep<T, D>;
+                                             float (&o)[GM][CPL]) {
+  using S = DecodeStep<T, D, CPL>;
   constexpr int KS = 16;
   constexpr int NBUF = PF + 1;
   const int lr = lane & 15, lgp = lane >> 4;
-  const int kg = lane / S::LPR, col0 = 8 * (lane % S::LPR);
-  const int G = a.G;
+  const int kg = lane / S::LPR, col0 = CPL * (lane % S::LPR);
   const float c2 = a.c2;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -125,19 +148,23 @@ __device__ __forceinline__ void decode_chunk(const DecodeArgs& a, float (*pls)[1
 #pragma unroll
   for (int g = 0; g < GM; ++g)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
+    for (int e = 0; e < CPL; ++e) o[g][e] = 0.f;
   const int nsteps = (int)((c1 - c0 + KS - 1) / KS);
+  // Loads are issued unconditionally (past the last step they repeat it, which the caches
+  // serve): a load under a branch makes the compiler wait for every load in flight,
+  // prefetches included, before the next use of loaded data.
+  const int64_t k_last = c0 + (int64_t)(nsteps - 1) * KS;
+  auto step_key = [&](int64_t k) { return k < k_last ? k : k_last; };
   S buf[NBUF];
 #pragma unroll
-  for (int p = 0; p < PF; ++p)
-    if (p < nsteps) buf[p].load(kr, vr, c0 + p * KS, lr, lgp, kg, col0);
+  for (int p = 0; p < PF; ++p) buf[p].load(kr, vr, step_key(c0 + p * KS), lr, lgp, kg, col0);
   for (int it0 = 0; it0 < nsteps; it0 += NBUF) {
 #pragma unroll
     for (int u = 0; u < NBUF; ++u) {
       const int it = it0 + u;
       if (it >= nsteps) break;
       const int64_t k0 = c0 + (int64_t)it * KS;
-      if (it + PF < nsteps) buf[(u + PF) % NBUF].load(kr, vr, k0 + PF * KS, lr, lgp, kg, col0);
+      buf[(u + PF) % NBUF].load(kr, vr, step_key(k0 + PF * KS), lr, lgp, kg, col0);
       const S& cur = buf[u];
       f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -170,18 +197,17 @@ __device__ __forceinline__ void decode_chunk(const DecodeArgs& a, float (*pls)[1
       wave_sync();
       if (EXACT && moved) {
 #pragma unroll
-        for (int g = 0; g < GM; ++g)
-          if (g < G) {
-            const float al = als[it & 1][g];
+        for (int g = 0; g < GM; ++g) {
+          const float al = als[it & 1][g];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) o[g][e] *= al;
-          }
+          for (int e = 0; e < CPL; ++e) o[g][e] *= al;
+        }
       }
       // P.V for this lane's value rows and columns
 #pragma unroll
       for (int u2 = 0; u2 < S::VPL; ++u2) {
         const int kk = kg + S::KG * u2;
-        float v[8];
+        float v[CPL];
         cur.value_row(u2, v);
         float pk[GM];
 #pragma unroll
@@ -192,29 +218,30 @@ __device__ __forceinline__ void decode_chunk(const DecodeArgs& a, float (*pls)[1
           if (g4 + 2 < GM) pk[g4 + 2] = q4[2];
           if (g4 + 3 < GM) pk[g4 + 3] = q4[3];
         }
+        // every row of the padded group: rows past G (zero queries) are never written out,
+        // and a branch per head would split the step into blocks that each wait on LDS
 #pragma unroll
         for (int g = 0; g < GM; ++g)
-          if (g < G) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) o[g][e] = fmaf(pk[g], v[e], o[g][e]);
-          }
+          for (int e = 0; e < CPL; ++e) o[g][e] = fmaf(pk[g], v[e], o[g][e]);
       }
     }
   }
 }
 
-// GM = compile-time bound on the group size (8 or 16); PF = steps of K/V in
-// flight ahead of the one being computed. Each wave owns one chunk of a
-// segment: chunk index = 4*blockIdx.x + wave.
-template <typename T, int D, int GM, int PF>
-__global__ __launch_bounds__(kBlock, 2) void decode_split_kernel(DecodeArgs a) {
-  using S = DecodeStep<T, D>;
+// CPL = value columns per lane; GM = compile-time bound on the group size (8
+// or 16); PF = steps of K/V in flight ahead of the one being computed; OCC =
+// workgroups per CU the registers are sized for. Each wave owns one chunk of
+// a segment: chunk index = 4*blockIdx.x + wave.
+template <typename T, int D, int CPL, int GM, int PF, int OCC>
+__global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a) {
+  using S = DecodeStep<T, D, CPL>;
   __shared__ __attribute__((aligned(16))) float pls[kWaves][2][16][16];  // probabilities [key][head]
   __shared__ __attribute__((aligned(16))) float als[kWaves][2][16];      // per-head rescale (exact pass)
 
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
-  const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, wid = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   int64_t r0, r1;
   clamp_segment(a, seg, r0, r1);
   const int64_t len = r1 - r0;
@@ -233,8 +260,8 @@ __global__ __launch_bounds__(kBlock, 2) void decode_split_kernel(DecodeArgs a) {
 #pragma unroll
   for (int c = 0; c < S::NC; ++c) qa[c] = gload_frag<T>(qr, (uint32_t)(lr * S::RB + (32 * c + 8 * lgp) * S::EB));
 
-  float m[4], s[4], o[GM][8];
-  decode_chunk<T, D, GM, PF, false>(a, pls[wid], als[wid], kr, vr, c0, c1, qa, lane, m, s, o);
+  float m[4], s[4], o[GM][CPL];
+  decode_chunk<T, D, CPL, GM, PF, false>(a, pls[wid], als[wid], kr, vr, c0, c1, qa, lane, m, s, o);
   // 2^64 bounds every probability, so s and o stay finite unless V is huge or the
   // first step's maximum sat far below a later logit: then redo with rescaling
   bool bad = false;
@@ -243,8 +270,8 @@ __global__ __launch_bounds__(kBlock, 2) void decode_split_kernel(DecodeArgs a) {
 #pragma unroll
   for (int g = 0; g < GM; ++g)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) bad |= !(fabsf(o[g][e]) < INFINITY);
-  if (__any(bad)) decode_chunk<T, D, GM, PF, true>(a, pls[wid], als[wid], kr, vr, c0, c1, qa, lane, m, s, o);
+    for (int e = 0; e < CPL; ++e) bad |= !(fabsf(o[g][e]) < INFINITY);
+  if (__any(bad)) decode_chunk<T, D, CPL, GM, PF, true>(a, pls[wid], als[wid], kr, vr, c0, c1, qa, lane, m, s, o);
 
   // Reduce within the wave: the 16 lanes of each head's sum, the KG key groups of o.
 #pragma unroll
@@ -252,47 +279,51 @@ __global__ __launch_bounds__(kBlock, 2) void decode_split_kernel(DecodeArgs a) {
 #pragma unroll
   for (int g = 0; g < GM; ++g)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
+    for (int e = 0; e < CPL; ++e) {
       float x = o[g][e];
 #pragma unroll
       for (int sft = S::LPR; sft < 64; sft <<= 1) x += __shfl_xor(x, sft, 64);
       o[g][e] = x;
     }
-  // write this chunk's partial (m, s, o[D]) for each of the G heads
-  const int stride = D + 2;
+  // write this chunk's partial for each of the G heads: (m, s) and o[D] in two arrays, one
+  // descriptor each for the whole group (per-lane descriptors would cost waterfall loops)
   const int64_t bq0 = (int64_t)b * a.Hq + (int64_t)h * G;
+  const int64_t ncm = a.n_chunk_max;
   if (lr == 0) {
+    const rsrc_t mr = make_rsrc(a.part_ms + bq0 * ncm * 2, (uint64_t)G * ncm * 8);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int hd = 4 * lgp + i;
-      if (hd < G) {
-        const rsrc_t pr = make_rsrc(a.part + ((bq0 + hd) * a.n_chunk_max + chunk) * stride, (uint64_t)stride * 4);
-        stf(pr, 0, m[i]);
-        stf(pr, 4, s[i]);
-      }
+      if (hd < G)
+        st64(mr, (uint32_t)(((int64_t)hd * ncm + chunk) * 8),
+             (uint64_t)__float_as_uint(m[i]) | ((uint64_t)__float_as_uint(s[i]) << 32));
     }
   }
-  const int kg = lane / S::LPR, col0 = 8 * (lane % S::LPR);
+  const int kg = lane / S::LPR, col0 = CPL * (lane % S::LPR);
   if (kg == 0) {
+    const rsrc_t orr = make_rsrc(a.part + bq0 * ncm * D, (uint64_t)G * ncm * D * 4);
 #pragma unroll
     for (int g = 0; g < GM; ++g) {
       if (g < G) {
-        const rsrc_t pr = make_rsrc(a.part + ((bq0 + g) * a.n_chunk_max + chunk) * stride, (uint64_t)stride * 4);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) stf(pr, (uint32_t)(8 + (col0 + e) * 4), o[g][e]);
+        for (int e = 0; e < CPL; e += 4)
+          st128(orr, (uint32_t)((((int64_t)g * ncm + chunk) * D + col0 + e) * 4),
+                u32x4{__float_as_uint(o[g][e]), __float_as_uint(o[g][e + 1]), __float_as_uint(o[g][e + 2]),
+                      __float_as_uint(o[g][e + 3])});
       }
     }
   }
 }
 
-// One workgroup per (sequence, query head). Thread = (chunk group, column):
-// groups stride over the chunk partials with independent loads, then merge
-// in group order through LDS.
+// One 1024-thread workgroup per (sequence, query head). The global maximum of
+// the chunk references comes first; then thread (group, c4) sums the chunks
+// group, group + NG, ... (eight independent loads in flight) for columns
+// 4*c4 .. 4*c4+3, and the NG group sums are added in group order.
 template <int D>
-__global__ __launch_bounds__(kBlock) void decode_combine_kernel(DecodeArgs a) {
-  constexpr int NG = kBlock / D;  // chunk groups
-  __shared__ float red_m[kBlock / 64];
-  __shared__ float red_o[NG][D];
+__global__ __launch_bounds__(1024) void decode_combine_kernel(DecodeArgs a) {
+  constexpr int NT = 1024, TPR = D / 4, NG = NT / TPR, U = 8;
+  __shared__ float red_m[NT / 64];
+  __shared__ __attribute__((aligned(16))) float red_o[NG][D];
   __shared__ float red_s[NG];
   const int bq = blockIdx.x;
   const int b = bq / a.Hq, qh = bq % a.Hq, h = qh / a.G;
@@ -300,67 +331,65 @@ __global__ __launch_bounds__(kBlock) void decode_combine_kernel(DecodeArgs a) {
   int64_t r0, r1;
   clamp_segment(a, seg, r0, r1);
   const int64_t len = r1 - r0;
+  const int64_t ncm = a.n_chunk_max;
   int64_t nch = (len + a.chunk - 1) / a.chunk;
-  if (nch > a.n_chunk_max) nch = a.n_chunk_max;
-  const int tid = threadIdx.x, col = tid % D, grp = tid / D;
-  const int stride = D + 2;
-  const rsrc_t pr = make_rsrc(a.part + (int64_t)bq * a.n_chunk_max * stride, (uint64_t)a.n_chunk_max * stride * 4);
-  // global max over the chunks
+  if (nch > ncm) nch = ncm;
+  const int tid = threadIdx.x, c4 = tid % TPR, grp = tid / TPR;
+  const rsrc_t mr = make_rsrc(a.part_ms + (int64_t)bq * ncm * 2, (uint64_t)ncm * 8);
+  const rsrc_t orr = make_rsrc(a.part + (int64_t)bq * ncm * D, (uint64_t)ncm * D * 4);
   float M = -INFINITY;
-  for (int64_t c = tid; c < nch; c += kBlock) M = fmaxf(M, ldf(pr, (uint32_t)(c * stride * 4)));
+  for (int64_t c = tid; c < nch; c += NT) M = fmaxf(M, ldf(mr, (uint32_t)(c * 8)));
   M = wave_max(M);
   if ((tid & 63) == 0) red_m[tid >> 6] = M;
   __syncthreads();
   M = red_m[0];
 #pragma unroll
-  for (int u = 1; u < kBlock / 64; ++u) M = fmaxf(M, red_m[u]);
-  float S = 0.f, O = 0.f;
+  for (int u = 1; u < NT / 64; ++u) M = fmaxf(M, red_m[u]);
+  float S = 0.f, O[4] = {0.f, 0.f, 0.f, 0.f};
   if (M != -INFINITY) {
-    int64_t c = grp;
-    for (; c + 3 * NG < nch; c += 4 * NG) {
-      float mc[4], sc[4], oc[4];
+    for (int64_t c = grp; c < nch; c += U * NG) {
+      uint64_t ms[U];
+      u32x4 ov[U];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const uint32_t base = (uint32_t)((c + u * NG) * stride * 4);
-        mc[u] = ldf(pr, base);
-        sc[u] = ldf(pr, base + 4);
-        oc[u] = ldf(pr, base + 8 + col * 4);
+      for (int u = 0; u < U; ++u) {  // chunks past nch read as zeros (offset past the buffer)
+        const int64_t cc = c + u * NG;
+        const bool ok = cc < nch;
+        ms[u] = ld64(mr, ok ? (uint32_t)(cc * 8) : (uint32_t)(ncm * 8));
+        ov[u] = ld128(orr, ok ? (uint32_t)((cc * D + 4 * c4) * 4) : (uint32_t)(ncm * D * 4));
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float e = (mc[u] == -INFINITY) ? 0.f : fast_exp2(mc[u] - M);
-        S += sc[u] * e;
-        O += oc[u] * e;
+      for (int u = 0; u < U; ++u) {
+        const float mc = __uint_as_float((uint32_t)ms[u]), sc = __uint_as_float((uint32_t)(ms[u] >> 32));
+        const float e = (c + u * NG < nch && mc != -INFINITY) ? fast_exp2(mc - M) : 0.f;
+        S += sc * e;
+        O[0] += __uint_as_float(ov[u].x) * e;
+        O[1] += __uint_as_float(ov[u].y) * e;
+        O[2] += __uint_as_float(ov[u].z) * e;
+        O[3] += __uint_as_float(ov[u].w) * e;
       }
-    }
-    for (; c < nch; c += NG) {
-      const uint32_t base = (uint32_t)(c * stride * 4);
-      const float mc = ldf(pr, base);
-      const float e = (mc == -INFINITY) ? 0.f : fast_exp2(mc - M);
-      S += ldf(pr, base + 4) * e;
-      O += ldf(pr, base + 8 + col * 4) * e;
     }
   }
-  red_o[grp][col] = O;
-  if (col == 0) red_s[grp] = S;
+  *reinterpret_cast<f32x4*>(&red_o[grp][4 * c4]) = f32x4{O[0], O[1], O[2], O[3]};
+  if (c4 == 0) red_s[grp] = S;
   __syncthreads();
-  if (grp != 0) return;
+  if (tid >= D) return;
+  const int col = tid;
   S = red_s[0];
-  O = red_o[0][col];
+  float Oc = red_o[0][col];
 #pragma unroll
   for (int g = 1; g < NG; ++g) {
     S += red_s[g];
-    O += red_o[g][col];
+    Oc += red_o[g][col];
   }
   const bool empty = !(S > 0.f);
-  const float res = empty ? 0.f : O / S;
+  const float res = empty ? 0.f : Oc / S;
   if (a.out_dtype == 1) {
-    const rsrc_t orr = make_rsrc(static_cast<char*>(a.out) + (int64_t)bq * D * 2, (uint64_t)D * 2);
+    const rsrc_t outr = make_rsrc(static_cast<char*>(a.out) + (int64_t)bq * D * 2, (uint64_t)D * 2);
     const float other = __shfl_xor(res, 1, 64);  // two columns per 32-bit store
-    if ((col & 1) == 0) st32(orr, (uint32_t)col * 2, f32_to_bf16_bits(res) | (f32_to_bf16_bits(other) << 16));
+    if ((col & 1) == 0) st32(outr, (uint32_t)col * 2, f32_to_bf16_bits(res) | (f32_to_bf16_bits(other) << 16));
   } else {
-    const rsrc_t orr = make_rsrc(static_cast<char*>(a.out) + (int64_t)bq * D * 4, (uint64_t)D * 4);
-    stf(orr, (uint32_t)col * 4, res);
+    const rsrc_t outr = make_rsrc(static_cast<char*>(a.out) + (int64_t)bq * D * 4, (uint64_t)D * 4);
+    stf(outr, (uint32_t)col * 4, res);
   }
   if (a.lse_out != nullptr && col == 0) {
     const rsrc_t lr = make_rsrc(a.lse_out, (uint64_t)a.B * a.Hq * 4);
@@ -370,18 +399,27 @@ __global__ __launch_bounds__(kBlock) void decode_combine_kernel(DecodeArgs a) {
 }
 
 #ifndef SGDKV_DECODE_PF
-#define SGDKV_DECODE_PF 2
+#define SGDKV_DECODE_PF 1
+#endif
+#ifndef SGDKV_DECODE_CPL
+#define SGDKV_DECODE_CPL 8
+#endif
+#ifndef SGDKV_DECODE_OCC
+#define SGDKV_DECODE_OCC 2
 #endif
 
-// Two steps in flight where the registers allow it (bf16, groups up to 8), else one.
+// One step of K/V in flight ahead of the one being computed (more measured no faster).
 template <typename T, int D>
 static void launch_decode_t(const DecodeArgs& a, hipStream_t st) {
   const dim3 grid((a.n_chunk_max + kWaves - 1) / kWaves, a.B * a.Hkv);
-  constexpr int PF = sizeof(T) == 2 ? SGDKV_DECODE_PF : 1;
+  constexpr bool wide = sizeof(T) == 2;
+  constexpr int PF = wide ? SGDKV_DECODE_PF : 1;
+  constexpr int CPL = wide ? SGDKV_DECODE_CPL : 8;
+  constexpr int OCC = wide ? SGDKV_DECODE_OCC : 2;
   if (a.G <= 8)
-    SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, 8, PF>), grid, dim3(kBlock), st, a);
+    SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, CPL, 8, PF, OCC>), grid, dim3(kBlock), st, a);
   else
-    SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, 16, 1>), grid, dim3(kBlock), st, a);
+    SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, 8, 16, 1, 2>), grid, dim3(kBlock), st, a);
 }
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {
@@ -395,9 +433,9 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {
     }
   }
   if (a.D == 128)
-    SGDKV_LAUNCH("decode_combine", decode_combine_kernel<128>, dim3(a.B * a.Hq), dim3(kBlock), st, a);
+    SGDKV_LAUNCH("decode_combine", decode_combine_kernel<128>, dim3(a.B * a.Hq), dim3(1024), st, a);
   else
-    SGDKV_LAUNCH("decode_combine", decode_combine_kernel<64>, dim3(a.B * a.Hq), dim3(kBlock), st, a);
+    SGDKV_LAUNCH("decode_combine", decode_combine_kernel<64>, dim3(a.B * a.Hq), dim3(1024), st, a);
   return hipGetLastError();
 }
 

@@ -540,6 +540,7 @@ sgdkv_status sgdkv_decode_attention(const sgdkv_decode_desc* desc, const void* q
   a.out = out;
   a.lse_out = lse_out;
   a.part = static_cast<float*>(workspace);
+  a.part_ms = a.part + (size_t)a.B * a.Hq * a.n_chunk_max * a.D;
   hipError_t e = hipGetLastError();
   (void)e;
   e = sgdkv::launch_decode(a, static_cast<hipStream_t>(stream));

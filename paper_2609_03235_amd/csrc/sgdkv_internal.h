@@ -84,7 +84,8 @@ struct DecodeArgs {
   int64_t total_rows;  // offsets_host[B*Hkv]: device offsets are clamped to it
   void* out;
   float* lse_out;
-  float* part;        // [B*Hq][n_chunk_max][D+2]: (m, s, o[D]) per split
+  float* part;        // [B*Hq][n_chunk_max][D]: o per split (16-byte aligned rows)
+  float* part_ms;     // [B*Hq][n_chunk_max][2]: (m, s) per split
   int64_t chunk;      // rows per split (multiple of 128)
   int n_chunk_max;    // max over segments of ceil(len / chunk)
 };
