@@ -492,7 +492,8 @@ sgdkv_status plan_decode(const sgdkv_decode_desc* d, const int64_t* offsets_host
   const double scale = d->scale > 0.f ? (double)d->scale : 1.0 / std::sqrt((double)d->head_dim);
   a.c2 = (float)(scale * 1.4426950408889634074);
   a.total_rows = total;
-  // rows per wave-sized split: about 8192 splits over the whole batch, at least 256 rows
+  // rows per wave-sized split: about 8192 splits over the whole batch (four rounds of the
+  // 2048 resident waves), at least 256 rows; one round of longer splits measured slower
   a.chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(total - offsets_host[0], 8192), 64), 256), 1 << 24);
   a.n_chunk_max = (int)ceil_div(longest, a.chunk);
   p.bytes = align256((size_t)a.B * a.Hq * a.n_chunk_max * (a.D + 2) * sizeof(float));

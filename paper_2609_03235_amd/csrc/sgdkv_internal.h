@@ -86,7 +86,7 @@ struct DecodeArgs {
   float* lse_out;
   float* part;        // [B*Hq][n_chunk_max][D]: o per split (16-byte aligned rows)
   float* part_ms;     // [B*Hq][n_chunk_max][2]: (m, s) per split
-  int64_t chunk;      // rows per split (multiple of 128)
+  int64_t chunk;      // rows per split (multiple of 64, at least 256)
   int n_chunk_max;    // max over segments of ceil(len / chunk)
 };
 

@@ -268,7 +268,7 @@ def test_decode_fixed_reference_redo():
     overflows while s does not. Both must match the oracle."""
     rng = np.random.Generator(np.random.PCG64(21))
     d, Hq, Hkv = 128, 8, 4
-    lens = [600, 300, 900, 40]  # B=1; 256-row chunks
+    lens = [600, 300, 900, 40]  # B=1; 256-row chunks: every planted key is past its first step
     offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
     q = rng.standard_normal((1, Hq, d))
     kc = rng.standard_normal((offs[-1], d))

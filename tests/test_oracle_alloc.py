@@ -95,10 +95,13 @@ def test_invariants(p, mode):
         for c in range(n):
             if scores[a] > scores[c]:
                 assert b[a] >= b[c], (scores, b)
-    # normalisation makes the allocation invariant under scaling by a power of two
+    # normalisation makes the allocation invariant under scaling by a power of two, wherever
+    # that scaling is exact (a denormal score scaled down can round or flush to zero)
     for k in (-7, 3):
-        b2 = oracle.allocate_budgets(scores * (2.0 ** k), L, H, C, s, W, total, mode)
-        assert np.array_equal(b, b2)
+        scaled = scores * (2.0 ** k)
+        if np.array_equal(scaled * (2.0 ** -k), scores):
+            b2 = oracle.allocate_budgets(scaled, L, H, C, s, W, total, mode)
+            assert np.array_equal(b, b2)
     # without any capping the budgets are the exact shares rounded by largest remainder
     T = total - n * (s + W)
     x = _exact_shares(scores, T)
