@@ -55,13 +55,14 @@ def _load():
     lib.orc_reduce_group_max.argtypes = [P, i32, i32, i32, P]
     lib.orc_total_from_ratio.argtypes = [f64, i32, i32, i64, i64, i64, i32, P]
     lib.orc_allocate_budgets.argtypes = [P, i32, i32, i64, i64, i64, i64, i32, P]
+    lib.orc_allocate_variant.argtypes = [P, P, i32, i32, i64, i64, i64, i64, i32, i32, f64, P]
     lib.orc_window_lse.argtypes = [P, P, i32, i32, i32, i32, i64, i32, f64, P]
     lib.orc_window_colsum.argtypes = [P, P, P, i32, i32, i32, i32, i64, i32, f64, P]
     lib.orc_pool.argtypes = [P, i64, i64, i32, P]
     lib.orc_select.argtypes = [P, i64, i32, i64, i64, i64, P]
     lib.orc_decode.argtypes = [P, P, P, P, i32, i32, i32, i32, f64, P, P]
     lib.orc_num_threads.argtypes = []
-    for f in ("orc_reduce_group_max", "orc_total_from_ratio", "orc_allocate_budgets",
+    for f in ("orc_reduce_group_max", "orc_total_from_ratio", "orc_allocate_budgets", "orc_allocate_variant",
               "orc_window_lse", "orc_window_colsum", "orc_pool", "orc_select", "orc_decode",
               "orc_num_threads"):
         getattr(lib, f).restype = i32
@@ -120,6 +121,25 @@ def allocate_budgets(scores, L: int, H: int, C: int, s: int, W: int, total: int,
     out = np.zeros(L * H, dtype=np.int64)
     _check(_load().orc_allocate_budgets(_ptr(sc), L, H, C, s, W, int(total), int(mode), _ptr(out)),
            "allocate_budgets")
+    return out
+
+
+ALLOC_PLAIN, ALLOC_THR, ALLOC_REVERSE, ALLOC_MIX, ALLOC_BINARY, ALLOC_BINARY_REVERSE = range(6)
+
+
+def allocate_variant(scores, L: int, H: int, C: int, s: int, W: int, total: int, variant: int,
+                     mode: int = 0, scores2=None, full_fraction: float = 0.0) -> np.ndarray:
+    """Allocation variants of the head-configuration ablation (Appendix A.7, Table 5)."""
+    sc = _f64(scores).reshape(-1)
+    if sc.size != L * H:
+        raise OracleError("scores must hold L*H values")
+    s2 = None if scores2 is None else _f64(scores2).reshape(-1)
+    if s2 is not None and s2.size != L * H:
+        raise OracleError("scores2 must hold L*H values")
+    out = np.zeros(L * H, dtype=np.int64)
+    _check(_load().orc_allocate_variant(_ptr(sc), _ptr(s2) if s2 is not None else None, L, H, C, s, W,
+                                        int(total), int(mode), int(variant), ctypes.c_double(full_fraction),
+                                        _ptr(out)), "allocate_variant")
     return out
 
 

@@ -254,6 +254,82 @@ int orc_allocate_budgets(const double* sigma, int L, int H, int64_t C, int64_t s
 }
 
 /* ------------------------------------------------------------------ */
+/* Allocation variants of the head-configuration ablation (Appendix A.7,
+ * Table 5):
+ *   0 PLAIN           orc_allocate_budgets.
+ *   1 THR             scores below the mean of all L*H scores become 0 before
+ *                     the allocation ("SGD-KV (thr)").
+ *   2 REVERSE         the allocation is inverted head by head: a head that
+ *                     keeps m_h of its M middle rows keeps M - m_h instead
+ *                     ("SGD-KV (Reverse)": 10 % becomes 90 %). The total is
+ *                     then L*H*(C + s + W) - total.
+ *   3 MIX             the scores are the average of the normalised
+ *                     summarization scores and a second normalised score
+ *                     vector sigma2 ("SGD-KV + HeadKV" with R2 scores); an
+ *                     all-zero vector normalises to uniform.
+ *   4 BINARY          the floor(f*n) heads first in (score descending, index
+ *                     ascending) order keep all C rows, the others only
+ *                     s + W ("DuoAttention (Sum.)"); total is not used.
+ *   5 BINARY_REVERSE  the floor(f*n) heads last in that order keep all rows
+ *                     ("DuoAttention (Sum., Reverse)", f = 0.75).          */
+int orc_allocate_variant(const double* sigma, const double* sigma2, int L, int H, int64_t C, int64_t s,
+                         int64_t W, int64_t total, int mode, int variant, double f, int64_t* budgets) {
+  if (L < 1 || H < 1 || C < 1 || s < 0 || W < 0 || s + W > C) return ORC_INVALID;
+  int64_t n = (int64_t)L * H;
+  int64_t M = C - s - W;
+  for (int64_t h = 0; h < n; ++h)
+    if (!(sigma[h] >= 0.0) || isinf(sigma[h])) return ORC_INVALID;
+  if (variant == 0) return orc_allocate_budgets(sigma, L, H, C, s, W, total, mode, budgets);
+  if (variant == 1) {
+    double sum = 0.0;
+    for (int64_t h = 0; h < n; ++h) sum += sigma[h];
+    double mean = sum / (double)n;
+    double* t = (double*)malloc(sizeof(double) * (size_t)n);
+    for (int64_t h = 0; h < n; ++h) t[h] = sigma[h] < mean ? 0.0 : sigma[h];
+    int rc = orc_allocate_budgets(t, L, H, C, s, W, total, mode, budgets);
+    free(t);
+    return rc;
+  }
+  if (variant == 2) {
+    int rc = orc_allocate_budgets(sigma, L, H, C, s, W, total, mode, budgets);
+    if (rc != ORC_OK) return rc;
+    for (int64_t h = 0; h < n; ++h) budgets[h] = s + W + (M - (budgets[h] - s - W));
+    return ORC_OK;
+  }
+  if (variant == 3) {
+    if (!sigma2) return ORC_INVALID;
+    double s1 = 0.0, s2 = 0.0;
+    for (int64_t h = 0; h < n; ++h) {
+      if (!(sigma2[h] >= 0.0) || isinf(sigma2[h])) return ORC_INVALID;
+      s1 += sigma[h];
+      s2 += sigma2[h];
+    }
+    if (isinf(s1) || isinf(s2)) return ORC_INVALID;
+    double* t = (double*)malloc(sizeof(double) * (size_t)n);
+    for (int64_t h = 0; h < n; ++h) {
+      double a = s1 > 0.0 ? sigma[h] / s1 : 1.0 / (double)n;
+      double b = s2 > 0.0 ? sigma2[h] / s2 : 1.0 / (double)n;
+      t[h] = (a + b) / 2.0;
+    }
+    int rc = orc_allocate_budgets(t, L, H, C, s, W, total, mode, budgets);
+    free(t);
+    return rc;
+  }
+  if (variant == 4 || variant == 5) {
+    if (!(f >= 0.0 && f <= 1.0)) return ORC_INVALID;
+    int64_t k = (int64_t)floor(f * (double)n);
+    orc_head_t* order = (orc_head_t*)malloc(sizeof(orc_head_t) * (size_t)n);
+    for (int64_t h = 0; h < n; ++h) { order[h].sigma = sigma[h]; order[h].idx = h; }
+    qsort(order, (size_t)n, sizeof(orc_head_t), orc_cmp_head);
+    for (int64_t h = 0; h < n; ++h) budgets[h] = s + W;
+    for (int64_t j = 0; j < k; ++j) budgets[order[variant == 4 ? j : n - 1 - j].idx] = C;
+    free(order);
+    return ORC_OK;
+  }
+  return ORC_INVALID;
+}
+
+/* ------------------------------------------------------------------ */
 /* Observation-window attention (Sec. 3.3 last paragraph, Sec. 5).
  * Window row i of query head q sits at prompt position C-w+i and attends
  * causally to keys 0..C-w+i:  l_ij = scale * <q_i, k_j>.

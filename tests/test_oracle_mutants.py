@@ -17,6 +17,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 ALLOC = "tests/test_oracle_alloc.py"
 SCORES = "tests/test_oracle_scores.py"
 SELDEC = "tests/test_oracle_select_decode.py"
+VARIANTS = "tests/test_oracle_alloc_variants.py"
 
 MUTANTS = {
     "lse_not_causal": ("int64_t last = C - w + i; /* causal: keys 0..last */",
@@ -38,6 +39,14 @@ MUTANTS = {
                              "if (a->frac < b->frac) return -1;\n  if (a->frac > b->frac) return 1;", ALLOC),
     "decode_no_normalise": ("for (int t = 0; t < d; ++t) o[t] /= z;", "", SELDEC),
     "decode_wrong_group": ("int64_t b = bq / Hq, qh = bq % Hq, h = qh / G;", "int64_t b = bq / Hq, qh = bq % Hq, h = qh % Hkv;", SELDEC),
+    "thr_at_mean": ("t[h] = sigma[h] < mean ? 0.0 : sigma[h];", "t[h] = sigma[h] <= mean ? 0.0 : sigma[h];", VARIANTS),
+    "reverse_whole_budget": ("budgets[h] = s + W + (M - (budgets[h] - s - W));", "budgets[h] = s + W + (M - budgets[h]);",
+                             VARIANTS),
+    "mix_precedence": ("t[h] = (a + b) / 2.0;", "t[h] = a + b / 2.0;", VARIANTS),
+    "binary_round_up": ("int64_t k = (int64_t)floor(f * (double)n);", "int64_t k = (int64_t)ceil(f * (double)n);",
+                        VARIANTS),
+    "binary_reverse_same_side": ("budgets[order[variant == 4 ? j : n - 1 - j].idx] = C;", "budgets[order[j].idx] = C;",
+                                 VARIANTS),
 }
 
 
