@@ -63,6 +63,11 @@ def parse():
     ap.add_argument("--ratio", type=float, default=0.25, help="budget as a fraction of all rows")
     ap.add_argument("--caller-lse", action="store_true",
                     help="hand each layer its window-row LSE (as prefill attention would), skipping pass 1")
+    ap.add_argument("--alloc-variant", default="plain",
+                    choices=["plain", "thr", "reverse", "mix", "binary", "binary_reverse"],
+                    help="budget allocation variant of the head-configuration ablation (default plain)")
+    ap.add_argument("--full-fraction", type=float, default=0.25,
+                    help="fraction of heads with full KV for the binary variants")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0, metavar="MIB",
                     help="first run three elementwise copies of MIB MiB (fp32 x 1.0), untimed: under "
@@ -200,7 +205,15 @@ def main():
     t0 = time.perf_counter()
     scores = workloads.head_scores(wl)
     total = sg.total_from_ratio(args.ratio, L, Hkv, C, s, W)
-    budgets = sg.allocate_budgets(scores, L, Hkv, C, s, W, total).reshape(L, Hkv)
+    variant = ["plain", "thr", "reverse", "mix", "binary", "binary_reverse"].index(args.alloc_variant)
+    # the mix variant's second score vector stands in for retrieval-head scores the paper mixes in
+    scores2 = np.random.Generator(np.random.PCG64(wl.seed + 100)).beta(0.5, 2.0, size=scores.size)
+
+    def allocate():
+        return sg.allocate_budgets_variant(scores, L, Hkv, C, s, W, total, variant, scores2=scores2,
+                                           full_fraction=args.full_fraction)
+
+    budgets = allocate().reshape(L, Hkv)
     layers = [workloads.torch_layer_tensors(wl, l, dev) for l in range(L)]
     lse_in = [None] * L
     if args.caller_lse:
@@ -246,7 +259,7 @@ def main():
 
     def step():
         # S0 on the host, then every layer's compression, then every layer's decode
-        sg.allocate_budgets(scores, L, Hkv, C, s, W, total)
+        allocate()
         for l in range(L):
             t = layers[l]
             sg.compress_layer(t["q_win"], t["k"], t["v"], budgets[l], pool_kernel=kp, b_sink=s, b_window=W,
@@ -355,7 +368,8 @@ def main():
         dtype=wl.dtype, data="synthetic",
         config=dict(workload=wl.name, layers=L, batch=B, prompt=C, q_heads=Hq, kv_heads=Hkv, head_dim=d,
                     obs_window=w, pool_kernel=kp, b_sink=s, b_window=W, budget_ratio=args.ratio,
-                    total_budget_rows=int(total), window_lse="caller" if args.caller_lse else "computed"),
+                    total_budget_rows=int(budgets.sum()), window_lse="caller" if args.caller_lse else "computed",
+                    alloc_variant=args.alloc_variant),
         compress_tokens_per_s=round(tokens / (comp_ms / 1e3), 1) if comp_ms > 0 else None,
         decode=dict(gbps=round(dec_bytes / (dec_ms / 1e3) / 1e9, 1) if dec_ms > 0 else None,
                     frac_of_peak=round(dec_bytes / (dec_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4) if dec_ms > 0 else None,

@@ -94,6 +94,40 @@ sgdkv_status sgdkv_allocate_budgets(const double* head_scores, int32_t L, int32_
                                     int64_t b_sink, int64_t b_window, int64_t total_budget,
                                     int32_t mode, int64_t* budgets_out);
 
+/* Allocation variants of the head-configuration ablation (Appendix A.7,
+ * Table 5). With M = C - s - W and m_h the middle of the plain allocation:
+ *   SGDKV_ALLOC_PLAIN           sgdkv_allocate_budgets.
+ *   SGDKV_ALLOC_THR             scores strictly below the mean of all L*H
+ *                               scores become 0, then the plain allocation
+ *                               ("SGD-KV (thr)").
+ *   SGDKV_ALLOC_REVERSE         each head keeps M - m_h middle rows instead of
+ *                               m_h ("SGD-KV (Reverse)": 10 % becomes 90 %); the
+ *                               budgets then sum to L*H*(C + s + W) - total.
+ *   SGDKV_ALLOC_MIX             the plain allocation of the average of the
+ *                               normalised head_scores and the normalised
+ *                               second_scores (an all-zero vector normalises to
+ *                               uniform) ("SGD-KV + HeadKV" with R2 scores).
+ *   SGDKV_ALLOC_BINARY          the floor(full_fraction*L*H) heads first in
+ *                               (score descending, index ascending) order get
+ *                               C rows, the others s + W ("DuoAttention (Sum.)");
+ *                               total_budget and mode are not used.
+ *   SGDKV_ALLOC_BINARY_REVERSE  the same number of heads last in that order get
+ *                               C rows ("DuoAttention (Sum., Reverse)").
+ * second_scores: host [L][H], required by MIX only (else may be NULL).
+ * budgets_out: host [L][H] int64. Errors (nothing written): those of
+ * sgdkv_allocate_budgets for the variants that use it; an unknown variant;
+ * MIX without valid second_scores; full_fraction outside [0,1] (BINARY*). */
+#define SGDKV_ALLOC_PLAIN 0
+#define SGDKV_ALLOC_THR 1
+#define SGDKV_ALLOC_REVERSE 2
+#define SGDKV_ALLOC_MIX 3
+#define SGDKV_ALLOC_BINARY 4
+#define SGDKV_ALLOC_BINARY_REVERSE 5
+sgdkv_status sgdkv_allocate_budgets_variant(const double* head_scores, const double* second_scores, int32_t L,
+                                            int32_t H, int64_t C, int64_t b_sink, int64_t b_window,
+                                            int64_t total_budget, int32_t mode, int32_t variant,
+                                            double full_fraction, int64_t* budgets_out);
+
 /* ------------------------------------------------------------------ */
 /* One layer's compression (device).                                   */
 

@@ -25,7 +25,8 @@ LIB_PATH = os.path.join(_HERE, "libsgdkv.so")
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, 1, 2, 3, 4
 DTYPE_F32, DTYPE_BF16 = 0, 1
 SYMBOLS = ("sgdkv_last_error", "sgdkv_version", "sgdkv_reduce_query_head_scores", "sgdkv_total_from_ratio",
-           "sgdkv_allocate_budgets", "sgdkv_compress_workspace_size", "sgdkv_compress_layer",
+           "sgdkv_allocate_budgets", "sgdkv_allocate_budgets_variant", "sgdkv_compress_workspace_size",
+           "sgdkv_compress_layer",
            "sgdkv_decode_workspace_size", "sgdkv_decode_attention", "sgdkv_profile_enable",
            "sgdkv_profile_reset", "sgdkv_profile_read")
 
@@ -75,6 +76,7 @@ def load_library():
         "sgdkv_reduce_query_head_scores": [P, i32, i32, i32, P],
         "sgdkv_total_from_ratio": [f64, i32, i32, i64, i64, i64, i32, P],
         "sgdkv_allocate_budgets": [P, i32, i32, i64, i64, i64, i64, i32, P],
+        "sgdkv_allocate_budgets_variant": [P, P, i32, i32, i64, i64, i64, i64, i32, i32, f64, P],
         "sgdkv_compress_workspace_size": [P, P],
         "sgdkv_compress_layer": [P, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
         "sgdkv_decode_workspace_size": [P, P, P],
@@ -128,6 +130,26 @@ def allocate_budgets(scores, L: int, H: int, C: int, b_sink: int, b_window: int,
     out = np.zeros(L * H, dtype=np.int64)
     _check(load_library().sgdkv_allocate_budgets(_np_ptr(sc), L, H, C, b_sink, b_window, int(total), int(mode),
                                                  _np_ptr(out)))
+    return out
+
+
+ALLOC_PLAIN, ALLOC_THR, ALLOC_REVERSE, ALLOC_MIX, ALLOC_BINARY, ALLOC_BINARY_REVERSE = range(6)
+
+
+def allocate_budgets_variant(scores, L: int, H: int, C: int, b_sink: int, b_window: int, total: int,
+                             variant: int, mode: int = 0, scores2=None, full_fraction: float = 0.0) -> np.ndarray:
+    sc = np.ascontiguousarray(np.asarray(scores, dtype=np.float64).reshape(-1))
+    if sc.size != L * H:
+        raise SgdkvError(ERR_INVALID_ARG, "scores must hold L*H values")
+    s2 = None
+    if scores2 is not None:
+        s2 = np.ascontiguousarray(np.asarray(scores2, dtype=np.float64).reshape(-1))
+        if s2.size != L * H:
+            raise SgdkvError(ERR_INVALID_ARG, "scores2 must hold L*H values")
+    out = np.zeros(L * H, dtype=np.int64)
+    _check(load_library().sgdkv_allocate_budgets_variant(
+        _np_ptr(sc), _np_ptr(s2) if s2 is not None else None, L, H, C, b_sink, b_window, int(total), int(mode),
+        int(variant), float(full_fraction), _np_ptr(out)))
     return out
 
 

@@ -363,6 +363,70 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, CompressPlan& p) {
 
 extern "C" {
 
+sgdkv_status sgdkv_allocate_budgets_variant(const double* head_scores, const double* second_scores, int32_t L,
+                                            int32_t H, int64_t C, int64_t b_sink, int64_t b_window,
+                                            int64_t total_budget, int32_t mode, int32_t variant,
+                                            double full_fraction, int64_t* budgets_out) {
+  if (!head_scores || !budgets_out) return fail(SGDKV_ERR_INVALID_ARG, "NULL pointer");
+  if (sgdkv_status st = check_sizes(L, H, C, b_sink, b_window)) return st;
+  const int64_t n = (int64_t)L * H;
+  const int64_t reserve = b_sink + b_window;
+  const int64_t M = C - reserve;
+  for (int64_t h = 0; h < n; ++h)
+    if (!(head_scores[h] >= 0.0) || std::isinf(head_scores[h]))
+      return fail(SGDKV_ERR_INVALID_ARG, "score %lld is %g", (long long)h, head_scores[h]);
+  switch (variant) {
+    case SGDKV_ALLOC_PLAIN:
+      return sgdkv_allocate_budgets(head_scores, L, H, C, b_sink, b_window, total_budget, mode, budgets_out);
+    case SGDKV_ALLOC_THR: {
+      double sum = 0.0;
+      for (int64_t h = 0; h < n; ++h) sum += head_scores[h];
+      const double mean = sum / (double)n;
+      std::vector<double> kept(n);
+      for (int64_t h = 0; h < n; ++h) kept[h] = head_scores[h] < mean ? 0.0 : head_scores[h];
+      return sgdkv_allocate_budgets(kept.data(), L, H, C, b_sink, b_window, total_budget, mode, budgets_out);
+    }
+    case SGDKV_ALLOC_REVERSE: {
+      std::vector<int64_t> plain(n);
+      if (sgdkv_status st =
+              sgdkv_allocate_budgets(head_scores, L, H, C, b_sink, b_window, total_budget, mode, plain.data()))
+        return st;
+      for (int64_t h = 0; h < n; ++h) budgets_out[h] = reserve + (M - (plain[h] - reserve));
+      return ok();
+    }
+    case SGDKV_ALLOC_MIX: {
+      if (!second_scores) return fail(SGDKV_ERR_INVALID_ARG, "the mix variant needs second_scores");
+      double s1 = 0.0, s2 = 0.0;
+      for (int64_t h = 0; h < n; ++h) {
+        if (!(second_scores[h] >= 0.0) || std::isinf(second_scores[h]))
+          return fail(SGDKV_ERR_INVALID_ARG, "second score %lld is %g", (long long)h, second_scores[h]);
+        s1 += head_scores[h];
+        s2 += second_scores[h];
+      }
+      if (std::isinf(s1) || std::isinf(s2)) return fail(SGDKV_ERR_INVALID_ARG, "scores sum to infinity");
+      std::vector<double> avg(n);
+      for (int64_t h = 0; h < n; ++h) {
+        const double u = s1 > 0.0 ? head_scores[h] / s1 : 1.0 / (double)n;
+        const double v = s2 > 0.0 ? second_scores[h] / s2 : 1.0 / (double)n;
+        avg[h] = (u + v) / 2.0;
+      }
+      return sgdkv_allocate_budgets(avg.data(), L, H, C, b_sink, b_window, total_budget, mode, budgets_out);
+    }
+    case SGDKV_ALLOC_BINARY:
+    case SGDKV_ALLOC_BINARY_REVERSE: {
+      if (!(full_fraction >= 0.0 && full_fraction <= 1.0))
+        return fail(SGDKV_ERR_INVALID_ARG, "full_fraction %g outside [0, 1]", full_fraction);
+      const int64_t k = (int64_t)std::floor(full_fraction * (double)n);
+      const std::vector<int64_t> order = score_order(std::vector<double>(head_scores, head_scores + n));
+      for (int64_t h = 0; h < n; ++h) budgets_out[h] = reserve;
+      for (int64_t j = 0; j < k; ++j) budgets_out[order[variant == SGDKV_ALLOC_BINARY ? j : n - 1 - j]] = C;
+      return ok();
+    }
+    default:
+      return fail(SGDKV_ERR_INVALID_ARG, "unknown allocation variant %d", variant);
+  }
+}
+
 sgdkv_status sgdkv_compress_workspace_size(const sgdkv_compress_desc* desc, size_t* bytes) {
   if (!bytes) return fail(SGDKV_ERR_INVALID_ARG, "NULL bytes");
   CompressPlan p;

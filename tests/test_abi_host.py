@@ -111,6 +111,64 @@ def test_allocation_errors_leave_output_untouched():
         sg.total_from_ratio(1.5, 1, 4, 100, 2, 2)
 
 
+@settings(max_examples=300, deadline=None, suppress_health_check=[HealthCheck.too_slow])
+@given(problem, st.sampled_from([0, 1]), st.integers(0, 5), st.floats(0.0, 1.0),
+       st.lists(st.one_of(st.floats(0.0, 1.0), st.sampled_from([0.0, 1.0])), min_size=32, max_size=32))
+def test_allocation_variants_bit_exact_vs_oracle(p, mode, variant, f, second):
+    L, H, scores, C, s, W, frac = p
+    if s + W > C:
+        return
+    n = L * H
+    total = n * (s + W) + int(frac * n * (C - s - W))
+    sc2 = np.array(second[:n])
+    got = sg.allocate_budgets_variant(scores, L, H, C, s, W, total, variant, mode=mode, scores2=sc2,
+                                      full_fraction=f)
+    ref = oracle.allocate_variant(np.array(scores), L, H, C, s, W, total, variant, mode=mode, scores2=sc2,
+                                  full_fraction=f)
+    assert np.array_equal(got, ref)
+
+
+def test_allocation_variant_workloads_bit_exact():
+    import workloads
+    for wl in workloads.WORKLOADS.values():
+        sc = workloads.head_scores(wl)
+        sc2 = np.random.Generator(np.random.PCG64(7)).random(sc.size)  # stand-in for R2 scores
+        n = sc.size
+        for R in wl.ratios:
+            total = sg.total_from_ratio(R, wl.layers, wl.num_kv_heads, wl.seq_len, wl.b_sink, wl.b_window)
+            for v in range(6):
+                args = (sc, wl.layers, wl.num_kv_heads, wl.seq_len, wl.b_sink, wl.b_window, total, v)
+                kw = dict(scores2=sc2, full_fraction=0.25)
+                got = sg.allocate_budgets_variant(*args, **kw)
+                assert np.array_equal(got, oracle.allocate_variant(*args, **kw)), (wl.key, R, v)
+                if v == sg.ALLOC_BINARY:
+                    assert int((got == wl.seq_len).sum()) == n // 4
+
+
+def test_allocation_variant_errors_leave_output_untouched():
+    lib = sg.load_library()
+    out = np.full(4, -7, dtype=np.int64)
+    P = sg._np_ptr
+    sc = np.array([0.1, 0.4, 0.2, 0.3])
+    bad = [
+        (sc, None, 100, 2, 2, 50, 0, sg.ALLOC_MIX, 0.0),                             # no second vector
+        (sc, np.array([0.1, -1.0, 0.2, 0.3]), 100, 2, 2, 50, 0, sg.ALLOC_MIX, 0.0),  # bad second vector
+        (sc, None, 100, 2, 2, 50, 0, sg.ALLOC_BINARY, 1.5),                          # fraction
+        (sc, None, 100, 2, 2, 50, 0, sg.ALLOC_BINARY_REVERSE, -0.1),
+        (sc, None, 100, 2, 2, 50, 0, 6, 0.0),                                        # variant
+        (sc, None, 100, 2, 2, 15, 0, sg.ALLOC_REVERSE, 0.0),                         # total below the reserve
+        (sc, None, 100, 2, 2, 50, 3, sg.ALLOC_THR, 0.0),                             # mode
+        (np.array([0.1, np.nan, 0.2, 0.3]), None, 100, 2, 2, 50, 0, sg.ALLOC_BINARY, 0.5),
+    ]
+    for sc1, sc2, C, s, W, total, mode, variant, f in bad:
+        sc2p = P(np.ascontiguousarray(sc2)) if sc2 is not None else None
+        rc = lib.sgdkv_allocate_budgets_variant(P(np.ascontiguousarray(sc1)), sc2p, 1, 4, C, s, W, total, mode,
+                                                variant, f, P(out))
+        assert rc == sg.ERR_INVALID_ARG, (variant, f, total, mode)
+        assert lib.sgdkv_last_error()
+        assert np.all(out == -7)
+
+
 FAKE = 0x7F0000000000  # 256-aligned stand-in device address; validation never dereferences it
 
 
