@@ -58,12 +58,13 @@ def _load():
     lib.orc_allocate_variant.argtypes = [P, P, i32, i32, i64, i64, i64, i64, i32, i32, f64, P]
     lib.orc_window_lse.argtypes = [P, P, i32, i32, i32, i32, i64, i32, f64, P]
     lib.orc_window_colsum.argtypes = [P, P, P, i32, i32, i32, i32, i64, i32, f64, P]
+    lib.orc_window_colsum_ipt.argtypes = [P, P, P, i32, i32, i32, i32, i64, i32, f64, P, i32, P]
     lib.orc_pool.argtypes = [P, i64, i64, i32, P]
     lib.orc_select.argtypes = [P, i64, i32, i64, i64, i64, P]
     lib.orc_decode.argtypes = [P, P, P, P, i32, i32, i32, i32, f64, P, P]
     lib.orc_num_threads.argtypes = []
     for f in ("orc_reduce_group_max", "orc_total_from_ratio", "orc_allocate_budgets", "orc_allocate_variant",
-              "orc_window_lse", "orc_window_colsum", "orc_pool", "orc_select", "orc_decode",
+              "orc_window_lse", "orc_window_colsum", "orc_window_colsum_ipt", "orc_pool", "orc_select", "orc_decode",
               "orc_num_threads"):
         getattr(lib, f).restype = i32
     _lib = lib
@@ -160,16 +161,27 @@ def window_lse(q_win, k, num_kv_heads: int | None = None, scale=None) -> np.ndar
     return out
 
 
-def window_colsum(q_win, k, lse, scale=None) -> np.ndarray:
-    """Group-mean cumulative window attention of each scored key; [B, Hkv, C-w]."""
+GROUP_MEAN, GROUP_IPT_MAX, GROUP_IPT_MEAN, GROUP_IPT_ONLY = range(4)
+
+
+def window_colsum(q_win, k, lse, scale=None, agg: int = GROUP_MEAN, qhead_scores=None) -> np.ndarray:
+    """Cumulative window attention of each scored key, aggregated over the query group (the
+    plain mean, or an importance-weighted Ipt. variant, Appendix A.7); [B, Hkv, C-w]."""
     q = _f64(q_win)
     kk = _f64(k)
     ls = _f64(lse)
     B, Hq, w, d = q.shape
     _, Hkv, C, _ = kk.shape
     out = np.zeros((B, Hkv, C - w), dtype=np.float64)
-    _check(_load().orc_window_colsum(_ptr(q), _ptr(kk), _ptr(ls), B, Hq, Hkv, d, C, w,
-                                     _scale(d, scale), _ptr(out)), "window_colsum")
+    if agg == GROUP_MEAN:
+        _check(_load().orc_window_colsum(_ptr(q), _ptr(kk), _ptr(ls), B, Hq, Hkv, d, C, w,
+                                         _scale(d, scale), _ptr(out)), "window_colsum")
+        return out
+    qs = _f64(qhead_scores).reshape(-1)
+    if qs.size != Hq:
+        raise OracleError("qhead_scores must hold Hq values")
+    _check(_load().orc_window_colsum_ipt(_ptr(q), _ptr(kk), _ptr(ls), B, Hq, Hkv, d, C, w, _scale(d, scale),
+                                         _ptr(qs), int(agg), _ptr(out)), "window_colsum_ipt")
     return out
 
 
@@ -195,7 +207,7 @@ def select(pooled_row, C: int, w: int, s: int, W: int, m: int) -> np.ndarray:
 
 # -------------------------------------------------------------- full steps
 def compress(q_win, k, v, budgets, *, w: int, kp: int, s: int, W: int, scale=None,
-             lse=None) -> dict:
+             lse=None, agg: int = GROUP_MEAN, qhead_scores=None) -> dict:
     """One layer's compression: scores, pooling, per-head selection and gather.
 
     budgets: [Hkv] int (the layer's rows per KV head, shared by every sequence).
@@ -212,7 +224,7 @@ def compress(q_win, k, v, budgets, *, w: int, kp: int, s: int, W: int, scale=Non
     assert budgets.size == Hkv
     if lse is None:
         lse = window_lse(q, kk, scale=scale)
-    colsum = window_colsum(q, kk, lse, scale=scale)
+    colsum = window_colsum(q, kk, lse, scale=scale, agg=agg, qhead_scores=qhead_scores)
     pooled = pool(colsum, kp)
     T = int(budgets.sum())
     kept = np.zeros(B * T, dtype=np.int32)

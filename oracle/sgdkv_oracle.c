@@ -392,6 +392,56 @@ int orc_window_colsum(const double* q_win, const double* k, const double* lse, i
   return ORC_OK;
 }
 
+/* Importance-weighted group aggregation (Appendix A.7, "Ipt." rows of
+ * Table 5). With A_g[j] = sum_{i<w} exp(l_{q,i,j} - lse[b,q,i]) the window
+ * attention of query head q = h*G + g and sigma_q its summarization score
+ * (qscore[Hq], the same for every sequence):
+ *   agg 1 (Ipt., max):  a_j = max_g sigma_q * A_g[j]
+ *   agg 2 (Ipt., mean): a_j = (1/G) sum_g sigma_q * A_g[j]
+ *   agg 3 (Ipt., only): a_j = A_{g*}[j], g* the group's head with the largest
+ *                       sigma (ties: lower g); every head inherits its scores.
+ * agg 0 is the plain group mean (orc_window_colsum). Output [B][Hkv][C-w]. */
+int orc_window_colsum_ipt(const double* q_win, const double* k, const double* lse, int B, int Hq,
+                          int Hkv, int d, int64_t C, int w, double scale, const double* qscore, int agg,
+                          double* colsum) {
+  if (agg == 0) return orc_window_colsum(q_win, k, lse, B, Hq, Hkv, d, C, w, scale, colsum);
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || d < 1 || w < 1 || w > C || agg < 1 || agg > 3 || !qscore)
+    return ORC_INVALID;
+  for (int q = 0; q < Hq; ++q)
+    if (!(qscore[q] >= 0.0) || isinf(qscore[q])) return ORC_INVALID;
+  int G = Hq / Hkv;
+  int64_t n = C - w;
+  int64_t cols = (int64_t)B * Hkv * n;
+#pragma omp parallel for schedule(static)
+  for (int64_t c = 0; c < cols; ++c) {
+    int64_t j = c % n, h = (c / n) % Hkv, b = c / (n * Hkv);
+    const double* kj = k + (((int64_t)b * Hkv + h) * C + j) * d;
+    int gstar = 0;
+    for (int g = 1; g < G; ++g)
+      if (qscore[h * G + g] > qscore[h * G + gstar]) gstar = g;
+    double out = 0.0;
+    for (int g = 0; g < G; ++g) {
+      if (agg == 3 && g != gstar) continue;
+      int64_t q = h * G + g;
+      double A = 0.0;
+      for (int i = 0; i < w; ++i) {
+        int64_t r = ((int64_t)b * Hq + q) * w + i;
+        A += exp(scale * orc_dot(q_win + r * d, kj, d) - lse[r]);
+      }
+      if (agg == 1) {
+        double v = qscore[q] * A;
+        out = (g == 0 || v > out) ? v : out;
+      } else if (agg == 2) {
+        out += qscore[q] * A;
+      } else {
+        out = A;
+      }
+    }
+    colsum[c] = agg == 2 ? out / (double)G : out;
+  }
+  return ORC_OK;
+}
+
 /* 1-D average pooling along the key axis: odd kernel kp, stride 1, zero
  * padding of r = (kp-1)/2 on both ends, divisor always kp.
  * a and pooled are [rows][n].                                              */

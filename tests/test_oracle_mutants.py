@@ -18,6 +18,7 @@ ALLOC = "tests/test_oracle_alloc.py"
 SCORES = "tests/test_oracle_scores.py"
 SELDEC = "tests/test_oracle_select_decode.py"
 VARIANTS = "tests/test_oracle_alloc_variants.py"
+IPT = "tests/test_oracle_ipt.py"
 
 MUTANTS = {
     "lse_not_causal": ("int64_t last = C - w + i; /* causal: keys 0..last */",
@@ -47,6 +48,11 @@ MUTANTS = {
                         VARIANTS),
     "binary_reverse_same_side": ("budgets[order[variant == 4 ? j : n - 1 - j].idx] = C;", "budgets[order[j].idx] = C;",
                                  VARIANTS),
+    "ipt_max_as_min": ("out = (g == 0 || v > out) ? v : out;", "out = (g == 0 || v < out) ? v : out;", IPT),
+    "ipt_mean_no_divide": ("colsum[c] = agg == 2 ? out / (double)G : out;", "colsum[c] = out;", IPT),
+    "ipt_only_tie_high": ("if (qscore[h * G + g] > qscore[h * G + gstar]) gstar = g;",
+                          "if (qscore[h * G + g] >= qscore[h * G + gstar]) gstar = g;", IPT),
+    "ipt_unweighted": ("double v = qscore[q] * A;", "double v = A;", IPT),
 }
 
 
