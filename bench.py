@@ -68,6 +68,9 @@ def parse():
                     help="budget allocation variant of the head-configuration ablation (default plain)")
     ap.add_argument("--full-fraction", type=float, default=0.25,
                     help="fraction of heads with full KV for the binary variants")
+    ap.add_argument("--group-agg", default="mean", choices=["mean", "ipt_max", "ipt_mean", "ipt_only"],
+                    help="aggregation of a KV head's query heads: the plain mean (default) or an Ipt. variant; "
+                         "the Ipt. runs draw per-query-head scores and allocate on their group maxima")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0, metavar="MIB",
                     help="first run three elementwise copies of MIB MiB (fp32 x 1.0), untimed: under "
@@ -204,6 +207,14 @@ def main():
     # ------------------------------------------------------------ inputs (HBM-resident)
     t0 = time.perf_counter()
     scores = workloads.head_scores(wl)
+    agg = ["mean", "ipt_max", "ipt_mean", "ipt_only"].index(args.group_agg)
+    qscores = [None] * L
+    if agg:
+        # per-attention-head scores (Beta(0.5, 2), the workload's distribution); the allocation uses
+        # their maximum over each group, as the paper does for GQA models
+        qs = np.random.Generator(np.random.PCG64(wl.seed + 200)).beta(0.5, 2.0, size=(L, Hq))
+        scores = sg.reduce_query_head_scores(qs, Hkv).reshape(-1)
+        qscores = [qs[l] for l in range(L)]
     total = sg.total_from_ratio(args.ratio, L, Hkv, C, s, W)
     variant = ["plain", "thr", "reverse", "mix", "binary", "binary_reverse"].index(args.alloc_variant)
     # the mix variant's second score vector stands in for retrieval-head scores the paper mixes in
@@ -263,7 +274,8 @@ def main():
         for l in range(L):
             t = layers[l]
             sg.compress_layer(t["q_win"], t["k"], t["v"], budgets[l], pool_kernel=kp, b_sink=s, b_window=W,
-                              window_lse=lse_in[l], out=outs[l], workspace=ws_c, stream=stream)
+                              window_lse=lse_in[l], group_agg=agg, qhead_scores=qscores[l], out=outs[l],
+                              workspace=ws_c, stream=stream)
         for l in range(L):
             o = outs[l]
             sg.decode_attention(layers[l]["q"], o["k_c"], o["v_c"], o["offsets"], offsets_host[l], Hkv,
@@ -354,7 +366,7 @@ def main():
         vv = t["v"][:1].cpu().double().numpy()
         qq = t["q"][:1].cpu().double().numpy()
         tc0 = time.perf_counter()
-        res = oracle.compress(q_win, kk, vv, budgets[0], w=w, kp=kp, s=s, W=W)
+        res = oracle.compress(q_win, kk, vv, budgets[0], w=w, kp=kp, s=s, W=W, agg=agg, qhead_scores=qscores[0])
         oracle.decode(qq, res["k_c"], res["v_c"], res["offsets"], Hkv)
         cpu_s = time.perf_counter() - tc0
         cpu = dict(value=round(C / cpu_s, 1), unit="tokens/s per layer", cores=oracle.num_threads(), kind="oracle",
@@ -369,7 +381,7 @@ def main():
         config=dict(workload=wl.name, layers=L, batch=B, prompt=C, q_heads=Hq, kv_heads=Hkv, head_dim=d,
                     obs_window=w, pool_kernel=kp, b_sink=s, b_window=W, budget_ratio=args.ratio,
                     total_budget_rows=int(budgets.sum()), window_lse="caller" if args.caller_lse else "computed",
-                    alloc_variant=args.alloc_variant),
+                    alloc_variant=args.alloc_variant, group_agg=args.group_agg),
         compress_tokens_per_s=round(tokens / (comp_ms / 1e3), 1) if comp_ms > 0 else None,
         decode=dict(gbps=round(dec_bytes / (dec_ms / 1e3) / 1e9, 1) if dec_ms > 0 else None,
                     frac_of_peak=round(dec_bytes / (dec_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4) if dec_ms > 0 else None,

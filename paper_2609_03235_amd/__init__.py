@@ -26,7 +26,7 @@ OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, 1, 2, 3, 4
 DTYPE_F32, DTYPE_BF16 = 0, 1
 SYMBOLS = ("sgdkv_last_error", "sgdkv_version", "sgdkv_reduce_query_head_scores", "sgdkv_total_from_ratio",
            "sgdkv_allocate_budgets", "sgdkv_allocate_budgets_variant", "sgdkv_compress_workspace_size",
-           "sgdkv_compress_layer",
+           "sgdkv_compress_layer", "sgdkv_compress_layer_grouped",
            "sgdkv_decode_workspace_size", "sgdkv_decode_attention", "sgdkv_profile_enable",
            "sgdkv_profile_reset", "sgdkv_profile_read")
 
@@ -79,6 +79,7 @@ def load_library():
         "sgdkv_allocate_budgets_variant": [P, P, i32, i32, i64, i64, i64, i64, i32, i32, f64, P],
         "sgdkv_compress_workspace_size": [P, P],
         "sgdkv_compress_layer": [P, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
+        "sgdkv_compress_layer_grouped": [P, P, i32, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
         "sgdkv_decode_workspace_size": [P, P, P],
         "sgdkv_decode_attention": [P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
         "sgdkv_profile_enable": [i32],
@@ -201,10 +202,16 @@ def alloc_workspace(nbytes: int, device):
     return ws
 
 
+GROUP_MEAN, GROUP_IPT_MAX, GROUP_IPT_MEAN, GROUP_IPT_ONLY = range(4)
+
+
 def compress_layer(q_win, k, v, layer_budgets, *, pool_kernel: int, b_sink: int, b_window: int,
                    scale: float = 0.0, window_lse=None, scores_only: bool = False, with_scores: bool = True,
+                   group_agg: int = GROUP_MEAN, qhead_scores=None,
                    workspace=None, out: dict | None = None, stream=None) -> dict:
-    """Compress one layer (sgdkv_compress_layer). Returns k_c, v_c, kept_pos, offsets, scores."""
+    """Compress one layer (sgdkv_compress_layer_grouped; group_agg selects the plain group mean or an
+    Ipt. aggregation with the layer's per-query-head scores). Returns k_c, v_c, kept_pos, offsets,
+    scores."""
     import torch
     desc = compress_desc(q_win, k, pool_kernel=pool_kernel, b_sink=b_sink, b_window=b_window, scale=scale)
     B, Hkv, C, d = k.shape
@@ -227,8 +234,14 @@ def compress_layer(q_win, k, v, layer_budgets, *, pool_kernel: int, b_sink: int,
         res.setdefault("scores", torch.empty((B, Hkv, C - q_win.shape[2]), dtype=torch.float32, device=dev))
     if workspace is None:
         workspace = alloc_workspace(compress_workspace_size(desc), dev)
-    st = load_library().sgdkv_compress_layer(
-        ctypes.byref(desc), None if budgets is None else _np_ptr(budgets), _ptr(q_win), _ptr(k),
+    qs = None
+    if qhead_scores is not None:
+        qs = np.ascontiguousarray(np.asarray(qhead_scores, dtype=np.float64).reshape(-1))
+        if qs.size != q_win.shape[1]:
+            raise SgdkvError(ERR_INVALID_ARG, "qhead_scores must hold num_q_heads values")
+    st = load_library().sgdkv_compress_layer_grouped(
+        ctypes.byref(desc), None if budgets is None else _np_ptr(budgets), int(group_agg),
+        None if qs is None else _np_ptr(qs), _ptr(q_win), _ptr(k),
         _ptr(v) if v is not None else None, _ptr(window_lse), _ptr(res.get("k_c")), _ptr(res.get("v_c")),
         _ptr(res.get("kept_pos")), _ptr(res.get("offsets")), _ptr(res.get("scores")), _ptr(workspace),
         workspace.numel(), _stream(stream))

@@ -363,16 +363,27 @@ __global__ __launch_bounds__(kBlock) void lse_merge_kernel(CompressArgs a) {
 }
 
 // Pass 2: window-summed probabilities of every scored key --------------------
-template <typename T, int D, int NB>
-__device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float (*red)[kScoreWaves][kColTile], int seg,
-                             int wid, int lane, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
+//
+// Group aggregation. Row r of a KV head's window block belongs to query head
+// g = r / w of the group. The group mean, Ipt. mean and Ipt. only sum every
+// row with a weight (1, sigma_g, or 1 for the top-scored head and 0 for the
+// others), folded into the exp2 argument as log2 of the weight, so they cost
+// nothing extra. Ipt. max (MAXG) needs each query head's own column sum: the
+// waves keep one partial per row block (16 rows of a single head when w is a
+// multiple of 16), and the reduction adds each head's blocks, weights them
+// and takes the maximum.
+template <typename T, int D, int NB, int RBW, bool MAXG>
+__device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float (*red)[kScoreWaves][MAXG ? RBW : 1][kColTile],
+                             int seg, int wid, int lane, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
                              const rsrc_t& kr, int64_t key0, int64_t key_end) {
   constexpr int NBX = NB > 0 ? NB : 1;
   constexpr int TILE = kColTile;
   const int lr = lane & 15, lg = lane >> 4;
-  // -lse2 of this lane's row slots; rows past R get -inf so they add exp2(-inf) = 0
+  const int h = seg % a.Hkv;
+  // -lse2 (+ log2 of the row weight) of this lane's row slots; rows past R get -inf so they add 0
   const uint64_t nl = (uint64_t)a.B * a.Hkv * a.R;
   const bool natural = a.window_lse != nullptr;
+  const bool weighted = !MAXG && a.agg != 0;
   const rsrc_t lr2 = make_rsrc(natural ? (const void*)a.window_lse : (const void*)a.lse2, nl * sizeof(float));
   float nlse[NBX][4];
 #pragma unroll
@@ -382,7 +393,8 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float (*red)[kSc
       const int row = (wid + kScoreWaves * j) * 16 + 4 * lg + i;
       float l = ldf(lr2, (uint32_t)(((int64_t)seg * a.R + row) * 4));
       if (natural) l *= 1.44269504088896340736f;
-      nlse[j][i] = row < a.R ? -l : -INFINITY;
+      const float lw = weighted && row < a.R ? a.qweight[h * a.G + row / a.w] : 0.f;
+      nlse[j][i] = row < a.R ? lw - l : -INFINITY;
     }
   const float c2 = a.c2;
   const rsrc_t cr = make_rsrc(a.colsum + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
@@ -395,45 +407,70 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float (*red)[kSc
   static_assert(CPW <= 16 && 64 % CPW == 0 && PPL >= 1 && PPL * LPC == kScoreWaves, "reduction layout");
   const int rcol = CPW * wid + lane % CPW, rgrp = lane / CPW;
   auto reduce = [&](int64_t t) {  // t may be -1: nothing is stored
-    const float(*r)[TILE] = red[(t + 3) % 3];
-    float v = r[rgrp][rcol];
+    const float(*r)[MAXG ? RBW : 1][TILE] = red[(t + 3) % 3];
+    float v = 0.f;
+    if constexpr (MAXG) {
+      // the LPC lanes of a column take the group's heads in turn: sum a head's w/16 blocks
+      // (block b sits with wave b % 8, slot b / 8), weight it, keep the maximum
+      const int bph = a.w / 16;
+      for (int g = rgrp; g < a.G; g += LPC) {
+        float sum = 0.f;
+        for (int bb = g * bph; bb < (g + 1) * bph; ++bb) sum += r[bb % kScoreWaves][bb / kScoreWaves][rcol];
+        v = fmaxf(v, a.qweight[h * a.G + g] * sum);
+      }
 #pragma unroll
-    for (int k = 1; k < PPL; ++k) v += r[rgrp + LPC * k][rcol];
+      for (int o = CPW; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+      v = max_lane_groups(v);
+    } else {
+      v = r[rgrp][0][rcol];
 #pragma unroll
-    for (int o = CPW; o < 16; o <<= 1) v += __shfl_xor(v, o, 64);
-    v = sum_lane_groups(v);
+      for (int k = 1; k < PPL; ++k) v += r[rgrp + LPC * k][0][rcol];
+#pragma unroll
+      for (int o = CPW; o < 16; o <<= 1) v += __shfl_xor(v, o, 64);
+      v = sum_lane_groups(v);
+    }
     const int64_t key = key0 + t * TILE + rcol;
     const bool store = t >= 0 && lane < CPW && key < key_end;
-    stf(cr, store ? (uint32_t)(key * 4) : (uint32_t)(a.n_scored * 4), v * a.inv_G);
+    stf(cr, store ? (uint32_t)(key * 4) : (uint32_t)(a.n_scored * 4), v * a.out_scale);
   };
   const int64_t ntiles = (key_end - key0 + TILE - 1) / TILE;
   chunk_pipeline<T, D, NB, TILE>(
       kbuf, kr, key0, a.C, ntiles, lr, lg, qa, [](const f32x4(&)[NBX]) {},
       [&](int64_t t, int sub, const f32x4(&acc)[NBX]) {
-        float p = 0.f;
-        if constexpr (NB > 0) {
-          // four independent partial sums (one per row slot) keep the add chains short
-          float pp[4];
+        if constexpr (MAXG) {
+          // one column partial per row block (a single query head's rows)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) pp[i] = fast_exp2(fmaf(acc[0][i], c2, nlse[0][i]));
+          for (int j = 0; j < NB; ++j) {
+            const float p = (fast_exp2(fmaf(acc[j][0], c2, nlse[j][0])) + fast_exp2(fmaf(acc[j][1], c2, nlse[j][1]))) +
+                            (fast_exp2(fmaf(acc[j][2], c2, nlse[j][2])) + fast_exp2(fmaf(acc[j][3], c2, nlse[j][3])));
+            red[t % 3][wid][j][16 * sub + lr] = sum_lane_groups(p);
+          }
+        } else {
+          float p = 0.f;
+          if constexpr (NB > 0) {
+            // four independent partial sums (one per row slot) keep the add chains short
+            float pp[4];
 #pragma unroll
-          for (int j = 1; j < NB; ++j)
+            for (int i = 0; i < 4; ++i) pp[i] = fast_exp2(fmaf(acc[0][i], c2, nlse[0][i]));
 #pragma unroll
-            for (int i = 0; i < 4; ++i) pp[i] += fast_exp2(fmaf(acc[j][i], c2, nlse[j][i]));
-          p = sum_lane_groups((pp[0] + pp[1]) + (pp[2] + pp[3]));
+            for (int j = 1; j < NB; ++j)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) pp[i] += fast_exp2(fmaf(acc[j][i], c2, nlse[j][i]));
+            p = sum_lane_groups((pp[0] + pp[1]) + (pp[2] + pp[3]));
+          }
+          red[t % 3][wid][0][16 * sub + lr] = p;  // all four lane groups hold the same value
         }
-        red[t % 3][wid][16 * sub + lr] = p;  // all four lane groups hold the same value
       },
       [&](int64_t t) { reduce(t - 1); }, [](int64_t) {});
   __syncthreads();
   reduce(ntiles - 1);
 }
 
-template <typename T, int D, int RBW>
+template <typename T, int D, int RBW, bool MAXG>
 __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) {
   using G = TileGeom<T, D>;
   __shared__ __attribute__((aligned(16))) char ktile[2 * kColTile * G::LDS_STRIDE];
-  __shared__ float red[3][kScoreWaves][kColTile];
+  __shared__ float red[3][kScoreWaves][MAXG ? RBW : 1][kColTile];
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
   const int64_t key0 = (int64_t)blockIdx.x * a.score_chunk;
@@ -445,14 +482,14 @@ __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) 
   load_group_queries<T, D, RBW>(a, b, h, wid, lane, qa);
   const int nrb = (a.R + 15) / 16;
   if (wid + kScoreWaves * (RBW - 1) < nrb) {
-    colsum_chunk<T, D, RBW>(a, ktile, red, seg, wid, lane, qa, kr, key0, key_end);
+    colsum_chunk<T, D, RBW, RBW, MAXG>(a, ktile, red, seg, wid, lane, qa, kr, key0, key_end);
   } else {
     Frag<T> qb[RBW > 1 ? RBW - 1 : 1][G::NC];
 #pragma unroll
     for (int j = 0; j < RBW - 1; ++j)
 #pragma unroll
       for (int c = 0; c < G::NC; ++c) qb[j][c] = qa[j][c];
-    colsum_chunk<T, D, RBW - 1>(a, ktile, red, seg, wid, lane, qb, kr, key0, key_end);
+    colsum_chunk<T, D, RBW - 1, RBW, MAXG>(a, ktile, red, seg, wid, lane, qb, kr, key0, key_end);
   }
 }
 
@@ -467,8 +504,12 @@ static hipError_t launch_scores_t(const CompressArgs& a, hipStream_t st) {
     SGDKV_LAUNCH("lse_merge", lse_merge_kernel, dim3((unsigned)((nrows + rows_per_block - 1) / rows_per_block)),
                  dim3(kBlock), st, a);
   }
-  if (a.n_col_chunks > 0)
-    SGDKV_LAUNCH("score_colsum", (colsum_kernel<T, D, RBW>), dim3(a.n_col_chunks, a.B * a.Hkv), sblk, st, a);
+  if (a.n_col_chunks > 0) {
+    if (a.agg == 1)
+      SGDKV_LAUNCH("score_colsum", (colsum_kernel<T, D, RBW, true>), dim3(a.n_col_chunks, a.B * a.Hkv), sblk, st, a);
+    else
+      SGDKV_LAUNCH("score_colsum", (colsum_kernel<T, D, RBW, false>), dim3(a.n_col_chunks, a.B * a.Hkv), sblk, st, a);
+  }
   return hipGetLastError();
 }
 

@@ -323,7 +323,7 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, CompressPlan& p) {
   a.n_scored = a.C - a.w;
   const double scale = d->scale > 0.f ? (double)d->scale : 1.0 / std::sqrt((double)d->head_dim);
   a.c2 = (float)(scale * 1.4426950408889634074);
-  a.inv_G = 1.0f / (float)G;
+  a.out_scale = 1.0f / (float)G;
 
   const int64_t nseg = (int64_t)a.B * a.Hkv;
   // score workgroups: about 2048 in total; a chunk is a whole number of key tiles, so no
@@ -439,9 +439,47 @@ sgdkv_status sgdkv_compress_layer(const sgdkv_compress_desc* desc, const int64_t
                                   const void* q_win, const void* k, const void* v, const float* window_lse,
                                   void* k_out, void* v_out, int32_t* kept_pos_out, int64_t* offsets_out,
                                   float* scores_out, void* workspace, size_t workspace_bytes, void* stream) {
+  return sgdkv_compress_layer_grouped(desc, layer_budgets, SGDKV_GROUP_MEAN, nullptr, q_win, k, v, window_lse,
+                                      k_out, v_out, kept_pos_out, offsets_out, scores_out, workspace,
+                                      workspace_bytes, stream);
+}
+
+sgdkv_status sgdkv_compress_layer_grouped(const sgdkv_compress_desc* desc, const int64_t* layer_budgets,
+                                          int32_t group_agg, const double* qhead_scores, const void* q_win,
+                                          const void* k, const void* v, const float* window_lse, void* k_out,
+                                          void* v_out, int32_t* kept_pos_out, int64_t* offsets_out,
+                                          float* scores_out, void* workspace, size_t workspace_bytes,
+                                          void* stream) {
   CompressPlan p;
   if (sgdkv_status st = plan_compress(desc, p)) return st;
   sgdkv::CompressArgs& a = p.a;
+  if (group_agg < SGDKV_GROUP_MEAN || group_agg > SGDKV_GROUP_IPT_ONLY)
+    return fail(SGDKV_ERR_INVALID_ARG, "group_agg %d is not 0..3", group_agg);
+  a.agg = group_agg;
+  if (group_agg != SGDKV_GROUP_MEAN) {
+    if (!qhead_scores) return fail(SGDKV_ERR_INVALID_ARG, "group_agg %d needs qhead_scores", group_agg);
+    if (a.Hq > sgdkv::kMaxIptQHeads)
+      return fail(SGDKV_ERR_UNSUPPORTED, "num_q_heads %d > %d with an Ipt. aggregation", a.Hq, sgdkv::kMaxIptQHeads);
+    if (group_agg == SGDKV_GROUP_IPT_MAX && a.w % 16 != 0)
+      return fail(SGDKV_ERR_UNSUPPORTED, "Ipt. max needs obs_window %% 16 == 0 (got %d)", a.w);
+    for (int q = 0; q < a.Hq; ++q)
+      if (!(qhead_scores[q] >= 0.0) || std::isinf(qhead_scores[q]))
+        return fail(SGDKV_ERR_INVALID_ARG, "qhead_scores[%d] is %g", q, qhead_scores[q]);
+    for (int h = 0; h < a.Hkv; ++h) {
+      int top = 0;  // the group's highest score, lower query head on ties
+      for (int g = 1; g < a.G; ++g)
+        if (qhead_scores[h * a.G + g] > qhead_scores[h * a.G + top]) top = g;
+      for (int g = 0; g < a.G; ++g) {
+        const double sc = qhead_scores[h * a.G + g];
+        float wgt;
+        if (group_agg == SGDKV_GROUP_IPT_MAX) wgt = (float)sc;
+        else if (group_agg == SGDKV_GROUP_IPT_MEAN) wgt = sc > 0.0 ? (float)std::log2(sc) : -INFINITY;
+        else wgt = g == top ? 0.0f : -INFINITY;
+        a.qweight[h * a.G + g] = wgt;
+      }
+    }
+    a.out_scale = group_agg == SGDKV_GROUP_IPT_MEAN ? 1.0f / (float)a.G : 1.0f;
+  }
   const int n_out = (k_out != nullptr) + (v_out != nullptr) + (kept_pos_out != nullptr) + (offsets_out != nullptr);
   if (n_out != 0 && n_out != 4)
     return fail(SGDKV_ERR_INVALID_ARG, "k_out, v_out, kept_pos_out, offsets_out must be all set or all NULL");

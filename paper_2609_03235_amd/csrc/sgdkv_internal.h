@@ -11,6 +11,7 @@ namespace sgdkv {
 constexpr int kMaxKvHeads = 64;    // per-head tables travel by value in kernel arguments
 constexpr int kMaxGroupRows = 512; // G*w rows of one KV head's window queries
 constexpr int kMaxDecodeGroup = 16;
+constexpr int kMaxIptQHeads = 256;  // query heads per layer the Ipt. aggregations accept
 constexpr int kBlock = 256;        // threads per workgroup in every kernel
 constexpr int kLseTile = 128;      // keys staged in LDS per step of score pass 1
 constexpr int kColTile = 64;       // keys staged in LDS per step of score pass 2
@@ -37,7 +38,12 @@ struct CompressArgs {
   int B, Hq, Hkv, G, D, w, kp, R, dtype;
   int64_t C, s, W, n_scored;  // n_scored = C - w
   float c2;                   // logit scale * log2(e): scores work in base-2 units
-  float inv_G;
+  float out_scale;            // factor on each key's aggregated window sum: 1/G for the means, else 1
+  // group aggregation: 0 mean, 1 Ipt. max, 2 Ipt. mean, 3 Ipt. only (see sgdkv.h)
+  int agg;
+  // per query head q: log2 of its rows' weight (agg 2, 3; -inf for weight 0), or the weight
+  // itself (agg 1); unused for agg 0
+  float qweight[kMaxIptQHeads];
   // inputs
   const void* q_win;
   const void* k;

@@ -222,6 +222,36 @@ def test_compress_validation():
     assert _compress(_desc(), good, ws=None) == sg.ERR_WORKSPACE
 
 
+def _compress_grouped(desc, agg, qs, budgets=(512, 512)):
+    lib = sg.load_library()
+    need = ctypes.c_size_t(0)
+    lib.sgdkv_compress_workspace_size(ctypes.byref(desc), ctypes.byref(need))
+    b = np.ascontiguousarray(np.asarray(budgets, dtype=np.int64))
+    q = None if qs is None else np.ascontiguousarray(np.asarray(qs, dtype=np.float64))
+    return lib.sgdkv_compress_layer_grouped(
+        ctypes.byref(desc), sg._np_ptr(b), agg, None if q is None else sg._np_ptr(q), FAKE, FAKE, FAKE, None,
+        FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need.value, None)
+
+
+def test_grouped_compress_validation():
+    four = [0.5, 0.2, 0.1, 0.9]  # the default descriptor has 4 query heads
+    cases = [
+        (_desc(), 4, four, sg.ERR_INVALID_ARG),                           # unknown aggregation
+        (_desc(), -1, four, sg.ERR_INVALID_ARG),
+        (_desc(), sg.GROUP_IPT_MAX, None, sg.ERR_INVALID_ARG),            # scores needed
+        (_desc(), sg.GROUP_IPT_MEAN, [0.5, -0.2, 0.1, 0.9], sg.ERR_INVALID_ARG),
+        (_desc(), sg.GROUP_IPT_ONLY, [0.5, np.nan, 0.1, 0.9], sg.ERR_INVALID_ARG),
+        (_desc(obs_window=20), sg.GROUP_IPT_MAX, four, sg.ERR_UNSUPPORTED),  # w % 16
+        (_desc(num_q_heads=320, num_kv_heads=64, obs_window=32), sg.GROUP_IPT_MEAN, [0.1] * 320,
+         sg.ERR_UNSUPPORTED),                                               # too many query heads
+    ]
+    for desc, agg, qs, want in cases:
+        budgets = (512,) * desc.num_kv_heads
+        assert _compress_grouped(desc, agg, qs, budgets) == want, (agg, qs)
+        msg = sg.load_library().sgdkv_last_error().decode()
+        assert ("group" in msg or "Ipt" in msg or "qhead" in msg or "num_q_heads" in msg), msg
+
+
 def test_workspace_size_independent_of_budgets():
     n = sg.compress_workspace_size(_desc())
     assert n > 0 and n % 256 == 0

@@ -89,11 +89,13 @@ def _check_gather(res, k, v, budgets):
             assert torch.equal(res["v_c"][lo:hi], v[b, h][pos]), f"V gather b={b} h={h}"
 
 
-def _compress_both(q_win, k, v, budgets, *, kp, s, W, window_lse=None, orc_lse=None):
+def _compress_both(q_win, k, v, budgets, *, kp, s, W, window_lse=None, orc_lse=None, agg=0, qhead_scores=None):
     w = q_win.shape[2]
-    res = sg.compress_layer(q_win, k, v, budgets, pool_kernel=kp, b_sink=s, b_window=W, window_lse=window_lse)
+    res = sg.compress_layer(q_win, k, v, budgets, pool_kernel=kp, b_sink=s, b_window=W, window_lse=window_lse,
+                            group_agg=agg, qhead_scores=qhead_scores)
     torch.cuda.synchronize()
-    orc = oracle.compress(_f64(q_win), _f64(k), _f64(v), budgets, w=w, kp=kp, s=s, W=W, lse=orc_lse)
+    orc = oracle.compress(_f64(q_win), _f64(k), _f64(v), budgets, w=w, kp=kp, s=s, W=W, lse=orc_lse, agg=agg,
+                          qhead_scores=qhead_scores)
     return res, orc
 
 
@@ -179,6 +181,34 @@ def test_bf16_qwen_shaped(B, C, Hq, Hkv, d):
     _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "bf16")
     _check_gather(res, t["k"], t["v"], budgets)
     _decode_on_oracle_cache(orc, t["q"], Hkv, torch.bfloat16, 2e-2, "bf16")
+
+
+@pytest.mark.parametrize("agg", [sg.GROUP_IPT_MAX, sg.GROUP_IPT_MEAN, sg.GROUP_IPT_ONLY])
+@pytest.mark.parametrize("B,C,Hq,Hkv,d,w", [(2, 2600, 28, 4, 128, 64), (1, 1500, 16, 2, 64, 32)])
+def test_ipt_group_aggregation(agg, B, C, Hq, Hkv, d, w):
+    """Ipt. max / mean / only (Appendix A.7): per-query-head window attention weighted by the
+    summarization score, then max or mean over the group, or the top head's alone. The scores
+    include a zero, a tie for the top of a group and a spread of magnitudes."""
+    wl, t = _qwen_small(B, C, Hq=Hq, Hkv=Hkv, d=d, w=w)
+    s, W = wl.b_sink, wl.b_window
+    rng = np.random.Generator(np.random.PCG64(31 + agg))
+    qs = rng.beta(0.5, 2.0, size=Hq)
+    qs[1] = 0.0
+    qs[Hq // Hkv] = qs[Hq // Hkv + 1] = qs.max() + 0.05  # tie for the top of group 1
+    budgets = np.array([int(C * f) for f in (0.3, 0.5, 0.25, 0.4, 0.2, 0.6, 0.35, 0.45)[:Hkv]])
+    budgets = np.maximum(budgets, s + W)
+    _announce(f"Ipt agg={agg} B={B} C={C} Hq={Hq} Hkv={Hkv} d={d} w={w}")
+    res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=7, s=s, W=W, agg=agg, qhead_scores=qs)
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], f"ipt{agg}")
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, f"ipt{agg}")
+    _check_gather(res, t["k"], t["v"], budgets)
+    if agg == sg.GROUP_IPT_MEAN:
+        # unit scores reduce the weighted mean to the plain group mean, to the last bit
+        one = sg.compress_layer(t["q_win"], t["k"], t["v"], budgets, pool_kernel=7, b_sink=s, b_window=W,
+                                group_agg=agg, qhead_scores=np.ones(Hq))
+        plain = sg.compress_layer(t["q_win"], t["k"], t["v"], budgets, pool_kernel=7, b_sink=s, b_window=W)
+        torch.cuda.synchronize()
+        assert torch.equal(one["scores"], plain["scores"]) and torch.equal(one["kept_pos"], plain["kept_pos"])
 
 
 def test_caller_supplied_lse_and_scores_only():

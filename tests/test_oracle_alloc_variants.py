@@ -64,8 +64,12 @@ def test_thr_zeroes_below_mean(p):
     sc = np.array(sc)
     b = oracle.allocate_variant(sc, L, H, C, s, W, total, oracle.ALLOC_THR, mode=mode)
     assert int(b.sum()) == total and np.all(b >= s + W) and np.all(b <= C)
-    mean = Fraction(sum(Fraction(x) for x in sc.tolist())) / n
-    kept = [Fraction(x) >= mean for x in sc.tolist()]
+    # the threshold is the fp64 mean (sum in flat order, then / n), as the allocation defines it
+    tot64 = 0.0
+    for x in sc.tolist():
+        tot64 += x
+    mean = tot64 / n
+    kept = [x >= mean for x in sc.tolist()]
     # without caps, the shares of the surviving heads are exact rationals and a zeroed head gets nothing
     T = total - n * (s + W)
     tot = sum(Fraction(x) for x, k in zip(sc.tolist(), kept) if k)

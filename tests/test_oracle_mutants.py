@@ -25,7 +25,8 @@ MUTANTS = {
                        "int64_t last = C - 1;", SCORES),
     "lse_off_by_one": ("for (int64_t j = 0; j <= last; ++j) z +=", "for (int64_t j = 0; j < last; ++j) z +=", SCORES),
     "colsum_no_group_mean": ("colsum[c] = acc / (double)G;", "colsum[c] = acc;", SCORES),
-    "colsum_lse_sign": ("orc_dot(q_win + r * d, kj, d) - lse[r]", "orc_dot(q_win + r * d, kj, d) + lse[r] - 2.0 * lse[r] * (i == 0)", SCORES),
+    "colsum_lse_sign": ("acc += exp(scale * orc_dot(q_win + r * d, kj, d) - lse[r]",
+                        "acc += exp(scale * orc_dot(q_win + r * d, kj, d) + lse[r] - 2.0 * lse[r] * (i == 0)", SCORES),
     "colsum_no_scale": ("acc += exp(scale * orc_dot(q_win + r * d, kj, d)", "acc += exp(orc_dot(q_win + r * d, kj, d)", SCORES),
     "lse_wrong_group": ("int64_t h = q / G;\n    const double* qi", "int64_t h = q % Hkv;\n    const double* qi", SCORES),
     "pool_divisor": ("pooled[row * n + j] = s / (double)kp;", "pooled[row * n + j] = s / (double)(kp - 1);", SCORES),
@@ -53,6 +54,8 @@ MUTANTS = {
     "ipt_only_tie_high": ("if (qscore[h * G + g] > qscore[h * G + gstar]) gstar = g;",
                           "if (qscore[h * G + g] >= qscore[h * G + gstar]) gstar = g;", IPT),
     "ipt_unweighted": ("double v = qscore[q] * A;", "double v = A;", IPT),
+    "ipt_no_lse": ("A += exp(scale * orc_dot(q_win + r * d, kj, d) - lse[r]);",
+                   "A += exp(scale * orc_dot(q_win + r * d, kj, d));", IPT),
 }
 
 
