@@ -56,11 +56,11 @@ def _load():
     lib.orc_total_from_ratio.argtypes = [f64, i32, i32, i64, i64, i64, i32, P]
     lib.orc_allocate_budgets.argtypes = [P, i32, i32, i64, i64, i64, i64, i32, P]
     lib.orc_allocate_variant.argtypes = [P, P, i32, i32, i64, i64, i64, i64, i32, i32, f64, P]
-    lib.orc_window_lse.argtypes = [P, P, i32, i32, i32, i32, i64, i32, f64, P]
-    lib.orc_window_colsum.argtypes = [P, P, P, i32, i32, i32, i32, i64, i32, f64, P]
-    lib.orc_window_colsum_ipt.argtypes = [P, P, P, i32, i32, i32, i32, i64, i32, f64, P, i32, P]
+    lib.orc_window_lse.argtypes = [P, P, i32, i32, i32, i32, i64, i32, i64, f64, P]
+    lib.orc_window_colsum.argtypes = [P, P, P, i32, i32, i32, i32, i64, i32, i64, f64, P]
+    lib.orc_window_colsum_ipt.argtypes = [P, P, P, i32, i32, i32, i32, i64, i32, i64, f64, P, i32, P]
     lib.orc_pool.argtypes = [P, i64, i64, i32, P]
-    lib.orc_select.argtypes = [P, i64, i32, i64, i64, i64, P]
+    lib.orc_select.argtypes = [P, i64, i64, i64, i64, i64, P]
     lib.orc_decode.argtypes = [P, P, P, P, i32, i32, i32, i32, f64, P, P]
     lib.orc_num_threads.argtypes = []
     for f in ("orc_reduce_group_max", "orc_total_from_ratio", "orc_allocate_budgets", "orc_allocate_variant",
@@ -149,38 +149,47 @@ def _scale(d: int, scale):
     return 1.0 / math.sqrt(d) if scale is None or scale == 0 else float(scale)
 
 
-def window_lse(q_win, k, num_kv_heads: int | None = None, scale=None) -> np.ndarray:
-    """LSE of each observation-window row over its causal keys; [B, Hq, w]."""
+def _win0(C: int, w: int, win0):
+    return C - w if win0 is None else int(win0)
+
+
+def window_lse(q_win, k, num_kv_heads: int | None = None, scale=None, win0=None) -> np.ndarray:
+    """LSE of each observation-window row over its causal keys; [B, Hq, w]. Row i sits at position
+    win0 + i (default C - w: the last w prompt tokens)."""
     q = _f64(q_win)
     kk = _f64(k)
     B, Hq, w, d = q.shape
     _, Hkv, C, _ = kk.shape
     out = np.zeros((B, Hq, w), dtype=np.float64)
-    _check(_load().orc_window_lse(_ptr(q), _ptr(kk), B, Hq, Hkv, d, C, w, _scale(d, scale), _ptr(out)),
-           "window_lse")
+    _check(_load().orc_window_lse(_ptr(q), _ptr(kk), B, Hq, Hkv, d, C, w, _win0(C, w, win0), _scale(d, scale),
+                                  _ptr(out)), "window_lse")
     return out
 
 
 GROUP_MEAN, GROUP_IPT_MAX, GROUP_IPT_MEAN, GROUP_IPT_ONLY = range(4)
 
 
-def window_colsum(q_win, k, lse, scale=None, agg: int = GROUP_MEAN, qhead_scores=None) -> np.ndarray:
-    """Cumulative window attention of each scored key, aggregated over the query group (the
-    plain mean, or an importance-weighted Ipt. variant, Appendix A.7); [B, Hkv, C-w]."""
+def window_colsum(q_win, k, lse, scale=None, agg: int = GROUP_MEAN, qhead_scores=None, win0=None) -> np.ndarray:
+    """Cumulative window attention of each scored key (keys before the window, [0, win0)),
+    aggregated over the query group (the plain mean, or an importance-weighted Ipt. variant,
+    Appendix A.7); [B, Hkv, win0]."""
     q = _f64(q_win)
     kk = _f64(k)
     ls = _f64(lse)
     B, Hq, w, d = q.shape
     _, Hkv, C, _ = kk.shape
-    out = np.zeros((B, Hkv, C - w), dtype=np.float64)
+    p0 = _win0(C, w, win0)
+    if not 0 <= p0 <= C:
+        raise OracleError("win0 outside [0, C]")
+    out = np.zeros((B, Hkv, p0), dtype=np.float64)
     if agg == GROUP_MEAN:
-        _check(_load().orc_window_colsum(_ptr(q), _ptr(kk), _ptr(ls), B, Hq, Hkv, d, C, w,
+        _check(_load().orc_window_colsum(_ptr(q), _ptr(kk), _ptr(ls), B, Hq, Hkv, d, C, w, p0,
                                          _scale(d, scale), _ptr(out)), "window_colsum")
         return out
     qs = _f64(qhead_scores).reshape(-1)
     if qs.size != Hq:
         raise OracleError("qhead_scores must hold Hq values")
-    _check(_load().orc_window_colsum_ipt(_ptr(q), _ptr(kk), _ptr(ls), B, Hq, Hkv, d, C, w, _scale(d, scale),
+    _check(_load().orc_window_colsum_ipt(_ptr(q), _ptr(kk), _ptr(ls), B, Hq, Hkv, d, C, w, p0, _scale(d, scale),
                                          _ptr(qs), int(agg), _ptr(out)), "window_colsum_ipt")
     return out
 
@@ -195,24 +204,27 @@ def pool(a, kp: int) -> np.ndarray:
     return out
 
 
-def select(pooled_row, C: int, w: int, s: int, W: int, m: int) -> np.ndarray:
-    """Kept positions of one head, ascending: sink, top-m candidates, window."""
+def select(pooled_row, C: int, w: int, s: int, W: int, m: int, win0=None) -> np.ndarray:
+    """Kept positions of one head, ascending: sink, top-m candidates, window. The row holds the
+    scores of keys [0, win0) (default C - w)."""
     p = _f64(pooled_row).reshape(-1)
-    if p.size != C - w:
-        raise OracleError("pooled row must hold C-w scores")
+    n = _win0(C, w, win0)
+    if p.size != n:
+        raise OracleError("pooled row must hold one score per key before the window")
     out = np.zeros(s + m + W, dtype=np.int32)
-    _check(_load().orc_select(_ptr(p), C, w, s, W, m, _ptr(out)), "select")
+    _check(_load().orc_select(_ptr(p), C, n, s, W, m, _ptr(out)), "select")
     return out
 
 
 # -------------------------------------------------------------- full steps
 def compress(q_win, k, v, budgets, *, w: int, kp: int, s: int, W: int, scale=None,
-             lse=None, agg: int = GROUP_MEAN, qhead_scores=None) -> dict:
+             lse=None, agg: int = GROUP_MEAN, qhead_scores=None, win0=None) -> dict:
     """One layer's compression: scores, pooling, per-head selection and gather.
 
     budgets: [Hkv] int (the layer's rows per KV head, shared by every sequence).
+    win0: position of the first window row (default C - w; see window_lse).
     Returns kept_pos [B*T] int32, offsets [B*Hkv+1] int64, k_c/v_c [B*T, d] fp64
-    (exact copies of the input rows), colsum/pooled [B, Hkv, C-w], lse [B, Hq, w].
+    (exact copies of the input rows), colsum/pooled [B, Hkv, win0], lse [B, Hq, w].
     """
     q = _f64(q_win)
     kk = _f64(k)
@@ -223,8 +235,8 @@ def compress(q_win, k, v, budgets, *, w: int, kp: int, s: int, W: int, scale=Non
     budgets = np.asarray(budgets, dtype=np.int64).reshape(-1)
     assert budgets.size == Hkv
     if lse is None:
-        lse = window_lse(q, kk, scale=scale)
-    colsum = window_colsum(q, kk, lse, scale=scale, agg=agg, qhead_scores=qhead_scores)
+        lse = window_lse(q, kk, scale=scale, win0=win0)
+    colsum = window_colsum(q, kk, lse, scale=scale, agg=agg, qhead_scores=qhead_scores, win0=win0)
     pooled = pool(colsum, kp)
     T = int(budgets.sum())
     kept = np.zeros(B * T, dtype=np.int32)
@@ -236,7 +248,7 @@ def compress(q_win, k, v, budgets, *, w: int, kp: int, s: int, W: int, scale=Non
         for h in range(Hkv):
             offsets[b * Hkv + h] = row
             m = int(budgets[h]) - s - W
-            pos = select(pooled[b, h], C, w, s, W, m)
+            pos = select(pooled[b, h], C, w, s, W, m, win0=win0)
             n = pos.size
             kept[row:row + n] = pos
             k_c[row:row + n] = kk[b, h, pos]

@@ -331,9 +331,13 @@ int orc_allocate_variant(const double* sigma, const double* sigma2, int L, int H
 
 /* ------------------------------------------------------------------ */
 /* Observation-window attention (Sec. 3.3 last paragraph, Sec. 5).
- * Window row i of query head q sits at prompt position C-w+i and attends
- * causally to keys 0..C-w+i:  l_ij = scale * <q_i, k_j>.
- * lse[b,q,i] = log sum_{j <= C-w+i} exp(l_ij).
+ * Window row i of query head q sits at position win0+i and attends causally
+ * to the cached keys 0..min(win0+i, C-1):  l_ij = scale * <q_i, k_j>.
+ * lse[b,q,i] = log sum_{j <= min(win0+i, C-1)} exp(l_ij).
+ * win0 = C-w: the last w prompt tokens (Query-Aware, the default);
+ * win0 < C-w: a window before the final question (Query-Unaware);
+ * win0 = C:   rows after the prompt that see every cached key (Proxy-Query);
+ * the softmax runs over cached keys only.
  * Layouts: q_win [B][Hq][w][d], k [B][Hkv][C][d].                          */
 static double orc_dot(const double* a, const double* b, int d) {
   double s = 0.0;
@@ -342,8 +346,8 @@ static double orc_dot(const double* a, const double* b, int d) {
 }
 
 int orc_window_lse(const double* q_win, const double* k, int B, int Hq, int Hkv, int d, int64_t C,
-                   int w, double scale, double* lse) {
-  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || d < 1 || w < 1 || w > C) return ORC_INVALID;
+                   int w, int64_t win0, double scale, double* lse) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || d < 1 || w < 1 || win0 < 0 || win0 > C) return ORC_INVALID;
   int G = Hq / Hkv;
   int64_t rows = (int64_t)B * Hq * w;
 #pragma omp parallel for schedule(dynamic, 1)
@@ -352,7 +356,8 @@ int orc_window_lse(const double* q_win, const double* k, int B, int Hq, int Hkv,
     int64_t h = q / G;
     const double* qi = q_win + r * d;
     const double* kb = k + ((int64_t)b * Hkv + h) * C * d;
-    int64_t last = C - w + i; /* causal: keys 0..last */
+    int64_t last = win0 + i; /* causal: keys 0..last that the cache holds */
+    if (last > C - 1) last = C - 1;
     double mx = -INFINITY;
     for (int64_t j = 0; j <= last; ++j) {
       double l = scale * orc_dot(qi, kb + j * d, d);
@@ -367,13 +372,13 @@ int orc_window_lse(const double* q_win, const double* k, int B, int Hq, int Hkv,
 
 /* Cumulative window attention per scored key, averaged over the group:
  *   a[b,h,j] = (1/G) sum_{q in group h} sum_{i<w} exp(l_{q,i,j} - lse[b,q,i]),
- * for j in [0, C-w) (every window row sees all of these keys).
- * Output layout [B][Hkv][C-w].                                             */
+ * for the scored keys j in [0, win0) (every window row sees all of them).
+ * Output layout [B][Hkv][win0].                                            */
 int orc_window_colsum(const double* q_win, const double* k, const double* lse, int B, int Hq,
-                      int Hkv, int d, int64_t C, int w, double scale, double* colsum) {
-  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || d < 1 || w < 1 || w > C) return ORC_INVALID;
+                      int Hkv, int d, int64_t C, int w, int64_t win0, double scale, double* colsum) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || d < 1 || w < 1 || win0 < 0 || win0 > C) return ORC_INVALID;
   int G = Hq / Hkv;
-  int64_t n = C - w;
+  int64_t n = win0;
   int64_t cols = (int64_t)B * Hkv * n;
 #pragma omp parallel for schedule(static)
   for (int64_t c = 0; c < cols; ++c) {
@@ -400,17 +405,18 @@ int orc_window_colsum(const double* q_win, const double* k, const double* lse, i
  *   agg 2 (Ipt., mean): a_j = (1/G) sum_g sigma_q * A_g[j]
  *   agg 3 (Ipt., only): a_j = A_{g*}[j], g* the group's head with the largest
  *                       sigma (ties: lower g); every head inherits its scores.
- * agg 0 is the plain group mean (orc_window_colsum). Output [B][Hkv][C-w]. */
+ * agg 0 is the plain group mean (orc_window_colsum). Output [B][Hkv][win0]. */
 int orc_window_colsum_ipt(const double* q_win, const double* k, const double* lse, int B, int Hq,
-                          int Hkv, int d, int64_t C, int w, double scale, const double* qscore, int agg,
-                          double* colsum) {
-  if (agg == 0) return orc_window_colsum(q_win, k, lse, B, Hq, Hkv, d, C, w, scale, colsum);
-  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || d < 1 || w < 1 || w > C || agg < 1 || agg > 3 || !qscore)
+                          int Hkv, int d, int64_t C, int w, int64_t win0, double scale, const double* qscore,
+                          int agg, double* colsum) {
+  if (agg == 0) return orc_window_colsum(q_win, k, lse, B, Hq, Hkv, d, C, w, win0, scale, colsum);
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || d < 1 || w < 1 || win0 < 0 || win0 > C || agg < 1 || agg > 3 ||
+      !qscore)
     return ORC_INVALID;
   for (int q = 0; q < Hq; ++q)
     if (!(qscore[q] >= 0.0) || isinf(qscore[q])) return ORC_INVALID;
   int G = Hq / Hkv;
-  int64_t n = C - w;
+  int64_t n = win0;
   int64_t cols = (int64_t)B * Hkv * n;
 #pragma omp parallel for schedule(static)
   for (int64_t c = 0; c < cols; ++c) {
@@ -484,9 +490,10 @@ static int orc_cmp_i32(const void* pa, const void* pb) {
   return (a > b) - (a < b);
 }
 
-int orc_select(const double* pooled, int64_t C, int w, int64_t s, int64_t W, int64_t m,
+int orc_select(const double* pooled, int64_t C, int64_t n_scored, int64_t s, int64_t W, int64_t m,
                int32_t* kept) {
-  if (w < 1 || s < 0 || W < w || s + W > C || m < 0 || m > C - s - W) return ORC_INVALID;
+  /* every candidate in [s, C-W) needs a score: C - W <= n_scored */
+  if (n_scored < 0 || s < 0 || C - W > n_scored || s + W > C || m < 0 || m > C - s - W) return ORC_INVALID;
   int64_t M = C - s - W;
   orc_cand_t* cand = (orc_cand_t*)malloc(sizeof(orc_cand_t) * (size_t)(M > 0 ? M : 1));
   for (int64_t t = 0; t < M; ++t) { cand[t].j = s + t; cand[t].v = pooled[s + t]; }

@@ -19,10 +19,14 @@ SCORES = "tests/test_oracle_scores.py"
 SELDEC = "tests/test_oracle_select_decode.py"
 VARIANTS = "tests/test_oracle_alloc_variants.py"
 IPT = "tests/test_oracle_ipt.py"
+WINDOW = "tests/test_oracle_window.py"
 
 MUTANTS = {
-    "lse_not_causal": ("int64_t last = C - w + i; /* causal: keys 0..last */",
-                       "int64_t last = C - 1;", SCORES),
+    "lse_not_causal": ("int64_t last = win0 + i; /* causal: keys 0..last that the cache holds */",
+                       "int64_t last = C - 1 + 0 * i;", SCORES),
+    "lse_window_unclamped": ("    if (last > C - 1) last = C - 1;\n", "", WINDOW),
+    "select_scored_range": ("if (n_scored < 0 || s < 0 || C - W > n_scored ||", "if (n_scored < 0 || s < 0 || C - W > n_scored + 1 ||",
+                            WINDOW),
     "lse_off_by_one": ("for (int64_t j = 0; j <= last; ++j) z +=", "for (int64_t j = 0; j < last; ++j) z +=", SCORES),
     "colsum_no_group_mean": ("colsum[c] = acc / (double)G;", "colsum[c] = acc;", SCORES),
     "colsum_lse_sign": ("acc += exp(scale * orc_dot(q_win + r * d, kj, d) - lse[r]",
