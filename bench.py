@@ -71,6 +71,10 @@ def parse():
     ap.add_argument("--group-agg", default="mean", choices=["mean", "ipt_max", "ipt_mean", "ipt_only"],
                     help="aggregation of a KV head's query heads: the plain mean (default) or an Ipt. variant; "
                          "the Ipt. runs draw per-query-head scores and allocate on their group maxima")
+    ap.add_argument("--question-len", type=int, default=0,
+                    help="Query-Unaware window: the window ends this many tokens before the prompt's end")
+    ap.add_argument("--proxy-window", action="store_true",
+                    help="Proxy-Query window: the window rows follow the prompt and see every cached key")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0, metavar="MIB",
                     help="first run three elementwise copies of MIB MiB (fp32 x 1.0), untimed: under "
@@ -194,6 +198,8 @@ def main():
     L, B, Hq, Hkv, d = wl.layers, wl.batch, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
     C, w, s, W, kp = wl.seq_len, wl.obs_window, wl.b_sink, wl.b_window, wl.pool_kernel
     eb = 2 if wl.dtype == "bf16" else 4
+    win0 = C if args.proxy_window else C - w - args.question_len  # position of the first window row
+    n_scored = win0
     stream = torch.cuda.current_stream()
     traffic_of(None, wl.name, args.ratio)
     if args.calibrate_copy_mib:
@@ -232,7 +238,7 @@ def main():
         # row over its causal keys, one (sequence, KV head) block at a time, outside the timed region.
         G = Hq // Hkv
         scale = 1.0 / math.sqrt(d)
-        pos = torch.arange(C - w, C, device=dev)[:, None]
+        pos = torch.arange(win0, win0 + w, device=dev)[:, None]
         for l in range(L):
             out = torch.empty((B, Hq, w), dtype=torch.float32, device=dev)
             for b in range(B):
@@ -251,7 +257,7 @@ def main():
                          v_c=torch.empty((B * T, d), dtype=layers[l]["k"].dtype, device=dev),
                          kept_pos=torch.empty(B * T, dtype=torch.int32, device=dev),
                          offsets=torch.empty(B * Hkv + 1, dtype=torch.int64, device=dev),
-                         scores=torch.empty((B, Hkv, C - w), dtype=torch.float32, device=dev)))
+                         scores=torch.empty((B, Hkv, n_scored), dtype=torch.float32, device=dev)))
     dec_out = [torch.empty((B, Hq, d), dtype=torch.float32, device=dev) for _ in range(L)]
     dec_lse = [torch.empty((B, Hq), dtype=torch.float32, device=dev) for _ in range(L)]
     cdesc = sg.compress_desc(layers[0]["q_win"], layers[0]["k"], pool_kernel=kp, b_sink=s, b_window=W)
@@ -274,8 +280,8 @@ def main():
         for l in range(L):
             t = layers[l]
             sg.compress_layer(t["q_win"], t["k"], t["v"], budgets[l], pool_kernel=kp, b_sink=s, b_window=W,
-                              window_lse=lse_in[l], group_agg=agg, qhead_scores=qscores[l], out=outs[l],
-                              workspace=ws_c, stream=stream)
+                              window_lse=lse_in[l], group_agg=agg, qhead_scores=qscores[l], window_pos=win0,
+                              out=outs[l], workspace=ws_c, stream=stream)
         for l in range(L):
             o = outs[l]
             sg.decode_attention(layers[l]["q"], o["k_c"], o["v_c"], o["offsets"], offsets_host[l], Hkv,
@@ -366,7 +372,8 @@ def main():
         vv = t["v"][:1].cpu().double().numpy()
         qq = t["q"][:1].cpu().double().numpy()
         tc0 = time.perf_counter()
-        res = oracle.compress(q_win, kk, vv, budgets[0], w=w, kp=kp, s=s, W=W, agg=agg, qhead_scores=qscores[0])
+        res = oracle.compress(q_win, kk, vv, budgets[0], w=w, kp=kp, s=s, W=W, agg=agg, qhead_scores=qscores[0],
+                              win0=win0)
         oracle.decode(qq, res["k_c"], res["v_c"], res["offsets"], Hkv)
         cpu_s = time.perf_counter() - tc0
         cpu = dict(value=round(C / cpu_s, 1), unit="tokens/s per layer", cores=oracle.num_threads(), kind="oracle",
@@ -381,7 +388,7 @@ def main():
         config=dict(workload=wl.name, layers=L, batch=B, prompt=C, q_heads=Hq, kv_heads=Hkv, head_dim=d,
                     obs_window=w, pool_kernel=kp, b_sink=s, b_window=W, budget_ratio=args.ratio,
                     total_budget_rows=int(budgets.sum()), window_lse="caller" if args.caller_lse else "computed",
-                    alloc_variant=args.alloc_variant, group_agg=args.group_agg),
+                    alloc_variant=args.alloc_variant, group_agg=args.group_agg, window_start=win0),
         compress_tokens_per_s=round(tokens / (comp_ms / 1e3), 1) if comp_ms > 0 else None,
         decode=dict(gbps=round(dec_bytes / (dec_ms / 1e3) / 1e9, 1) if dec_ms > 0 else None,
                     frac_of_peak=round(dec_bytes / (dec_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4) if dec_ms > 0 else None,

@@ -189,31 +189,48 @@ sgdkv_status sgdkv_compress_layer(const sgdkv_compress_desc* desc, const int64_t
                                   int32_t* kept_pos_out, int64_t* offsets_out, float* scores_out,
                                   void* workspace, size_t workspace_bytes, void* stream);
 
-/* sgdkv_compress_layer with a choice of how the G query heads of a KV head
- * are aggregated into one score per key (Appendix A.7, the "Ipt." rows of
- * Table 5). With A_g[j] = sum_i exp(l_{q,i,j} - lse_{q,i}) the window
- * attention of query head q = h*G + g and sigma_q = qhead_scores[q]:
- *   SGDKV_GROUP_MEAN      a_j = (1/G) sum_g A_g[j]  (sgdkv_compress_layer);
+/* sgdkv_compress_layer with options (opts == NULL: the defaults, which make it
+ * sgdkv_compress_layer):
+ *
+ * group_agg: how the G query heads of a KV head are aggregated into one
+ * score per key (Appendix A.7, the "Ipt." rows of Table 5). With
+ * A_g[j] = sum_i exp(l_{q,i,j} - lse_{q,i}) the window attention of query
+ * head q = h*G + g and sigma_q = qhead_scores[q]:
+ *   SGDKV_GROUP_MEAN      a_j = (1/G) sum_g A_g[j]  (default);
  *   SGDKV_GROUP_IPT_MAX   a_j = max_g sigma_q * A_g[j]  (the paper's best);
  *   SGDKV_GROUP_IPT_MEAN  a_j = (1/G) sum_g sigma_q * A_g[j];
  *   SGDKV_GROUP_IPT_ONLY  a_j = A_{g*}[j], g* the group's head with the
  *                         largest sigma (ties: lower g).
- * Pooling and selection then proceed as in sgdkv_compress_layer.
  * qhead_scores: HOST [Hq] fp64 >= 0 finite, this layer's per-attention-head
  *   summarization scores (used by the Ipt. modes; may be NULL for MEAN).
- * Errors: those of sgdkv_compress_layer; group_agg not 0..3; NULL or invalid
- *   qhead_scores for an Ipt. mode; Hq > 256 with an Ipt. mode (UNSUPPORTED);
- *   IPT_MAX with obs_window not a multiple of 16 (UNSUPPORTED). */
+ * window_pos: position P0 of the first window row (Sec. 5). Row i sits at
+ *   P0 + i and attends to the cached keys 0..min(P0 + i, C - 1); the keys
+ *   [0, P0) are scored, so scores_out is [B][Hkv][P0] and every candidate
+ *   needs a score: b_window >= C - P0. -1 selects C - w (the last w prompt
+ *   tokens, Query-Aware); P0 < C - w places the window before a final
+ *   question of C - w - P0 tokens (Query-Unaware); P0 = C places it after
+ *   the prompt (Proxy-Query rows, which see every cached key; the softmax
+ *   then runs over cached keys only unless window_lse is supplied).
+ * Errors: those of sgdkv_compress_layer (with b_window >= C - P0 in place of
+ *   b_window >= w); group_agg not 0..3; NULL or invalid qhead_scores for an
+ *   Ipt. mode; Hq > 256 with an Ipt. mode (UNSUPPORTED); IPT_MAX with
+ *   obs_window not a multiple of 16 (UNSUPPORTED); window_pos outside
+ *   [-1, C]; reserved not 0. */
 #define SGDKV_GROUP_MEAN 0
 #define SGDKV_GROUP_IPT_MAX 1
 #define SGDKV_GROUP_IPT_MEAN 2
 #define SGDKV_GROUP_IPT_ONLY 3
-sgdkv_status sgdkv_compress_layer_grouped(const sgdkv_compress_desc* desc, const int64_t* layer_budgets,
-                                          int32_t group_agg, const double* qhead_scores, const void* q_win,
-                                          const void* k, const void* v, const float* window_lse, void* k_out,
-                                          void* v_out, int32_t* kept_pos_out, int64_t* offsets_out,
-                                          float* scores_out, void* workspace, size_t workspace_bytes,
-                                          void* stream);
+typedef struct sgdkv_compress_opts {
+  int32_t group_agg;           /* SGDKV_GROUP_* */
+  int32_t reserved;            /* must be 0 */
+  const double* qhead_scores;  /* host [Hq], Ipt. modes */
+  int64_t window_pos;          /* P0, or -1 for C - w */
+} sgdkv_compress_opts;
+sgdkv_status sgdkv_compress_layer_ex(const sgdkv_compress_desc* desc, const sgdkv_compress_opts* opts,
+                                     const int64_t* layer_budgets, const void* q_win, const void* k,
+                                     const void* v, const float* window_lse, void* k_out, void* v_out,
+                                     int32_t* kept_pos_out, int64_t* offsets_out, float* scores_out,
+                                     void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------ */
 /* Decode attention over the ragged compressed cache (device).         */

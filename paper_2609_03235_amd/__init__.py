@@ -26,7 +26,7 @@ OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, 1, 2, 3, 4
 DTYPE_F32, DTYPE_BF16 = 0, 1
 SYMBOLS = ("sgdkv_last_error", "sgdkv_version", "sgdkv_reduce_query_head_scores", "sgdkv_total_from_ratio",
            "sgdkv_allocate_budgets", "sgdkv_allocate_budgets_variant", "sgdkv_compress_workspace_size",
-           "sgdkv_compress_layer", "sgdkv_compress_layer_grouped",
+           "sgdkv_compress_layer", "sgdkv_compress_layer_ex",
            "sgdkv_decode_workspace_size", "sgdkv_decode_attention", "sgdkv_profile_enable",
            "sgdkv_profile_reset", "sgdkv_profile_read")
 
@@ -43,6 +43,11 @@ class CompressDesc(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("obs_window", ctypes.c_int32), ("pool_kernel", ctypes.c_int32),
                 ("seq_len", ctypes.c_int64), ("b_sink", ctypes.c_int64), ("b_window", ctypes.c_int64),
                 ("dtype", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
+class CompressOpts(ctypes.Structure):
+    _fields_ = [("group_agg", ctypes.c_int32), ("reserved", ctypes.c_int32), ("qhead_scores", ctypes.c_void_p),
+                ("window_pos", ctypes.c_int64)]
 
 
 class DecodeDesc(ctypes.Structure):
@@ -79,7 +84,7 @@ def load_library():
         "sgdkv_allocate_budgets_variant": [P, P, i32, i32, i64, i64, i64, i64, i32, i32, f64, P],
         "sgdkv_compress_workspace_size": [P, P],
         "sgdkv_compress_layer": [P, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
-        "sgdkv_compress_layer_grouped": [P, P, i32, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
+        "sgdkv_compress_layer_ex": [P, P, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
         "sgdkv_decode_workspace_size": [P, P, P],
         "sgdkv_decode_attention": [P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
         "sgdkv_profile_enable": [i32],
@@ -207,11 +212,12 @@ GROUP_MEAN, GROUP_IPT_MAX, GROUP_IPT_MEAN, GROUP_IPT_ONLY = range(4)
 
 def compress_layer(q_win, k, v, layer_budgets, *, pool_kernel: int, b_sink: int, b_window: int,
                    scale: float = 0.0, window_lse=None, scores_only: bool = False, with_scores: bool = True,
-                   group_agg: int = GROUP_MEAN, qhead_scores=None,
+                   group_agg: int = GROUP_MEAN, qhead_scores=None, window_pos: int = -1,
                    workspace=None, out: dict | None = None, stream=None) -> dict:
-    """Compress one layer (sgdkv_compress_layer_grouped; group_agg selects the plain group mean or an
-    Ipt. aggregation with the layer's per-query-head scores). Returns k_c, v_c, kept_pos, offsets,
-    scores."""
+    """Compress one layer (sgdkv_compress_layer_ex). group_agg selects the plain group mean or an
+    Ipt. aggregation with the layer's per-query-head scores; window_pos places the first window
+    row (-1: the last obs_window prompt tokens). Returns k_c, v_c, kept_pos, offsets, scores
+    (scores: [B, Hkv, window position])."""
     import torch
     desc = compress_desc(q_win, k, pool_kernel=pool_kernel, b_sink=b_sink, b_window=b_window, scale=scale)
     B, Hkv, C, d = k.shape
@@ -230,8 +236,9 @@ def compress_layer(q_win, k, v, layer_budgets, *, pool_kernel: int, b_sink: int,
         pre = np.concatenate([[0], np.cumsum(budgets)])
         oh = np.array([b * T + pre[h] for b in range(B) for h in range(Hkv)] + [B * T], dtype=np.int64)
         res["offsets_host"] = oh
+    n_scored = C - q_win.shape[2] if window_pos == -1 else int(window_pos)
     if with_scores or scores_only:
-        res.setdefault("scores", torch.empty((B, Hkv, C - q_win.shape[2]), dtype=torch.float32, device=dev))
+        res.setdefault("scores", torch.empty((B, Hkv, max(n_scored, 0)), dtype=torch.float32, device=dev))
     if workspace is None:
         workspace = alloc_workspace(compress_workspace_size(desc), dev)
     qs = None
@@ -239,9 +246,9 @@ def compress_layer(q_win, k, v, layer_budgets, *, pool_kernel: int, b_sink: int,
         qs = np.ascontiguousarray(np.asarray(qhead_scores, dtype=np.float64).reshape(-1))
         if qs.size != q_win.shape[1]:
             raise SgdkvError(ERR_INVALID_ARG, "qhead_scores must hold num_q_heads values")
-    st = load_library().sgdkv_compress_layer_grouped(
-        ctypes.byref(desc), None if budgets is None else _np_ptr(budgets), int(group_agg),
-        None if qs is None else _np_ptr(qs), _ptr(q_win), _ptr(k),
+    opts = CompressOpts(int(group_agg), 0, None if qs is None else qs.ctypes.data, int(window_pos))
+    st = load_library().sgdkv_compress_layer_ex(
+        ctypes.byref(desc), ctypes.byref(opts), None if budgets is None else _np_ptr(budgets), _ptr(q_win), _ptr(k),
         _ptr(v) if v is not None else None, _ptr(window_lse), _ptr(res.get("k_c")), _ptr(res.get("v_c")),
         _ptr(res.get("kept_pos")), _ptr(res.get("offsets")), _ptr(res.get("scores")), _ptr(workspace),
         workspace.numel(), _stream(stream))

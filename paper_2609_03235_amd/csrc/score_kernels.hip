@@ -187,7 +187,7 @@ __device__ __forceinline__ void chunk_pipeline(char* kbuf, const rsrc_t& kr, int
 // that the LDS buffers are free to move on. Padded rows (past R) keep m = 0.
 template <typename T, int D, int NB, int TILE>
 __device__ __forceinline__ void lse_exact_tile(const rsrc_t& kr, int lr, int lg, int wid, int w, int64_t tile0,
-                                            int64_t vis0, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
+                                            int64_t vis0, int64_t C, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
                                             float c2, float (&m)[NB > 0 ? NB : 1][4],
                                             float (&s)[NB > 0 ? NB : 1][4]) {
   using G = TileGeom<T, D>;
@@ -201,8 +201,9 @@ __device__ __forceinline__ void lse_exact_tile(const rsrc_t& kr, int lr, int lg,
       kb[c] = gload_frag<T>(kr, (uint32_t)((tile0 + 16 * t + lr) * G::RB + (32 * c + 8 * lg) * G::EB));
     f32x4 acc[NBX];
     subtile_mfma<T, D, NB>(qa, kb, acc);
-    const int64_t dk64 = tile0 + 16 * t + lr - vis0;
-    const int dk = dk64 < -(1 << 30) ? -(1 << 30) : (int)dk64;
+    const int64_t key = tile0 + 16 * t + lr;
+    const int64_t dk64 = key < C ? key - vis0 : (int64_t)1 << 30;  // keys past the head: never visible
+    const int dk = dk64 < -(1 << 30) ? -(1 << 30) : (dk64 > (1 << 30) ? (1 << 30) : (int)dk64);
 #pragma unroll
     for (int j = 0; j < NB; ++j)
 #pragma unroll
@@ -225,7 +226,7 @@ __device__ void lse_chunk(const CompressArgs& a, char* kbuf, int seg, int wid, i
   constexpr int NBX = NB > 0 ? NB : 1;
   constexpr int TILE = kLseTile;
   const int lr = lane & 15, lg = lane >> 4;
-  const int64_t vis0 = a.C - a.w;  // the row with window index i sees key j iff j - vis0 <= i
+  const int64_t vis0 = a.win0;  // the row with window index i sees key j iff j - vis0 <= i (and j < C)
   const float c2 = a.c2;
   float m[NBX][4], s[NBX][4], s0[NBX][4];
   bool real[NBX][4];
@@ -241,7 +242,7 @@ __device__ void lse_chunk(const CompressArgs& a, char* kbuf, int seg, int wid, i
   chunk_pipeline<T, D, NB, TILE>(
       kbuf, kr, key0, a.C, ntiles, lr, lg, qa,
       [&](const f32x4(&acc)[NBX]) {
-        if (key0 + TILE <= vis0) {  // uniform: every row sees every key of the first tile
+        if (key0 + TILE <= vis0 && key0 + TILE <= a.C) {  // uniform: every row sees every key of the first tile
 #pragma unroll
           for (int j = 0; j < NB; ++j)
 #pragma unroll
@@ -264,7 +265,7 @@ __device__ void lse_chunk(const CompressArgs& a, char* kbuf, int seg, int wid, i
       [&](int64_t) {},
       [&](int64_t t) {
         const int64_t tile0 = key0 + t * TILE;
-        bool bad = tile0 + TILE > vis0;
+        bool bad = tile0 + TILE > vis0 || tile0 + TILE > a.C;  // causal or past the head: exact path
 #pragma unroll
         for (int j = 0; j < NB; ++j)
 #pragma unroll
@@ -274,7 +275,7 @@ __device__ void lse_chunk(const CompressArgs& a, char* kbuf, int seg, int wid, i
           for (int j = 0; j < NBX; ++j)
 #pragma unroll
             for (int i = 0; i < 4; ++i) s[j][i] = s0[j][i];
-          lse_exact_tile<T, D, NB, TILE>(kr, lr, lg, wid, a.w, tile0, vis0, qa, c2, m, s);
+          lse_exact_tile<T, D, NB, TILE>(kr, lr, lg, wid, a.w, tile0, vis0, a.C, qa, c2, m, s);
         }
       });
   // Combine the 16 lanes (keys) of each row, then store (m, s) for the row.

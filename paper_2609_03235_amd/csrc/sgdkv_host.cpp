@@ -268,7 +268,9 @@ struct CompressPlan {
   size_t off_lse_part, off_lse2, off_colsum, off_pooled, off_hist, off_state, off_counts, bytes;
 };
 
-sgdkv_status plan_compress(const sgdkv_compress_desc* d, CompressPlan& p) {
+// win0 = position of the first window row (seq_len - obs_window for the default window); the
+// workspace is sized for any win0 (scores for up to seq_len keys), so its size depends on d only.
+sgdkv_status plan_compress(const sgdkv_compress_desc* d, int64_t win0, CompressPlan& p) {
   if (!d) return fail(SGDKV_ERR_INVALID_ARG, "NULL descriptor");
   if (d->batch < 1 || d->num_q_heads < 1 || d->num_kv_heads < 1)
     return fail(SGDKV_ERR_INVALID_ARG, "batch, num_q_heads, num_kv_heads must be >= 1");
@@ -288,9 +290,12 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, CompressPlan& p) {
     return fail(SGDKV_ERR_INVALID_ARG, "seq_len %lld outside [1, 2^31-1]", (long long)d->seq_len);
   if (d->b_sink < 0 || d->b_window < 0) return fail(SGDKV_ERR_INVALID_ARG, "b_sink, b_window must be >= 0");
   if (d->b_sink + d->b_window > d->seq_len) return fail(SGDKV_ERR_INVALID_ARG, "b_sink + b_window > seq_len");
-  if (d->b_window < d->obs_window)
-    return fail(SGDKV_ERR_INVALID_ARG, "b_window %lld < obs_window %d: recent candidates would have no score",
-                (long long)d->b_window, d->obs_window);
+  if (win0 < 0 || win0 > d->seq_len)
+    return fail(SGDKV_ERR_INVALID_ARG, "window position %lld outside [0, seq_len]", (long long)win0);
+  if (d->b_window < d->seq_len - win0)
+    return fail(SGDKV_ERR_INVALID_ARG,
+                "b_window %lld < %lld (keys from the window on): recent candidates would have no score",
+                (long long)d->b_window, (long long)(d->seq_len - win0));
   if (!(d->scale >= 0.f) || std::isinf(d->scale)) return fail(SGDKV_ERR_INVALID_ARG, "scale %g", d->scale);
   const int G = d->num_q_heads / d->num_kv_heads;
   const int64_t R = (int64_t)G * d->obs_window;
@@ -320,7 +325,8 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, CompressPlan& p) {
   a.C = d->seq_len;
   a.s = d->b_sink;
   a.W = d->b_window;
-  a.n_scored = a.C - a.w;
+  a.win0 = win0;
+  a.n_scored = win0;
   const double scale = d->scale > 0.f ? (double)d->scale : 1.0 / std::sqrt((double)d->head_dim);
   a.c2 = (float)(scale * 1.4426950408889634074);
   a.out_scale = 1.0f / (float)G;
@@ -346,9 +352,9 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, CompressPlan& p) {
   p.off_lse2 = off;
   off += align256((size_t)nseg * R * sizeof(float));
   p.off_colsum = off;
-  off += align256((size_t)nseg * a.n_scored * sizeof(float));
+  off += align256((size_t)nseg * a.C * sizeof(float));
   p.off_pooled = off;
-  off += align256((size_t)nseg * a.n_scored * sizeof(float));
+  off += align256((size_t)nseg * a.C * sizeof(float));
   p.off_hist = off;
   off += align256((size_t)nseg * 256 * sizeof(uint32_t));
   p.off_state = off;
@@ -429,8 +435,10 @@ sgdkv_status sgdkv_allocate_budgets_variant(const double* head_scores, const dou
 
 sgdkv_status sgdkv_compress_workspace_size(const sgdkv_compress_desc* desc, size_t* bytes) {
   if (!bytes) return fail(SGDKV_ERR_INVALID_ARG, "NULL bytes");
+  if (!desc) return fail(SGDKV_ERR_INVALID_ARG, "NULL descriptor");
   CompressPlan p;
-  if (sgdkv_status st = plan_compress(desc, p)) return st;
+  // the size does not depend on the window position; plan with the one every b_window allows
+  if (sgdkv_status st = plan_compress(desc, desc->seq_len, p)) return st;
   *bytes = p.bytes;
   return ok();
 }
@@ -439,20 +447,26 @@ sgdkv_status sgdkv_compress_layer(const sgdkv_compress_desc* desc, const int64_t
                                   const void* q_win, const void* k, const void* v, const float* window_lse,
                                   void* k_out, void* v_out, int32_t* kept_pos_out, int64_t* offsets_out,
                                   float* scores_out, void* workspace, size_t workspace_bytes, void* stream) {
-  return sgdkv_compress_layer_grouped(desc, layer_budgets, SGDKV_GROUP_MEAN, nullptr, q_win, k, v, window_lse,
-                                      k_out, v_out, kept_pos_out, offsets_out, scores_out, workspace,
-                                      workspace_bytes, stream);
+  return sgdkv_compress_layer_ex(desc, nullptr, layer_budgets, q_win, k, v, window_lse, k_out, v_out,
+                                 kept_pos_out, offsets_out, scores_out, workspace, workspace_bytes, stream);
 }
 
-sgdkv_status sgdkv_compress_layer_grouped(const sgdkv_compress_desc* desc, const int64_t* layer_budgets,
-                                          int32_t group_agg, const double* qhead_scores, const void* q_win,
-                                          const void* k, const void* v, const float* window_lse, void* k_out,
-                                          void* v_out, int32_t* kept_pos_out, int64_t* offsets_out,
-                                          float* scores_out, void* workspace, size_t workspace_bytes,
-                                          void* stream) {
+sgdkv_status sgdkv_compress_layer_ex(const sgdkv_compress_desc* desc, const sgdkv_compress_opts* opts,
+                                     const int64_t* layer_budgets, const void* q_win, const void* k,
+                                     const void* v, const float* window_lse, void* k_out, void* v_out,
+                                     int32_t* kept_pos_out, int64_t* offsets_out, float* scores_out,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  sgdkv_compress_opts o{SGDKV_GROUP_MEAN, 0, nullptr, -1};
+  if (opts) o = *opts;
+  if (!desc) return fail(SGDKV_ERR_INVALID_ARG, "NULL descriptor");
+  if (o.reserved != 0) return fail(SGDKV_ERR_INVALID_ARG, "opts.reserved must be 0");
+  if (o.window_pos < -1) return fail(SGDKV_ERR_INVALID_ARG, "window_pos %lld < -1", (long long)o.window_pos);
+  const int64_t win0 = o.window_pos == -1 ? desc->seq_len - desc->obs_window : o.window_pos;
   CompressPlan p;
-  if (sgdkv_status st = plan_compress(desc, p)) return st;
+  if (sgdkv_status st = plan_compress(desc, win0, p)) return st;
   sgdkv::CompressArgs& a = p.a;
+  const int32_t group_agg = o.group_agg;
+  const double* qhead_scores = o.qhead_scores;
   if (group_agg < SGDKV_GROUP_MEAN || group_agg > SGDKV_GROUP_IPT_ONLY)
     return fail(SGDKV_ERR_INVALID_ARG, "group_agg %d is not 0..3", group_agg);
   a.agg = group_agg;

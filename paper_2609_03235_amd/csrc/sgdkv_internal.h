@@ -36,7 +36,8 @@ void prof_end(hipStream_t stream);
 struct CompressArgs {
   // shapes
   int B, Hq, Hkv, G, D, w, kp, R, dtype;
-  int64_t C, s, W, n_scored;  // n_scored = C - w
+  int64_t C, s, W, n_scored;  // n_scored = win0: the keys before the window are scored
+  int64_t win0;               // position of window row 0; row i sees keys 0..min(win0 + i, C - 1)
   float c2;                   // logit scale * log2(e): scores work in base-2 units
   float out_scale;            // factor on each key's aggregated window sum: 1/G for the means, else 1
   // group aggregation: 0 mean, 1 Ipt. max, 2 Ipt. mean, 3 Ipt. only (see sgdkv.h)

@@ -222,34 +222,42 @@ def test_compress_validation():
     assert _compress(_desc(), good, ws=None) == sg.ERR_WORKSPACE
 
 
-def _compress_grouped(desc, agg, qs, budgets=(512, 512)):
+def _compress_ex(desc, agg, qs, budgets=(512, 512), window_pos=-1, reserved=0):
     lib = sg.load_library()
     need = ctypes.c_size_t(0)
     lib.sgdkv_compress_workspace_size(ctypes.byref(desc), ctypes.byref(need))
     b = np.ascontiguousarray(np.asarray(budgets, dtype=np.int64))
     q = None if qs is None else np.ascontiguousarray(np.asarray(qs, dtype=np.float64))
-    return lib.sgdkv_compress_layer_grouped(
-        ctypes.byref(desc), sg._np_ptr(b), agg, None if q is None else sg._np_ptr(q), FAKE, FAKE, FAKE, None,
+    opts = sg.CompressOpts(agg, reserved, None if q is None else q.ctypes.data, window_pos)
+    return lib.sgdkv_compress_layer_ex(
+        ctypes.byref(desc), ctypes.byref(opts), sg._np_ptr(b), FAKE, FAKE, FAKE, None,
         FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need.value, None)
 
 
-def test_grouped_compress_validation():
+def test_compress_options_validation():
     four = [0.5, 0.2, 0.1, 0.9]  # the default descriptor has 4 query heads
     cases = [
-        (_desc(), 4, four, sg.ERR_INVALID_ARG),                           # unknown aggregation
-        (_desc(), -1, four, sg.ERR_INVALID_ARG),
-        (_desc(), sg.GROUP_IPT_MAX, None, sg.ERR_INVALID_ARG),            # scores needed
-        (_desc(), sg.GROUP_IPT_MEAN, [0.5, -0.2, 0.1, 0.9], sg.ERR_INVALID_ARG),
-        (_desc(), sg.GROUP_IPT_ONLY, [0.5, np.nan, 0.1, 0.9], sg.ERR_INVALID_ARG),
-        (_desc(obs_window=20), sg.GROUP_IPT_MAX, four, sg.ERR_UNSUPPORTED),  # w % 16
-        (_desc(num_q_heads=320, num_kv_heads=64, obs_window=32), sg.GROUP_IPT_MEAN, [0.1] * 320,
-         sg.ERR_UNSUPPORTED),                                               # too many query heads
+        (_desc(), 4, four, -1, sg.ERR_INVALID_ARG, "group"),                   # unknown aggregation
+        (_desc(), -1, four, -1, sg.ERR_INVALID_ARG, "group"),
+        (_desc(), sg.GROUP_IPT_MAX, None, -1, sg.ERR_INVALID_ARG, "qhead"),    # scores needed
+        (_desc(), sg.GROUP_IPT_MEAN, [0.5, -0.2, 0.1, 0.9], -1, sg.ERR_INVALID_ARG, "qhead"),
+        (_desc(), sg.GROUP_IPT_ONLY, [0.5, np.nan, 0.1, 0.9], -1, sg.ERR_INVALID_ARG, "qhead"),
+        (_desc(obs_window=20), sg.GROUP_IPT_MAX, four, -1, sg.ERR_UNSUPPORTED, "Ipt"),  # w % 16
+        (_desc(num_q_heads=320, num_kv_heads=64, obs_window=32), sg.GROUP_IPT_MEAN, [0.1] * 320, -1,
+         sg.ERR_UNSUPPORTED, "num_q_heads"),                                   # too many query heads
+        (_desc(), 0, None, -2, sg.ERR_INVALID_ARG, "window_pos"),
+        (_desc(), 0, None, 2049, sg.ERR_INVALID_ARG, "window position"),      # past C
+        (_desc(), 0, None, 1900, sg.ERR_INVALID_ARG, "b_window"),             # W = 32 < C - P0
     ]
-    for desc, agg, qs, want in cases:
+    for desc, agg, qs, wp, want, word in cases:
         budgets = (512,) * desc.num_kv_heads
-        assert _compress_grouped(desc, agg, qs, budgets) == want, (agg, qs)
+        assert _compress_ex(desc, agg, qs, budgets, window_pos=wp) == want, (agg, qs, wp)
         msg = sg.load_library().sgdkv_last_error().decode()
-        assert ("group" in msg or "Ipt" in msg or "qhead" in msg or "num_q_heads" in msg), msg
+        assert word in msg, msg
+    assert _compress_ex(_desc(), 0, None, reserved=1) == sg.ERR_INVALID_ARG
+    # a window after the prompt needs no recent rows at all: validation passes, then no device
+    if not _gpu():
+        assert _compress_ex(_desc(b_window=0, b_sink=4), 0, None, budgets=(4, 4), window_pos=2048) == sg.ERR_HIP
 
 
 def test_workspace_size_independent_of_budgets():

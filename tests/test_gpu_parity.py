@@ -48,7 +48,7 @@ def _check_scores(g, o, tag=""):
                              f"first {idx.tolist()}")
 
 
-def _check_kept(res, orc, q_shape, C, w, s, W, budgets, tag=""):
+def _check_kept(res, orc, q_shape, C, w, s, W, budgets, tag="", win0=None):
     """Selection checks for every segment; returns True if GPU and oracle kept sets are identical."""
     B, Hq = q_shape[0], q_shape[1]
     Hkv = len(budgets)
@@ -63,7 +63,7 @@ def _check_kept(res, orc, q_shape, C, w, s, W, budgets, tag=""):
             seg = kept[offs[b * Hkv + h]:offs[b * Hkv + h + 1]]
             m = int(budgets[h]) - s - W
             # same decision in the kernel's precision: the oracle's top-k of the GPU's scores
-            ref_same = oracle.select(scores[b, h], C, w, s, W, m)
+            ref_same = oracle.select(scores[b, h], C, w, s, W, m, win0=win0)
             assert np.array_equal(seg, ref_same), f"{tag} b={b} h={h}: kept set differs from top-k of GPU scores"
             ref = orc["kept_pos"][orc["offsets"][b * Hkv + h]:orc["offsets"][b * Hkv + h + 1]]
             if not np.array_equal(seg, ref):
@@ -89,13 +89,14 @@ def _check_gather(res, k, v, budgets):
             assert torch.equal(res["v_c"][lo:hi], v[b, h][pos]), f"V gather b={b} h={h}"
 
 
-def _compress_both(q_win, k, v, budgets, *, kp, s, W, window_lse=None, orc_lse=None, agg=0, qhead_scores=None):
+def _compress_both(q_win, k, v, budgets, *, kp, s, W, window_lse=None, orc_lse=None, agg=0, qhead_scores=None,
+                   win0=None):
     w = q_win.shape[2]
     res = sg.compress_layer(q_win, k, v, budgets, pool_kernel=kp, b_sink=s, b_window=W, window_lse=window_lse,
-                            group_agg=agg, qhead_scores=qhead_scores)
+                            group_agg=agg, qhead_scores=qhead_scores, window_pos=-1 if win0 is None else win0)
     torch.cuda.synchronize()
     orc = oracle.compress(_f64(q_win), _f64(k), _f64(v), budgets, w=w, kp=kp, s=s, W=W, lse=orc_lse, agg=agg,
-                          qhead_scores=qhead_scores)
+                          qhead_scores=qhead_scores, win0=win0)
     return res, orc
 
 
@@ -209,6 +210,34 @@ def test_ipt_group_aggregation(agg, B, C, Hq, Hkv, d, w):
         plain = sg.compress_layer(t["q_win"], t["k"], t["v"], budgets, pool_kernel=7, b_sink=s, b_window=W)
         torch.cuda.synchronize()
         assert torch.equal(one["scores"], plain["scores"]) and torch.equal(one["kept_pos"], plain["kept_pos"])
+
+
+@pytest.mark.parametrize("case", ["unaware", "proxy", "unaware_ipt_max", "tiny_proxy", "tiny_unaware"])
+def test_window_placement(case):
+    """Window before a final question (Query-Unaware: rows at C - q_len - w + i, with masked keys
+    inside partial tiles) and after the prompt (Proxy-Query: every cached key visible, including
+    the partial last tile), against the oracle; also combined with Ipt. max."""
+    if case.startswith("tiny"):
+        wl, t = _tiny_inputs(B=2, C=1100, seed=8)
+        s, W, kp, w = 4, 96, 7, wl.obs_window
+        C = 1100
+        Hkv = 2
+        budgets = np.array([300, 500])
+        win0 = C if case == "tiny_proxy" else C - 45 - w
+    else:
+        wl, t = _qwen_small(2, 2300, Hq=28, Hkv=4, d=128, w=64)
+        s, W, kp, w, C = wl.b_sink, wl.b_window, 7, 64, 2300
+        Hkv = 4
+        budgets = np.array([700, 400, 1200, 300])
+        win0 = C if case == "proxy" else C - 37 - w
+    agg, qs = (sg.GROUP_IPT_MAX, np.linspace(0.2, 1.0, t["q_win"].shape[1])) if case.endswith("ipt_max") else (0, None)
+    _announce(f"window placement {case}: C={C} win0={win0}")
+    res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=kp, s=s, W=W, agg=agg, qhead_scores=qs,
+                              win0=win0)
+    assert res["scores"].shape[-1] == win0
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], case)
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, case, win0=win0)
+    _check_gather(res, t["k"], t["v"], budgets)
 
 
 def test_caller_supplied_lse_and_scores_only():
