@@ -62,9 +62,10 @@ def _load():
     lib.orc_pool.argtypes = [P, i64, i64, i32, P]
     lib.orc_select.argtypes = [P, i64, i64, i64, i64, i64, P]
     lib.orc_decode.argtypes = [P, P, P, P, i32, i32, i32, i32, f64, P, P]
+    lib.orc_decode_append.argtypes = [P, P, P, P, P, P, i64, i64, i32, i32, i32, i32, f64, P, P]
     lib.orc_num_threads.argtypes = []
     for f in ("orc_reduce_group_max", "orc_total_from_ratio", "orc_allocate_budgets", "orc_allocate_variant",
-              "orc_window_lse", "orc_window_colsum", "orc_window_colsum_ipt", "orc_pool", "orc_select", "orc_decode",
+              "orc_window_lse", "orc_window_colsum", "orc_window_colsum_ipt", "orc_pool", "orc_select", "orc_decode", "orc_decode_append",
               "orc_num_threads"):
         getattr(lib, f).restype = i32
     _lib = lib
@@ -257,6 +258,25 @@ def compress(q_win, k, v, budgets, *, w: int, kp: int, s: int, W: int, scale=Non
     offsets[B * Hkv] = row
     return dict(kept_pos=kept, offsets=offsets, k_c=k_c, v_c=v_c, colsum=colsum, pooled=pooled,
                 lse=lse)
+
+
+def decode_append(q, k_c, v_c, offsets, k_new, v_new, n_new: int, num_kv_heads: int, scale=None):
+    """Decode over each segment's compressed rows plus rows 0..n_new-1 of k_new/v_new
+    [B, Hkv, capacity, d] (the tokens appended since compression): (out [B,Hq,d], lse [B,Hq])."""
+    qq = _f64(q)
+    kc = _f64(k_c)
+    vc = _f64(v_c)
+    kn = _f64(k_new)
+    vn = _f64(v_new)
+    off = np.ascontiguousarray(np.asarray(offsets, dtype=np.int64))
+    B, Hq, d = qq.shape
+    cap = kn.shape[2]
+    out = np.zeros((B, Hq, d), dtype=np.float64)
+    lse = np.zeros((B, Hq), dtype=np.float64)
+    _check(_load().orc_decode_append(_ptr(qq), _ptr(kc), _ptr(vc), _ptr(off), _ptr(kn), _ptr(vn), cap, int(n_new),
+                                     B, Hq, num_kv_heads, d, _scale(d, scale), _ptr(out), _ptr(lse)),
+           "decode_append")
+    return out, lse
 
 
 def decode(q, k_c, v_c, offsets, num_kv_heads: int, scale=None):

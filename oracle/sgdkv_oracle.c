@@ -543,6 +543,48 @@ int orc_decode(const double* q, const double* kc, const double* vc, const int64_
   return ORC_OK;
 }
 
+/* Decode during generation (the step after compression, Appendix A.2 keeps
+ * one cache per KV head): each (b, h) also holds the rows appended since the
+ * compression, rows 0..n_new-1 of knew/vnew [B][Hkv][cap][d]. Query head q of
+ * sequence b attends to its segment's compressed rows followed by those:
+ *   out = sum over both sets of softmax(scale*<q,k>) v,  lse as in orc_decode. */
+int orc_decode_append(const double* q, const double* kc, const double* vc, const int64_t* offsets,
+                      const double* knew, const double* vnew, int64_t cap, int64_t n_new, int B, int Hq,
+                      int Hkv, int d, double scale, double* out, double* lse) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv || d < 1 || cap < 0 || n_new < 0 || n_new > cap) return ORC_INVALID;
+  int G = Hq / Hkv;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t bq = 0; bq < (int64_t)B * Hq; ++bq) {
+    int64_t b = bq / Hq, qh = bq % Hq, h = qh / G;
+    int64_t r0 = offsets[b * Hkv + h], r1 = offsets[b * Hkv + h + 1];
+    const double* kn = knew + ((int64_t)b * Hkv + h) * cap * d;
+    const double* vn = vnew + ((int64_t)b * Hkv + h) * cap * d;
+    const double* qv = q + bq * d;
+    double* o = out + bq * d;
+    for (int t = 0; t < d; ++t) o[t] = 0.0;
+    int64_t n = (r1 > r0 ? r1 - r0 : 0) + n_new;
+    if (n == 0) { lse[bq] = -INFINITY; continue; }
+    double mx = -INFINITY;
+    for (int64_t e = 0; e < n; ++e) {
+      const double* kr = e < r1 - r0 ? kc + (r0 + e) * d : kn + (e - (r1 - r0 > 0 ? r1 - r0 : 0)) * d;
+      double l = scale * orc_dot(qv, kr, d);
+      if (l > mx) mx = l;
+    }
+    double z = 0.0;
+    for (int64_t e = 0; e < n; ++e) {
+      int64_t nc = r1 - r0 > 0 ? r1 - r0 : 0;
+      const double* kr = e < nc ? kc + (r0 + e) * d : kn + (e - nc) * d;
+      const double* vr = e < nc ? vc + (r0 + e) * d : vn + (e - nc) * d;
+      double p = exp(scale * orc_dot(qv, kr, d) - mx);
+      z += p;
+      for (int t = 0; t < d; ++t) o[t] += p * vr[t];
+    }
+    for (int t = 0; t < d; ++t) o[t] /= z;
+    lse[bq] = mx + log(z);
+  }
+  return ORC_OK;
+}
+
 int orc_num_threads(void) {
 #ifdef _OPENMP
   extern int omp_get_max_threads(void);

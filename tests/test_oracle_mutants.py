@@ -20,10 +20,16 @@ SELDEC = "tests/test_oracle_select_decode.py"
 VARIANTS = "tests/test_oracle_alloc_variants.py"
 IPT = "tests/test_oracle_ipt.py"
 WINDOW = "tests/test_oracle_window.py"
+APPEND = "tests/test_oracle_decode_append.py"
 
 MUTANTS = {
     "lse_not_causal": ("int64_t last = win0 + i; /* causal: keys 0..last that the cache holds */",
                        "int64_t last = C - 1 + 0 * i;", SCORES),
+    "append_skips_new": ("int64_t n = (r1 > r0 ? r1 - r0 : 0) + n_new;", "int64_t n = (r1 > r0 ? r1 - r0 : 0);", APPEND),
+    "append_wrong_head": ("const double* kn = knew + ((int64_t)b * Hkv + h) * cap * d;",
+                          "const double* kn = knew + ((int64_t)b * Hkv) * cap * d;", APPEND),
+    "append_value_offset": ("const double* vr = e < nc ? vc + (r0 + e) * d : vn + (e - nc) * d;",
+                            "const double* vr = e < nc ? vc + (r0 + e) * d : vn + (e - nc + 1) * d;", APPEND),
     "lse_window_unclamped": ("    if (last > C - 1) last = C - 1;\n", "", WINDOW),
     "select_scored_range": ("if (n_scored < 0 || s < 0 || C - W > n_scored ||", "if (n_scored < 0 || s < 0 || C - W > n_scored + 1 ||",
                             WINDOW),
