@@ -75,6 +75,9 @@ def parse():
                     help="Query-Unaware window: the window ends this many tokens before the prompt's end")
     ap.add_argument("--proxy-window", action="store_true",
                     help="Proxy-Query window: the window rows follow the prompt and see every cached key")
+    ap.add_argument("--decode-new", type=int, default=0, metavar="N",
+                    help="generation: each layer's decode also attends to N rows appended since compression, "
+                         "and every step appends one row per KV head (sgdkv_append_kv) before decoding")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0, metavar="MIB",
                     help="first run three elementwise copies of MIB MiB (fp32 x 1.0), untimed: under "
@@ -259,6 +262,17 @@ def main():
                          offsets=torch.empty(B * Hkv + 1, dtype=torch.int64, device=dev),
                          scores=torch.empty((B, Hkv, n_scored), dtype=torch.float32, device=dev)))
     dec_out = [torch.empty((B, Hq, d), dtype=torch.float32, device=dev) for _ in range(L)]
+    n_new = args.decode_new
+    tails = [None] * L
+    if n_new > 0:
+        # rows appended since compression (one generated token per row), drawn like the cache
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(wl.seed + 300)
+        for l in range(L):
+            kn = torch.randn((B, Hkv, n_new, d), generator=gen, device=dev).to(layers[l]["k"].dtype)
+            vn = torch.randn((B, Hkv, n_new, d), generator=gen, device=dev).to(layers[l]["k"].dtype)
+            step_kv = torch.randn((2, B, Hkv, d), generator=gen, device=dev).to(layers[l]["k"].dtype)
+            tails[l] = (kn, vn, step_kv)
     dec_lse = [torch.empty((B, Hq), dtype=torch.float32, device=dev) for _ in range(L)]
     cdesc = sg.compress_desc(layers[0]["q_win"], layers[0]["k"], pool_kernel=kp, b_sink=s, b_window=W)
     ws_c = sg.alloc_workspace(sg.compress_workspace_size(cdesc), dev)
@@ -269,7 +283,7 @@ def main():
         offsets_host.append(np.array([b * T + pre[h] for b in range(B) for h in range(Hkv)] + [B * T],
                                      dtype=np.int64))
     ddesc = sg.decode_desc(layers[0]["q"], Hkv, torch.float32)
-    ws_d = sg.alloc_workspace(max(sg.decode_workspace_size(ddesc, oh) for oh in offsets_host), dev)
+    ws_d = sg.alloc_workspace(max(sg.decode_workspace_size(ddesc, oh, n_new) for oh in offsets_host), dev)
     torch.cuda.synchronize()
     log(f"[bench] inputs ready in {time.perf_counter() - t0:.1f}s: {wl.name}, total budget {total} rows "
         f"({args.ratio:.0%}), {L} layers x {B} sequences")
@@ -284,9 +298,14 @@ def main():
                               out=outs[l], workspace=ws_c, stream=stream)
         for l in range(L):
             o = outs[l]
+            kn = vn = None
+            if tails[l] is not None:
+                # this step's token goes into the last slot, then decode attends to all n_new rows
+                kn, vn, step_kv = tails[l]
+                sg.append_kv(layers[l]["q"], step_kv[0], step_kv[1], kn, vn, n_new - 1, stream=stream)
             sg.decode_attention(layers[l]["q"], o["k_c"], o["v_c"], o["offsets"], offsets_host[l], Hkv,
-                                out_dtype=torch.float32, workspace=ws_d, out=dec_out[l], lse=dec_lse[l],
-                                stream=stream)
+                                out_dtype=torch.float32, k_new=kn, v_new=vn, n_new=n_new, workspace=ws_d,
+                                out=dec_out[l], lse=dec_lse[l], stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -326,8 +345,8 @@ def main():
         "score_colsum": ("alu", flops_tok * B * (C - w), "TFLOP/s"),
         # read kept K and V rows, write them, write positions, read pooled scores of the candidates
         "gather": ("hbm", B * T_mean * (4 * d * eb + 4) + B * Hkv * C * 4.0, "GB/s"),
-        # read every kept K and V row once, plus the queries and outputs
-        "decode_split": ("hbm", B * T_mean * 2 * d * eb + B * Hq * d * (eb + 4.0), "GB/s"),
+        # read every kept K and V row once (and the rows appended since), plus the queries and outputs
+        "decode_split": ("hbm", B * (T_mean + Hkv * n_new) * 2 * d * eb + B * Hq * d * (eb + 4.0), "GB/s"),
     }
     kernels = {}
     for name, (count, ms) in sorted(kern.items(), key=lambda kv: -kv[1][1]):
@@ -374,7 +393,12 @@ def main():
         tc0 = time.perf_counter()
         res = oracle.compress(q_win, kk, vv, budgets[0], w=w, kp=kp, s=s, W=W, agg=agg, qhead_scores=qscores[0],
                               win0=win0)
-        oracle.decode(qq, res["k_c"], res["v_c"], res["offsets"], Hkv)
+        if n_new > 0:
+            kn, vn, _ = tails[0]
+            oracle.decode_append(qq, res["k_c"], res["v_c"], res["offsets"], kn[:1].cpu().double().numpy(),
+                                 vn[:1].cpu().double().numpy(), n_new, Hkv)
+        else:
+            oracle.decode(qq, res["k_c"], res["v_c"], res["offsets"], Hkv)
         cpu_s = time.perf_counter() - tc0
         cpu = dict(value=round(C / cpu_s, 1), unit="tokens/s per layer", cores=oracle.num_threads(), kind="oracle",
                    sample=f"sequence 0 of layer 0 ({Hkv} KV heads, C={C}): compress + decode, {cpu_s:.1f} s")
@@ -388,7 +412,8 @@ def main():
         config=dict(workload=wl.name, layers=L, batch=B, prompt=C, q_heads=Hq, kv_heads=Hkv, head_dim=d,
                     obs_window=w, pool_kernel=kp, b_sink=s, b_window=W, budget_ratio=args.ratio,
                     total_budget_rows=int(budgets.sum()), window_lse="caller" if args.caller_lse else "computed",
-                    alloc_variant=args.alloc_variant, group_agg=args.group_agg, window_start=win0),
+                    alloc_variant=args.alloc_variant, group_agg=args.group_agg, window_start=win0,
+                    decode_appended_rows=n_new),
         compress_tokens_per_s=round(tokens / (comp_ms / 1e3), 1) if comp_ms > 0 else None,
         decode=dict(gbps=round(dec_bytes / (dec_ms / 1e3) / 1e9, 1) if dec_ms > 0 else None,
                     frac_of_peak=round(dec_bytes / (dec_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4) if dec_ms > 0 else None,

@@ -266,6 +266,44 @@ sgdkv_status sgdkv_decode_attention(const sgdkv_decode_desc* desc, const void* q
                                     const int64_t* offsets_host, void* out, float* lse_out,
                                     void* workspace, size_t workspace_bytes, void* stream);
 
+/* Generation after compression: every KV head (b, h) keeps, beside its
+ * compressed segment, the rows appended since (one per generated token; the
+ * cache stays one per KV head, Appendix A.2). They live in a caller-owned
+ * region of `capacity` rows per (b, h); rows 0..n_new-1 are valid. */
+typedef struct sgdkv_decode_tail {
+  const void* k_new;  /* device [B][Hkv][capacity][d] kv_dtype */
+  const void* v_new;  /* device [B][Hkv][capacity][d] kv_dtype */
+  int64_t capacity;   /* rows per (b, h), >= 0 */
+  int64_t n_new;      /* valid rows per (b, h), 0 <= n_new <= capacity */
+} sgdkv_decode_tail;
+
+/* Writes one generated token's K and V rows into row `slot` of every (b, h)
+ * of the appended region. k_step, v_step: device [B][Hkv][d] kv_dtype;
+ * k_new, v_new: device [B][Hkv][capacity][d] kv_dtype (caller-owned).
+ * Errors (nothing enqueued): sizes as for sgdkv_decode_attention; slot
+ * outside [0, capacity); a region of 4 GiB or more (UNSUPPORTED); missing
+ * or misaligned pointers. */
+sgdkv_status sgdkv_append_kv(const sgdkv_decode_desc* desc, const void* k_step, const void* v_step, void* k_new,
+                             void* v_new, int64_t capacity, int64_t slot, void* stream);
+
+/* Workspace for sgdkv_decode_attention_ex with appended regions of up to
+ * `capacity` rows (capacity 0: the same as sgdkv_decode_workspace_size). */
+sgdkv_status sgdkv_decode_workspace_size_ex(const sgdkv_decode_desc* desc, const int64_t* offsets_host,
+                                            int64_t capacity, size_t* bytes);
+
+/* sgdkv_decode_attention over each segment's compressed rows followed by
+ * rows 0..tail->n_new-1 of its appended region (tail == NULL or n_new == 0:
+ * the compressed rows alone):
+ *   out = sum over both sets of softmax(scale*<q,k>) v, lse likewise.
+ * Errors: those of sgdkv_decode_attention; capacity < 0; n_new outside
+ *   [0, capacity]; NULL or misaligned k_new/v_new with n_new > 0; a region
+ *   of 4 GiB or more (UNSUPPORTED); a workspace planned for a smaller
+ *   capacity (WORKSPACE). */
+sgdkv_status sgdkv_decode_attention_ex(const sgdkv_decode_desc* desc, const void* q, const void* k_c,
+                                       const void* v_c, const int64_t* offsets, const int64_t* offsets_host,
+                                       const sgdkv_decode_tail* tail, void* out, float* lse_out, void* workspace,
+                                       size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------ */
 /* Kernel timing for benchmarks (not part of the method).             */
 

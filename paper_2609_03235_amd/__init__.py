@@ -27,7 +27,8 @@ DTYPE_F32, DTYPE_BF16 = 0, 1
 SYMBOLS = ("sgdkv_last_error", "sgdkv_version", "sgdkv_reduce_query_head_scores", "sgdkv_total_from_ratio",
            "sgdkv_allocate_budgets", "sgdkv_allocate_budgets_variant", "sgdkv_compress_workspace_size",
            "sgdkv_compress_layer", "sgdkv_compress_layer_ex",
-           "sgdkv_decode_workspace_size", "sgdkv_decode_attention", "sgdkv_profile_enable",
+           "sgdkv_decode_workspace_size", "sgdkv_decode_attention", "sgdkv_decode_workspace_size_ex",
+           "sgdkv_decode_attention_ex", "sgdkv_append_kv", "sgdkv_profile_enable",
            "sgdkv_profile_reset", "sgdkv_profile_read")
 
 
@@ -87,6 +88,9 @@ def load_library():
         "sgdkv_compress_layer_ex": [P, P, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
         "sgdkv_decode_workspace_size": [P, P, P],
         "sgdkv_decode_attention": [P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
+        "sgdkv_decode_workspace_size_ex": [P, P, i64, P],
+        "sgdkv_decode_attention_ex": [P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
+        "sgdkv_append_kv": [P, P, P, P, P, i64, i64, P],
         "sgdkv_profile_enable": [i32],
         "sgdkv_profile_reset": [],
         "sgdkv_profile_read": [i32, P, P, P, P],
@@ -262,33 +266,50 @@ def decode_desc(q, num_kv_heads: int, out_dtype=None, scale: float = 0.0) -> Dec
     return DecodeDesc(B, Hq, num_kv_heads, d, _dtype_code(q), od, float(scale))
 
 
-def decode_workspace_size(desc: DecodeDesc, offsets_host) -> int:
+def decode_workspace_size(desc: DecodeDesc, offsets_host, capacity: int = 0) -> int:
     oh = np.ascontiguousarray(np.asarray(offsets_host, dtype=np.int64))
     n = ctypes.c_size_t(0)
-    _check(load_library().sgdkv_decode_workspace_size(ctypes.byref(desc), _np_ptr(oh), ctypes.byref(n)))
+    _check(load_library().sgdkv_decode_workspace_size_ex(ctypes.byref(desc), _np_ptr(oh), int(capacity),
+                                                          ctypes.byref(n)))
     return int(n.value)
 
 
+class DecodeTail(ctypes.Structure):
+    _fields_ = [("k_new", ctypes.c_void_p), ("v_new", ctypes.c_void_p), ("capacity", ctypes.c_int64),
+                ("n_new", ctypes.c_int64)]
+
+
 def decode_attention(q, k_c, v_c, offsets, offsets_host, num_kv_heads: int, *, out_dtype=None,
-                     scale: float = 0.0, with_lse: bool = True, workspace=None, out=None, lse=None,
-                     stream=None):
-    """One decode step over the ragged cache (sgdkv_decode_attention). Returns (out, lse)."""
+                     scale: float = 0.0, with_lse: bool = True, k_new=None, v_new=None, n_new: int = 0,
+                     workspace=None, out=None, lse=None, stream=None):
+    """One decode step over the ragged cache (sgdkv_decode_attention_ex). k_new/v_new [B, Hkv, capacity, d]
+    hold the rows appended since compression, of which the first n_new are attended. Returns (out, lse)."""
     import torch
     desc = decode_desc(q, num_kv_heads, out_dtype, scale)
     oh = np.ascontiguousarray(np.asarray(offsets_host, dtype=np.int64))
     B, Hq, d = q.shape
+    cap = 0 if k_new is None else int(k_new.shape[2])
     if out is None:
         out = torch.empty((B, Hq, d), dtype=torch.bfloat16 if desc.out_dtype == DTYPE_BF16 else torch.float32,
                           device=q.device)
     if with_lse and lse is None:
         lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
     if workspace is None:
-        workspace = alloc_workspace(decode_workspace_size(desc, oh), q.device)
-    st = load_library().sgdkv_decode_attention(
-        ctypes.byref(desc), _ptr(q), _ptr(k_c), _ptr(v_c), _ptr(offsets), _np_ptr(oh), _ptr(out),
+        workspace = alloc_workspace(decode_workspace_size(desc, oh, cap), q.device)
+    tail = DecodeTail(_ptr(k_new), _ptr(v_new), cap, int(n_new))
+    st = load_library().sgdkv_decode_attention_ex(
+        ctypes.byref(desc), _ptr(q), _ptr(k_c), _ptr(v_c), _ptr(offsets), _np_ptr(oh), ctypes.byref(tail), _ptr(out),
         _ptr(lse) if with_lse else None, _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st)
     return out, (lse if with_lse else None)
+
+
+def append_kv(q_like, k_step, v_step, k_new, v_new, slot: int, stream=None):
+    """Write one generated token's K/V rows [B, Hkv, d] into row `slot` of k_new/v_new [B, Hkv, capacity, d]
+    (sgdkv_append_kv). q_like: the decode queries [B, Hq, d] (for the descriptor)."""
+    desc = decode_desc(q_like, k_step.shape[1])
+    _check(load_library().sgdkv_append_kv(ctypes.byref(desc), _ptr(k_step), _ptr(v_step), _ptr(k_new), _ptr(v_new),
+                                          int(k_new.shape[2]), int(slot), _stream(stream)))
 
 
 # ------------------------------------------------------- kernel timing

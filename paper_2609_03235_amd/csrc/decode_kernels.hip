@@ -16,6 +16,9 @@
 //
 // Work is a flattened (chunk, segment) grid, so unequal budgets (one head
 // with most of the rows, others with few) still spread over the whole chip.
+// Rows appended to a segment after compression (generation) live in a
+// separate region per (sequence, KV head) and get splits of their own after
+// the compressed ones; the combine merges both.
 #include "device_common.h"
 #include "mfma_frag.h"
 #include "sgdkv_internal.h"
@@ -245,15 +248,23 @@ __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a)
   int64_t r0, r1;
   clamp_segment(a, seg, r0, r1);
   const int64_t len = r1 - r0;
+  // splits 0 .. n_chunk_max-1 cover the segment's compressed rows, the next ones the rows
+  // appended since compression; a wave whose split is empty leaves (waves never synchronise)
   const int64_t chunk = (int64_t)blockIdx.x * kWaves + wid;
-  const int64_t c0 = chunk * a.chunk;
-  if (c0 >= len) return;  // this wave's chunk is past the segment (waves never synchronise)
-  const int64_t c1 = c0 + a.chunk < len ? c0 + a.chunk : len;
+  const bool appended = chunk >= a.n_chunk_max;
+  const int64_t rows = appended ? a.n_new : len;
+  const int64_t c0 = (appended ? chunk - a.n_chunk_max : chunk) * a.chunk;
+  if (c0 >= rows) return;
+  const int64_t c1 = c0 + a.chunk < rows ? c0 + a.chunk : rows;
 
   const int lr = lane & 15, lgp = lane >> 4;
   const int G = a.G;
-  const rsrc_t kr = make_rsrc(static_cast<const char*>(a.k_c) + r0 * S::RB, (uint64_t)len * S::RB);
-  const rsrc_t vr = make_rsrc(static_cast<const char*>(a.v_c) + r0 * S::RB, (uint64_t)len * S::RB);
+  const char* kbase = appended ? static_cast<const char*>(a.k_new) + (int64_t)seg * a.cap * S::RB
+                               : static_cast<const char*>(a.k_c) + r0 * S::RB;
+  const char* vbase = appended ? static_cast<const char*>(a.v_new) + (int64_t)seg * a.cap * S::RB
+                               : static_cast<const char*>(a.v_c) + r0 * S::RB;
+  const rsrc_t kr = make_rsrc(kbase, (uint64_t)rows * S::RB);
+  const rsrc_t vr = make_rsrc(vbase, (uint64_t)rows * S::RB);
   const rsrc_t qr = make_rsrc(static_cast<const char*>(a.q) + ((int64_t)b * a.Hq + (int64_t)h * G) * S::RB,
                               (uint64_t)G * S::RB);
   Frag<T> qa[S::NC];  // row lr = head; rows >= G read as zeros
@@ -288,7 +299,7 @@ __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a)
   // write this chunk's partial for each of the G heads: (m, s) and o[D] in two arrays, one
   // descriptor each for the whole group (per-lane descriptors would cost waterfall loops)
   const int64_t bq0 = (int64_t)b * a.Hq + (int64_t)h * G;
-  const int64_t ncm = a.n_chunk_max;
+  const int64_t ncm = a.n_part;
   if (lr == 0) {
     const rsrc_t mr = make_rsrc(a.part_ms + bq0 * ncm * 2, (uint64_t)G * ncm * 8);
 #pragma unroll
@@ -331,14 +342,18 @@ __global__ __launch_bounds__(1024) void decode_combine_kernel(DecodeArgs a) {
   int64_t r0, r1;
   clamp_segment(a, seg, r0, r1);
   const int64_t len = r1 - r0;
-  const int64_t ncm = a.n_chunk_max;
-  int64_t nch = (len + a.chunk - 1) / a.chunk;
-  if (nch > ncm) nch = ncm;
+  // valid splits: the segment's first nseg ones, then n_new_chunks from index n_chunk_max on;
+  // dense index c maps to split c (c < nseg) or n_chunk_max + c - nseg
+  const int64_t ncm = a.n_part;
+  int64_t nseg = (len + a.chunk - 1) / a.chunk;
+  if (nseg > a.n_chunk_max) nseg = a.n_chunk_max;
+  const int64_t nch = nseg + a.n_new_chunks;
+  auto slot = [&](int64_t c) { return c < nseg ? c : a.n_chunk_max + (c - nseg); };
   const int tid = threadIdx.x, c4 = tid % TPR, grp = tid / TPR;
   const rsrc_t mr = make_rsrc(a.part_ms + (int64_t)bq * ncm * 2, (uint64_t)ncm * 8);
   const rsrc_t orr = make_rsrc(a.part + (int64_t)bq * ncm * D, (uint64_t)ncm * D * 4);
   float M = -INFINITY;
-  for (int64_t c = tid; c < nch; c += NT) M = fmaxf(M, ldf(mr, (uint32_t)(c * 8)));
+  for (int64_t c = tid; c < nch; c += NT) M = fmaxf(M, ldf(mr, (uint32_t)(slot(c) * 8)));
   M = wave_max(M);
   if ((tid & 63) == 0) red_m[tid >> 6] = M;
   __syncthreads();
@@ -354,8 +369,9 @@ __global__ __launch_bounds__(1024) void decode_combine_kernel(DecodeArgs a) {
       for (int u = 0; u < U; ++u) {  // chunks past nch read as zeros (offset past the buffer)
         const int64_t cc = c + u * NG;
         const bool ok = cc < nch;
-        ms[u] = ld64(mr, ok ? (uint32_t)(cc * 8) : (uint32_t)(ncm * 8));
-        ov[u] = ld128(orr, ok ? (uint32_t)((cc * D + 4 * c4) * 4) : (uint32_t)(ncm * D * 4));
+        const int64_t sl = slot(cc);
+        ms[u] = ld64(mr, ok ? (uint32_t)(sl * 8) : (uint32_t)(ncm * 8));
+        ov[u] = ld128(orr, ok ? (uint32_t)((sl * D + 4 * c4) * 4) : (uint32_t)(ncm * D * 4));
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -411,7 +427,7 @@ __global__ __launch_bounds__(1024) void decode_combine_kernel(DecodeArgs a) {
 // One step of K/V in flight ahead of the one being computed (more measured no faster).
 template <typename T, int D>
 static void launch_decode_t(const DecodeArgs& a, hipStream_t st) {
-  const dim3 grid((a.n_chunk_max + kWaves - 1) / kWaves, a.B * a.Hkv);
+  const dim3 grid((a.n_chunk_max + a.n_new_chunks + kWaves - 1) / kWaves, a.B * a.Hkv);
   constexpr bool wide = sizeof(T) == 2;
   constexpr int PF = wide ? SGDKV_DECODE_PF : 1;
   constexpr int CPL = wide ? SGDKV_DECODE_CPL : 8;
@@ -422,8 +438,32 @@ static void launch_decode_t(const DecodeArgs& a, hipStream_t st) {
     SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, 8, 16, 1, 2>), grid, dim3(kBlock), st, a);
 }
 
+// Copies one token's K rows (blockIdx.y = 0) or V rows (1), [B*Hkv][d] each, into row `slot`
+// of every (b, h) of the appended regions: one 16-byte vector per thread.
+__global__ __launch_bounds__(kBlock) void append_kernel(DecodeArgs a, const void* k_step, const void* v_step,
+                                                         void* k_new, void* v_new, int64_t slot) {
+  const int rb = a.D * (a.kv_dtype == 1 ? 2 : 4);
+  const int v16 = rb / 16;
+  const int64_t nseg = (int64_t)a.B * a.Hkv;
+  const int64_t r = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (r >= nseg * v16) return;
+  const bool is_v = blockIdx.y == 1;
+  const int64_t seg = r / v16, c = r % v16;
+  const rsrc_t src = make_rsrc(is_v ? v_step : k_step, (uint64_t)nseg * rb);
+  const rsrc_t dst = make_rsrc(is_v ? v_new : k_new, (uint64_t)nseg * a.cap * rb);
+  st128(dst, (uint32_t)((seg * a.cap + slot) * rb + c * 16), ld128(src, (uint32_t)(seg * rb + c * 16)));
+}
+
+hipError_t launch_append(const DecodeArgs& a, const void* k_step, const void* v_step, void* k_new, void* v_new,
+                         int64_t slot, hipStream_t st) {
+  const int64_t n = (int64_t)a.B * a.Hkv * (a.D * (a.kv_dtype == 1 ? 2 : 4) / 16);
+  SGDKV_LAUNCH("append", append_kernel, dim3((unsigned)((n + kBlock - 1) / kBlock), 2), dim3(kBlock), st, a, k_step,
+               v_step, k_new, v_new, slot);
+  return hipGetLastError();
+}
+
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {
-  if (a.n_chunk_max > 0) {
+  if (a.n_chunk_max + a.n_new_chunks > 0) {
     if (a.kv_dtype == 1) {
       if (a.D == 128) launch_decode_t<__bf16, 128>(a, st);
       else launch_decode_t<__bf16, 64>(a, st);

@@ -567,8 +567,9 @@ struct DecodePlan {
   size_t bytes;
 };
 
-sgdkv_status plan_decode(const sgdkv_decode_desc* d, const int64_t* offsets_host, DecodePlan& p) {
+sgdkv_status plan_decode(const sgdkv_decode_desc* d, const int64_t* offsets_host, int64_t capacity, DecodePlan& p) {
   if (!d) return fail(SGDKV_ERR_INVALID_ARG, "NULL descriptor");
+  if (capacity < 0) return fail(SGDKV_ERR_INVALID_ARG, "capacity %lld < 0", (long long)capacity);
   if (!offsets_host) return fail(SGDKV_ERR_INVALID_ARG, "NULL offsets_host");
   if (d->batch < 1 || d->num_q_heads < 1 || d->num_kv_heads < 1)
     return fail(SGDKV_ERR_INVALID_ARG, "batch, num_q_heads, num_kv_heads must be >= 1");
@@ -612,7 +613,11 @@ sgdkv_status plan_decode(const sgdkv_decode_desc* d, const int64_t* offsets_host
   // 2048 resident waves), at least 256 rows; one round of longer splits measured slower
   a.chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(total - offsets_host[0], 8192), 64), 256), 1 << 24);
   a.n_chunk_max = (int)ceil_div(longest, a.chunk);
-  p.bytes = align256((size_t)a.B * a.Hq * a.n_chunk_max * (a.D + 2) * sizeof(float));
+  if ((int64_t)a.B * a.Hkv * capacity * rb > 0xFFFFFFFFll)
+    return fail(SGDKV_ERR_UNSUPPORTED, "appended regions of %lld rows per head exceed 4 GiB", (long long)capacity);
+  a.cap = capacity;
+  a.n_part = a.n_chunk_max + (int)ceil_div(capacity, a.chunk);
+  p.bytes = align256((size_t)a.B * a.Hq * a.n_part * (a.D + 2) * sizeof(float));
   return SGDKV_OK;
 }
 
@@ -622,9 +627,14 @@ extern "C" {
 
 sgdkv_status sgdkv_decode_workspace_size(const sgdkv_decode_desc* desc, const int64_t* offsets_host,
                                          size_t* bytes) {
+  return sgdkv_decode_workspace_size_ex(desc, offsets_host, 0, bytes);
+}
+
+sgdkv_status sgdkv_decode_workspace_size_ex(const sgdkv_decode_desc* desc, const int64_t* offsets_host,
+                                            int64_t capacity, size_t* bytes) {
   if (!bytes) return fail(SGDKV_ERR_INVALID_ARG, "NULL bytes");
   DecodePlan p;
-  if (sgdkv_status st = plan_decode(desc, offsets_host, p)) return st;
+  if (sgdkv_status st = plan_decode(desc, offsets_host, capacity, p)) return st;
   *bytes = p.bytes;
   return ok();
 }
@@ -633,14 +643,28 @@ sgdkv_status sgdkv_decode_attention(const sgdkv_decode_desc* desc, const void* q
                                     const void* v_c, const int64_t* offsets, const int64_t* offsets_host,
                                     void* out, float* lse_out, void* workspace, size_t workspace_bytes,
                                     void* stream) {
+  return sgdkv_decode_attention_ex(desc, q, k_c, v_c, offsets, offsets_host, nullptr, out, lse_out, workspace,
+                                   workspace_bytes, stream);
+}
+
+sgdkv_status sgdkv_decode_attention_ex(const sgdkv_decode_desc* desc, const void* q, const void* k_c,
+                                       const void* v_c, const int64_t* offsets, const int64_t* offsets_host,
+                                       const sgdkv_decode_tail* tail, void* out, float* lse_out, void* workspace,
+                                       size_t workspace_bytes, void* stream) {
+  const sgdkv_decode_tail none{nullptr, nullptr, 0, 0};
+  const sgdkv_decode_tail& t = tail ? *tail : none;
   DecodePlan p;
-  if (sgdkv_status st = plan_decode(desc, offsets_host, p)) return st;
+  if (sgdkv_status st = plan_decode(desc, offsets_host, t.capacity, p)) return st;
   sgdkv::DecodeArgs& a = p.a;
+  if (t.n_new < 0 || t.n_new > t.capacity)
+    return fail(SGDKV_ERR_INVALID_ARG, "n_new %lld outside [0, capacity %lld]", (long long)t.n_new,
+                (long long)t.capacity);
+  if (t.n_new > 0 && (!t.k_new || !t.v_new)) return fail(SGDKV_ERR_INVALID_ARG, "NULL k_new or v_new");
   if (!q || !offsets || !out) return fail(SGDKV_ERR_INVALID_ARG, "NULL q, offsets or out");
   if (a.total_rows > 0 && (!k_c || !v_c)) return fail(SGDKV_ERR_INVALID_ARG, "NULL k_c or v_c");
-  const void* ptrs[] = {q, k_c, v_c, offsets, out, lse_out};
-  const char* names[] = {"q", "k_c", "v_c", "offsets", "out", "lse_out"};
-  for (int i = 0; i < 6; ++i)
+  const void* ptrs[] = {q, k_c, v_c, offsets, out, lse_out, t.k_new, t.v_new};
+  const char* names[] = {"q", "k_c", "v_c", "offsets", "out", "lse_out", "k_new", "v_new"};
+  for (int i = 0; i < 8; ++i)
     if (ptrs[i] && !aligned16(ptrs[i])) return fail(SGDKV_ERR_INVALID_ARG, "%s is not 16-byte aligned", names[i]);
   if (p.bytes > 0) {
     if (!workspace) return fail(SGDKV_ERR_WORKSPACE, "NULL workspace (%zu bytes needed)", p.bytes);
@@ -656,12 +680,43 @@ sgdkv_status sgdkv_decode_attention(const sgdkv_decode_desc* desc, const void* q
   a.offsets = offsets;
   a.out = out;
   a.lse_out = lse_out;
+  a.k_new = t.k_new;
+  a.v_new = t.v_new;
+  a.n_new = t.n_new;
+  a.n_new_chunks = (int)ceil_div(t.n_new, a.chunk);
   a.part = static_cast<float*>(workspace);
-  a.part_ms = a.part + (size_t)a.B * a.Hq * a.n_chunk_max * a.D;
+  a.part_ms = a.part + (size_t)a.B * a.Hq * a.n_part * a.D;
   hipError_t e = hipGetLastError();
   (void)e;
   e = sgdkv::launch_decode(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "decode kernels: %s", hipGetErrorString(e));
+  return ok();
+}
+
+sgdkv_status sgdkv_append_kv(const sgdkv_decode_desc* desc, const void* k_step, const void* v_step, void* k_new,
+                             void* v_new, int64_t capacity, int64_t slot, void* stream) {
+  if (!desc) return fail(SGDKV_ERR_INVALID_ARG, "NULL descriptor");
+  if (desc->batch < 1 || desc->num_kv_heads < 1)
+    return fail(SGDKV_ERR_INVALID_ARG, "batch, num_q_heads, num_kv_heads must be >= 1");
+  const int64_t nseg = (int64_t)desc->batch * desc->num_kv_heads;
+  if (nseg > 65535) return fail(SGDKV_ERR_UNSUPPORTED, "batch * num_kv_heads = %lld > 65535", (long long)nseg);
+  // plan with empty segments: checks the sizes and the bound of the appended region
+  const std::vector<int64_t> offs((size_t)nseg + 1, 0);
+  DecodePlan p;
+  if (sgdkv_status st = plan_decode(desc, offs.data(), capacity, p)) return st;
+  if (slot < 0 || slot >= capacity)
+    return fail(SGDKV_ERR_INVALID_ARG, "slot %lld outside [0, capacity %lld)", (long long)slot, (long long)capacity);
+  const void* ptrs[] = {k_step, v_step, k_new, v_new};
+  const char* names[] = {"k_step", "v_step", "k_new", "v_new"};
+  for (int i = 0; i < 4; ++i) {
+    if (!ptrs[i]) return fail(SGDKV_ERR_INVALID_ARG, "NULL %s", names[i]);
+    if (!aligned16(ptrs[i])) return fail(SGDKV_ERR_INVALID_ARG, "%s is not 16-byte aligned", names[i]);
+  }
+  if (sgdkv_status st = check_device()) return st;
+  hipError_t e = hipGetLastError();
+  (void)e;
+  e = sgdkv::launch_append(p.a, k_step, v_step, k_new, v_new, slot, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "append kernel: %s", hipGetErrorString(e));
   return ok();
 }
 

@@ -91,12 +91,21 @@ struct DecodeArgs {
   int64_t total_rows;  // offsets_host[B*Hkv]: device offsets are clamped to it
   void* out;
   float* lse_out;
-  float* part;        // [B*Hq][n_chunk_max][D]: o per split (16-byte aligned rows)
-  float* part_ms;     // [B*Hq][n_chunk_max][2]: (m, s) per split
+  float* part;        // [B*Hq][n_part][D]: o per split (16-byte aligned rows)
+  float* part_ms;     // [B*Hq][n_part][2]: (m, s) per split
   int64_t chunk;      // rows per split (multiple of 64, at least 256)
-  int n_chunk_max;    // max over segments of ceil(len / chunk)
+  int n_chunk_max;    // max over segments of ceil(len / chunk): splits of the compressed rows
+  // rows appended after compression: (b, h) owns rows [0, n_new) of k_new/v_new + (b*Hkv+h)*cap rows;
+  // their splits come after the compressed ones, at index n_chunk_max + j
+  const void* k_new;
+  const void* v_new;
+  int64_t cap, n_new;
+  int n_new_chunks;   // ceil(n_new / chunk)
+  int n_part;         // split slots per (b, q): n_chunk_max + ceil(capacity / chunk)
 };
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
+hipError_t launch_append(const DecodeArgs& a, const void* k_step, const void* v_step, void* k_new, void* v_new,
+                         int64_t slot, hipStream_t stream);
 
 }  // namespace sgdkv

@@ -290,6 +290,42 @@ def test_decode_validation():
     assert _decode(d, oh, ws_bytes=8) == sg.ERR_WORKSPACE
 
 
+def test_append_and_tail_validation():
+    lib = sg.load_library()
+    desc = sg.DecodeDesc(2, 8, 4, 128, sg.DTYPE_BF16, sg.DTYPE_F32, 0.0)
+    oh = np.array([0, 10, 20, 30, 40, 50, 60, 70, 80], dtype=np.int64)
+    P = sg._np_ptr
+    need = ctypes.c_size_t(0)
+    assert lib.sgdkv_decode_workspace_size_ex(ctypes.byref(desc), P(oh), -1, ctypes.byref(need)) == sg.ERR_INVALID_ARG
+    assert lib.sgdkv_decode_workspace_size_ex(ctypes.byref(desc), P(oh), 0, ctypes.byref(need)) == sg.OK
+    n0 = need.value
+    assert lib.sgdkv_decode_workspace_size_ex(ctypes.byref(desc), P(oh), 1000, ctypes.byref(need)) == sg.OK
+    assert need.value > n0
+    ws = need.value
+
+    def dec(tail, ws_bytes=ws):
+        return lib.sgdkv_decode_attention_ex(ctypes.byref(desc), FAKE, FAKE, FAKE, FAKE, P(oh), ctypes.byref(tail),
+                                             FAKE, None, FAKE, ws_bytes, None)
+    assert dec(sg.DecodeTail(FAKE, FAKE, 100, 101)) == sg.ERR_INVALID_ARG      # n_new > capacity
+    assert dec(sg.DecodeTail(FAKE, FAKE, 100, -1)) == sg.ERR_INVALID_ARG
+    assert dec(sg.DecodeTail(None, FAKE, 100, 5)) == sg.ERR_INVALID_ARG        # k_new missing
+    assert dec(sg.DecodeTail(FAKE + 8, FAKE, 100, 5)) == sg.ERR_INVALID_ARG    # misaligned
+    assert dec(sg.DecodeTail(FAKE, FAKE, 1000, 5), ws_bytes=n0) == sg.ERR_WORKSPACE  # planned for no tail
+    assert dec(sg.DecodeTail(FAKE, FAKE, 1 << 40, 5)) == sg.ERR_UNSUPPORTED    # region over 4 GiB
+
+    def app(cap, slot, ptrs=(FAKE, FAKE, FAKE, FAKE)):
+        return lib.sgdkv_append_kv(ctypes.byref(desc), *ptrs, cap, slot, None)
+    assert app(10, 10) == sg.ERR_INVALID_ARG
+    assert app(10, -1) == sg.ERR_INVALID_ARG
+    assert app(10, 3, (FAKE, None, FAKE, FAKE)) == sg.ERR_INVALID_ARG
+    assert app(10, 3, (FAKE, FAKE, FAKE + 4, FAKE)) == sg.ERR_INVALID_ARG
+    assert app(1 << 40, 3) == sg.ERR_UNSUPPORTED
+    bad = sg.DecodeDesc(0, 8, 4, 128, sg.DTYPE_BF16, sg.DTYPE_F32, 0.0)
+    assert lib.sgdkv_append_kv(ctypes.byref(bad), FAKE, FAKE, FAKE, FAKE, 10, 3, None) == sg.ERR_INVALID_ARG
+    if not _gpu():
+        assert app(10, 3) == sg.ERR_HIP  # validation passed; no device here
+
+
 @pytest.mark.skipif(_gpu(), reason="checks the no-device path")
 def test_no_device_fails_after_validation():
     assert _compress(_desc(), [512, 512]) == sg.ERR_HIP

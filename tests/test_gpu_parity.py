@@ -349,6 +349,45 @@ def test_decode_fixed_reference_redo():
     assert np.abs(lse.cpu().numpy() - ref_lse).max() <= 2e-2
 
 
+@pytest.mark.parametrize("dtype,cap", [(torch.bfloat16, 300), (torch.float32, 20)])
+def test_decode_with_appended_rows(dtype, cap):
+    """Generation after compression: each step appends one K/V row per KV head (sgdkv_append_kv)
+    and decodes over the compressed segment plus the rows appended so far, against the oracle.
+    A capacity of 300 rows spans two 256-row splits of the appended region; one segment kept
+    no rows at all, so it attends to its appended rows alone."""
+    rng = np.random.Generator(np.random.PCG64(77))
+    B, Hq, Hkv, d = 2, 8, 4, 128 if dtype == torch.bfloat16 else 64
+    lens = [300, 0, 17, 1000, 5, 256, 1, 700]
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    mk = lambda *shape: torch.from_numpy(rng.standard_normal(shape)).to(dtype).to(DEV)
+    kc, vc = mk(offs[-1], d), mk(offs[-1], d)
+    k_new = torch.zeros((B, Hkv, cap, d), dtype=dtype, device=DEV)
+    v_new = torch.zeros_like(k_new)
+    off_d = torch.from_numpy(offs).to(DEV)
+    atol = 2e-2 if dtype == torch.bfloat16 else 1e-5
+    steps = list(range(5)) + ([cap - 1] if cap > 5 else [])
+    n = 0
+    for t in steps:
+        q = mk(B, Hq, d)
+        # fill the region up to slot t (each step appends one row; a jump fills the rows between)
+        while n <= t:
+            sg.append_kv(q, mk(B, Hkv, d), mk(B, Hkv, d), k_new, v_new, n)
+            n += 1
+        _announce(f"decode with {n} appended rows ({dtype}, capacity {cap})")
+        out, lse = sg.decode_attention(q, kc, vc, off_d, offs, Hkv, out_dtype=torch.float32, k_new=k_new,
+                                       v_new=v_new, n_new=n)
+        torch.cuda.synchronize()
+        ref, ref_lse = oracle.decode_append(_f64(q), _f64(kc), _f64(vc), offs, _f64(k_new), _f64(v_new), n, Hkv)
+        assert np.abs(out.cpu().numpy() - ref).max() <= atol, t
+        assert np.abs(lse.cpu().numpy() - ref_lse).max() <= max(atol, 1e-5), t
+    # with nothing appended the extended call is plain decode, bit for bit
+    q = mk(B, Hq, d)
+    a, la = sg.decode_attention(q, kc, vc, off_d, offs, Hkv, out_dtype=torch.float32, k_new=k_new, v_new=v_new, n_new=0)
+    b, lb = sg.decode_attention(q, kc, vc, off_d, offs, Hkv, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b) and torch.equal(la, lb)
+
+
 def test_run_twice_bitwise():
     wl, t = _qwen_small(2, 2222)
     budgets = np.array([700, 500, 1500, 400])

@@ -49,8 +49,13 @@ MUTANTS = {
                                "if (a->sigma < b->sigma) return -1;\n  if (a->sigma > b->sigma) return 1;\n  return (a->idx < b->idx) ? -1 : (a->idx > b->idx);\n}\n\nint orc_allocate", ALLOC),
     "alloc_round_smallest": ("if (a->frac > b->frac) return -1;\n  if (a->frac < b->frac) return 1;",
                              "if (a->frac < b->frac) return -1;\n  if (a->frac > b->frac) return 1;", ALLOC),
-    "decode_no_normalise": ("for (int t = 0; t < d; ++t) o[t] /= z;", "", SELDEC),
-    "decode_wrong_group": ("int64_t b = bq / Hq, qh = bq % Hq, h = qh / G;", "int64_t b = bq / Hq, qh = bq % Hq, h = qh % Hkv;", SELDEC),
+    "decode_no_normalise": ("for (int t = 0; t < d; ++t) o[t] += p * vc[r * d + t];\n    }\n    for (int t = 0; t < d; ++t) o[t] /= z;",
+                            "for (int t = 0; t < d; ++t) o[t] += p * vc[r * d + t];\n    }\n", SELDEC),
+    "append_no_normalise": ("for (int t = 0; t < d; ++t) o[t] += p * vr[t];\n    }\n    for (int t = 0; t < d; ++t) o[t] /= z;",
+                            "for (int t = 0; t < d; ++t) o[t] += p * vr[t];\n    }\n", APPEND),
+    "decode_wrong_group": ("int64_t b = bq / Hq, qh = bq % Hq, h = qh / G;\n    int64_t r0 = offsets[b * Hkv + h], r1 = offsets[b * Hkv + h + 1];\n    const double* qv",
+                           "int64_t b = bq / Hq, qh = bq % Hq, h = qh % Hkv;\n    int64_t r0 = offsets[b * Hkv + h], r1 = offsets[b * Hkv + h + 1];\n    const double* qv",
+                           SELDEC),
     "thr_at_mean": ("t[h] = sigma[h] < mean ? 0.0 : sigma[h];", "t[h] = sigma[h] <= mean ? 0.0 : sigma[h];", VARIANTS),
     "reverse_whole_budget": ("budgets[h] = s + W + (M - (budgets[h] - s - W));", "budgets[h] = s + W + (M - budgets[h]);",
                              VARIANTS),
