@@ -108,7 +108,7 @@ def source_sha(name):
 
 
 def traffic_path(workload, ratio):
-    return os.path.join(ROOT, "profiles", f"traffic_{workload}_r{int(round(ratio * 100))}.json")
+    return os.path.join(ROOT, "profiles", f"traffic_{workload}_ratio{int(round(ratio * 100))}.json")
 
 
 _TRAFFIC = {}

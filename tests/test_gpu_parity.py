@@ -4,11 +4,12 @@ Every check calls the library through the C ABI (paper_2609_03235_amd) and
 compares with the oracle on the same seeded inputs:
 
 * budgets, offsets and the gathered K/V rows: bit-exact;
-* pooled window scores: |gpu - oracle| <= 1e-5 * max(|oracle|, 1e-12 * max);
+* pooled window scores: |gpu - oracle| <= rtol * max(|oracle|, 1e-12 * max), rtol 1e-5 for
+  fp32 inputs and 2e-5 for bf16 inputs (the bf16 MFMA's accumulation error, see SCORE_RTOL_BF16);
 * kept positions: bit-exact against the oracle's selection applied to the
   GPU's own fp32 scores (both sides decide in the kernel's precision), and
   against the oracle's fp64 selection except inside the near-tie band
-  (|score - tau| <= 1e-5 * tau);
+  (|score - tau| <= rtol * tau);
 * decode: the oracle's compressed cache fed to the GPU decode, within 1e-5
   absolute for fp32 inputs and 2e-2 absolute (fp32 output) for bf16 inputs.
 """
@@ -25,6 +26,11 @@ import workloads
 pytestmark = pytest.mark.gpu
 
 SCORE_RTOL = 1e-5
+# bf16 inputs: the bf16 MFMA's fp32 accumulation is off by up to about 2^-23 * sum_d |q_d k_d| per
+# logit (measured on gfx950 for a chain of four 16x16x32 instructions), and a window score carries
+# the difference of its own logit's error and its row LSE's. Keys scaled x8 reach
+# scale * sum_d |q_d k_d| of about 60, so scores may be off by up to about 1.4e-5 of their value.
+SCORE_RTOL_BF16 = 2e-5
 DEV = "cuda"
 
 
@@ -36,19 +42,24 @@ def _f64(t):
     return t.detach().cpu().double().numpy()
 
 
-def _check_scores(g, o, tag=""):
+def _score_rtol(q_win):
+    return SCORE_RTOL_BF16 if q_win.dtype == torch.bfloat16 else SCORE_RTOL
+
+
+def _check_scores(g, o, tag="", rtol=SCORE_RTOL):
     g = np.asarray(g, dtype=np.float64)
     floor = 1e-12 * np.max(np.abs(o), axis=-1, keepdims=True)
-    tol = SCORE_RTOL * np.maximum(np.abs(o), floor)
+    tol = rtol * np.maximum(np.abs(o), floor)
     bad = np.abs(g - o) > tol
     if bad.any():
         idx = np.argwhere(bad)[:5]
         rel = (np.abs(g - o) / np.maximum(np.abs(o), 1e-300))[bad]
-        raise AssertionError(f"{tag} {bad.sum()} scores outside rtol {SCORE_RTOL}; worst rel {rel.max():.3e}; "
+        raise AssertionError(f"{tag} {bad.sum()} scores outside rtol {rtol}; worst rel {rel.max():.3e}; "
                              f"first {idx.tolist()}")
+    return float((np.abs(g - o) / np.maximum(np.abs(o), floor)).max()) if o.size else 0.0
 
 
-def _check_kept(res, orc, q_shape, C, w, s, W, budgets, tag="", win0=None):
+def _check_kept(res, orc, q_shape, C, w, s, W, budgets, tag="", win0=None, rtol=SCORE_RTOL):
     """Selection checks for every segment; returns True if GPU and oracle kept sets are identical."""
     B, Hq = q_shape[0], q_shape[1]
     Hkv = len(budgets)
@@ -72,7 +83,7 @@ def _check_kept(res, orc, q_shape, C, w, s, W, budgets, tag="", win0=None):
                 cand = np.sort(po[s:C - W])[::-1]
                 tau = cand[m - 1]
                 diff = np.setxor1d(seg, ref)
-                assert np.all(np.abs(po[diff] - tau) <= SCORE_RTOL * tau), \
+                assert np.all(np.abs(po[diff] - tau) <= rtol * tau), \
                     f"{tag} b={b} h={h}: kept sets differ outside the near-tie band"
     return identical
 
@@ -133,8 +144,9 @@ def test_tiny_end_to_end():
     budgets = sg.allocate_budgets(sc, 1, 2, wl.seq_len, wl.b_sink, wl.b_window, total)
     assert np.array_equal(budgets, oracle.allocate_budgets(sc, 1, 2, wl.seq_len, wl.b_sink, wl.b_window, total))
     res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=wl.pool_kernel, s=wl.b_sink, W=wl.b_window)
-    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "tiny")
-    _check_kept(res, orc, t["q_win"].shape, wl.seq_len, wl.obs_window, wl.b_sink, wl.b_window, budgets, "tiny")
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "tiny", rtol=_score_rtol(t["q_win"]))
+    _check_kept(res, orc, t["q_win"].shape, wl.seq_len, wl.obs_window, wl.b_sink, wl.b_window, budgets, "tiny",
+                rtol=_score_rtol(t["q_win"]))
     _check_gather(res, t["k"], t["v"], budgets)
     _decode_on_oracle_cache(orc, t["q"], 2, torch.float32, 1e-5, "tiny")
     # end to end on the GPU's own cache
@@ -155,8 +167,8 @@ def test_tiny_ragged_batches(B, C, budget_kind):
         budgets = rng.integers(s + W, C + 1, size=2)
     _announce(f"tiny ragged B={B} C={C} budgets={budgets.tolist()}")
     res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=7, s=s, W=W)
-    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "ragged")
-    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "ragged")
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "ragged", rtol=_score_rtol(t["q_win"]))
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "ragged", rtol=_score_rtol(t["q_win"]))
     _check_gather(res, t["k"], t["v"], budgets)
     _decode_on_oracle_cache(orc, t["q"], 2, torch.float32, 1e-5, "ragged")
 
@@ -178,8 +190,8 @@ def test_bf16_qwen_shaped(B, C, Hq, Hkv, d):
     budgets = sg.allocate_budgets(sc, 1, Hkv, C, s, W, total)
     _announce(f"bf16 B={B} C={C} Hq={Hq} Hkv={Hkv} d={d} budgets={budgets.tolist()}")
     res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=7, s=s, W=W)
-    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "bf16")
-    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "bf16")
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "bf16", rtol=_score_rtol(t["q_win"]))
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "bf16", rtol=_score_rtol(t["q_win"]))
     _check_gather(res, t["k"], t["v"], budgets)
     _decode_on_oracle_cache(orc, t["q"], Hkv, torch.bfloat16, 2e-2, "bf16")
 
@@ -200,8 +212,8 @@ def test_ipt_group_aggregation(agg, B, C, Hq, Hkv, d, w):
     budgets = np.maximum(budgets, s + W)
     _announce(f"Ipt agg={agg} B={B} C={C} Hq={Hq} Hkv={Hkv} d={d} w={w}")
     res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=7, s=s, W=W, agg=agg, qhead_scores=qs)
-    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], f"ipt{agg}")
-    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, f"ipt{agg}")
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], f"ipt{agg}", rtol=_score_rtol(t["q_win"]))
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, f"ipt{agg}", rtol=_score_rtol(t["q_win"]))
     _check_gather(res, t["k"], t["v"], budgets)
     if agg == sg.GROUP_IPT_MEAN:
         # unit scores reduce the weighted mean to the plain group mean, to the last bit
@@ -235,8 +247,8 @@ def test_window_placement(case):
     res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=kp, s=s, W=W, agg=agg, qhead_scores=qs,
                               win0=win0)
     assert res["scores"].shape[-1] == win0
-    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], case)
-    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, case, win0=win0)
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], case, rtol=_score_rtol(t["q_win"]))
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, case, win0=win0, rtol=_score_rtol(t["q_win"]))
     _check_gather(res, t["k"], t["v"], budgets)
 
 
@@ -249,8 +261,8 @@ def test_caller_supplied_lse_and_scores_only():
     _announce("caller-supplied window LSE")
     res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=7, s=s, W=W, window_lse=lse_t,
                               orc_lse=lse_t.cpu().double().numpy())
-    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "lse-in")
-    _check_kept(res, orc, t["q_win"].shape, 2100, 64, s, W, budgets, "lse-in")
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "lse-in", rtol=_score_rtol(t["q_win"]))
+    _check_kept(res, orc, t["q_win"].shape, 2100, 64, s, W, budgets, "lse-in", rtol=_score_rtol(t["q_win"]))
     _check_gather(res, t["k"], t["v"], budgets)
     _announce("scores-only mode")
     only = sg.compress_layer(t["q_win"], t["k"], None, None, pool_kernel=7, b_sink=s, b_window=W,
@@ -421,8 +433,8 @@ def test_lse_exact_redo_paths():
     budgets = np.array([s + W + 15, s + W + 5])  # selection stays among the keys near the spikes
     _announce("pass-1 exact redo paths")
     res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=7, s=s, W=W)
-    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "redo")
-    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "redo")
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "redo", rtol=_score_rtol(t["q_win"]))
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "redo", rtol=_score_rtol(t["q_win"]))
 
 
 @pytest.mark.parametrize("w,W", [(100, 128), (200, 200)])
@@ -435,6 +447,73 @@ def test_long_window_spans_masked_tiles(w, W):
     budgets = np.array([s + W + 300, s + W + 17])
     _announce(f"long window w={w} W={W}")
     res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=5, s=s, W=W)
-    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "longwin")
-    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "longwin")
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "longwin", rtol=_score_rtol(t["q_win"]))
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "longwin", rtol=_score_rtol(t["q_win"]))
     _check_gather(res, t["k"], t["v"], budgets)
+
+
+# ---------------------------------------------------------------------- full workload sizes
+# Each workload at its full shape and batch, with the launch configuration the benchmark times
+# (layer 0 of the workload's stack, budgets from the 25 % allocation over every layer's heads).
+# Every sequence is checked by what holds at any size: offsets, the kept set equal to the top-k
+# of the GPU's own scores, the gathered rows equal to the input rows. The oracle then runs the
+# whole layer on the listed sequences: scores, kept sets and decode are compared element by
+# element there.
+FULL_CASES = [("qwen25_32k", (0,)), ("qwen25_128k", (0, 7)), ("qwen3_256k", (15,)), ("qwen25_1m", (31,))]
+
+
+@pytest.mark.parametrize("key,oracle_seqs", FULL_CASES, ids=[c[0] for c in FULL_CASES])
+def test_full_size(key, oracle_seqs):
+    wl = workloads.WORKLOADS[key]
+    L, B, Hq, Hkv, d, C = wl.layers, wl.batch, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.seq_len
+    w, kp, s, W = wl.obs_window, wl.pool_kernel, wl.b_sink, wl.b_window
+    sc = workloads.head_scores(wl)
+    total = sg.total_from_ratio(0.25, L, Hkv, C, s, W)
+    budgets_all = sg.allocate_budgets(sc, L, Hkv, C, s, W, total)
+    assert np.array_equal(budgets_all, oracle.allocate_budgets(sc, L, Hkv, C, s, W, total))
+    budgets = budgets_all.reshape(L, Hkv)[0]
+    _announce(f"full size {wl.name}: B={B} C={C} Hq={Hq} Hkv={Hkv} budgets={budgets.tolist()}")
+    t = workloads.torch_layer_tensors(wl, 0, DEV)
+    rtol = _score_rtol(t["q_win"])
+    res = sg.compress_layer(t["q_win"], t["k"], t["v"], budgets, pool_kernel=kp, b_sink=s, b_window=W)
+    out, lse = sg.decode_attention(t["q"], res["k_c"], res["v_c"], res["offsets"], res["offsets_host"], Hkv,
+                                   out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    offs = res["offsets"].cpu().numpy()
+    assert np.array_equal(offs, res["offsets_host"])
+    T = int(budgets.sum())
+    pre = np.concatenate([[0], np.cumsum(budgets)])
+    assert np.array_equal(offs, np.array([b * T + pre[h] for b in range(B) for h in range(Hkv)] + [B * T]))
+    scores = res["scores"].cpu().numpy()
+    kept = res["kept_pos"].cpu().numpy()
+    assert np.isfinite(scores).all() and (scores >= 0).all()
+    for b in range(B):
+        for h in range(Hkv):
+            seg = kept[offs[b * Hkv + h]:offs[b * Hkv + h + 1]]
+            ref = oracle.select(scores[b, h].astype(np.float64), C, w, s, W, int(budgets[h]) - s - W)
+            assert np.array_equal(seg, ref), f"b={b} h={h}: kept set differs from top-k of GPU scores"
+    _check_gather(res, t["k"], t["v"], budgets)
+    _announce(f"full size {wl.name}: properties hold for all {B} sequences; oracle on {list(oracle_seqs)}")
+    for b in oracle_seqs:
+        orc = oracle.compress(_f64(t["q_win"][b:b + 1]), _f64(t["k"][b:b + 1]), _f64(t["v"][b:b + 1]), budgets,
+                              w=w, kp=kp, s=s, W=W)
+        worst = _check_scores(scores[b:b + 1], orc["pooled"], f"full {key} b={b}", rtol=rtol)
+        for h in range(Hkv):
+            seg = kept[offs[b * Hkv + h]:offs[b * Hkv + h + 1]]
+            ref = orc["kept_pos"][orc["offsets"][h]:orc["offsets"][h + 1]]
+            if not np.array_equal(seg, ref):
+                po = orc["pooled"][0, h]
+                tau = np.sort(po[s:C - W])[::-1][int(budgets[h]) - s - W - 1]
+                diff = np.setxor1d(seg, ref)
+                assert np.all(np.abs(po[diff] - tau) <= rtol * tau), \
+                    f"full {key} b={b} h={h}: kept sets differ outside the near-tie band"
+        del orc
+        # decode of this sequence over the GPU's compressed cache (shown above to be the input rows)
+        lo, hi = offs[b * Hkv], offs[(b + 1) * Hkv]
+        ref_out, ref_lse = oracle.decode(_f64(t["q"][b:b + 1]), _f64(res["k_c"][lo:hi]), _f64(res["v_c"][lo:hi]),
+                                         offs[b * Hkv:(b + 1) * Hkv + 1] - lo, Hkv)
+        err = np.abs(out[b:b + 1].cpu().numpy() - ref_out).max()
+        assert err <= 2e-2, f"full {key} b={b}: decode max abs err {err:.3e}"
+        assert np.abs(lse[b:b + 1].cpu().numpy() - ref_lse).max() <= 2e-2
+        _announce(f"full size {wl.name}: sequence {b} matches the oracle (worst score rel err {worst:.3e}, "
+                  f"decode err {err:.2e})")
