@@ -38,7 +38,7 @@ template <typename T, int D>
 struct TileGeom {
   static constexpr int EB = elt_bytes<T>();
   static constexpr int RB = D * EB;           // bytes per key row
-  static constexpr int LDS_STRIDE = RB + 16;  // padded row pitch: conflict-free 16-B fragment reads
+  static constexpr int LDS_STRIDE = RB + 32;  // padded row pitch: 16-B fragment reads free of bank conflicts (measured)
   static constexpr int NC = D / 32;           // 32-wide k chunks
   static constexpr int V16 = RB / 16;         // 16-byte vectors per row
 };
@@ -177,14 +177,17 @@ __device__ __forceinline__ void chunk_pipeline(char* kbuf, const rsrc_t& kr, int
 // Pass 1: per-chunk partial log-sum-exp of every window row -------------------
 //
 // Each lane keeps, for each of its 4*NB row slots, a reference m and a sum
-// s = sum 2^(y - m) over the keys it has seen (y = logit * log2 e). m is fixed
-// within a tile, so each logit costs one fma, one exp2 and one add; it starts
-// at the lane's own logit of the chunk's first key. After each tile, if any
-// slot's sum left [0, 2^96] (a logit more than ~96 above its reference, or
-// inf/NaN), and on every tile that reaches the causal window block, the wave
-// restores the sums and redoes the tile with the exact online update (two
-// exp2 per logit, m = running max), reading the keys from global memory so
-// that the LDS buffers are free to move on. Padded rows (past R) keep m = 0.
+// s = sum 2^(y - m) over the keys it has seen (y = logit * log2 e). The tiles
+// of the chunk that every window row sees in full run through the pipeline
+// with m fixed at the row's largest logit among the chunk's first 16 keys, so
+// each logit costs one fma, one exp2 and one add and the loop has no branch.
+// A sum can only overflow if a later logit exceeds that maximum by about 100
+// (base 2); the chunk's sums are checked once at its end and, if any left
+// [0, 2^126] (inf and NaN included), the whole chunk is recomputed with the
+// exact online update (two exp2 per logit, m = running max), reading the keys
+// from global memory. The tiles that reach the window block (causal mask) or
+// pass the end of the head always take that exact path. Padded rows (past R)
+// keep m = 0.
 template <typename T, int D, int NB, int TILE>
 __device__ __forceinline__ void lse_exact_tile(const rsrc_t& kr, int lr, int lg, int wid, int w, int64_t tile0,
                                             int64_t vis0, int64_t C, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
@@ -193,12 +196,19 @@ __device__ __forceinline__ void lse_exact_tile(const rsrc_t& kr, int lr, int lg,
   using G = TileGeom<T, D>;
   constexpr int NBX = NB > 0 ? NB : 1;
   const bool masked = tile0 + TILE > vis0;
+  auto load = [&](int t, Frag<T>(&kb)[D / 32]) {
+#pragma unroll
+    for (int c = 0; c < G::NC; ++c)
+      kb[c] = gload_frag<T>(kr, (uint32_t)((tile0 + 16 * t + lr) * G::RB + (32 * c + 8 * lg) * G::EB));
+  };
+  Frag<T> kn[D / 32];
+  load(0, kn);
 #pragma unroll 1
   for (int t = 0; t < TILE / 16; ++t) {
     Frag<T> kb[D / 32];
 #pragma unroll
-    for (int c = 0; c < G::NC; ++c)
-      kb[c] = gload_frag<T>(kr, (uint32_t)((tile0 + 16 * t + lr) * G::RB + (32 * c + 8 * lg) * G::EB));
+    for (int c = 0; c < G::NC; ++c) kb[c] = kn[c];
+    load(t + 1 < TILE / 16 ? t + 1 : t, kn);  // the next subtile's keys are in flight during this one
     f32x4 acc[NBX];
     subtile_mfma<T, D, NB>(qa, kb, acc);
     const int64_t key = tile0 + 16 * t + lr;
@@ -220,7 +230,7 @@ __device__ __forceinline__ void lse_exact_tile(const rsrc_t& kr, int lr, int lg,
 }
 
 template <typename T, int D, int NB>
-__device__ void lse_chunk(const CompressArgs& a, char* kbuf, int seg, int wid, int lane,
+__device__ void lse_chunk(const CompressArgs& a, char* kbuf, int seg, int chunk, int wid, int lane,
                           const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], const rsrc_t& kr, int64_t key0,
                           int64_t key_end) {
   constexpr int NBX = NB > 0 ? NB : 1;
@@ -228,58 +238,60 @@ __device__ void lse_chunk(const CompressArgs& a, char* kbuf, int seg, int wid, i
   const int lr = lane & 15, lg = lane >> 4;
   const int64_t vis0 = a.win0;  // the row with window index i sees key j iff j - vis0 <= i (and j < C)
   const float c2 = a.c2;
-  float m[NBX][4], s[NBX][4], s0[NBX][4];
+  float m[NBX][4], s[NBX][4];
   bool real[NBX][4];
+  auto reset = [&]() {
+#pragma unroll
+    for (int j = 0; j < NBX; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        m[j][i] = real[j][i] ? -INFINITY : 0.f;  // a padded row must not force the exact path
+        s[j][i] = 0.f;
+      }
+  };
 #pragma unroll
   for (int j = 0; j < NBX; ++j)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      real[j][i] = (wid + kScoreWaves * j) * 16 + 4 * lg + i < a.R;
-      m[j][i] = real[j][i] ? -INFINITY : 0.f;  // a padded row must not force the exact path
-      s[j][i] = 0.f;
-    }
+    for (int i = 0; i < 4; ++i) real[j][i] = (wid + kScoreWaves * j) * 16 + 4 * lg + i < a.R;
+  reset();
+  // whole tiles every row sees (keys below both the window block and the end of the head)
+  const int64_t open_end = vis0 < a.C ? vis0 : a.C;
+  const int64_t fast_end = key_end < open_end ? key_end : open_end;
+  const int64_t nfast = fast_end > key0 ? (fast_end - key0) / TILE : 0;
   const int64_t ntiles = (key_end - key0 + TILE - 1) / TILE;
-  chunk_pipeline<T, D, NB, TILE>(
-      kbuf, kr, key0, a.C, ntiles, lr, lg, qa,
-      [&](const f32x4(&acc)[NBX]) {
-        if (key0 + TILE <= vis0 && key0 + TILE <= a.C) {  // uniform: every row sees every key of the first tile
+  if (nfast > 0) {
+    chunk_pipeline<T, D, NB, TILE>(
+        kbuf, kr, key0, a.C, nfast, lr, lg, qa,
+        [&](const f32x4(&acc)[NBX]) {
 #pragma unroll
           for (int j = 0; j < NB; ++j)
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-              if (real[j][i]) m[j][i] = acc[j][i] * c2;
-        }
-      },
-      [&](int64_t, int sub, const f32x4(&acc)[NBX]) {
-        if (sub == 0) {
+            for (int i = 0; i < 4; ++i) {
+              const float mx = row16_max(acc[j][i] * c2);  // every lane of the 16-lane row takes part
+              if (real[j][i]) m[j][i] = mx;
+            }
+        },
+        [&](int64_t, int, const f32x4(&acc)[NBX]) {
 #pragma unroll
-          for (int j = 0; j < NBX; ++j)
+          for (int j = 0; j < NB; ++j)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) s0[j][i] = s[j][i];
-        }
+            for (int i = 0; i < 4; ++i) s[j][i] += fast_exp2(fmaf(acc[j][i], c2, -m[j][i]));
+        },
+        [&](int64_t) {}, [&](int64_t) {});
+    bool bad = false;
 #pragma unroll
-        for (int j = 0; j < NB; ++j)
+    for (int j = 0; j < NB; ++j)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) s[j][i] += fast_exp2(fmaf(acc[j][i], c2, -m[j][i]));
-      },
-      [&](int64_t) {},
-      [&](int64_t t) {
-        const int64_t tile0 = key0 + t * TILE;
-        bool bad = tile0 + TILE > vis0 || tile0 + TILE > a.C;  // causal or past the head: exact path
-#pragma unroll
-        for (int j = 0; j < NB; ++j)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) bad |= !(s[j][i] <= 7.9228162514264338e28f);  // 2^96; catches inf and NaN
-        if (__any(bad)) {
-#pragma unroll
-          for (int j = 0; j < NBX; ++j)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) s[j][i] = s0[j][i];
-          lse_exact_tile<T, D, NB, TILE>(kr, lr, lg, wid, a.w, tile0, vis0, a.C, qa, c2, m, s);
-        }
-      });
+      for (int i = 0; i < 4; ++i) bad |= !(s[j][i] <= 8.5070591730234616e37f);  // 2^126; catches inf and NaN
+    if (__any(bad)) {
+      reset();
+      for (int64_t t = 0; t < nfast; ++t)
+        lse_exact_tile<T, D, NB, TILE>(kr, lr, lg, wid, a.w, key0 + t * TILE, vis0, a.C, qa, c2, m, s);
+    }
+  }
+  for (int64_t t = nfast; t < ntiles; ++t)
+    lse_exact_tile<T, D, NB, TILE>(kr, lr, lg, wid, a.w, key0 + t * TILE, vis0, a.C, qa, c2, m, s);
   // Combine the 16 lanes (keys) of each row, then store (m, s) for the row.
-  const int chunk = blockIdx.x;
   float* part = a.lse_part + ((int64_t)seg * a.n_lse_chunks + chunk) * a.R * 2;
   const rsrc_t pr = make_rsrc(part, (uint64_t)a.R * 2 * sizeof(float));
 #pragma unroll
@@ -311,7 +323,9 @@ __global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
   __shared__ __attribute__((aligned(16))) char ktile[2 * kLseTile * G::LDS_STRIDE];
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
-  const int64_t key0 = (int64_t)blockIdx.x * a.score_chunk;
+  // the last chunks go first: the one with the window block ends with its exact (masked) tiles
+  const int chunk = (int)(gridDim.x - 1 - blockIdx.x);
+  const int64_t key0 = (int64_t)chunk * a.score_chunk;
   if (key0 >= a.C) return;
   const int64_t key_end = key0 + a.score_chunk < a.C ? key0 + a.score_chunk : a.C;
   const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
@@ -321,14 +335,14 @@ __global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
   // blocks this wave owns: RBW or RBW-1 (uniform per wave)
   const int nrb = (a.R + 15) / 16;
   if (wid + kScoreWaves * (RBW - 1) < nrb) {
-    lse_chunk<T, D, RBW>(a, ktile, seg, wid, lane, qa, kr, key0, key_end);
+    lse_chunk<T, D, RBW>(a, ktile, seg, chunk, wid, lane, qa, kr, key0, key_end);
   } else {
     Frag<T> qb[RBW > 1 ? RBW - 1 : 1][G::NC];
 #pragma unroll
     for (int j = 0; j < RBW - 1; ++j)
 #pragma unroll
       for (int c = 0; c < G::NC; ++c) qb[j][c] = qa[j][c];
-    lse_chunk<T, D, RBW - 1>(a, ktile, seg, wid, lane, qb, kr, key0, key_end);
+    lse_chunk<T, D, RBW - 1>(a, ktile, seg, chunk, wid, lane, qb, kr, key0, key_end);
   }
 }
 
