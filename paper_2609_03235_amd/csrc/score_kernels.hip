@@ -17,8 +17,8 @@
 //
 // Work split: workgroup = 8 waves; wave v holds row blocks v, v+8, v+16, ...
 // (16 rows each) as MFMA A-fragments in registers, so a SIMD (waves v and
-// v+4) covers a quarter of the rows. Each key tile (128 keys in pass 1, 64 in
-// pass 2) is staged once in LDS and read by all eight waves as B-fragments;
+// v+4) covers a quarter of the rows. Each key tile (128 keys; 64 in pass 2
+// for fp32 keys) is staged once in LDS and read by all eight waves as B-fragments;
 // blocks past the last row are skipped. MFMA 16x16x32 bf16 (or 8 x 16x16x4
 // f32 for fp32 inputs) accumulates in fp32.
 // Output layout of a 16x16 MFMA: lane l holds rows 4*(l/16)+0..3 of key
@@ -34,6 +34,11 @@
 namespace sgdkv {
 
 // Shared pieces of both passes ------------------------------------------------
+template <typename T>
+constexpr int col_tile() {
+  return sizeof(T) == 2 ? kColTileBf16 : kColTileF32;
+}
+
 template <typename T, int D>
 struct TileGeom {
   static constexpr int EB = elt_bytes<T>();
@@ -102,9 +107,10 @@ __device__ __forceinline__ void load_group_queries(const CompressArgs& a, int b,
 // before its end, makes that buffer readable; the buffer written at the start
 // of tile t was last read before the barrier of tile t-1. The MFMAs of the
 // subtile after the chunk's last one run on whatever keys follow (zeros past
-// the head) and are discarded. On gfx950 MFMA and vector instructions of one
-// SIMD issue one after the other, so the two waves of a SIMD hide each
-// other's latencies rather than overlapping the two units.
+// the head) and are discarded. On gfx950 a wave's own MFMAs and vector
+// instructions issue one after the other, and exp2 overlaps little with the
+// MFMAs of the SIMD's other wave; the two waves of a SIMD mainly hide each
+// other's latencies.
 template <typename T, int D, int NB>
 __device__ __forceinline__ void subtile_mfma(const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
                                              const Frag<T> (&kb)[D / 32], f32x4 (&acc)[NB > 0 ? NB : 1]) {
@@ -388,11 +394,12 @@ __global__ __launch_bounds__(kBlock) void lse_merge_kernel(CompressArgs a) {
 // multiple of 16), and the reduction adds each head's blocks, weights them
 // and takes the maximum.
 template <typename T, int D, int NB, int RBW, bool MAXG>
-__device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float (*red)[kScoreWaves][MAXG ? RBW : 1][kColTile],
+__device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
+                             float (*red)[kScoreWaves][MAXG ? RBW : 1][col_tile<T>()],
                              int seg, int wid, int lane, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
                              const rsrc_t& kr, int64_t key0, int64_t key_end) {
   constexpr int NBX = NB > 0 ? NB : 1;
-  constexpr int TILE = kColTile;
+  constexpr int TILE = col_tile<T>();
   const int lr = lane & 15, lg = lane >> 4;
   const int h = seg % a.Hkv;
   // -lse2 (+ log2 of the row weight) of this lane's row slots; rows past R get -inf so they add 0
@@ -484,8 +491,8 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float (*red)[kSc
 template <typename T, int D, int RBW, bool MAXG>
 __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) {
   using G = TileGeom<T, D>;
-  __shared__ __attribute__((aligned(16))) char ktile[2 * kColTile * G::LDS_STRIDE];
-  __shared__ float red[3][kScoreWaves][MAXG ? RBW : 1][kColTile];
+  __shared__ __attribute__((aligned(16))) char ktile[2 * col_tile<T>() * G::LDS_STRIDE];
+  __shared__ float red[3][kScoreWaves][MAXG ? RBW : 1][col_tile<T>()];
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
   const int64_t key0 = (int64_t)blockIdx.x * a.score_chunk;

@@ -332,10 +332,11 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, int64_t win0, CompressP
   a.out_scale = 1.0f / (float)G;
 
   const int64_t nseg = (int64_t)a.B * a.Hkv;
-  // score workgroups: about 2048 in total; a chunk is a whole number of key tiles, so no
+  // score workgroups: about 512 in total (two per CU, one resident at a time: fewer, longer
+  // workgroups measured faster than more, shorter ones); a chunk is a whole number of key tiles, so no
   // tile of pass 1 reaches into the next chunk (which would count those keys twice)
   a.score_chunk = std::min<int64_t>(
-      std::max<int64_t>(round_up(ceil_div(nseg * a.C, 2048), sgdkv::kScoreChunkQuantum),
+      std::max<int64_t>(round_up(ceil_div(nseg * a.C, 512), sgdkv::kScoreChunkQuantum),
                         2 * sgdkv::kScoreChunkQuantum),
       1 << 16);
   a.n_lse_chunks = (int)ceil_div(a.C, a.score_chunk);

@@ -14,7 +14,8 @@ constexpr int kMaxDecodeGroup = 16;
 constexpr int kMaxIptQHeads = 256;  // query heads per layer the Ipt. aggregations accept
 constexpr int kBlock = 256;        // threads per workgroup in every kernel
 constexpr int kLseTile = 128;      // keys staged in LDS per step of score pass 1
-constexpr int kColTile = 64;       // keys staged in LDS per step of score pass 2
+constexpr int kColTileBf16 = 128;  // keys staged in LDS per step of score pass 2 (bf16 keys)
+constexpr int kColTileF32 = 64;    // the same for fp32 keys (LDS holds half as many)
 constexpr int kScoreChunkQuantum = 128;  // score chunks are whole tiles of both passes
 #ifndef SGDKV_SCORE_WAVES
 #define SGDKV_SCORE_WAVES 8
