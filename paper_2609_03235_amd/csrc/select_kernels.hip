@@ -16,8 +16,8 @@
 //
 // Kernels (grid y = segment b*Hkv + h):
 //   select_init    zero histograms, seed the radix state, write offsets
-//   pool           pooled_j = (1/k_p) sum_{|t-j|<=r} a_t (zero outside)
-//   radix_hist<p>  digit-p histogram of candidates matching the prefix
+//   radix_pass<p>  digit-p histogram of candidates matching the prefix; pass 0
+//                  also pools: pooled_j = (1/k_p) sum_{|t-j|<=r} a_t (zero outside)
 //   radix_digit<p> pick digit p of tau; clear the histogram
 //   sel_count      per chunk: sink/window rows, candidates > tau, == tau
 //   compact        ordered ballot/prefix compaction of a chunk -> kept_pos
@@ -86,44 +86,84 @@ __global__ __launch_bounds__(kBlock) void select_init_kernel(CompressArgs a, int
   }
 }
 
-__global__ __launch_bounds__(kBlock) void pool_kernel(CompressArgs a) {
-  const int seg = blockIdx.y;
-  const int64_t j0 = (int64_t)blockIdx.x * a.sel_chunk;
-  const int64_t j1 = j0 + a.sel_chunk < a.n_scored ? j0 + a.sel_chunk : a.n_scored;
-  const rsrc_t cr = make_rsrc(a.colsum + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
-  const rsrc_t pr = make_rsrc(a.pooled + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
-  const int r = (a.kp - 1) / 2;
-  const float fk = (float)a.kp;
-  for (int64_t j = j0 + threadIdx.x; j < j1; j += kBlock) {
-    float s = 0.f;
-    // neighbours outside [0, n_scored) fall outside the descriptor and read as 0
-    for (int t = -r; t <= r; ++t) s += ldf(cr, (uint32_t)((j + t) * 4));
-    stf(pr, (uint32_t)(j * 4), s / fk);
-  }
-}
-
-template <int PASS>
-__global__ __launch_bounds__(kBlock) void radix_hist_kernel(CompressArgs a) {
+// Pooling and the histogram of one digit of the radix select. Workgroup
+// (x, seg) covers the scored positions [j0, j1) = [x*hist_chunk,
+// (x+1)*hist_chunk) of segment seg.
+//   POOL (digit 0 only): pooled_j = (1/k_p) sum_{t=-r..r} a_{j+t}, added in
+//     order of t, zeros outside [0, n_scored); the column sums of
+//     [j0-r, j1+r) are staged in LDS when r <= kPoolHalo.
+//   HIST: histogram of digit PASS over the candidates [s, C-W) of the range
+//     whose higher digits match the prefix found so far, added to the
+//     segment's histogram with integer atomics.
+template <int PASS, bool POOL, bool HIST>
+__global__ __launch_bounds__(kBlock) void radix_pass_kernel(CompressArgs a) {
   __shared__ uint32_t lh[256];
-  const int seg = blockIdx.y;
+  __shared__ float win[POOL ? kHistChunkMax + 2 * kPoolHalo : 1];
+  const int seg = blockIdx.y, tid = threadIdx.x;
   const SegState st = load_state(a, seg);
-  if (st.rem == 0) return;  // nothing (left) to choose in this segment
+  const bool hist = HIST && st.rem != 0;  // uniform per segment: nothing (left) to choose otherwise
+  if (!POOL && !hist) return;
   constexpr int shift = 24 - 8 * PASS;
-  lh[threadIdx.x] = 0;
-  __syncthreads();
-  const int64_t cend = a.C - a.W;
-  const int64_t j0 = a.s + (int64_t)blockIdx.x * a.sel_chunk;
-  const int64_t j1 = j0 + a.sel_chunk < cend ? j0 + a.sel_chunk : cend;
+  lh[tid] = 0;
+  const int64_t j0 = (int64_t)blockIdx.x * a.hist_chunk;
+  const int64_t j1 = j0 + a.hist_chunk < a.n_scored ? j0 + a.hist_chunk : a.n_scored;
+  const int64_t cbeg = a.s, cend = a.C - a.W;
   const rsrc_t pr = make_rsrc(a.pooled + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
-  for (int64_t j = j0 + threadIdx.x; j < j1; j += kBlock) {
-    const uint32_t bits = ld32(pr, (uint32_t)(j * 4));
-    if ((bits & st.mask) == st.prefix) atomicAdd(&lh[(bits >> shift) & 255u], 1u);
+  // Loads go out in batches of U per thread, issued before any is used: positions past the
+  // range read whatever the descriptor gives (zero past its end) and are not used.
+  constexpr int U = 8;
+  if constexpr (POOL) {
+    const rsrc_t cr = make_rsrc(a.colsum + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
+    const int r = (a.kp - 1) / 2;
+    const float fk = (float)a.kp;
+    const bool staged = r <= kPoolHalo;
+    if (staged) {
+      // positions before 0 or past n_scored fall outside the descriptor and read as 0
+      const int64_t n = (j1 - j0) + 2 * r;
+      for (int64_t i0 = 0; i0 < n; i0 += U * kBlock) {
+        float x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) x[u] = ldf(cr, (uint32_t)((j0 - r + i0 + tid + u * kBlock) * 4));
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (i0 + tid + u * kBlock < n) win[i0 + tid + u * kBlock] = x[u];
+      }
+    }
+    __syncthreads();
+    for (int64_t j = j0 + tid; j < j1; j += kBlock) {
+      float sum = 0.f;
+      if (staged) {
+        const float* wp = win + (j - j0);
+        for (int t = 0; t <= 2 * r; ++t) sum += wp[t];
+      } else {
+        for (int t = -r; t <= r; ++t) sum += ldf(cr, (uint32_t)((j + t) * 4));
+      }
+      const float v = sum / fk;
+      stf(pr, (uint32_t)(j * 4), v);
+      if (hist && j >= cbeg && j < cend) {
+        const uint32_t bits = __float_as_uint(v);
+        if ((bits & st.mask) == st.prefix) atomicAdd(&lh[(bits >> shift) & 255u], 1u);
+      }
+    }
+  } else {
+    __syncthreads();
+    const int64_t c0 = j0 > cbeg ? j0 : cbeg, c1 = j1 < cend ? j1 : cend;
+    for (int64_t jb = c0; jb < c1; jb += U * kBlock) {
+      uint32_t x[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) x[u] = ld32(pr, (uint32_t)((jb + tid + u * kBlock) * 4));
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (jb + tid + u * kBlock < c1 && (x[u] & st.mask) == st.prefix) atomicAdd(&lh[(x[u] >> shift) & 255u], 1u);
+    }
   }
+  if (!hist) return;
   __syncthreads();
-  const uint32_t v = lh[threadIdx.x];
-  if (v) atomicAdd(a.hist + (int64_t)seg * 256 + threadIdx.x, v);
+  const uint32_t v = lh[tid];
+  if (v) atomicAdd(a.hist + (int64_t)seg * 256 + tid, v);
 }
 
+// Picks digit PASS of tau from the segment's histogram and clears it.
 template <int PASS>
 __global__ __launch_bounds__(kBlock) void radix_digit_kernel(CompressArgs a) {
   __shared__ uint32_t sh[256];
@@ -316,16 +356,19 @@ hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t st
   const int nseg = a.B * a.Hkv;
   const dim3 blk(kBlock);
   SGDKV_LAUNCH("select_init", select_init_kernel, dim3(nseg), blk, st, a, scores_only ? 0 : 1);
-  if (a.n_pool_chunks > 0) SGDKV_LAUNCH("pool", pool_kernel, dim3(a.n_pool_chunks, nseg), blk, st, a);
-  if (scores_only) return hipGetLastError();
-  if (a.n_cand_chunks > 0) {
-    SGDKV_LAUNCH("radix_hist", radix_hist_kernel<0>, dim3(a.n_cand_chunks, nseg), blk, st, a);
+  const dim3 hgrid(a.n_hist_chunks, nseg);
+  const bool cands = a.C - a.s - a.W > 0;
+  if (scores_only || !cands) {
+    if (a.n_hist_chunks > 0) SGDKV_LAUNCH("pool", (radix_pass_kernel<0, true, false>), hgrid, blk, st, a);
+    if (scores_only) return hipGetLastError();
+  } else {
+    SGDKV_LAUNCH("pool_radix_hist", (radix_pass_kernel<0, true, true>), hgrid, blk, st, a);
     SGDKV_LAUNCH("radix_digit", radix_digit_kernel<0>, dim3(nseg), blk, st, a);
-    SGDKV_LAUNCH("radix_hist", radix_hist_kernel<1>, dim3(a.n_cand_chunks, nseg), blk, st, a);
+    SGDKV_LAUNCH("radix_hist", (radix_pass_kernel<1, false, true>), hgrid, blk, st, a);
     SGDKV_LAUNCH("radix_digit", radix_digit_kernel<1>, dim3(nseg), blk, st, a);
-    SGDKV_LAUNCH("radix_hist", radix_hist_kernel<2>, dim3(a.n_cand_chunks, nseg), blk, st, a);
+    SGDKV_LAUNCH("radix_hist", (radix_pass_kernel<2, false, true>), hgrid, blk, st, a);
     SGDKV_LAUNCH("radix_digit", radix_digit_kernel<2>, dim3(nseg), blk, st, a);
-    SGDKV_LAUNCH("radix_hist", radix_hist_kernel<3>, dim3(a.n_cand_chunks, nseg), blk, st, a);
+    SGDKV_LAUNCH("radix_hist", (radix_pass_kernel<3, false, true>), hgrid, blk, st, a);
     SGDKV_LAUNCH("radix_digit", radix_digit_kernel<3>, dim3(nseg), blk, st, a);
   }
   SGDKV_LAUNCH("sel_count", sel_count_kernel, dim3(a.n_sel_chunks, nseg), blk, st, a);

@@ -343,8 +343,10 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, int64_t win0, CompressP
   a.n_col_chunks = (int)ceil_div(a.n_scored, a.score_chunk);
   // selection workgroups: about 4096 in total
   a.sel_chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(nseg * a.C, 4096), 256), 1024), 1 << 20);
-  a.n_pool_chunks = (int)ceil_div(a.n_scored, a.sel_chunk);
-  a.n_cand_chunks = (int)ceil_div(a.C - a.s - a.W, a.sel_chunk);
+  // pooling and radix passes: about 1024 workgroups, at most kHistChunkMax positions each
+  a.hist_chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(nseg * a.n_scored, 1024), 256), 256),
+                                   sgdkv::kHistChunkMax);
+  a.n_hist_chunks = (int)ceil_div(a.n_scored, a.hist_chunk);
   a.n_sel_chunks = (int)ceil_div(a.C, a.sel_chunk);
 
   size_t off = 0;

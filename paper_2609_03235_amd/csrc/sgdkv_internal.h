@@ -17,6 +17,8 @@ constexpr int kLseTile = 128;      // keys staged in LDS per step of score pass 
 constexpr int kColTileBf16 = 128;  // keys staged in LDS per step of score pass 2 (bf16 keys)
 constexpr int kColTileF32 = 64;    // the same for fp32 keys (LDS holds half as many)
 constexpr int kScoreChunkQuantum = 128;  // score chunks are whole tiles of both passes
+constexpr int kHistChunkMax = 8192;      // positions per pooling / radix-pass workgroup, at most
+constexpr int kPoolHalo = 64;            // pooling radii up to this are staged in LDS
 #ifndef SGDKV_SCORE_WAVES
 #define SGDKV_SCORE_WAVES 8
 #endif
@@ -69,8 +71,8 @@ struct CompressArgs {
   int n_lse_chunks;     // ceil(C / score_chunk)
   int n_col_chunks;     // ceil(n_scored / score_chunk)
   int64_t sel_chunk;    // positions per selection workgroup
-  int n_pool_chunks;    // ceil(n_scored / sel_chunk)
-  int n_cand_chunks;    // ceil(M / sel_chunk), M = C - s - W candidates
+  int64_t hist_chunk;   // scored positions per pooling / radix-pass workgroup (multiple of 256)
+  int n_hist_chunks;    // ceil(n_scored / hist_chunk)
   int n_sel_chunks;     // ceil(C / sel_chunk)
   // per KV head of this layer (shared by every sequence)
   int64_t T_layer;
