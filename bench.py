@@ -9,6 +9,10 @@ One step is the whole path over one batch of synthetic, HBM-resident input:
          sequence and query head over that layer's compressed cache)
 Layers are compressed first and decoded afterwards, so no decode reads a
 cache still warm in the 256 MB last-level cache from its own compression.
+With --streams 2, layer l is compressed on stream l mod 2 (each stream with
+its own workspace): the layers are independent, so one layer's selection and
+gather run beside the next layer's scoring. The default serialises them, so
+each kernel's measured duration is its own.
 
 Default workload: the 28-layer Qwen2.5-7B-shaped stack (28 query / 4 KV
 heads, head dim 128) at a 131072-token prompt, batch 8, bf16, 25 % budget,
@@ -78,6 +82,10 @@ def parse():
     ap.add_argument("--decode-new", type=int, default=0, metavar="N",
                     help="generation: each layer's decode also attends to N rows appended since compression, "
                          "and every step appends one row per KV head (sgdkv_append_kv) before decoding")
+    ap.add_argument("--streams", type=int, default=1, choices=[1, 2],
+                    help="compress layer l on stream l %% STREAMS (own workspace per stream), so one layer's "
+                         "selection and gather overlap the next layer's scoring; decode follows on the first. "
+                         "With 2 the per-kernel durations include the other stream's work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0, metavar="MIB",
                     help="first run three elementwise copies of MIB MiB (fp32 x 1.0), untimed: under "
@@ -275,7 +283,9 @@ def main():
             tails[l] = (kn, vn, step_kv)
     dec_lse = [torch.empty((B, Hq), dtype=torch.float32, device=dev) for _ in range(L)]
     cdesc = sg.compress_desc(layers[0]["q_win"], layers[0]["k"], pool_kernel=kp, b_sink=s, b_window=W)
-    ws_c = sg.alloc_workspace(sg.compress_workspace_size(cdesc), dev)
+    # one compression workspace per stream; every stream keeps torch's default priority
+    streams = [stream] + [torch.cuda.Stream(device=dev) for _ in range(args.streams - 1)]
+    ws_c = [sg.alloc_workspace(sg.compress_workspace_size(cdesc), dev) for _ in streams]
     offsets_host = []
     for l in range(L):
         pre = np.concatenate([[0], np.cumsum(budgets[l])])
@@ -291,11 +301,21 @@ def main():
     def step():
         # S0 on the host, then every layer's compression, then every layer's decode
         allocate()
+        if len(streams) > 1:
+            fork = torch.cuda.Event()
+            fork.record(stream)
+            for st in streams[1:]:
+                st.wait_event(fork)
         for l in range(L):
             t = layers[l]
+            i = l % len(streams)
             sg.compress_layer(t["q_win"], t["k"], t["v"], budgets[l], pool_kernel=kp, b_sink=s, b_window=W,
                               window_lse=lse_in[l], group_agg=agg, qhead_scores=qscores[l], window_pos=win0,
-                              out=outs[l], workspace=ws_c, stream=stream)
+                              out=outs[l], workspace=ws_c[i], stream=streams[i])
+        for st in streams[1:]:
+            join = torch.cuda.Event()
+            join.record(st)
+            stream.wait_event(join)
         for l in range(L):
             o = outs[l]
             kn = vn = None
@@ -343,8 +363,8 @@ def main():
         # MFMA flops of the logits; bound by MFMA + vector issue, see score_logit_seconds
         "score_lse": ("alu", flops_tok * B * C, "TFLOP/s"),
         "score_colsum": ("alu", flops_tok * B * (C - w), "TFLOP/s"),
-        # read kept K and V rows, write them, write positions, read pooled scores of the candidates
-        "gather": ("hbm", B * T_mean * (4 * d * eb + 4) + B * Hkv * C * 4.0, "GB/s"),
+        # read the kept K and V rows and their positions, write the rows
+        "gather": ("hbm", B * T_mean * (4 * d * eb + 4), "GB/s"),
         # read every kept K and V row once (and the rows appended since), plus the queries and outputs
         "decode_split": ("hbm", B * (T_mean + Hkv * n_new) * 2 * d * eb + B * Hq * d * (eb + 4.0), "GB/s"),
     }
@@ -413,7 +433,7 @@ def main():
                     obs_window=w, pool_kernel=kp, b_sink=s, b_window=W, budget_ratio=args.ratio,
                     total_budget_rows=int(budgets.sum()), window_lse="caller" if args.caller_lse else "computed",
                     alloc_variant=args.alloc_variant, group_agg=args.group_agg, window_start=win0,
-                    decode_appended_rows=n_new),
+                    decode_appended_rows=n_new, compress_streams=args.streams),
         compress_tokens_per_s=round(tokens / (comp_ms / 1e3), 1) if comp_ms > 0 else None,
         decode=dict(gbps=round(dec_bytes / (dec_ms / 1e3) / 1e9, 1) if dec_ms > 0 else None,
                     frac_of_peak=round(dec_bytes / (dec_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4) if dec_ms > 0 else None,
