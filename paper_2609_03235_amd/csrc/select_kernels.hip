@@ -16,10 +16,12 @@
 //
 // Kernels (grid y = segment b*Hkv + h):
 //   select_init    zero histograms, seed the radix state, write offsets
-//   radix_pass<p>  digit-p histogram of candidates matching the prefix; pass 0
-//                  also pools: pooled_j = (1/k_p) sum_{|t-j|<=r} a_t (zero outside)
-//   radix_digit<p> pick digit p of tau; clear the histogram
-//   sel_count      per chunk: sink/window rows, candidates > tau, == tau
+//   radix_pass<p>  digit-p histogram of candidates matching the digits
+//                  before it (each workgroup picks those from the earlier
+//                  histograms itself); pass 0 also pools:
+//                  pooled_j = (1/k_p) sum_{|t-j|<=r} a_t (zero outside)
+//   sel_count      picks the last digit (tau and q complete); per chunk:
+//                  sink/window rows, candidates > tau, == tau
 //   compact        ordered ballot/prefix compaction of a chunk -> kept_pos
 //   copy_rows      K and V rows of the kept positions -> the ragged cache
 #include <algorithm>
@@ -70,8 +72,9 @@ __global__ __launch_bounds__(kBlock) void select_init_kernel(CompressArgs a, int
   const int seg = blockIdx.x;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
   const int nseg = a.B * a.Hkv;
-  const rsrc_t hr = make_rsrc(a.hist + (int64_t)seg * 256, 256 * 4);
-  st32(hr, threadIdx.x * 4, 0u);
+  const rsrc_t hr = make_rsrc(a.hist + (int64_t)seg * 4 * 256, 4 * 256 * 4);
+#pragma unroll
+  for (int p = 0; p < 4; ++p) st32(hr, (p * 256 + threadIdx.x) * 4, 0u);
   if (threadIdx.x == 0) {
     const rsrc_t sr = make_rsrc(a.state + (int64_t)seg * 4, 16);
     st32(sr, 0, 0u);
@@ -86,6 +89,52 @@ __global__ __launch_bounds__(kBlock) void select_init_kernel(CompressArgs a, int
   }
 }
 
+// The radix state after digits 0 .. NPASS-1: every digit is picked from its
+// histogram (complete once the pass that built it has ended) as the unique
+// digit t with S(t) >= rem > S(t+1), S the suffix sums of the bins; rem then
+// drops by S(t+1). Runs in every workgroup that needs it (256 threads; `sh`
+// holds 256 + 8 words of LDS); the result is the same in all of them.
+template <int NPASS>
+__device__ __forceinline__ SegState derive_state(const CompressArgs& a, int seg, uint32_t* sh) {
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  SegState st;
+  st.prefix = 0u;
+  st.mask = 0u;
+  st.rem = (uint32_t)a.m[seg % a.Hkv];
+  if (NPASS == 0 || st.rem == 0) return st;
+  const rsrc_t hr = make_rsrc(a.hist + (int64_t)seg * 4 * 256, 4 * 256 * 4);
+  uint32_t hv[NPASS > 0 ? NPASS : 1];
+#pragma unroll
+  for (int p = 0; p < NPASS; ++p) hv[p] = ld32(hr, (p * 256 + tid) * 4);  // all issued before any use
+#pragma unroll
+  for (int p = 0; p < NPASS; ++p) {
+    const int shift = 24 - 8 * p;
+    // suffix sums: within the wave (lanes above), then the waves above
+    uint32_t v = hv[p];
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t t = __shfl_down(v, o, 64);
+      v += lane + o < 64 ? t : 0u;
+    }
+    if (lane == 0) sh[256 + wid] = v;
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kBlock / 64; ++u) v += u > wid ? sh[256 + u] : 0u;
+    const uint32_t S = v, Sn = v - hv[p];
+    if (S >= st.rem && Sn < st.rem) {  // exactly one digit satisfies this
+      sh[256 + 4] = (uint32_t)tid;
+      sh[256 + 5] = Sn;
+    }
+    __syncthreads();
+    const uint32_t dg = sh[256 + 4], below = sh[256 + 5];
+    __syncthreads();
+    st.prefix |= dg << shift;
+    st.mask |= 0xFFu << shift;
+    st.rem -= below;
+  }
+  return st;
+}
+
 // Pooling and the histogram of one digit of the radix select. Workgroup
 // (x, seg) covers the scored positions [j0, j1) = [x*hist_chunk,
 // (x+1)*hist_chunk) of segment seg.
@@ -97,10 +146,10 @@ __global__ __launch_bounds__(kBlock) void select_init_kernel(CompressArgs a, int
 //     segment's histogram with integer atomics.
 template <int PASS, bool POOL, bool HIST>
 __global__ __launch_bounds__(kBlock) void radix_pass_kernel(CompressArgs a) {
-  __shared__ uint32_t lh[256];
+  __shared__ uint32_t lh[256 + 8];
   __shared__ float win[POOL ? kHistChunkMax + 2 * kPoolHalo : 1];
   const int seg = blockIdx.y, tid = threadIdx.x;
-  const SegState st = load_state(a, seg);
+  const SegState st = derive_state<PASS>(a, seg, lh);
   const bool hist = HIST && st.rem != 0;  // uniform per segment: nothing (left) to choose otherwise
   if (!POOL && !hist) return;
   constexpr int shift = 24 - 8 * PASS;
@@ -160,44 +209,20 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(CompressArgs a) {
   if (!hist) return;
   __syncthreads();
   const uint32_t v = lh[tid];
-  if (v) atomicAdd(a.hist + (int64_t)seg * 256 + tid, v);
-}
-
-// Picks digit PASS of tau from the segment's histogram and clears it.
-template <int PASS>
-__global__ __launch_bounds__(kBlock) void radix_digit_kernel(CompressArgs a) {
-  __shared__ uint32_t sh[256];
-  const int seg = blockIdx.x;
-  const int tid = threadIdx.x;
-  constexpr int shift = 24 - 8 * PASS;
-  const rsrc_t hr = make_rsrc(a.hist + (int64_t)seg * 256, 256 * 4);
-  const uint32_t hv = ld32(hr, tid * 4);
-  const SegState st = load_state(a, seg);
-  sh[tid] = hv;
-  __syncthreads();
-  st32(hr, tid * 4, 0u);  // ready for the next pass
-  if (st.rem == 0) return;
-  // inclusive suffix sums S[t] = sum_{u >= t} hist[u]
-  for (int off = 1; off < 256; off <<= 1) {
-    const uint32_t add = tid + off < 256 ? sh[tid + off] : 0u;
-    __syncthreads();
-    sh[tid] += add;
-    __syncthreads();
-  }
-  const uint32_t S = sh[tid];
-  const uint32_t Sn = tid < 255 ? sh[tid + 1] : 0u;
-  if (S >= st.rem && Sn < st.rem) {  // exactly one digit satisfies this
-    const rsrc_t sr = make_rsrc(a.state + (int64_t)seg * 4, 16);
-    st32(sr, 0, st.prefix | ((uint32_t)tid << shift));
-    st32(sr, 4, st.mask | (0xFFu << shift));
-    st32(sr, 8, st.rem - Sn);
-  }
+  if (v) atomicAdd(a.hist + ((int64_t)seg * 4 + PASS) * 256 + tid, v);
 }
 
 __global__ __launch_bounds__(kBlock) void sel_count_kernel(CompressArgs a) {
   __shared__ uint32_t red[3][kBlock / 64];
+  __shared__ uint32_t sh[256 + 8];
   const int seg = blockIdx.y, h = seg % a.Hkv;
-  const SegState st = load_state(a, seg);
+  const SegState st = derive_state<4>(a, seg, sh);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {  // tau and q for the compaction
+    const rsrc_t sr = make_rsrc(a.state + (int64_t)seg * 4, 16);
+    st32(sr, 0, st.prefix);
+    st32(sr, 4, st.mask);
+    st32(sr, 8, st.rem);
+  }
   const bool active = a.m[h] > 0;
   const uint32_t tau = st.prefix;
   const int64_t j0 = (int64_t)blockIdx.x * a.sel_chunk;
@@ -363,13 +388,9 @@ hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t st
     if (scores_only) return hipGetLastError();
   } else {
     SGDKV_LAUNCH("pool_radix_hist", (radix_pass_kernel<0, true, true>), hgrid, blk, st, a);
-    SGDKV_LAUNCH("radix_digit", radix_digit_kernel<0>, dim3(nseg), blk, st, a);
     SGDKV_LAUNCH("radix_hist", (radix_pass_kernel<1, false, true>), hgrid, blk, st, a);
-    SGDKV_LAUNCH("radix_digit", radix_digit_kernel<1>, dim3(nseg), blk, st, a);
     SGDKV_LAUNCH("radix_hist", (radix_pass_kernel<2, false, true>), hgrid, blk, st, a);
-    SGDKV_LAUNCH("radix_digit", radix_digit_kernel<2>, dim3(nseg), blk, st, a);
     SGDKV_LAUNCH("radix_hist", (radix_pass_kernel<3, false, true>), hgrid, blk, st, a);
-    SGDKV_LAUNCH("radix_digit", radix_digit_kernel<3>, dim3(nseg), blk, st, a);
   }
   SGDKV_LAUNCH("sel_count", sel_count_kernel, dim3(a.n_sel_chunks, nseg), blk, st, a);
   SGDKV_LAUNCH("compact", compact_kernel, dim3(a.n_sel_chunks, nseg), blk, st, a);

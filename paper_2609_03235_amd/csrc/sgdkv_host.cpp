@@ -359,7 +359,7 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, int64_t win0, CompressP
   p.off_pooled = off;
   off += align256((size_t)nseg * a.C * sizeof(float));
   p.off_hist = off;
-  off += align256((size_t)nseg * 256 * sizeof(uint32_t));
+  off += align256((size_t)nseg * 4 * 256 * sizeof(uint32_t));  // one 256-bin histogram per radix digit
   p.off_state = off;
   off += align256((size_t)nseg * 4 * sizeof(uint32_t));
   p.off_counts = off;

@@ -63,7 +63,7 @@ struct CompressArgs {
   float* lse_part;  // [B*Hkv][n_lse_chunks][R][2]  (m, s) in base-2 units
   float* lse2;      // [B*Hkv][R]                   base-2 LSE of each window row
   float* colsum;    // [B*Hkv][n_scored]
-  uint32_t* hist;   // [B*Hkv][256]
+  uint32_t* hist;   // [B*Hkv][4][256]: histogram of each radix digit
   uint32_t* state;  // [B*Hkv][4]: prefix, mask, rows still to place, unused
   uint32_t* counts; // [B*Hkv][n_sel_chunks][4]: fixed, greater, equal, unused
   // chunking
