@@ -395,7 +395,7 @@ __global__ __launch_bounds__(kBlock) void lse_merge_kernel(CompressArgs a) {
 // and takes the maximum.
 template <typename T, int D, int NB, int RBW, bool MAXG>
 __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
-                             float (*red)[kScoreWaves][MAXG ? RBW : 1][col_tile<T>()],
+                             float (*red)[kScoreWaves][MAXG ? RBW : 4][col_tile<T>()],
                              int seg, int wid, int lane, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
                              const rsrc_t& kr, int64_t key0, int64_t key_end) {
   constexpr int NBX = NB > 0 ? NB : 1;
@@ -422,14 +422,15 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
   const rsrc_t cr = make_rsrc(a.colsum + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
   // Partials of tile t sit in red[t % 3]: written during tile t, complete at the barrier of
   // tile t+1, summed right after it, rewritten only after the barrier of tile t+2. Each
-  // wave sums CPW columns: the LPC lanes of a column read PPL partials each, shuffles add
-  // them, and the first CPW lanes store. Branch-free: a store that must not happen gets an
+  // wave sums CPW columns: the LPC lanes of a column read the partials of PPL waves each
+  // (one per lane group of the wave for the group mean), shuffles add them, and the first
+  // CPW lanes store. Branch-free: a store that must not happen gets an
   // offset past the buffer, which the hardware drops.
   constexpr int CPW = TILE / kScoreWaves, LPC = 64 / CPW, PPL = kScoreWaves / LPC;
   static_assert(CPW <= 16 && 64 % CPW == 0 && PPL >= 1 && PPL * LPC == kScoreWaves, "reduction layout");
   const int rcol = CPW * wid + lane % CPW, rgrp = lane / CPW;
   auto reduce = [&](int64_t t) {  // t may be -1: nothing is stored
-    const float(*r)[MAXG ? RBW : 1][TILE] = red[(t + 3) % 3];
+    const float(*r)[MAXG ? RBW : 4][TILE] = red[(t + 3) % 3];
     float v = 0.f;
     if constexpr (MAXG) {
       // the LPC lanes of a column take the group's heads in turn: sum a head's w/16 blocks
@@ -444,9 +445,11 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
       for (int o = CPW; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
       v = max_lane_groups(v);
     } else {
-      v = r[rgrp][0][rcol];
+      // the partials of every wave and lane group of the column, in a fixed order
 #pragma unroll
-      for (int k = 1; k < PPL; ++k) v += r[rgrp + LPC * k][0][rcol];
+      for (int k = 0; k < PPL; ++k)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) v += r[rgrp + LPC * k][g][rcol];
 #pragma unroll
       for (int o = CPW; o < 16; o <<= 1) v += __shfl_xor(v, o, 64);
       v = sum_lane_groups(v);
@@ -478,9 +481,9 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
             for (int j = 1; j < NB; ++j)
 #pragma unroll
               for (int i = 0; i < 4; ++i) pp[i] += fast_exp2(fmaf(acc[j][i], c2, nlse[j][i]));
-            p = sum_lane_groups((pp[0] + pp[1]) + (pp[2] + pp[3]));
+            p = (pp[0] + pp[1]) + (pp[2] + pp[3]);
           }
-          red[t % 3][wid][0][16 * sub + lr] = p;  // all four lane groups hold the same value
+          red[t % 3][wid][lg][16 * sub + lr] = p;  // one partial per lane group; the reduction adds them
         }
       },
       [&](int64_t t) { reduce(t - 1); }, [](int64_t) {});
@@ -492,7 +495,7 @@ template <typename T, int D, int RBW, bool MAXG>
 __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) {
   using G = TileGeom<T, D>;
   __shared__ __attribute__((aligned(16))) char ktile[2 * col_tile<T>() * G::LDS_STRIDE];
-  __shared__ float red[3][kScoreWaves][MAXG ? RBW : 1][col_tile<T>()];
+  __shared__ float red[3][kScoreWaves][MAXG ? RBW : 4][col_tile<T>()];
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
   const int64_t key0 = (int64_t)blockIdx.x * a.score_chunk;

@@ -341,8 +341,8 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, int64_t win0, CompressP
       1 << 16);
   a.n_lse_chunks = (int)ceil_div(a.C, a.score_chunk);
   a.n_col_chunks = (int)ceil_div(a.n_scored, a.score_chunk);
-  // selection workgroups: about 4096 in total
-  a.sel_chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(nseg * a.C, 4096), 256), 1024), 1 << 20);
+  // selection workgroups: about 2048 in total
+  a.sel_chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(nseg * a.C, 2048), 256), 1024), 1 << 20);
   // pooling and radix passes: about 1024 workgroups, at most kHistChunkMax positions each
   a.hist_chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(nseg * a.n_scored, 1024), 256), 256),
                                    sgdkv::kHistChunkMax);
