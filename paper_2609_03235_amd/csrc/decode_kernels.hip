@@ -4,7 +4,9 @@
 // for GQA (Appendix A.2), so one segment of rows serves the G query heads of
 // its group. Decode reads each segment once for all G heads:
 //
-//   decode_split: each wave owns one chunk of a segment's rows. Logits of the
+//   decode_split: each wave owns one split of a segment's rows: the splits of
+//     a segment take its 16-row steps in turn, so together they sweep the
+//     segment front to back (a wave keeps its own partial). Logits of the
 //     G heads against 16 keys at a time are one 16x16 MFMA (the G query rows
 //     padded to 16 form the A operand). The wave keeps an online softmax
 //     (running max m and sum s per head, base-2 units) and accumulates P.V in
@@ -118,7 +120,8 @@ __device__ __forceinline__ void wave_sync() {
 // writes before the reads and the reads before the writes two steps later).
 template <typename T, int D, int CPL, int GM, int PF, bool EXACT>
 __device__ __forceinline__ void decode_chunk(const DecodeArgs& a, float (*pls)[16][16], float (*als)[16],
-                                             const rsrc_t& kr, const rsrc_t& vr, int64_t c0, int64_t c1,
+                                             const rsrc_t& kr, const rsrc_t& vr, int64_t c0, int64_t stride,
+                                             int64_t c1, int nsteps,
                                              const Frag<T> (&qa)[D / 32], int lane, float (&m)[4], float (&s)[4],
                                              float (&o)[GM][CPL]) {
   using S = DecodeStep<T, D, CPL>;
@@ -136,22 +139,21 @@ __device__ __forceinline__ void decode_chunk(const DecodeArgs& a, float (*pls)[1
   for (int g = 0; g < GM; ++g)
 #pragma unroll
     for (int e = 0; e < CPL; ++e) o[g][e] = 0.f;
-  const int nsteps = (int)((c1 - c0 + KS - 1) / KS);
   // Loads are issued unconditionally (past the last step they repeat it, which the caches
   // serve): a load under a branch makes the compiler wait for every load in flight,
   // prefetches included, before the next use of loaded data.
-  const int64_t k_last = c0 + (int64_t)(nsteps - 1) * KS;
+  const int64_t k_last = c0 + (int64_t)(nsteps - 1) * stride;
   auto step_key = [&](int64_t k) { return k < k_last ? k : k_last; };
   S buf[NBUF];
 #pragma unroll
-  for (int p = 0; p < PF; ++p) buf[p].load(kr, vr, step_key(c0 + p * KS), lr, lgp, kg, col0);
+  for (int p = 0; p < PF; ++p) buf[p].load(kr, vr, step_key(c0 + p * stride), lr, lgp, kg, col0);
   for (int it0 = 0; it0 < nsteps; it0 += NBUF) {
 #pragma unroll
     for (int u = 0; u < NBUF; ++u) {
       const int it = it0 + u;
       if (it >= nsteps) break;
-      const int64_t k0 = c0 + (int64_t)it * KS;
-      buf[(u + PF) % NBUF].load(kr, vr, step_key(k0 + PF * KS), lr, lgp, kg, col0);
+      const int64_t k0 = c0 + (int64_t)it * stride;
+      buf[(u + PF) % NBUF].load(kr, vr, step_key(k0 + PF * stride), lr, lgp, kg, col0);
       const S& cur = buf[u];
       f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -218,8 +220,8 @@ __device__ __forceinline__ void decode_chunk(const DecodeArgs& a, float (*pls)[1
 
 // CPL = value columns per lane; GM = compile-time bound on the group size (8
 // or 16); PF = steps of K/V in flight ahead of the one being computed; OCC =
-// workgroups per CU the registers are sized for. Each wave owns one chunk of
-// a segment: chunk index = 4*blockIdx.x + wave.
+// workgroups per CU the registers are sized for. Each wave owns one split of
+// a segment: split index = 4*blockIdx.x + wave.
 template <typename T, int D, int CPL, int GM, int PF, int OCC>
 __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a) {
   using S = DecodeStep<T, D, CPL>;
@@ -237,9 +239,27 @@ __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a)
   const int64_t chunk = (int64_t)blockIdx.x * kWaves + wid;
   const bool appended = chunk >= a.n_chunk_max;
   const int64_t rows = appended ? a.n_new : len;
-  const int64_t c0 = (appended ? chunk - a.n_chunk_max : chunk) * a.chunk;
-  if (c0 >= rows) return;
-  const int64_t c1 = c0 + a.chunk < rows ? c0 + a.chunk : rows;
+  // The compressed rows of a segment are dealt to its nck splits 16 rows at a time (split w
+  // takes steps w, w + nck, ...), so the splits of a segment sweep it together from front to
+  // back; appended rows form contiguous splits.
+  int64_t c0, stride, c1;
+  int nsteps;
+  if (appended) {
+    c0 = (chunk - a.n_chunk_max) * a.chunk;
+    if (c0 >= rows) return;
+    stride = 16;
+    c1 = c0 + a.chunk < rows ? c0 + a.chunk : rows;
+    nsteps = (int)((c1 - c0 + 15) / 16);
+  } else {
+    int64_t nck = (rows + a.chunk - 1) / a.chunk;
+    if (nck > a.n_chunk_max) nck = a.n_chunk_max;  // device offsets beyond the host's: fewer, longer splits
+    const int64_t total_steps = (rows + 15) / 16;
+    if (chunk >= nck) return;
+    c0 = chunk * 16;
+    stride = nck * 16;
+    c1 = rows;
+    nsteps = (int)((total_steps - chunk + nck - 1) / nck);
+  }
 
   const int lr = lane & 15, lgp = lane >> 4;
   const int G = a.G;
@@ -256,7 +276,7 @@ __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a)
   for (int c = 0; c < S::NC; ++c) qa[c] = gload_frag<T>(qr, (uint32_t)(lr * S::RB + (32 * c + 8 * lgp) * S::EB));
 
   float m[4], s[4], o[GM][CPL];
-  decode_chunk<T, D, CPL, GM, PF, false>(a, pls[wid], als[wid], kr, vr, c0, c1, qa, lane, m, s, o);
+  decode_chunk<T, D, CPL, GM, PF, false>(a, pls[wid], als[wid], kr, vr, c0, stride, c1, nsteps, qa, lane, m, s, o);
   // 2^64 bounds every probability, so s and o stay finite unless V is huge or the
   // first step's maximum sat far below a later logit: then redo with rescaling
   bool bad = false;
@@ -266,7 +286,8 @@ __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a)
   for (int g = 0; g < GM; ++g)
 #pragma unroll
     for (int e = 0; e < CPL; ++e) bad |= !(fabsf(o[g][e]) < INFINITY);
-  if (__any(bad)) decode_chunk<T, D, CPL, GM, PF, true>(a, pls[wid], als[wid], kr, vr, c0, c1, qa, lane, m, s, o);
+  if (__any(bad))
+    decode_chunk<T, D, CPL, GM, PF, true>(a, pls[wid], als[wid], kr, vr, c0, stride, c1, nsteps, qa, lane, m, s, o);
 
   // Reduce within the wave: the 16 lanes of each head's sum, the KG key groups of o.
 #pragma unroll
