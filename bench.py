@@ -212,7 +212,7 @@ def main():
     win0 = C if args.proxy_window else C - w - args.question_len  # position of the first window row
     n_scored = win0
     stream = torch.cuda.current_stream()
-    traffic_of(None, wl.name, args.ratio)
+    traffic_of(None, args.workload, args.ratio)
     if args.calibrate_copy_mib:
         src = torch.ones(args.calibrate_copy_mib << 18, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
