@@ -173,6 +173,22 @@ def test_tiny_ragged_batches(B, C, budget_kind):
     _decode_on_oracle_cache(orc, t["q"], 2, torch.float32, 1e-5, "ragged")
 
 
+@pytest.mark.parametrize("kp", [1, 129, 131, 301])
+def test_pool_kernel_widths(kp):
+    """Pooling radii up to 64 are staged in LDS with their halo; wider ones read the column sums
+    from global memory. Both sum the taps in the same order and must match the oracle."""
+    B, C = 2, 1500
+    wl, t = _tiny_inputs(B=B, C=C, seed=kp)
+    s, W, w = 4, 32, wl.obs_window
+    rng = np.random.Generator(np.random.PCG64(kp))
+    budgets = rng.integers(s + W, C + 1, size=2)
+    _announce(f"pool kernel {kp}, B={B} C={C} budgets={budgets.tolist()}")
+    res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=kp, s=s, W=W)
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], f"pool {kp}", rtol=_score_rtol(t["q_win"]))
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, f"pool {kp}", rtol=_score_rtol(t["q_win"]))
+    _check_gather(res, t["k"], t["v"], budgets)
+
+
 def _qwen_small(B, C, seed_layer=0, Hq=28, Hkv=4, d=128, w=64):
     wl = workloads.WORKLOADS["qwen25_32k"]
     wl = workloads.Workload(wl.key, wl.name, 1, Hq, Hkv, d, C, w, 7, 64, 128, B, "bf16", 11, "beta")
@@ -415,10 +431,11 @@ def test_run_twice_bitwise():
 
 
 def test_lse_exact_redo_paths():
-    """Pass 1 keeps a per-slot reference fixed within a tile and redoes a tile exactly when a sum
-    leaves [0, 2^96]. Every 16th key is strongly anti-aligned with the window queries (logit about
-    -120) and three keys inside later chunks are strongly aligned (logit about +70, i.e. ~101 in
-    base 2), which forces the exact redo after the reference was set by ordinary keys."""
+    """Pass 1 fixes each row's reference at its largest logit among the chunk's first 16 keys and
+    redoes a chunk exactly when a sum leaves [0, 2^126] (fp32 overflow included). Every 16th key
+    is strongly anti-aligned with the window queries (logit about -120) and three keys inside
+    later chunks are strongly aligned (logit about +100, i.e. ~144 in base 2, far above any
+    chunk-start reference), which forces the exact redo of their chunks."""
     rng = np.random.Generator(np.random.PCG64(31))
     B, Hq, Hkv, d, C, w, s, W = 1, 4, 2, 64, 3000, 32, 4, 32
     common = rng.standard_normal((Hkv, d))
@@ -427,7 +444,7 @@ def test_lse_exact_redo_paths():
     k = rng.standard_normal((B, Hkv, C, d))
     k[:, :, ::16, :] = -15.0 * common[None, :, None, :]  # <common, key>/sqrt(d) = -120
     for pos in (700, 1500, 2300):
-        k[:, :, pos, :] = 8.75 * common  # <common, key>/sqrt(d) = +70
+        k[:, :, pos, :] = 12.5 * common  # <common, key>/sqrt(d) = +100
     v = rng.standard_normal((B, Hkv, C, d))
     t = {n: torch.from_numpy(x.astype(np.float32)).to(DEV) for n, x in dict(q_win=q_win, k=k, v=v).items()}
     budgets = np.array([s + W + 15, s + W + 5])  # selection stays among the keys near the spikes
