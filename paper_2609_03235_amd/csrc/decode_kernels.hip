@@ -125,7 +125,6 @@ __device__ __forceinline__ void decode_chunk(const DecodeArgs& a, float (*pls)[1
                                              const Frag<T> (&qa)[D / 32], int lane, float (&m)[4], float (&s)[4],
                                              float (&o)[GM][CPL]) {
   using S = DecodeStep<T, D, CPL>;
-  constexpr int KS = 16;
   constexpr int NBUF = PF + 1;
   const int lr = lane & 15, lgp = lane >> 4;
   const int kg = lane / S::LPR, col0 = CPL * (lane % S::LPR);
