@@ -456,7 +456,7 @@ def test_lse_exact_redo_paths():
 
 @pytest.mark.parametrize("w,W", [(100, 128), (200, 200)])
 def test_long_window_spans_masked_tiles(w, W):
-    """Window rows spanning several 64-key tiles of the causal block."""
+    """Window rows spanning more than one key tile of the causal (masked) block."""
     rng = np.random.Generator(np.random.PCG64(w))
     B, Hq, Hkv, d, C, s = 2, 4, 2, 64, 1500, 8
     t = {n: torch.from_numpy(rng.standard_normal(shape).astype(np.float32)).to(DEV)
