@@ -46,6 +46,26 @@ __device__ __forceinline__ SegState load_state(const CompressArgs& a, int seg) {
   return st;
 }
 
+// Adds one to bin `bin` of an LDS histogram for every lane with `valid` (call
+// with the whole wave). Scores crowd into a few bins, where one atomic per
+// lane would serialise: the wave takes the distinct bins in turn and adds each
+// bin's lane count with one atomic; after four bins the remaining lanes add
+// one by one.
+__device__ __forceinline__ void hist_add(uint32_t* lh, uint32_t bin, bool valid) {
+  const int lane = threadIdx.x & 63;
+  unsigned long long pending = __ballot(valid);
+#pragma unroll
+  for (int round = 0; round < 4; ++round) {
+    if (pending == 0ull) return;  // uniform
+    const int leader = __builtin_ctzll(pending);
+    const uint32_t lb = (uint32_t)__shfl((int)bin, leader, 64);
+    const unsigned long long same = __ballot(bin == lb) & pending;
+    if (lane == leader) atomicAdd(&lh[lb], (uint32_t)__popcll(same));
+    pending &= ~same;
+  }
+  if ((pending >> lane) & 1ull) atomicAdd(&lh[bin], 1u);
+}
+
 // Exclusive rank of `flag` among the threads of a 256-thread block, and the
 // block total. Uses wave ballots plus one LDS exchange; `wtot` holds 4 words.
 __device__ __forceinline__ uint32_t block_rank(bool flag, uint32_t* wtot, uint32_t& total) {
@@ -179,19 +199,24 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(CompressArgs a) {
       }
     }
     __syncthreads();
-    for (int64_t j = j0 + tid; j < j1; j += kBlock) {
-      float sum = 0.f;
-      if (staged) {
-        const float* wp = win + (j - j0);
-        for (int t = 0; t <= 2 * r; ++t) sum += wp[t];
-      } else {
-        for (int t = -r; t <= r; ++t) sum += ldf(cr, (uint32_t)((j + t) * 4));
+    for (int64_t jb = j0; jb < j1; jb += kBlock) {  // uniform trip count: hist_add needs the whole wave
+      const int64_t j = jb + tid;
+      const bool in = j < j1;
+      float v = 0.f;
+      if (in) {
+        float sum = 0.f;
+        if (staged) {
+          const float* wp = win + (j - j0);
+          for (int t = 0; t <= 2 * r; ++t) sum += wp[t];
+        } else {
+          for (int t = -r; t <= r; ++t) sum += ldf(cr, (uint32_t)((j + t) * 4));
+        }
+        v = sum / fk;
+        stf(pr, (uint32_t)(j * 4), v);
       }
-      const float v = sum / fk;
-      stf(pr, (uint32_t)(j * 4), v);
-      if (hist && j >= cbeg && j < cend) {
+      if (hist) {
         const uint32_t bits = __float_as_uint(v);
-        if ((bits & st.mask) == st.prefix) atomicAdd(&lh[(bits >> shift) & 255u], 1u);
+        hist_add(lh, (bits >> shift) & 255u, in && j >= cbeg && j < cend && (bits & st.mask) == st.prefix);
       }
     }
   } else {
@@ -201,6 +226,7 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(CompressArgs a) {
       uint32_t x[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) x[u] = ld32(pr, (uint32_t)((jb + tid + u * kBlock) * 4));
+      // few candidates still match the prefix here, spread over more bins: one atomic per lane
 #pragma unroll
       for (int u = 0; u < U; ++u)
         if (jb + tid + u * kBlock < c1 && (x[u] & st.mask) == st.prefix) atomicAdd(&lh[(x[u] >> shift) & 255u], 1u);
@@ -230,13 +256,23 @@ __global__ __launch_bounds__(kBlock) void sel_count_kernel(CompressArgs a) {
   const int64_t cend = a.C - a.W;
   const rsrc_t pr = make_rsrc(a.pooled + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
   uint32_t nf = 0, ng = 0, ne = 0;
-  for (int64_t j = j0 + threadIdx.x; j < j1; j += kBlock) {
-    if (j < a.s || j >= cend) {
-      ++nf;
-    } else if (active) {
-      const uint32_t bits = ld32(pr, (uint32_t)(j * 4));
-      ng += bits > tau;
-      ne += bits == tau;
+  // U loads per thread in flight before any is used; positions past the scored range read 0
+  // (outside the descriptor) and are window rows anyway
+  constexpr int U = 8;
+  for (int64_t base = j0; base < j1; base += U * kBlock) {
+    uint32_t x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) x[u] = ld32(pr, (uint32_t)((base + u * kBlock + threadIdx.x) * 4));
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t j = base + u * kBlock + threadIdx.x;
+      if (j >= j1) continue;
+      if (j < a.s || j >= cend) {
+        ++nf;
+      } else if (active) {
+        ng += x[u] > tau;
+        ne += x[u] == tau;
+      }
     }
   }
   // fixed-order block reduction
@@ -320,12 +356,21 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(CompressArgs a) {
   const int64_t j0 = (int64_t)chunk * a.sel_chunk;
   const int64_t j1 = j0 + a.sel_chunk < a.C ? j0 + a.sel_chunk : a.C;
   const int64_t cend = a.C - a.W;
-  for (int64_t base = j0; base < j1; base += kBlock) {
+  // positions in order, 256 at a time; the scores of the next U*256 are loaded together first
+  constexpr int U = 8;
+  for (int64_t ubase = j0; ubase < j1; ubase += U * kBlock) {
+    uint32_t x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) x[u] = ld32(pr, (uint32_t)((ubase + u * kBlock + tid) * 4));
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t base = ubase + u * kBlock;
+    if (base >= j1) break;  // uniform
     const int64_t j = base + tid;
     const bool inr = j < j1;
     const bool fixed = inr && (j < a.s || j >= cend);
     const bool cand = inr && !fixed && active;
-    const uint32_t bits = cand ? ld32(pr, (uint32_t)(j * 4)) : 0u;
+    const uint32_t bits = cand ? x[u] : 0u;
     const bool gt = cand && bits > tau;
     const bool eq = cand && bits == tau;
     uint32_t n_eq, n_keep;
@@ -335,6 +380,7 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(CompressArgs a) {
     if (keep) st32(kp, (run_keep + r) * 4u, (uint32_t)j);
     run_eq += n_eq;
     run_keep += n_keep;
+  }
   }
 }
 
