@@ -106,12 +106,17 @@ SHARED_SOURCES = ("device_common.h", "mfma_frag.h", "sgdkv_internal.h")
 
 
 def source_sha(name):
-    """Hash of the source a kernel is built from: counters taken before a change do not apply."""
+    """Hash of the code a kernel is built from, comments and blank space left out: counters taken
+    before a change to that code do not apply."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in (SOURCE_OF[name],) + SHARED_SOURCES:
-        with open(os.path.join(ROOT, "paper_2609_03235_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2609_03235_amd", "csrc", f)) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -2,18 +2,20 @@
 //
 // Token selection keeps, inside each KV head's budget, the keys with the
 // largest cumulative attention of a final observation window (SGD-KV
-// Sec. 3.3, last paragraph, SnapKV-style; Sec. 5 Query-Aware window). Window
-// row i of query head q sits at prompt position C-w+i and attends causally to
-// keys 0..C-w+i. For each KV head the G*w rows of its query group are one
-// dense block R x d, so the logits of a key tile are an R x 16 MFMA product.
+// Sec. 3.3, last paragraph, SnapKV-style; Sec. 5 window placements). Window
+// row i of query head q sits at prompt position P0+i (P0 = C-w for the
+// Query-Aware window) and attends causally to keys 0..P0+i. For each KV head
+// the G*w rows of its query group are one dense block R x d, so the logits of
+// a key tile are an R x 16 MFMA product.
 //
 //   pass 1 (lse_kernel + lse_merge_kernel): base-2 log-sum-exp of every
 //     window row over its causal keys. Each workgroup covers one chunk of
-//     keys and leaves per-row partials (m, s); the merge combines the chunks
-//     in a fixed order, in fp64.
-//   pass 2 (colsum_kernel): for every scored key j < C-w,
-//     a_j = (1/G) sum_rows exp2(l_rj*log2(e) - lse2_r),
-//     a fixed-order reduction with no float atomics.
+//     keys (about 512 workgroups per launch) and leaves per-row partials
+//     (m, s); the merge combines the chunks in a fixed order, in fp64.
+//   pass 2 (colsum_kernel): for every scored key j < P0,
+//     a_j = (1/G) sum_rows exp2(l_rj*log2(e) - lse2_r) (group mean; the Ipt.
+//     aggregations below weight or pick rows), a fixed-order reduction with
+//     no float atomics.
 //
 // Work split: workgroup = 8 waves; wave v holds row blocks v, v+8, v+16, ...
 // (16 rows each) as MFMA A-fragments in registers, so a SIMD (waves v and
