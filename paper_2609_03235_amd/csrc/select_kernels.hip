@@ -15,7 +15,7 @@
 // else is fixed-order, so results are bitwise reproducible.
 //
 // Kernels (grid y = segment b*Hkv + h):
-//   select_init    zero histograms, seed the radix state, write offsets
+//   select_init    zero the histograms, write the offsets
 //   radix_pass<p>  digit-p histogram of candidates matching the digits
 //                  before it (each workgroup picks those from the earlier
 //                  histograms itself); pass 0 also pools:
@@ -33,6 +33,9 @@ namespace sgdkv {
 
 namespace {
 
+// Radix-select state of a segment: the digits of tau found so far (prefix,
+// under mask) and how many rows are still to place among the candidates that
+// match them. sel_count stores the final one (tau, q) for the compaction.
 struct SegState {
   uint32_t prefix, mask, rem;
 };
@@ -95,17 +98,10 @@ __global__ __launch_bounds__(kBlock) void select_init_kernel(CompressArgs a, int
   const rsrc_t hr = make_rsrc(a.hist + (int64_t)seg * 4 * 256, 4 * 256 * 4);
 #pragma unroll
   for (int p = 0; p < 4; ++p) st32(hr, (p * 256 + threadIdx.x) * 4, 0u);
-  if (threadIdx.x == 0) {
-    const rsrc_t sr = make_rsrc(a.state + (int64_t)seg * 4, 16);
-    st32(sr, 0, 0u);
-    st32(sr, 4, 0u);
-    st32(sr, 8, (uint32_t)a.m[h]);
-    st32(sr, 12, 0u);
-    if (write_offsets) {
-      const rsrc_t orr = make_rsrc(a.offsets, (uint64_t)(nseg + 1) * 8);
-      st64(orr, (uint32_t)seg * 8, (uint64_t)((int64_t)b * a.T_layer + a.prefix[h]));
-      if (seg == nseg - 1) st64(orr, (uint32_t)nseg * 8, (uint64_t)((int64_t)a.B * a.T_layer));
-    }
+  if (threadIdx.x == 0 && write_offsets) {
+    const rsrc_t orr = make_rsrc(a.offsets, (uint64_t)(nseg + 1) * 8);
+    st64(orr, (uint32_t)seg * 8, (uint64_t)((int64_t)b * a.T_layer + a.prefix[h]));
+    if (seg == nseg - 1) st64(orr, (uint32_t)nseg * 8, (uint64_t)((int64_t)a.B * a.T_layer));
   }
 }
 

@@ -64,7 +64,7 @@ struct CompressArgs {
   float* lse2;      // [B*Hkv][R]                   base-2 LSE of each window row
   float* colsum;    // [B*Hkv][n_scored]
   uint32_t* hist;   // [B*Hkv][4][256]: histogram of each radix digit
-  uint32_t* state;  // [B*Hkv][4]: prefix, mask, rows still to place, unused
+  uint32_t* state;  // [B*Hkv][4]: tau, its mask, q (rows equal to tau to keep), unused
   uint32_t* counts; // [B*Hkv][n_sel_chunks][4]: fixed, greater, equal, unused
   // chunking
   int64_t score_chunk;  // keys per score workgroup (multiple of kScoreChunkQuantum)
