@@ -334,8 +334,10 @@ __global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
   // the last chunks go first: the one with the window block ends with its exact (masked) tiles
   const int chunk = (int)(gridDim.x - 1 - blockIdx.x);
   const int64_t key0 = (int64_t)chunk * a.score_chunk;
-  if (key0 >= a.C) return;
-  const int64_t key_end = key0 + a.score_chunk < a.C ? key0 + a.score_chunk : a.C;
+  // keys past the last window row's position are seen by no row
+  const int64_t vis_end = a.win0 + a.w < a.C ? a.win0 + a.w : a.C;
+  if (key0 >= vis_end) return;
+  const int64_t key_end = key0 + a.score_chunk < vis_end ? key0 + a.score_chunk : vis_end;
   const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
   const rsrc_t kr = make_rsrc(static_cast<const T*>(a.k) + (int64_t)seg * a.C * D, (uint64_t)a.C * G::RB);
   Frag<T> qa[RBW][G::NC];

@@ -339,7 +339,8 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, int64_t win0, CompressP
       std::max<int64_t>(round_up(ceil_div(nseg * a.C, 512), sgdkv::kScoreChunkQuantum),
                         2 * sgdkv::kScoreChunkQuantum),
       1 << 16);
-  a.n_lse_chunks = (int)ceil_div(a.C, a.score_chunk);
+  // pass 1 covers the keys some window row sees: [0, min(C, win0 + w))
+  a.n_lse_chunks = (int)ceil_div(std::min<int64_t>(a.C, win0 + a.w), a.score_chunk);
   a.n_col_chunks = (int)ceil_div(a.n_scored, a.score_chunk);
   // selection workgroups: about 2048 in total
   a.sel_chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(nseg * a.C, 2048), 256), 1024), 1 << 20);

@@ -68,7 +68,7 @@ struct CompressArgs {
   uint32_t* counts; // [B*Hkv][n_sel_chunks][4]: fixed, greater, equal, unused
   // chunking
   int64_t score_chunk;  // keys per score workgroup (multiple of kScoreChunkQuantum)
-  int n_lse_chunks;     // ceil(C / score_chunk)
+  int n_lse_chunks;     // ceil(min(C, win0 + w) / score_chunk): keys some window row sees
   int n_col_chunks;     // ceil(n_scored / score_chunk)
   int64_t sel_chunk;    // positions per selection workgroup
   int64_t hist_chunk;   // scored positions per pooling / radix-pass workgroup (multiple of 256)
