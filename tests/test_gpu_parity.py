@@ -430,6 +430,40 @@ def test_run_twice_bitwise():
     assert torch.equal(oa, ob) and torch.equal(la, lb)
 
 
+def test_two_streams_two_workspaces():
+    """Calls are reentrant across streams given distinct workspaces: two layers compressed and
+    decoded on two streams at once match the same calls made one after the other."""
+    wl, t0 = _qwen_small(2, 2600, seed_layer=0)
+    _, t1 = _qwen_small(2, 2600, seed_layer=1)
+    budgets = [np.array([900, 300, 1200, 400]), np.array([350, 1700, 500, 800])]
+    kw = dict(pool_kernel=7, b_sink=64, b_window=128)
+    _announce("two streams")
+    serial = []
+    for t, bud in ((t0, budgets[0]), (t1, budgets[1])):
+        r = sg.compress_layer(t["q_win"], t["k"], t["v"], bud, **kw)
+        o, l = sg.decode_attention(t["q"], r["k_c"], r["v_c"], r["offsets"], r["offsets_host"], 4)
+        serial.append((r, o, l))
+    torch.cuda.synchronize()
+    desc = sg.compress_desc(t0["q_win"], t0["k"], **kw)
+    wss = [sg.alloc_workspace(sg.compress_workspace_size(desc), DEV) for _ in range(2)]
+    streams = [torch.cuda.Stream(device=DEV) for _ in range(2)]
+    start = torch.cuda.Event()
+    start.record(torch.cuda.current_stream())
+    conc = []
+    for i, (t, bud) in enumerate(((t0, budgets[0]), (t1, budgets[1]))):
+        streams[i].wait_event(start)
+        with torch.cuda.stream(streams[i]):
+            r = sg.compress_layer(t["q_win"], t["k"], t["v"], bud, workspace=wss[i], stream=streams[i], **kw)
+            o, l = sg.decode_attention(t["q"], r["k_c"], r["v_c"], r["offsets"], r["offsets_host"], 4,
+                                       stream=streams[i])
+        conc.append((r, o, l))
+    torch.cuda.synchronize()
+    for (ra, oa, la), (rb, ob, lb) in zip(serial, conc):
+        for key in ("scores", "kept_pos", "offsets", "k_c", "v_c"):
+            assert torch.equal(ra[key], rb[key]), key
+        assert torch.equal(oa, ob) and torch.equal(la, lb)
+
+
 def test_lse_exact_redo_paths():
     """Pass 1 fixes each row's reference at its largest logit among the chunk's first 16 keys and
     redoes a chunk exactly when a sum leaves [0, 2^126] (fp32 overflow included). Every 16th key
