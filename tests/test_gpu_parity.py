@@ -268,6 +268,47 @@ def test_window_placement(case):
     _check_gather(res, t["k"], t["v"], budgets)
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_random_shapes(seed):
+    """Seeded random shapes against the oracle: batch, heads and group size, head dim, dtype,
+    window length and placement, sink/window sizes, pooling width and budgets (empty and full
+    middles included), so that chunk, tile and selection boundaries fall in varied places."""
+    rng = np.random.Generator(np.random.PCG64(1000 + seed))
+    B = int(rng.integers(1, 4))
+    Hkv = int(rng.choice([1, 2, 4]))
+    d = int(rng.choice([64, 128]))
+    dtype = torch.bfloat16 if rng.random() < 0.6 else torch.float32
+    w = int(rng.choice([16, 32, 48, 64]))
+    G = int(rng.integers(1, 512 // w + 1)) if w > 16 else int(rng.integers(1, 9))
+    G = min(G, 8)
+    Hq = G * Hkv
+    s = int(rng.integers(0, 65))
+    placement = rng.choice(["aware", "unaware", "proxy"])
+    q_len = int(rng.integers(1, 200)) if placement == "unaware" else 0
+    C = int(rng.integers(s + w + q_len + 300, 3200))
+    win0 = C if placement == "proxy" else C - w - q_len
+    W = int(rng.integers(C - win0 if placement != "aware" else w, min(C - win0 + 300, C - s) + 1))
+    W = max(W, w, C - win0)
+    kp = int(rng.choice([1, 3, 5, 7, 9]))
+    budgets = rng.integers(s + W, C + 1, size=Hkv)
+    budgets[0] = s + W if seed % 3 == 0 else budgets[0]  # an empty middle
+    if Hkv > 1 and seed % 4 == 1:
+        budgets[-1] = C  # a full middle
+    tt = {n: torch.from_numpy(rng.standard_normal(shape).astype(np.float32)).to(dtype).to(DEV)
+          for n, shape in dict(q_win=(B, Hq, w, d), k=(B, Hkv, C, d), v=(B, Hkv, C, d), q=(B, Hq, d)).items()}
+    _announce(f"random shapes seed={seed}: B={B} Hq={Hq} Hkv={Hkv} d={d} {dtype} w={w} C={C} s={s} W={W} "
+              f"kp={kp} {placement} win0={win0} budgets={budgets.tolist()}")
+    res, orc = _compress_both(tt["q_win"], tt["k"], tt["v"], budgets, kp=kp, s=s, W=W,
+                              win0=None if placement == "aware" else win0)
+    rtol = _score_rtol(tt["q_win"])
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], f"random {seed}", rtol=rtol)
+    _check_kept(res, orc, tt["q_win"].shape, C, w, s, W, budgets, f"random {seed}",
+                win0=None if placement == "aware" else win0, rtol=rtol)
+    _check_gather(res, tt["k"], tt["v"], budgets)
+    _decode_on_oracle_cache(orc, tt["q"], Hkv, dtype, 2e-2 if dtype == torch.bfloat16 else 1e-5,
+                            f"random {seed}")
+
+
 def test_caller_supplied_lse_and_scores_only():
     wl, t = _qwen_small(1, 2100)
     s, W = wl.b_sink, wl.b_window
