@@ -9,10 +9,11 @@ One step is the whole path over one batch of synthetic, HBM-resident input:
          sequence and query head over that layer's compressed cache)
 Layers are compressed first and decoded afterwards, so no decode reads a
 cache still warm in the 256 MB last-level cache from its own compression.
-With --streams 2, layer l is compressed on stream l mod 2 (each stream with
-its own workspace): the layers are independent, so one layer's selection and
-gather run beside the next layer's scoring. The default serialises them, so
-each kernel's measured duration is its own.
+Each layer's row gather goes on a second stream (the gather_stream option of
+sgdkv_compress_layer_ex) and runs beside the next layer's window scoring, which
+is bound by instruction issue and leaves HBM bandwidth unused; the decode
+waits for the last gather. --no-gather-stream keeps every kernel on one
+stream, so that each kernel's measured duration is its own.
 
 Default workload: the 28-layer Qwen2.5-7B-shaped stack (28 query / 4 KV
 heads, head dim 128) at a 131072-token prompt, batch 8, bf16, 25 % budget,
@@ -82,10 +83,9 @@ def parse():
     ap.add_argument("--decode-new", type=int, default=0, metavar="N",
                     help="generation: each layer's decode also attends to N rows appended since compression, "
                          "and every step appends one row per KV head (sgdkv_append_kv) before decoding")
-    ap.add_argument("--streams", type=int, default=1, choices=[1, 2],
-                    help="compress layer l on stream l %% STREAMS (own workspace per stream), so one layer's "
-                         "selection and gather overlap the next layer's scoring; decode follows on the first. "
-                         "With 2 the per-kernel durations include the other stream's work")
+    ap.add_argument("--no-gather-stream", action="store_true",
+                    help="run each layer's row gather on the main stream instead of a second stream beside "
+                         "the next layer's scoring (then no kernel shares the GPU with another)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0, metavar="MIB",
                     help="first run three elementwise copies of MIB MiB (fp32 x 1.0), untimed: under "
@@ -288,9 +288,9 @@ def main():
             tails[l] = (kn, vn, step_kv)
     dec_lse = [torch.empty((B, Hq), dtype=torch.float32, device=dev) for _ in range(L)]
     cdesc = sg.compress_desc(layers[0]["q_win"], layers[0]["k"], pool_kernel=kp, b_sink=s, b_window=W)
-    # one compression workspace per stream; every stream keeps torch's default priority
-    streams = [stream] + [torch.cuda.Stream(device=dev) for _ in range(args.streams - 1)]
-    ws_c = [sg.alloc_workspace(sg.compress_workspace_size(cdesc), dev) for _ in streams]
+    # the gathers' stream keeps torch's default priority; the gather does not use the workspace
+    gstream = None if args.no_gather_stream else torch.cuda.Stream(device=dev)
+    ws_c = sg.alloc_workspace(sg.compress_workspace_size(cdesc), dev)
     offsets_host = []
     for l in range(L):
         pre = np.concatenate([[0], np.cumsum(budgets[l])])
@@ -306,21 +306,13 @@ def main():
     def step():
         # S0 on the host, then every layer's compression, then every layer's decode
         allocate()
-        if len(streams) > 1:
-            fork = torch.cuda.Event()
-            fork.record(stream)
-            for st in streams[1:]:
-                st.wait_event(fork)
         for l in range(L):
             t = layers[l]
-            i = l % len(streams)
             sg.compress_layer(t["q_win"], t["k"], t["v"], budgets[l], pool_kernel=kp, b_sink=s, b_window=W,
                               window_lse=lse_in[l], group_agg=agg, qhead_scores=qscores[l], window_pos=win0,
-                              out=outs[l], workspace=ws_c[i], stream=streams[i])
-        for st in streams[1:]:
-            join = torch.cuda.Event()
-            join.record(st)
-            stream.wait_event(join)
+                              out=outs[l], workspace=ws_c, stream=stream, gather_stream=gstream)
+        if gstream is not None:
+            stream.wait_stream(gstream)  # every layer's compressed cache is complete before decode
         for l in range(L):
             o = outs[l]
             kn = vn = None
@@ -401,7 +393,9 @@ def main():
     decode = roof("decode_split") if "decode_split" in kern else None
     dec_ms = (kern.get("decode_split", (0, 0))[1] + kern.get("decode_combine", (0, 0))[1]) / args.steps
     dec_bytes = work["decode_split"][1] * L
-    comp_ms = sum(ms for n, (c, ms) in kern.items() if not n.startswith("decode")) / args.steps
+    # compression time: the step minus its decode kernels (the gathers overlap other kernels, so
+    # a sum of kernel durations would count them twice)
+    comp_ms = ms_per_step - dec_ms
 
     tokens = float(B) * C * L  # prompt tokens per step, over all layers
     value = tokens / (ms_per_step / 1e3)
@@ -446,7 +440,7 @@ def main():
                     obs_window=w, pool_kernel=kp, b_sink=s, b_window=W, budget_ratio=args.ratio,
                     total_budget_rows=int(budgets.sum()), window_lse="caller" if args.caller_lse else "computed",
                     alloc_variant=args.alloc_variant, group_agg=args.group_agg, window_start=win0,
-                    decode_appended_rows=n_new, compress_streams=args.streams),
+                    decode_appended_rows=n_new, gather_stream=not args.no_gather_stream),
         compress_tokens_per_s=round(tokens / (comp_ms / 1e3), 1) if comp_ms > 0 else None,
         decode=dict(gbps=round(dec_bytes / (dec_ms / 1e3) / 1e9, 1) if dec_ms > 0 else None,
                     frac_of_peak=round(dec_bytes / (dec_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4) if dec_ms > 0 else None,

@@ -211,6 +211,17 @@ sgdkv_status sgdkv_compress_layer(const sgdkv_compress_desc* desc, const int64_t
  *   question of C - w - P0 tokens (Query-Unaware); P0 = C places it after
  *   the prompt (Proxy-Query rows, which see every cached key; the softmax
  *   then runs over cached keys only unless window_lse is supplied).
+ * gather_stream: NULL (or equal to `stream`): all work goes on `stream`.
+ *   Otherwise the last step, copying the kept K and V rows into k_out and
+ *   v_out, is enqueued on gather_stream, ordered after this call's selection
+ *   on `stream` by an event the library records, and runs on about half of
+ *   the compute units, so that it overlaps the work the caller enqueues next
+ *   on `stream` (for example the next layer's window scoring, which leaves
+ *   memory bandwidth unused). k_out and v_out are then complete only when
+ *   gather_stream reaches this point, and k and v must stay unchanged until
+ *   then; kept_pos_out, offsets_out and scores_out are complete on `stream`
+ *   as usual. The copy does not touch the workspace, which is free for the
+ *   next call on `stream` at once. Not used in scores-only mode.
  * Errors: those of sgdkv_compress_layer (with b_window >= C - P0 in place of
  *   b_window >= w); group_agg not 0..3; NULL or invalid qhead_scores for an
  *   Ipt. mode; Hq > 256 with an Ipt. mode (UNSUPPORTED); IPT_MAX with
@@ -225,6 +236,7 @@ typedef struct sgdkv_compress_opts {
   int32_t reserved;            /* must be 0 */
   const double* qhead_scores;  /* host [Hq], Ipt. modes */
   int64_t window_pos;          /* P0, or -1 for C - w */
+  void* gather_stream;         /* hipStream_t for the row gather, or NULL */
 } sgdkv_compress_opts;
 sgdkv_status sgdkv_compress_layer_ex(const sgdkv_compress_desc* desc, const sgdkv_compress_opts* opts,
                                      const int64_t* layer_budgets, const void* q_win, const void* k,

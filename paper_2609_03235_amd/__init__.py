@@ -48,7 +48,7 @@ class CompressDesc(ctypes.Structure):
 
 class CompressOpts(ctypes.Structure):
     _fields_ = [("group_agg", ctypes.c_int32), ("reserved", ctypes.c_int32), ("qhead_scores", ctypes.c_void_p),
-                ("window_pos", ctypes.c_int64)]
+                ("window_pos", ctypes.c_int64), ("gather_stream", ctypes.c_void_p)]
 
 
 class DecodeDesc(ctypes.Structure):
@@ -217,11 +217,12 @@ GROUP_MEAN, GROUP_IPT_MAX, GROUP_IPT_MEAN, GROUP_IPT_ONLY = range(4)
 def compress_layer(q_win, k, v, layer_budgets, *, pool_kernel: int, b_sink: int, b_window: int,
                    scale: float = 0.0, window_lse=None, scores_only: bool = False, with_scores: bool = True,
                    group_agg: int = GROUP_MEAN, qhead_scores=None, window_pos: int = -1,
-                   workspace=None, out: dict | None = None, stream=None) -> dict:
+                   workspace=None, out: dict | None = None, stream=None, gather_stream=None) -> dict:
     """Compress one layer (sgdkv_compress_layer_ex). group_agg selects the plain group mean or an
     Ipt. aggregation with the layer's per-query-head scores; window_pos places the first window
-    row (-1: the last obs_window prompt tokens). Returns k_c, v_c, kept_pos, offsets, scores
-    (scores: [B, Hkv, window position])."""
+    row (-1: the last obs_window prompt tokens). gather_stream (optional) takes the copy of the
+    kept rows into k_c and v_c, which are then complete only on that stream. Returns k_c, v_c,
+    kept_pos, offsets, scores (scores: [B, Hkv, window position])."""
     import torch
     desc = compress_desc(q_win, k, pool_kernel=pool_kernel, b_sink=b_sink, b_window=b_window, scale=scale)
     B, Hkv, C, d = k.shape
@@ -250,7 +251,8 @@ def compress_layer(q_win, k, v, layer_budgets, *, pool_kernel: int, b_sink: int,
         qs = np.ascontiguousarray(np.asarray(qhead_scores, dtype=np.float64).reshape(-1))
         if qs.size != q_win.shape[1]:
             raise SgdkvError(ERR_INVALID_ARG, "qhead_scores must hold num_q_heads values")
-    opts = CompressOpts(int(group_agg), 0, None if qs is None else qs.ctypes.data, int(window_pos))
+    opts = CompressOpts(int(group_agg), 0, None if qs is None else qs.ctypes.data, int(window_pos),
+                        None if gather_stream is None else _stream(gather_stream).value)
     st = load_library().sgdkv_compress_layer_ex(
         ctypes.byref(desc), ctypes.byref(opts), None if budgets is None else _np_ptr(budgets), _ptr(q_win), _ptr(k),
         _ptr(v) if v is not None else None, _ptr(window_lse), _ptr(res.get("k_c")), _ptr(res.get("v_c")),

@@ -380,19 +380,23 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(CompressArgs a) {
   }
 }
 
-// Copies the kept K and V rows of one segment into the ragged cache. Each
-// workgroup moves kCopyRows output rows; every thread keeps several 16-byte
-// loads in flight before storing. RB = bytes per row.
-constexpr int kCopyRows = 64;
+// Copies the kept K and V rows into the ragged cache. A work item is
+// kCopyRows output rows of one segment (item = seg * copy_blocks + block);
+// workgroups take items in a grid-stride loop, so the grid may be smaller
+// than the item count (the library shrinks it when the copy runs beside
+// other work). Every thread keeps several 16-byte loads in flight before
+// storing. RB = bytes per row.
 template <int RB>
 __global__ __launch_bounds__(kBlock) void copy_rows_kernel(CompressArgs a) {
   constexpr int V16 = RB / 16;                        // 16-byte pieces per row
   constexpr int PER = kCopyRows * V16 / kBlock;       // pieces per thread per tensor
   static_assert(PER >= 1 && (kCopyRows * V16) % kBlock == 0, "copy tile must split evenly");
-  const int seg = blockIdx.y, b = seg / a.Hkv, h = seg % a.Hkv;
+  const int64_t items = (int64_t)a.copy_blocks * a.B * a.Hkv;
+  for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
+  const int seg = (int)(item / a.copy_blocks), b = seg / a.Hkv, h = seg % a.Hkv;
   const int64_t seg_len = a.prefix[h + 1] - a.prefix[h];
-  const int64_t row0 = (int64_t)blockIdx.x * kCopyRows;
-  if (row0 >= seg_len) return;
+  const int64_t row0 = (item % a.copy_blocks) * kCopyRows;
+  if (row0 >= seg_len) continue;  // uniform per workgroup
   const int64_t seg_off = (int64_t)b * a.T_layer + a.prefix[h];
   const rsrc_t kp = make_rsrc(a.kept_pos + seg_off, (uint64_t)seg_len * 4);
   const rsrc_t ko = make_rsrc(static_cast<char*>(a.k_out) + seg_off * RB, (uint64_t)seg_len * RB);
@@ -417,6 +421,7 @@ __global__ __launch_bounds__(kBlock) void copy_rows_kernel(CompressArgs a) {
     st128(ko, dst[u], kx[u]);
     st128(vo, dst[u], vx[u]);
   }
+  }
 }
 
 hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t st) {
@@ -436,17 +441,19 @@ hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t st
   }
   SGDKV_LAUNCH("sel_count", sel_count_kernel, dim3(a.n_sel_chunks, nseg), blk, st, a);
   SGDKV_LAUNCH("compact", compact_kernel, dim3(a.n_sel_chunks, nseg), blk, st, a);
-  int64_t longest = 0;
-  for (int hh = 0; hh < a.Hkv; ++hh) longest = std::max<int64_t>(longest, a.prefix[hh + 1] - a.prefix[hh]);
-  const unsigned copy_blocks = (unsigned)((longest + kCopyRows - 1) / kCopyRows);
-  if (copy_blocks > 0) {
-    const int rb = a.D * (a.dtype == 1 ? 2 : 4);
-    switch (rb) {
-      case 128: SGDKV_LAUNCH("gather", copy_rows_kernel<128>, dim3(copy_blocks, nseg), blk, st, a); break;
-      case 256: SGDKV_LAUNCH("gather", copy_rows_kernel<256>, dim3(copy_blocks, nseg), blk, st, a); break;
-      case 512: SGDKV_LAUNCH("gather", copy_rows_kernel<512>, dim3(copy_blocks, nseg), blk, st, a); break;
-      default: return hipErrorInvalidValue;
-    }
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const CompressArgs& a, int max_blocks, hipStream_t st) {
+  const int64_t items = (int64_t)a.copy_blocks * a.B * a.Hkv;
+  if (items == 0) return hipSuccess;
+  const unsigned grid = (unsigned)(max_blocks > 0 ? std::min<int64_t>(items, max_blocks) : items);
+  const dim3 blk(kBlock);
+  switch (a.D * (a.dtype == 1 ? 2 : 4)) {
+    case 128: SGDKV_LAUNCH("gather", copy_rows_kernel<128>, dim3(grid), blk, st, a); break;
+    case 256: SGDKV_LAUNCH("gather", copy_rows_kernel<256>, dim3(grid), blk, st, a); break;
+    case 512: SGDKV_LAUNCH("gather", copy_rows_kernel<512>, dim3(grid), blk, st, a); break;
+    default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }

@@ -45,23 +45,30 @@ int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // The kernels are built for gfx950 only; check the current device once per device.
-sgdkv_status check_device() {
+// cus_out (optional) receives the device's compute-unit count.
+sgdkv_status check_device(int* cus_out = nullptr) {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "no HIP device: %s", hipGetErrorString(e));
   static std::mutex mu;
   static std::vector<int> verdict;  // -1 unknown, 0 unsupported, 1 gfx950
+  static std::vector<int> cus;
   std::lock_guard<std::mutex> lock(mu);
-  if ((int)verdict.size() <= dev) verdict.resize(dev + 1, -1);
+  if ((int)verdict.size() <= dev) {
+    verdict.resize(dev + 1, -1);
+    cus.resize(dev + 1, 0);
+  }
   if (verdict[dev] < 0) {
     hipDeviceProp_t prop;
     e = hipGetDeviceProperties(&prop, dev);
     if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
     verdict[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 0;
+    cus[dev] = prop.multiProcessorCount;
     if (!verdict[dev]) return fail(SGDKV_ERR_UNSUPPORTED, "device %d is %s; kernels are built for gfx950",
                                    dev, prop.gcnArchName);
   }
   if (!verdict[dev]) return fail(SGDKV_ERR_UNSUPPORTED, "device %d is not gfx950", dev);
+  if (cus_out) *cus_out = cus[dev];
   return SGDKV_OK;
 }
 
@@ -132,7 +139,7 @@ extern "C" {
 
 const char* sgdkv_last_error(void) { return g_error.c_str(); }
 
-int32_t sgdkv_version(void) { return 100; }
+int32_t sgdkv_version(void) { return 101; }
 
 sgdkv_status sgdkv_reduce_query_head_scores(const double* per_qhead, int32_t L, int32_t Hq, int32_t Hkv,
                                             double* per_kvhead_out) {
@@ -460,7 +467,7 @@ sgdkv_status sgdkv_compress_layer_ex(const sgdkv_compress_desc* desc, const sgdk
                                      const void* v, const float* window_lse, void* k_out, void* v_out,
                                      int32_t* kept_pos_out, int64_t* offsets_out, float* scores_out,
                                      void* workspace, size_t workspace_bytes, void* stream) {
-  sgdkv_compress_opts o{SGDKV_GROUP_MEAN, 0, nullptr, -1};
+  sgdkv_compress_opts o{SGDKV_GROUP_MEAN, 0, nullptr, -1, nullptr};
   if (opts) o = *opts;
   if (!desc) return fail(SGDKV_ERR_INVALID_ARG, "NULL descriptor");
   if (o.reserved != 0) return fail(SGDKV_ERR_INVALID_ARG, "opts.reserved must be 0");
@@ -524,6 +531,9 @@ sgdkv_status sgdkv_compress_layer_ex(const sgdkv_compress_desc* desc, const sgdk
     }
     a.prefix[a.Hkv] = run;
     a.T_layer = run;
+    int64_t longest = 0;
+    for (int h = 0; h < a.Hkv; ++h) longest = std::max<int64_t>(longest, layer_budgets[h]);
+    a.copy_blocks = scores_only ? 0 : (int)ceil_div(longest, sgdkv::kCopyRows);
   }
   if (p.bytes > 0) {
     if (!workspace) return fail(SGDKV_ERR_WORKSPACE, "NULL workspace (%zu bytes needed)", p.bytes);
@@ -532,7 +542,8 @@ sgdkv_status sgdkv_compress_layer_ex(const sgdkv_compress_desc* desc, const sgdk
     if (workspace_bytes < p.bytes)
       return fail(SGDKV_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.bytes);
   }
-  if (sgdkv_status st = check_device()) return st;
+  int cus = 0;
+  if (sgdkv_status st = check_device(&cus)) return st;
 
   char* ws = static_cast<char*>(workspace);
   a.q_win = q_win;
@@ -558,6 +569,26 @@ sgdkv_status sgdkv_compress_layer_ex(const sgdkv_compress_desc* desc, const sgdk
   if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "score kernels: %s", hipGetErrorString(e));
   e = sgdkv::launch_select(a, scores_only, st);
   if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "selection kernels: %s", hipGetErrorString(e));
+  if (scores_only) return ok();
+  hipStream_t gs = static_cast<hipStream_t>(o.gather_stream);
+  if (gs && gs != st) {
+    // The gather waits for the selection through an event, then runs on its own stream with
+    // half as many workgroups as the device has compute units, so that it fits beside
+    // whatever the caller enqueues next on `stream`.
+    hipEvent_t ev = nullptr;
+    e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+    if (e == hipSuccess) {
+      e = hipEventRecord(ev, st);
+      if (e == hipSuccess) e = hipStreamWaitEvent(gs, ev, 0);
+      const hipError_t e2 = hipEventDestroy(ev);  // released once the recorded work completes
+      if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "ordering the gather stream: %s", hipGetErrorString(e));
+    e = sgdkv::launch_gather(a, std::max(1, cus / 2), gs);
+  } else {
+    e = sgdkv::launch_gather(a, 0, st);
+  }
+  if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "gather kernel: %s", hipGetErrorString(e));
   return ok();
 }
 

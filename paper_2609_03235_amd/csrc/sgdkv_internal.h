@@ -19,6 +19,7 @@ constexpr int kColTileF32 = 64;    // the same for fp32 keys (LDS holds half as 
 constexpr int kScoreChunkQuantum = 128;  // score chunks are whole tiles of both passes
 constexpr int kHistChunkMax = 8192;      // positions per pooling / radix-pass workgroup, at most
 constexpr int kPoolHalo = 64;            // pooling radii up to this are staged in LDS
+constexpr int kCopyRows = 64;            // output rows per work item of the row gather
 #ifndef SGDKV_SCORE_WAVES
 #define SGDKV_SCORE_WAVES 8
 #endif
@@ -78,10 +79,13 @@ struct CompressArgs {
   int64_t T_layer;
   int64_t m[kMaxKvHeads];           // middle rows kept per head
   int64_t prefix[kMaxKvHeads + 1];  // exclusive prefix sums of the budgets
+  int copy_blocks = 0;              // gather work items per segment: ceil(max_h b_h / kCopyRows)
 };
 
 hipError_t launch_scores(const CompressArgs& a, hipStream_t stream);      // passes 1 and 2
-hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t stream);
+hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t stream);  // pool .. compact
+// The row gather; max_blocks > 0 caps its grid (the copy then runs beside other work).
+hipError_t launch_gather(const CompressArgs& a, int max_blocks, hipStream_t stream);
 
 // ------------------------------------------------------------------ decode
 struct DecodeArgs {

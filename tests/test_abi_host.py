@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol():
     lib = sg.load_library()
     for name in declared:
         assert hasattr(lib, name), name
-    assert sg.version() == 100
+    assert sg.version() == 101
 
 
 problem = st.integers(min_value=1, max_value=4).flatmap(

@@ -505,6 +505,39 @@ def test_two_streams_two_workspaces():
         assert torch.equal(oa, ob) and torch.equal(la, lb)
 
 
+@pytest.mark.parametrize("dtype,d", [(torch.bfloat16, 128), (torch.bfloat16, 64), (torch.float32, 128)])
+def test_gather_stream(dtype, d):
+    """With a gather stream the kept rows are copied on that stream, after an event on the main
+    stream, by a grid-stride copy with half as many workgroups as compute units (here fewer than
+    the work items, so workgroups loop). Three layers through one workspace, each gather
+    overlapping the next layer's scoring, give the same outputs as plain calls, and the copied
+    rows equal the input rows at the kept positions (16-, 8- and 32-piece rows)."""
+    rng = np.random.Generator(np.random.PCG64(77 + d))
+    B, Hq, Hkv, C, w, s, W = 2, 8, 4, 6000, 32, 16, 64
+    kw = dict(pool_kernel=5, b_sink=s, b_window=W)
+    layers, budgets = [], []
+    for layer in range(3):
+        layers.append({n: torch.from_numpy(rng.standard_normal(shape).astype(np.float32)).to(dtype).to(DEV)
+                       for n, shape in dict(q_win=(B, Hq, w, d), k=(B, Hkv, C, d), v=(B, Hkv, C, d)).items()})
+        bud = rng.integers(s + W, C + 1, size=Hkv)
+        bud[layer % Hkv] = C if layer == 1 else s + W  # a full and an empty middle
+        budgets.append(bud)
+    _announce(f"gather stream {dtype} d={d} budgets={[b.tolist() for b in budgets]}")
+    plain = [sg.compress_layer(t["q_win"], t["k"], t["v"], bud, **kw) for t, bud in zip(layers, budgets)]
+    torch.cuda.synchronize()
+    ws = sg.alloc_workspace(sg.compress_workspace_size(sg.compress_desc(layers[0]["q_win"], layers[0]["k"], **kw)),
+                            DEV)
+    main, gs = torch.cuda.current_stream(), torch.cuda.Stream(device=DEV)
+    side = [sg.compress_layer(t["q_win"], t["k"], t["v"], bud, workspace=ws, stream=main, gather_stream=gs, **kw)
+            for t, bud in zip(layers, budgets)]
+    main.wait_stream(gs)
+    torch.cuda.synchronize()
+    for t, bud, ra, rb in zip(layers, budgets, plain, side):
+        for key in ("scores", "kept_pos", "offsets", "k_c", "v_c"):
+            assert torch.equal(ra[key], rb[key]), key
+        _check_gather(rb, t["k"], t["v"], bud)
+
+
 def test_lse_exact_redo_paths():
     """Pass 1 fixes each row's reference at its largest logit among the chunk's first 16 keys and
     redoes a chunk exactly when a sum leaves [0, 2^126] (fp32 overflow included). Every 16th key
