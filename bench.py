@@ -9,10 +9,12 @@ One step is the whole path over one batch of synthetic, HBM-resident input:
          sequence and query head over that layer's compressed cache)
 Layers are compressed first and decoded afterwards, so no decode reads a
 cache still warm in the 256 MB last-level cache from its own compression.
-Each layer's row gather goes on a second stream (the gather_stream option of
-sgdkv_compress_layer_ex) and runs beside the next layer's window scoring, which
-is bound by instruction issue and leaves HBM bandwidth unused; the decode
-waits for the last gather. --no-gather-stream keeps every kernel on one
+Each layer's row gather but the last goes on a second stream (the
+gather_stream option of sgdkv_compress_layer_ex) and runs beside the next
+layer's window scoring, which is bound by instruction issue and leaves HBM
+bandwidth unused; the decode waits for the gathers. The last layer's gather
+(the only one of a one-layer workload) has nothing to overlap and runs on the
+main stream with its full grid. --no-gather-stream keeps every kernel on one
 stream, so that each kernel's measured duration is its own.
 
 Default workload: the 28-layer Qwen2.5-7B-shaped stack (28 query / 4 KV
@@ -310,8 +312,9 @@ def main():
             t = layers[l]
             sg.compress_layer(t["q_win"], t["k"], t["v"], budgets[l], pool_kernel=kp, b_sink=s, b_window=W,
                               window_lse=lse_in[l], group_agg=agg, qhead_scores=qscores[l], window_pos=win0,
-                              out=outs[l], workspace=ws_c, stream=stream, gather_stream=gstream)
-        if gstream is not None:
+                              out=outs[l], workspace=ws_c, stream=stream,
+                              gather_stream=gstream if l < L - 1 else None)  # nothing follows the last
+        if gstream is not None and L > 1:
             stream.wait_stream(gstream)  # every layer's compressed cache is complete before decode
         for l in range(L):
             o = outs[l]
