@@ -359,32 +359,29 @@ __global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
 // Merge the per-chunk partials of every window row in fp64: one wave per row,
 // lanes stride over the chunks, fixed-order shuffle trees for max and sum.
 __global__ __launch_bounds__(kBlock) void lse_merge_kernel(CompressArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int64_t idx = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
-  const int64_t nrows = (int64_t)a.B * a.Hkv * a.R;
-  if (idx >= nrows) return;  // uniform per wave
-  const int64_t seg = idx / a.R, row = idx % a.R;
-  const float* part = a.lse_part + (seg * a.n_lse_chunks) * a.R * 2;
-  const rsrc_t pr = make_rsrc(part, (uint64_t)a.n_lse_chunks * a.R * 2 * sizeof(float));
+  // one thread per window row of segment blockIdx.y; the row's chunk partials are merged in
+  // chunk order (max first, then the rescaled sums in fp64)
+  const int64_t seg = blockIdx.y;
+  const int row = blockIdx.x * kBlock + threadIdx.x;
+  if (row >= a.R) return;
+  const int n = a.n_lse_chunks;
+  const rsrc_t pr = make_rsrc(a.lse_part + seg * n * a.R * 2, (uint64_t)n * a.R * 2 * sizeof(float));
+  auto off = [&](int c) { return (uint32_t)(((int64_t)c * a.R + row) * 8); };
   float mx = -INFINITY;
-  for (int c = lane; c < a.n_lse_chunks; c += 64)
-    mx = fmaxf(mx, ldf(pr, (uint32_t)(((int64_t)c * a.R + row) * 8)));
-  mx = wave_max(mx);
+#pragma unroll 8
+  for (int c = 0; c < n; ++c) mx = fmaxf(mx, ldf(pr, off(c)));
   double sum = 0.0;
   if (mx != -INFINITY) {
-    for (int c = lane; c < a.n_lse_chunks; c += 64) {
-      const float mc = ldf(pr, (uint32_t)(((int64_t)c * a.R + row) * 8));
-      const float sc = ldf(pr, (uint32_t)(((int64_t)c * a.R + row) * 8 + 4));
+#pragma unroll 8
+    for (int c = 0; c < n; ++c) {
+      const uint64_t ms = ld64(pr, off(c));
+      const float mc = __uint_as_float((uint32_t)ms), sc = __uint_as_float((uint32_t)(ms >> 32));
       if (mc != -INFINITY) sum += (double)sc * exp2((double)mc - (double)mx);
     }
   }
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o, 64);
-  if (lane == 0) {
-    const float lse2 = (mx == -INFINITY || !(sum > 0.0)) ? -INFINITY : (float)((double)mx + log2(sum));
-    const rsrc_t lr = make_rsrc(a.lse2, (uint64_t)nrows * sizeof(float));
-    stf(lr, (uint32_t)(idx * 4), lse2);
-  }
+  const float lse2 = (mx == -INFINITY || !(sum > 0.0)) ? -INFINITY : (float)((double)mx + log2(sum));
+  const rsrc_t lr = make_rsrc(a.lse2 + seg * a.R, (uint64_t)a.R * sizeof(float));
+  stf(lr, (uint32_t)row * 4u, lse2);
 }
 
 // Pass 2: window-summed probabilities of every scored key --------------------
@@ -528,9 +525,7 @@ static hipError_t launch_scores_t(const CompressArgs& a, hipStream_t st) {
   const dim3 sblk(kScoreBlock);
   if (a.window_lse == nullptr) {
     SGDKV_LAUNCH("score_lse", (lse_kernel<T, D, RBW>), dim3(a.n_lse_chunks, a.B * a.Hkv), sblk, st, a);
-    const int64_t nrows = (int64_t)a.B * a.Hkv * a.R;
-    const int64_t rows_per_block = kBlock / 64;
-    SGDKV_LAUNCH("lse_merge", lse_merge_kernel, dim3((unsigned)((nrows + rows_per_block - 1) / rows_per_block)),
+    SGDKV_LAUNCH("lse_merge", lse_merge_kernel, dim3((unsigned)((a.R + kBlock - 1) / kBlock), a.B * a.Hkv),
                  dim3(kBlock), st, a);
   }
   if (a.n_col_chunks > 0) {
