@@ -356,11 +356,10 @@ __global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
   }
 }
 
-// Merge the per-chunk partials of every window row in fp64: one wave per row,
-// lanes stride over the chunks, fixed-order shuffle trees for max and sum.
+// Merge the per-chunk partials of every window row: one thread per row of segment
+// blockIdx.y takes the maximum of the chunk references, then adds the rescaled sums in
+// chunk order, in fp64. Neighbouring threads read neighbouring rows, so the loads coalesce.
 __global__ __launch_bounds__(kBlock) void lse_merge_kernel(CompressArgs a) {
-  // one thread per window row of segment blockIdx.y; the row's chunk partials are merged in
-  // chunk order (max first, then the rescaled sums in fp64)
   const int64_t seg = blockIdx.y;
   const int row = blockIdx.x * kBlock + threadIdx.x;
   if (row >= a.R) return;
