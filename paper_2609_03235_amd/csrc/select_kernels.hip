@@ -160,10 +160,13 @@ __device__ __forceinline__ SegState derive_state(const CompressArgs& a, int seg,
 //   HIST: histogram of digit PASS over the candidates [s, C-W) of the range
 //     whose higher digits match the prefix found so far, added to the
 //     segment's histogram with integer atomics.
-template <int PASS, bool POOL, bool HIST>
+//   KP: the pooling width when it is one of the widths built in (1..15, odd): each thread
+//     then pools four consecutive positions from values it reads once with 16-byte LDS
+//     loads (same additions in the same order as the general loop); 0: any width.
+template <int PASS, bool POOL, bool HIST, int KP = 0>
 __global__ __launch_bounds__(kBlock) void radix_pass_kernel(CompressArgs a) {
   __shared__ uint32_t lh[256 + 8];
-  __shared__ float win[POOL ? kHistChunkMax + 2 * kPoolHalo : 1];
+  __shared__ __attribute__((aligned(16))) float win[POOL ? kHistChunkMax + 2 * kPoolHalo + 16 : 1];
   const int seg = blockIdx.y, tid = threadIdx.x;
   const SegState st = derive_state<PASS>(a, seg, lh);
   const bool hist = HIST && st.rem != 0;  // uniform per segment: nothing (left) to choose otherwise
@@ -195,6 +198,53 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(CompressArgs a) {
       }
     }
     __syncthreads();
+    if constexpr (KP > 0) {
+      // positions j .. j+3 need win[j - j0 .. j - j0 + 3 + 2R]: NV 16-byte reads from a
+      // 16-byte aligned start (the last few values are read past the staged ones and unused)
+      constexpr int R = (KP - 1) / 2, NV = (4 + 2 * R + 3) / 4;
+      const bool aligned = (((int64_t)seg * a.n_scored) & 3) == 0;  // pooled rows start 16-byte aligned
+      for (int64_t jb = j0; jb < j1; jb += 4 * kBlock) {  // uniform trip count
+        const int64_t j = jb + 4 * tid;
+        float x[4 * NV];
+#pragma unroll
+        for (int q = 0; q < NV; ++q) {
+          const f32x4 w4 = *reinterpret_cast<const f32x4*>(win + (j - j0) + 4 * q);
+          x[4 * q] = w4.x;
+          x[4 * q + 1] = w4.y;
+          x[4 * q + 2] = w4.z;
+          x[4 * q + 3] = w4.w;
+        }
+        float v[4];
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          float sum = 0.f;
+#pragma unroll
+          for (int t = 0; t <= 2 * R; ++t) sum += x[p + t];
+          v[p] = sum / fk;
+        }
+        if (aligned && j + 3 < j1) {
+          u32x4 o;
+          o.x = __float_as_uint(v[0]);
+          o.y = __float_as_uint(v[1]);
+          o.z = __float_as_uint(v[2]);
+          o.w = __float_as_uint(v[3]);
+          st128(pr, (uint32_t)(j * 4), o);
+        } else {
+#pragma unroll
+          for (int p = 0; p < 4; ++p)
+            if (j + p < j1) stf(pr, (uint32_t)((j + p) * 4), v[p]);
+        }
+        if (hist) {
+#pragma unroll
+          for (int p = 0; p < 4; ++p) {
+            const uint32_t bits = __float_as_uint(v[p]);
+            const int64_t jp = j + p;
+            hist_add(lh, (bits >> shift) & 255u,
+                     jp < j1 && jp >= cbeg && jp < cend && (bits & st.mask) == st.prefix);
+          }
+        }
+      }
+    } else
     for (int64_t jb = j0; jb < j1; jb += kBlock) {  // uniform trip count: hist_add needs the whole wave
       const int64_t j = jb + tid;
       const bool in = j < j1;
@@ -424,6 +474,24 @@ __global__ __launch_bounds__(kBlock) void copy_rows_kernel(CompressArgs a) {
   }
 }
 
+// Pooling (+ the digit-0 histogram) with the width built in where one is.
+template <bool HIST>
+static void launch_pool(const CompressArgs& a, dim3 grid, hipStream_t st) {
+  const dim3 blk(kBlock);
+  const char* name = HIST ? "pool_radix_hist" : "pool";
+  switch (a.kp) {
+    case 1: SGDKV_LAUNCH(name, (radix_pass_kernel<0, true, HIST, 1>), grid, blk, st, a); break;
+    case 3: SGDKV_LAUNCH(name, (radix_pass_kernel<0, true, HIST, 3>), grid, blk, st, a); break;
+    case 5: SGDKV_LAUNCH(name, (radix_pass_kernel<0, true, HIST, 5>), grid, blk, st, a); break;
+    case 7: SGDKV_LAUNCH(name, (radix_pass_kernel<0, true, HIST, 7>), grid, blk, st, a); break;
+    case 9: SGDKV_LAUNCH(name, (radix_pass_kernel<0, true, HIST, 9>), grid, blk, st, a); break;
+    case 11: SGDKV_LAUNCH(name, (radix_pass_kernel<0, true, HIST, 11>), grid, blk, st, a); break;
+    case 13: SGDKV_LAUNCH(name, (radix_pass_kernel<0, true, HIST, 13>), grid, blk, st, a); break;
+    case 15: SGDKV_LAUNCH(name, (radix_pass_kernel<0, true, HIST, 15>), grid, blk, st, a); break;
+    default: SGDKV_LAUNCH(name, (radix_pass_kernel<0, true, HIST, 0>), grid, blk, st, a); break;
+  }
+}
+
 hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t st) {
   const int nseg = a.B * a.Hkv;
   const dim3 blk(kBlock);
@@ -431,10 +499,10 @@ hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t st
   const dim3 hgrid(a.n_hist_chunks, nseg);
   const bool cands = a.C - a.s - a.W > 0;
   if (scores_only || !cands) {
-    if (a.n_hist_chunks > 0) SGDKV_LAUNCH("pool", (radix_pass_kernel<0, true, false>), hgrid, blk, st, a);
+    if (a.n_hist_chunks > 0) launch_pool<false>(a, hgrid, st);
     if (scores_only) return hipGetLastError();
   } else {
-    SGDKV_LAUNCH("pool_radix_hist", (radix_pass_kernel<0, true, true>), hgrid, blk, st, a);
+    launch_pool<true>(a, hgrid, st);
     SGDKV_LAUNCH("radix_hist", (radix_pass_kernel<1, false, true>), hgrid, blk, st, a);
     SGDKV_LAUNCH("radix_hist", (radix_pass_kernel<2, false, true>), hgrid, blk, st, a);
     SGDKV_LAUNCH("radix_hist", (radix_pass_kernel<3, false, true>), hgrid, blk, st, a);

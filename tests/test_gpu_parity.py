@@ -173,11 +173,13 @@ def test_tiny_ragged_batches(B, C, budget_kind):
     _decode_on_oracle_cache(orc, t["q"], 2, torch.float32, 1e-5, "ragged")
 
 
-@pytest.mark.parametrize("kp", [1, 129, 131, 301])
+@pytest.mark.parametrize("kp", [1, 3, 15, 17, 129, 131, 301])
 def test_pool_kernel_widths(kp):
-    """Pooling radii up to 64 are staged in LDS with their halo; wider ones read the column sums
-    from global memory. Both sum the taps in the same order and must match the oracle."""
-    B, C = 2, 1500
+    """Pooling radii up to 64 are staged in LDS with their halo (widths 1..15 pool four positions
+    per thread from 16-byte LDS reads, wider ones one position per thread); radii past 64 read
+    the column sums from global memory. All sum the taps in the same order and must match the
+    oracle. An odd number of scored keys leaves the second segment's pooled row unaligned."""
+    B, C = 2, 1500 + kp % 4
     wl, t = _tiny_inputs(B=B, C=C, seed=kp)
     s, W, w = 4, 32, wl.obs_window
     rng = np.random.Generator(np.random.PCG64(kp))
