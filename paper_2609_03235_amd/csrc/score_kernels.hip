@@ -28,6 +28,7 @@
 #include "device_common.h"
 #include "mfma_frag.h"
 #include "sgdkv_internal.h"
+#include "segment_init.h"
 
 // Row blocks per wave the dispatch instantiates: at most 512 rows over all waves.
 #define SGDKV_SCORE_WAVES_MAX_RBW (kMaxGroupRowsMacro / (16 * SGDKV_SCORE_WAVES))
@@ -498,6 +499,7 @@ __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) 
   __shared__ float red[3][kScoreWaves][MAXG ? RBW : 4][col_tile<T>()];
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
+  if (blockIdx.x == 0) init_segment(a, seg);  // histograms and offsets for the selection that follows
   const int64_t key0 = (int64_t)blockIdx.x * a.score_chunk;
   if (key0 >= a.n_scored) return;
   const int64_t key_end = key0 + a.score_chunk < a.n_scored ? key0 + a.score_chunk : a.n_scored;

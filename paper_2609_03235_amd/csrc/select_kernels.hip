@@ -15,7 +15,8 @@
 // else is fixed-order, so results are bitwise reproducible.
 //
 // Kernels (grid y = segment b*Hkv + h):
-//   select_init    zero the histograms, write the offsets
+//   select_init    zero the histograms, write the offsets (when the column-sum pass,
+//                  which otherwise does it, does not run)
 //   radix_pass<p>  digit-p histogram of candidates matching the digits
 //                  before it (each workgroup picks those from the earlier
 //                  histograms itself); pass 0 also pools:
@@ -28,6 +29,7 @@
 
 #include "device_common.h"
 #include "sgdkv_internal.h"
+#include "segment_init.h"
 
 namespace sgdkv {
 
@@ -91,19 +93,8 @@ __device__ __forceinline__ uint32_t block_rank(bool flag, uint32_t* wtot, uint32
 
 }  // namespace
 
-__global__ __launch_bounds__(kBlock) void select_init_kernel(CompressArgs a, int write_offsets) {
-  const int seg = blockIdx.x;
-  const int b = seg / a.Hkv, h = seg % a.Hkv;
-  const int nseg = a.B * a.Hkv;
-  const rsrc_t hr = make_rsrc(a.hist + (int64_t)seg * 4 * 256, 4 * 256 * 4);
-#pragma unroll
-  for (int p = 0; p < 4; ++p) st32(hr, (p * 256 + threadIdx.x) * 4, 0u);
-  if (threadIdx.x == 0 && write_offsets) {
-    const rsrc_t orr = make_rsrc(a.offsets, (uint64_t)(nseg + 1) * 8);
-    st64(orr, (uint32_t)seg * 8, (uint64_t)((int64_t)b * a.T_layer + a.prefix[h]));
-    if (seg == nseg - 1) st64(orr, (uint32_t)nseg * 8, (uint64_t)((int64_t)a.B * a.T_layer));
-  }
-}
+// Only when no column-sum pass ran (no scored keys): that pass otherwise does this set-up.
+__global__ __launch_bounds__(kBlock) void select_init_kernel(CompressArgs a) { init_segment(a, blockIdx.x); }
 
 // The radix state after digits 0 .. NPASS-1: every digit is picked from its
 // histogram (complete once the pass that built it has ended) as the unique
@@ -495,7 +486,7 @@ static void launch_pool(const CompressArgs& a, dim3 grid, hipStream_t st) {
 hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t st) {
   const int nseg = a.B * a.Hkv;
   const dim3 blk(kBlock);
-  SGDKV_LAUNCH("select_init", select_init_kernel, dim3(nseg), blk, st, a, scores_only ? 0 : 1);
+  if (a.n_col_chunks == 0) SGDKV_LAUNCH("select_init", select_init_kernel, dim3(nseg), blk, st, a);
   const dim3 hgrid(a.n_hist_chunks, nseg);
   const bool cands = a.C - a.s - a.W > 0;
   if (scores_only || !cands) {
