@@ -101,11 +101,12 @@ def _check_gather(res, k, v, budgets):
 
 
 def _compress_both(q_win, k, v, budgets, *, kp, s, W, window_lse=None, orc_lse=None, agg=0, qhead_scores=None,
-                   win0=None):
+                   win0=None, gather_stream=None):
     w = q_win.shape[2]
     res = sg.compress_layer(q_win, k, v, budgets, pool_kernel=kp, b_sink=s, b_window=W, window_lse=window_lse,
-                            group_agg=agg, qhead_scores=qhead_scores, window_pos=-1 if win0 is None else win0)
-    torch.cuda.synchronize()
+                            group_agg=agg, qhead_scores=qhead_scores, window_pos=-1 if win0 is None else win0,
+                            gather_stream=gather_stream)
+    torch.cuda.synchronize()  # waits for the gather stream too
     orc = oracle.compress(_f64(q_win), _f64(k), _f64(v), budgets, w=w, kp=kp, s=s, W=W, lse=orc_lse, agg=agg,
                           qhead_scores=qhead_scores, win0=win0)
     return res, orc
@@ -270,11 +271,12 @@ def test_window_placement(case):
     _check_gather(res, t["k"], t["v"], budgets)
 
 
-@pytest.mark.parametrize("seed", range(12))
+@pytest.mark.parametrize("seed", range(24))
 def test_random_shapes(seed):
     """Seeded random shapes against the oracle: batch, heads and group size, head dim, dtype,
     window length and placement, sink/window sizes, pooling width and budgets (empty and full
-    middles included), so that chunk, tile and selection boundaries fall in varied places."""
+    middles included), so that chunk, tile and selection boundaries fall in varied places. Odd
+    seeds copy the kept rows on a second stream (the capped, grid-stride gather)."""
     rng = np.random.Generator(np.random.PCG64(1000 + seed))
     B = int(rng.integers(1, 4))
     Hkv = int(rng.choice([1, 2, 4]))
@@ -301,7 +303,8 @@ def test_random_shapes(seed):
     _announce(f"random shapes seed={seed}: B={B} Hq={Hq} Hkv={Hkv} d={d} {dtype} w={w} C={C} s={s} W={W} "
               f"kp={kp} {placement} win0={win0} budgets={budgets.tolist()}")
     res, orc = _compress_both(tt["q_win"], tt["k"], tt["v"], budgets, kp=kp, s=s, W=W,
-                              win0=None if placement == "aware" else win0)
+                              win0=None if placement == "aware" else win0,
+                              gather_stream=torch.cuda.Stream(device=DEV) if seed % 2 else None)
     rtol = _score_rtol(tt["q_win"])
     _check_scores(res["scores"].cpu().numpy(), orc["pooled"], f"random {seed}", rtol=rtol)
     _check_kept(res, orc, tt["q_win"].shape, C, w, s, W, budgets, f"random {seed}",
