@@ -104,7 +104,7 @@ KERNEL_OF = {"score_lse": "lse_kernel", "score_colsum": "colsum_kernel", "gather
              "decode_split": "decode_split_kernel"}
 SOURCE_OF = {"score_lse": "score_kernels.hip", "score_colsum": "score_kernels.hip",
              "gather": "select_kernels.hip", "decode_split": "decode_kernels.hip"}
-SHARED_SOURCES = ("device_common.h", "mfma_frag.h", "sgdkv_internal.h")
+SHARED_SOURCES = ("device_common.h", "mfma_frag.h", "sgdkv_internal.h", "segment_init.h")
 
 
 def source_sha(name):
@@ -151,21 +151,26 @@ def summarize_traffic(fetch_csv, write_csv, args):
     import statistics
 
     def per_kernel(path, counter):
-        vals = {}
+        vals, calib = {}, []
         with open(path, newline="") as fh:
             for row in csv.DictReader(fh):
-                if row["Counter_Name"] == counter:
-                    vals.setdefault(row["Kernel_Name"], []).append(float(row["Counter_Value"]))
-        return vals
+                if row["Counter_Name"] != counter:
+                    continue
+                name, v = row["Kernel_Name"], float(row["Counter_Value"])
+                vals.setdefault(name, []).append(v)
+                if "elementwise_kernel" in name and "MulFunctor" in name:
+                    calib.append((int(row["Dispatch_Id"]), v))
+        return vals, calib
 
-    fetch, write = per_kernel(fetch_csv, "FETCH_SIZE"), per_kernel(write_csv, "WRITE_SIZE")
+    (fetch, fcal), (write, wcal) = per_kernel(fetch_csv, "FETCH_SIZE"), per_kernel(write_csv, "WRITE_SIZE")
     kib = args.calibrate_copy_mib * 1024.0
 
-    def copy_median(vals):
-        xs = [v for n, vs in vals.items() if "elementwise_kernel" in n for v in vs if v > 0.5 * kib]
-        return statistics.median(xs) if xs else None
+    def copy_median(calib):
+        # the three calibration copies (torch.mul by 1.0) are the first multiplications the run makes
+        xs = [v for _, v in sorted(calib)[:3]]
+        return statistics.median(xs) if len(xs) == 3 and min(xs) > 0.25 * kib else None
 
-    cf, cw = copy_median(fetch), copy_median(write)
+    cf, cw = copy_median(fcal), copy_median(wcal)
     if not kib or cf is None or cw is None:
         sys.exit("no calibration copy found: run the counter passes with --calibrate-copy-mib")
     out = dict(workload=args.workload, ratio=args.ratio, unit="KiB per dispatch",
