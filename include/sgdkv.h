@@ -214,10 +214,10 @@ sgdkv_status sgdkv_compress_layer(const sgdkv_compress_desc* desc, const int64_t
  * gather_stream: NULL (or equal to `stream`): all work goes on `stream`.
  *   Otherwise the last step, copying the kept K and V rows into k_out and
  *   v_out, is enqueued on gather_stream, ordered after this call's selection
- *   on `stream` by an event the library records, and runs on about half of
- *   the compute units, so that it overlaps the work the caller enqueues next
- *   on `stream` (for example the next layer's window scoring, which leaves
- *   memory bandwidth unused). k_out and v_out are then complete only when
+ *   on `stream` by an event the library records, as a grid of half as many
+ *   workgroups as the device has compute units, so that it fits beside the
+ *   work the caller enqueues next on `stream` (for example the next layer's
+ *   window scoring, which leaves memory bandwidth unused). k_out and v_out are then complete only when
  *   gather_stream reaches this point, and k and v must stay unchanged until
  *   then; kept_pos_out, offsets_out and scores_out are complete on `stream`
  *   as usual. The copy does not touch the workspace, which is free for the
