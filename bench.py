@@ -310,7 +310,7 @@ def main():
     log(f"[bench] inputs ready in {time.perf_counter() - t0:.1f}s: {wl.name}, total budget {total} rows "
         f"({args.ratio:.0%}), {L} layers x {B} sequences")
 
-    def step():
+    def step(gs=gstream):
         # S0 on the host, then every layer's compression, then every layer's decode
         allocate()
         for l in range(L):
@@ -318,9 +318,9 @@ def main():
             sg.compress_layer(t["q_win"], t["k"], t["v"], budgets[l], pool_kernel=kp, b_sink=s, b_window=W,
                               window_lse=lse_in[l], group_agg=agg, qhead_scores=qscores[l], window_pos=win0,
                               out=outs[l], workspace=ws_c, stream=stream,
-                              gather_stream=gstream if l < L - 1 else None)  # nothing follows the last
-        if gstream is not None and L > 1:
-            stream.wait_stream(gstream)  # every layer's compressed cache is complete before decode
+                              gather_stream=gs if l < L - 1 else None)  # nothing follows the last
+        if gs is not None and L > 1:
+            stream.wait_stream(gs)  # every layer's compressed cache is complete before decode
         for l in range(L):
             o = outs[l]
             kn = vn = None
@@ -360,6 +360,18 @@ def main():
     prof_ms_per_step = ev0.elapsed_time(ev1) / args.steps
     kern = sg.profile_read()
 
+    # ------------------------------------------------------------ untimed: every kernel on one stream
+    # (only with a gather stream: the same kernels without overlap, for the serial roofline)
+    kern_serial = None
+    if gstream is not None and L > 1:
+        sg.profile_reset()
+        sg.profile_enable(True)
+        for _ in range(args.steps):
+            step(gs=None)
+        torch.cuda.synchronize()
+        sg.profile_enable(False)
+        kern_serial = sg.profile_read()
+
     # ------------------------------------------------------------ algorithmic work per launch
     T_layers = budgets.sum(axis=1)
     T_mean = float(T_layers.mean())
@@ -379,7 +391,7 @@ def main():
                              avg_us=1e3 * ms / count, share=ms / max(1e-9, sum(v[1] for v in kern.values())))
     dominant = max(kern.items(), key=lambda kv: kv[1][1])[0]
 
-    def roof(name):
+    def roof(name, kern=kern):
         count, ms = kern[name]
         bound, amount, unit = work[name]
         avg_s = ms / count / 1e3
@@ -398,6 +410,11 @@ def main():
                     work_per_launch=amount, **extra)
 
     roofline = roof(dominant) if dominant in work else None
+    roofline_serial = None
+    if kern_serial is not None and dominant in work and dominant in kern_serial:
+        roofline_serial = dict(roof(dominant, kern_serial),
+                               note="same kernel, every kernel on one stream (an extra untimed run); "
+                                    "roofline above is the timed run, where the gathers overlap the scoring")
     decode = roof("decode_split") if "decode_split" in kern else None
     dec_ms = (kern.get("decode_split", (0, 0))[1] + kern.get("decode_combine", (0, 0))[1]) / args.steps
     dec_bytes = work["decode_split"][1] * L
@@ -453,7 +470,8 @@ def main():
         decode=dict(gbps=round(dec_bytes / (dec_ms / 1e3) / 1e9, 1) if dec_ms > 0 else None,
                     frac_of_peak=round(dec_bytes / (dec_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4) if dec_ms > 0 else None,
                     ms_per_step=round(dec_ms, 4), split_kernel=decode),
-        roofline=roofline, kernels=kernels, profiled_ms_per_step=round(prof_ms_per_step, 4),
+        roofline=roofline, roofline_serial=roofline_serial, kernels=kernels,
+        profiled_ms_per_step=round(prof_ms_per_step, 4),
         wall_ms_per_step=round(wall_ms, 4), cpu_baseline=cpu,
     )
     print(json.dumps(line), flush=True)
