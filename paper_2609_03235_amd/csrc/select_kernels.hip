@@ -235,25 +235,26 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(CompressArgs a) {
           }
         }
       }
-    } else
-    for (int64_t jb = j0; jb < j1; jb += kBlock) {  // uniform trip count: hist_add needs the whole wave
-      const int64_t j = jb + tid;
-      const bool in = j < j1;
-      float v = 0.f;
-      if (in) {
-        float sum = 0.f;
-        if (staged) {
-          const float* wp = win + (j - j0);
-          for (int t = 0; t <= 2 * r; ++t) sum += wp[t];
-        } else {
-          for (int t = -r; t <= r; ++t) sum += ldf(cr, (uint32_t)((j + t) * 4));
+    } else {
+      for (int64_t jb = j0; jb < j1; jb += kBlock) {  // uniform trip count: hist_add needs the whole wave
+        const int64_t j = jb + tid;
+        const bool in = j < j1;
+        float v = 0.f;
+        if (in) {
+          float sum = 0.f;
+          if (staged) {
+            const float* wp = win + (j - j0);
+            for (int t = 0; t <= 2 * r; ++t) sum += wp[t];
+          } else {
+            for (int t = -r; t <= r; ++t) sum += ldf(cr, (uint32_t)((j + t) * 4));
+          }
+          v = sum / fk;
+          stf(pr, (uint32_t)(j * 4), v);
         }
-        v = sum / fk;
-        stf(pr, (uint32_t)(j * 4), v);
-      }
-      if (hist) {
-        const uint32_t bits = __float_as_uint(v);
-        hist_add(lh, (bits >> shift) & 255u, in && j >= cbeg && j < cend && (bits & st.mask) == st.prefix);
+        if (hist) {
+          const uint32_t bits = __float_as_uint(v);
+          hist_add(lh, (bits >> shift) & 255u, in && j >= cbeg && j < cend && (bits & st.mask) == st.prefix);
+        }
       }
     }
   } else {
@@ -434,34 +435,34 @@ __global__ __launch_bounds__(kBlock) void copy_rows_kernel(CompressArgs a) {
   static_assert(PER >= 1 && (kCopyRows * V16) % kBlock == 0, "copy tile must split evenly");
   const int64_t items = (int64_t)a.copy_blocks * a.B * a.Hkv;
   for (int64_t item = blockIdx.x; item < items; item += gridDim.x) {
-  const int seg = (int)(item / a.copy_blocks), b = seg / a.Hkv, h = seg % a.Hkv;
-  const int64_t seg_len = a.prefix[h + 1] - a.prefix[h];
-  const int64_t row0 = (item % a.copy_blocks) * kCopyRows;
-  if (row0 >= seg_len) continue;  // uniform per workgroup
-  const int64_t seg_off = (int64_t)b * a.T_layer + a.prefix[h];
-  const rsrc_t kp = make_rsrc(a.kept_pos + seg_off, (uint64_t)seg_len * 4);
-  const rsrc_t ko = make_rsrc(static_cast<char*>(a.k_out) + seg_off * RB, (uint64_t)seg_len * RB);
-  const rsrc_t vo = make_rsrc(static_cast<char*>(a.v_out) + seg_off * RB, (uint64_t)seg_len * RB);
-  const rsrc_t ki = make_rsrc(static_cast<const char*>(a.k) + (int64_t)seg * a.C * RB, (uint64_t)a.C * RB);
-  const rsrc_t vi = make_rsrc(static_cast<const char*>(a.v) + (int64_t)seg * a.C * RB, (uint64_t)a.C * RB);
-  u32x4 kx[PER], vx[PER];
-  uint32_t dst[PER];
+    const int seg = (int)(item / a.copy_blocks), b = seg / a.Hkv, h = seg % a.Hkv;
+    const int64_t seg_len = a.prefix[h + 1] - a.prefix[h];
+    const int64_t row0 = (item % a.copy_blocks) * kCopyRows;
+    if (row0 >= seg_len) continue;  // uniform per workgroup
+    const int64_t seg_off = (int64_t)b * a.T_layer + a.prefix[h];
+    const rsrc_t kp = make_rsrc(a.kept_pos + seg_off, (uint64_t)seg_len * 4);
+    const rsrc_t ko = make_rsrc(static_cast<char*>(a.k_out) + seg_off * RB, (uint64_t)seg_len * RB);
+    const rsrc_t vo = make_rsrc(static_cast<char*>(a.v_out) + seg_off * RB, (uint64_t)seg_len * RB);
+    const rsrc_t ki = make_rsrc(static_cast<const char*>(a.k) + (int64_t)seg * a.C * RB, (uint64_t)a.C * RB);
+    const rsrc_t vi = make_rsrc(static_cast<const char*>(a.v) + (int64_t)seg * a.C * RB, (uint64_t)a.C * RB);
+    u32x4 kx[PER], vx[PER];
+    uint32_t dst[PER];
 #pragma unroll
-  for (int u = 0; u < PER; ++u) {
-    const int x = threadIdx.x + u * kBlock;
-    const int r = x / V16, c16 = x % V16;
-    const int64_t row = row0 + r;  // rows past the segment read position 0 and store out of range
-    const uint32_t pos = ld32(kp, (uint32_t)(row * 4));
-    const uint32_t src = pos * RB + c16 * 16;
-    dst[u] = (uint32_t)(row * RB + c16 * 16);
-    kx[u] = ld128(ki, src);
-    vx[u] = ld128(vi, src);
-  }
+    for (int u = 0; u < PER; ++u) {
+      const int x = threadIdx.x + u * kBlock;
+      const int r = x / V16, c16 = x % V16;
+      const int64_t row = row0 + r;  // rows past the segment read position 0 and store out of range
+      const uint32_t pos = ld32(kp, (uint32_t)(row * 4));
+      const uint32_t src = pos * RB + c16 * 16;
+      dst[u] = (uint32_t)(row * RB + c16 * 16);
+      kx[u] = ld128(ki, src);
+      vx[u] = ld128(vi, src);
+    }
 #pragma unroll
-  for (int u = 0; u < PER; ++u) {
-    st128(ko, dst[u], kx[u]);
-    st128(vo, dst[u], vx[u]);
-  }
+    for (int u = 0; u < PER; ++u) {
+      st128(ko, dst[u], kx[u]);
+      st128(vo, dst[u], vx[u]);
+    }
   }
 }
 
