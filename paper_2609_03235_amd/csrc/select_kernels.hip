@@ -507,7 +507,8 @@ hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t st
 hipError_t launch_gather(const CompressArgs& a, int max_blocks, hipStream_t st) {
   const int64_t items = (int64_t)a.copy_blocks * a.B * a.Hkv;
   if (items == 0) return hipSuccess;
-  const unsigned grid = (unsigned)(max_blocks > 0 ? std::min<int64_t>(items, max_blocks) : items);
+  // a full grid is capped too (the loop covers the rest), keeping blocks x threads below 2^32
+  const unsigned grid = (unsigned)std::min<int64_t>(items, max_blocks > 0 ? max_blocks : (1 << 20));
   const dim3 blk(kBlock);
   switch (a.D * (a.dtype == 1 ? 2 : 4)) {
     case 128: SGDKV_LAUNCH("gather", copy_rows_kernel<128>, dim3(grid), blk, st, a); break;
