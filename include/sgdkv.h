@@ -12,8 +12,11 @@
  *
  * Conventions shared by every entry point:
  *   - Every function returns an sgdkv_status; no exception crosses the ABI.
- *     On any error nothing has been written to any output and nothing has
- *     been enqueued; sgdkv_last_error() describes the failure.
+ *     Arguments are checked before anything is enqueued: on an
+ *     INVALID_ARG, UNSUPPORTED or WORKSPACE error nothing has been written
+ *     and nothing enqueued. SGDKV_ERR_HIP from a kernel launch partway
+ *     through a call can leave the call's earlier kernels enqueued (their
+ *     outputs are then undefined). sgdkv_last_error() describes the failure.
  *   - The caller owns all memory. The library never allocates device memory;
  *     scratch space comes from a caller buffer sized by *_workspace_size.
  *   - Device work is enqueued on `stream` (a hipStream_t passed as void*;

@@ -565,30 +565,36 @@ sgdkv_status sgdkv_compress_layer_ex(const sgdkv_compress_desc* desc, const sgdk
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = hipGetLastError();  // clear a stale error left by earlier, unrelated work
   (void)e;
-  e = sgdkv::launch_scores(a, st);
-  if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "score kernels: %s", hipGetErrorString(e));
-  e = sgdkv::launch_select(a, scores_only, st);
-  if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "selection kernels: %s", hipGetErrorString(e));
-  if (scores_only) return ok();
+  // With a gather stream, the gather waits for the selection through an event, then runs on
+  // its own stream with half as many workgroups as the device has compute units, so that it
+  // fits beside whatever the caller enqueues next on `stream`. The event is created before
+  // anything is enqueued.
   hipStream_t gs = static_cast<hipStream_t>(o.gather_stream);
-  if (gs && gs != st) {
-    // The gather waits for the selection through an event, then runs on its own stream with
-    // half as many workgroups as the device has compute units, so that it fits beside
-    // whatever the caller enqueues next on `stream`.
-    hipEvent_t ev = nullptr;
+  const bool side = !scores_only && gs && gs != st;
+  hipEvent_t ev = nullptr;
+  if (side) {
     e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
-    if (e == hipSuccess) {
-      e = hipEventRecord(ev, st);
-      if (e == hipSuccess) e = hipStreamWaitEvent(gs, ev, 0);
-      const hipError_t e2 = hipEventDestroy(ev);  // released once the recorded work completes
-      if (e == hipSuccess) e = e2;
-    }
-    if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "ordering the gather stream: %s", hipGetErrorString(e));
-    e = sgdkv::launch_gather(a, std::max(1, cus / 2), gs);
+    if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "hipEventCreateWithFlags: %s", hipGetErrorString(e));
+  }
+  auto release = [&]() {
+    if (ev) (void)hipEventDestroy(ev);  // released once the recorded work completes
+  };
+  e = sgdkv::launch_scores(a, st);
+  if (e == hipSuccess) e = sgdkv::launch_select(a, scores_only, st);
+  if (e != hipSuccess) {
+    release();
+    return fail(SGDKV_ERR_HIP, "score or selection kernels: %s", hipGetErrorString(e));
+  }
+  if (scores_only) return ok();
+  if (side) {
+    e = hipEventRecord(ev, st);
+    if (e == hipSuccess) e = hipStreamWaitEvent(gs, ev, 0);
+    release();
+    if (e == hipSuccess) e = sgdkv::launch_gather(a, std::max(1, cus / 2), gs);
   } else {
     e = sgdkv::launch_gather(a, 0, st);
   }
-  if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "gather kernel: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "gather: %s", hipGetErrorString(e));
   return ok();
 }
 
