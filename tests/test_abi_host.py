@@ -222,13 +222,13 @@ def test_compress_validation():
     assert _compress(_desc(), good, ws=None) == sg.ERR_WORKSPACE
 
 
-def _compress_ex(desc, agg, qs, budgets=(512, 512), window_pos=-1, reserved=0):
+def _compress_ex(desc, agg, qs, budgets=(512, 512), window_pos=-1, reserved=0, gather_stream=None):
     lib = sg.load_library()
     need = ctypes.c_size_t(0)
     lib.sgdkv_compress_workspace_size(ctypes.byref(desc), ctypes.byref(need))
     b = np.ascontiguousarray(np.asarray(budgets, dtype=np.int64))
     q = None if qs is None else np.ascontiguousarray(np.asarray(qs, dtype=np.float64))
-    opts = sg.CompressOpts(agg, reserved, None if q is None else q.ctypes.data, window_pos)
+    opts = sg.CompressOpts(agg, reserved, None if q is None else q.ctypes.data, window_pos, gather_stream)
     return lib.sgdkv_compress_layer_ex(
         ctypes.byref(desc), ctypes.byref(opts), sg._np_ptr(b), FAKE, FAKE, FAKE, None,
         FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need.value, None)
@@ -255,6 +255,12 @@ def test_compress_options_validation():
         msg = sg.load_library().sgdkv_last_error().decode()
         assert word in msg, msg
     assert _compress_ex(_desc(), 0, None, reserved=1) == sg.ERR_INVALID_ARG
+    # with a gather stream too, arguments are checked before any stream is touched (a bogus
+    # handle here would fail if it were used)
+    bogus = 0x7F0000001000
+    assert _compress_ex(_desc(), 4, None, gather_stream=bogus) == sg.ERR_INVALID_ARG
+    assert _compress_ex(_desc(), 0, None, budgets=(512, 9999), gather_stream=bogus) == sg.ERR_INVALID_ARG
+    assert "layer_budgets" in sg.load_library().sgdkv_last_error().decode()
     # a window after the prompt needs no recent rows at all: validation passes, then no device
     if not _gpu():
         assert _compress_ex(_desc(b_window=0, b_sink=4), 0, None, budgets=(4, 4), window_pos=2048) == sg.ERR_HIP
