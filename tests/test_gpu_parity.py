@@ -393,6 +393,45 @@ def test_decode_edge_segments_and_bf16_output():
     assert np.all(np.abs(ob - ref) <= 2e-2 + ulp)
 
 
+@pytest.mark.parametrize("dtype,G", [(torch.bfloat16, 16), (torch.bfloat16, 12), (torch.float32, 16),
+                                     (torch.float32, 9)])
+def test_decode_large_groups(dtype, G):
+    """Groups of 9..16 query heads per KV head take the 16-row decode instantiation (the G query
+    rows padded to 16 in the logit MFMA, 16 heads' partial sums per lane)."""
+    rng = np.random.Generator(np.random.PCG64(40 + G))
+    d, Hkv, B = 128, 2, 2
+    Hq = G * Hkv
+    lens = [700, 0, 33, 1500]
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    kc = torch.from_numpy(rng.standard_normal((offs[-1], d)) * 2).to(dtype).to(DEV)
+    vc = torch.from_numpy(rng.standard_normal((offs[-1], d))).to(dtype).to(DEV)
+    q = torch.from_numpy(rng.standard_normal((B, Hq, d))).to(dtype).to(DEV)
+    _announce(f"decode large groups {dtype} G={G}")
+    out, lse = sg.decode_attention(q, kc, vc, torch.from_numpy(offs).to(DEV), offs, Hkv, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref, ref_lse = oracle.decode(_f64(q), _f64(kc), _f64(vc), offs, Hkv)
+    atol = 2e-2 if dtype == torch.bfloat16 else 1e-5
+    assert np.abs(out.cpu().numpy() - ref).max() <= atol
+    fin = np.isfinite(ref_lse)
+    assert np.abs(lse.cpu().numpy()[fin] - ref_lse[fin]).max() <= max(atol, 1e-5)
+    assert np.all(np.isneginf(lse.cpu().numpy()[~fin]))
+
+
+def test_compress_group_of_16():
+    """A KV head with 16 query heads and a 32-row window: 512 window rows, the most one score
+    workgroup holds (four 16-row blocks per wave), then decode with the 16-row instantiation."""
+    B, C, Hq, Hkv, d, w = 1, 2200, 32, 2, 128, 32
+    wl, t = _qwen_small(B, C, Hq=Hq, Hkv=Hkv, d=d, w=w)
+    s, W, kp = 16, 64, 7
+    budgets = np.array([900, 333])
+    _announce(f"group of 16: B={B} C={C} Hq={Hq} Hkv={Hkv} w={w} budgets={budgets.tolist()}")
+    res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=kp, s=s, W=W)
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "g16", rtol=_score_rtol(t["q_win"]))
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "g16", rtol=_score_rtol(t["q_win"]))
+    _check_gather(res, t["k"], t["v"], budgets)
+    _decode_on_oracle_cache(orc, t["q"], Hkv, torch.bfloat16, 2e-2, "g16")
+
+
 def test_decode_fixed_reference_redo():
     """Decode keeps each head's reference fixed at the largest logit of a chunk's first 16 keys and
     reruns the chunk with a running maximum when a sum could overflow. Keys planted later in three
