@@ -298,12 +298,7 @@ def main():
     # the gathers' stream keeps torch's default priority; the gather does not use the workspace
     gstream = None if args.no_gather_stream else torch.cuda.Stream(device=dev)
     ws_c = sg.alloc_workspace(sg.compress_workspace_size(cdesc), dev)
-    offsets_host = []
-    for l in range(L):
-        pre = np.concatenate([[0], np.cumsum(budgets[l])])
-        T = int(budgets[l].sum())
-        offsets_host.append(np.array([b * T + pre[h] for b in range(B) for h in range(Hkv)] + [B * T],
-                                     dtype=np.int64))
+    offsets_host = [sg.segment_offsets(budgets[l], B) for l in range(L)]
     ddesc = sg.decode_desc(layers[0]["q"], Hkv, torch.float32)
     ws_d = sg.alloc_workspace(max(sg.decode_workspace_size(ddesc, oh, n_new) for oh in offsets_host), dev)
     torch.cuda.synchronize()

@@ -82,7 +82,10 @@ sgdkv_status sgdkv_total_from_ratio(double R, int32_t L, int32_t H, int64_t C, i
  * b_sink initial and b_window recent rows; the rest of total_budget,
  * T = total_budget - L*H*(b_sink+b_window), is shared over the middles of
  * length M = C - b_sink - b_window in proportion to the score:
- *   x_h = (sigma_h * T) / sum(sigma)   (all-zero scores: uniform shares).
+ *   x_h = (sigma_h / sum(sigma)) * T   (all-zero scores: uniform shares),
+ * evaluated in fp64 in exactly that order (the quotient first, then the
+ * product; sum(sigma) added in flat layer-major order), since the rounding
+ * decides the integer budgets.
  * mode 0 (default, Algorithm 1): x_h rounded by largest remainder (ties:
  *   larger score, then lower flat index); every middle capped at M; the
  *   excess handed to the remaining heads in descending score order (ties:
@@ -131,6 +134,20 @@ sgdkv_status sgdkv_allocate_budgets_variant(const double* head_scores, const dou
                                             int64_t total_budget, int32_t mode, int32_t variant,
                                             double full_fraction, int64_t* budgets_out);
 
+/* Row offsets of the ragged per-KV-head cache of one layer (host only). The
+ * cache is kept per KV head, before GQA repetition (Appendix A.2): segment
+ * (b, h) holds the b_h kept rows of KV head h of sequence b, segments in
+ * (b, h) order. With T_layer = sum_h layer_budgets[h]:
+ *   offsets_out[b*Hkv + h] = b*T_layer + sum_{h' < h} layer_budgets[h'],
+ *   offsets_out[B*Hkv]     = B*T_layer.
+ * These are the values sgdkv_compress_layer writes to its device offsets_out
+ * for the same budgets; sgdkv_decode_attention takes them as offsets_host.
+ * layer_budgets: host [Hkv] int64 >= 0. offsets_out: host [B*Hkv+1] int64.
+ * Errors (nothing written): batch or num_kv_heads < 1; a negative budget;
+ * B*T_layer beyond 2^62; NULL pointers. */
+sgdkv_status sgdkv_segment_offsets(const int64_t* layer_budgets, int32_t batch, int32_t num_kv_heads,
+                                   int64_t* offsets_out);
+
 /* ------------------------------------------------------------------ */
 /* One layer's compression (device).                                   */
 
@@ -176,7 +193,8 @@ sgdkv_status sgdkv_compress_workspace_size(const sgdkv_compress_desc* desc, size
  *   offsets_out[b*Hkv+h] .. offsets_out[b*Hkv+h+1]-1 in kept order.
  * kept_pos_out: device [B*T_layer] int32 prompt positions of the kept rows.
  * offsets_out: device [B*Hkv+1] int64, offsets[b*Hkv+h] = b*T_layer +
- *   sum_{h'<h} layer_budgets[h'].
+ *   sum_{h'<h} layer_budgets[h'] (sgdkv_segment_offsets gives the same
+ *   values on the host).
  * k_out, v_out, kept_pos_out and offsets_out are either all non-NULL, or
  *   all NULL (scores-only mode: only scores_out is produced).
  * scores_out: optional device [B][Hkv][C-w] fp32 pooled scores (the values

@@ -25,7 +25,8 @@ LIB_PATH = os.path.join(_HERE, "libsgdkv.so")
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, 1, 2, 3, 4
 DTYPE_F32, DTYPE_BF16 = 0, 1
 SYMBOLS = ("sgdkv_last_error", "sgdkv_version", "sgdkv_reduce_query_head_scores", "sgdkv_total_from_ratio",
-           "sgdkv_allocate_budgets", "sgdkv_allocate_budgets_variant", "sgdkv_compress_workspace_size",
+           "sgdkv_allocate_budgets", "sgdkv_allocate_budgets_variant", "sgdkv_segment_offsets",
+           "sgdkv_compress_workspace_size",
            "sgdkv_compress_layer", "sgdkv_compress_layer_ex",
            "sgdkv_decode_workspace_size", "sgdkv_decode_attention", "sgdkv_decode_workspace_size_ex",
            "sgdkv_decode_attention_ex", "sgdkv_append_kv", "sgdkv_profile_enable",
@@ -83,6 +84,7 @@ def load_library():
         "sgdkv_total_from_ratio": [f64, i32, i32, i64, i64, i64, i32, P],
         "sgdkv_allocate_budgets": [P, i32, i32, i64, i64, i64, i64, i32, P],
         "sgdkv_allocate_budgets_variant": [P, P, i32, i32, i64, i64, i64, i64, i32, i32, f64, P],
+        "sgdkv_segment_offsets": [P, i32, i32, P],
         "sgdkv_compress_workspace_size": [P, P],
         "sgdkv_compress_layer": [P, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
         "sgdkv_compress_layer_ex": [P, P, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
@@ -163,6 +165,15 @@ def allocate_budgets_variant(scores, L: int, H: int, C: int, b_sink: int, b_wind
     return out
 
 
+def segment_offsets(layer_budgets, batch: int) -> np.ndarray:
+    """Host copy of the ragged cache's row offsets [batch * Hkv + 1] for one layer's budgets
+    (sgdkv_segment_offsets): the values compress_layer writes to its device offsets."""
+    bud = np.ascontiguousarray(np.asarray(layer_budgets, dtype=np.int64).reshape(-1))
+    out = np.zeros(int(batch) * bud.size + 1, dtype=np.int64)
+    _check(load_library().sgdkv_segment_offsets(_np_ptr(bud), int(batch), bud.size, _np_ptr(out)))
+    return out
+
+
 # ---------------------------------------------------------------- device
 def _dtype_code(t) -> int:
     import torch
@@ -222,7 +233,10 @@ def compress_layer(q_win, k, v, layer_budgets, *, pool_kernel: int, b_sink: int,
     Ipt. aggregation with the layer's per-query-head scores; window_pos places the first window
     row (-1: the last obs_window prompt tokens). gather_stream (optional) takes the copy of the
     kept rows into k_c and v_c, which are then complete only on that stream. Returns k_c, v_c,
-    kept_pos, offsets, scores (scores: [B, Hkv, window position])."""
+    kept_pos, offsets, offsets_host, scores (scores: [B, Hkv, window position]). With gather_stream, the
+    tensors the copy reads or writes (k, v, k_c, v_c, kept_pos) are marked as in use on that stream (for a
+    torch.cuda.Stream; a raw stream handle leaves keeping them alive to the caller), so torch's allocator
+    does not hand their memory to other work before the copy is done."""
     import torch
     desc = compress_desc(q_win, k, pool_kernel=pool_kernel, b_sink=b_sink, b_window=b_window, scale=scale)
     B, Hkv, C, d = k.shape
@@ -237,10 +251,7 @@ def compress_layer(q_win, k, v, layer_budgets, *, pool_kernel: int, b_sink: int,
         res.setdefault("v_c", torch.empty((B * T, d), dtype=v.dtype, device=dev))
         res.setdefault("kept_pos", torch.empty(B * T, dtype=torch.int32, device=dev))
         res.setdefault("offsets", torch.empty(B * Hkv + 1, dtype=torch.int64, device=dev))
-        # the offsets the kernels write, known on the host: b*T + prefix(h), then B*T
-        pre = np.concatenate([[0], np.cumsum(budgets)])
-        oh = np.array([b * T + pre[h] for b in range(B) for h in range(Hkv)] + [B * T], dtype=np.int64)
-        res["offsets_host"] = oh
+        res["offsets_host"] = segment_offsets(budgets, B)
     n_scored = C - q_win.shape[2] if window_pos == -1 else int(window_pos)
     if with_scores or scores_only:
         res.setdefault("scores", torch.empty((B, Hkv, max(n_scored, 0)), dtype=torch.float32, device=dev))
@@ -259,6 +270,9 @@ def compress_layer(q_win, k, v, layer_budgets, *, pool_kernel: int, b_sink: int,
         _ptr(res.get("kept_pos")), _ptr(res.get("offsets")), _ptr(res.get("scores")), _ptr(workspace),
         workspace.numel(), _stream(stream))
     _check(st)
+    if isinstance(gather_stream, torch.cuda.Stream) and not scores_only:
+        for t in (k, v, res["k_c"], res["v_c"], res["kept_pos"]):
+            t.record_stream(gather_stream)
     return res
 
 

@@ -192,9 +192,11 @@ __device__ __forceinline__ void chunk_pipeline(char* kbuf, const rsrc_t& kr, int
 // each logit costs one fma, one exp2 and one add and the loop has no branch.
 // A sum can only overflow if a later logit exceeds that maximum by about 100
 // (base 2); the chunk's sums are checked once at its end and, if any left
-// [0, 2^126] (inf and NaN included), the whole chunk is recomputed with the
+// [0, 2^122] (inf and NaN included), the whole chunk is recomputed with the
 // exact online update (two exp2 per logit, m = running max), reading the keys
-// from global memory. The tiles that reach the window block (causal mask) or
+// from global memory. The bound leaves room for the 16 lanes of a row, which
+// share the reference and are then added as they are: 16 * 2^122 = 2^126 stays
+// finite. The tiles that reach the window block (causal mask) or
 // pass the end of the head always take that exact path. Padded rows (past R)
 // keep m = 0.
 template <typename T, int D, int NB, int TILE>
@@ -291,7 +293,7 @@ __device__ void lse_chunk(const CompressArgs& a, char* kbuf, int seg, int chunk,
 #pragma unroll
     for (int j = 0; j < NB; ++j)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) bad |= !(s[j][i] <= 8.5070591730234616e37f);  // 2^126; catches inf and NaN
+      for (int i = 0; i < 4; ++i) bad |= !(s[j][i] <= 5.3169119831396635e36f);  // 2^122; catches inf and NaN
     if (__any(bad)) {
       reset();
       for (int64_t t = 0; t < nfast; ++t)

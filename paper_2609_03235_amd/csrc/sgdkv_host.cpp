@@ -139,7 +139,7 @@ extern "C" {
 
 const char* sgdkv_last_error(void) { return g_error.c_str(); }
 
-int32_t sgdkv_version(void) { return 101; }
+int32_t sgdkv_version(void) { return 102; }
 
 sgdkv_status sgdkv_reduce_query_head_scores(const double* per_qhead, int32_t L, int32_t Hq, int32_t Hkv,
                                             double* per_kvhead_out) {
@@ -262,6 +262,30 @@ sgdkv_status sgdkv_allocate_budgets(const double* head_scores, int32_t L, int32_
     }
   }
   for (int64_t h = 0; h < n; ++h) budgets_out[h] = reserve + mid[h];
+  return ok();
+}
+
+sgdkv_status sgdkv_segment_offsets(const int64_t* layer_budgets, int32_t batch, int32_t num_kv_heads,
+                                   int64_t* offsets_out) {
+  if (!layer_budgets || !offsets_out) return fail(SGDKV_ERR_INVALID_ARG, "NULL pointer");
+  if (batch < 1 || num_kv_heads < 1)
+    return fail(SGDKV_ERR_INVALID_ARG, "batch=%d and num_kv_heads=%d must be >= 1", batch, num_kv_heads);
+  const int64_t limit = (int64_t)1 << 62;
+  int64_t T = 0;
+  for (int32_t h = 0; h < num_kv_heads; ++h) {
+    if (layer_budgets[h] < 0)
+      return fail(SGDKV_ERR_INVALID_ARG, "layer_budgets[%d] = %lld < 0", h, (long long)layer_budgets[h]);
+    if (layer_budgets[h] > limit / batch - T) return fail(SGDKV_ERR_INVALID_ARG, "batch * T_layer exceeds 2^62");
+    T += layer_budgets[h];
+  }
+  for (int32_t b = 0; b < batch; ++b) {
+    int64_t run = (int64_t)b * T;
+    for (int32_t h = 0; h < num_kv_heads; ++h) {
+      offsets_out[(int64_t)b * num_kv_heads + h] = run;
+      run += layer_budgets[h];
+    }
+  }
+  offsets_out[(int64_t)batch * num_kv_heads] = (int64_t)batch * T;
   return ok();
 }
 

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol():
     lib = sg.load_library()
     for name in declared:
         assert hasattr(lib, name), name
-    assert sg.version() == 101
+    assert sg.version() == 102
 
 
 problem = st.integers(min_value=1, max_value=4).flatmap(
@@ -330,6 +330,43 @@ def test_append_and_tail_validation():
     assert lib.sgdkv_append_kv(ctypes.byref(bad), FAKE, FAKE, FAKE, FAKE, 10, 3, None) == sg.ERR_INVALID_ARG
     if not _gpu():
         assert app(10, 3) == sg.ERR_HIP  # validation passed; no device here
+
+
+@settings(max_examples=200, deadline=None, suppress_health_check=[HealthCheck.too_slow])
+@given(st.lists(st.integers(0, 1 << 20), min_size=1, max_size=64), st.integers(1, 40))
+def test_segment_offsets_lay_out_segments_in_order(budgets, B):
+    """The ragged cache holds segment (b, h) after every segment before it in (b, h) order."""
+    got = sg.segment_offsets(budgets, B)
+    row, want = 0, []
+    for b in range(B):
+        for n in budgets:
+            want.append(row)
+            row += n
+    want.append(row)
+    assert got.tolist() == want
+
+
+def test_segment_offsets_match_the_oracle_cache():
+    rng = np.random.Generator(np.random.PCG64(5))
+    B, Hq, Hkv, d, C, w, s, W = 3, 6, 3, 64, 300, 8, 2, 16
+    q_win = rng.standard_normal((B, Hq, w, d))
+    k, v = rng.standard_normal((B, Hkv, C, d)), rng.standard_normal((B, Hkv, C, d))
+    budgets = np.array([s + W, C, s + W + 77])
+    orc = oracle.compress(q_win, k, v, budgets, w=w, kp=3, s=s, W=W)
+    assert np.array_equal(sg.segment_offsets(budgets, B), orc["offsets"])
+
+
+def test_segment_offsets_errors():
+    lib = sg.load_library()
+    out = np.full(5, -7, dtype=np.int64)
+    P = sg._np_ptr
+    assert lib.sgdkv_segment_offsets(P(np.array([1, -1], dtype=np.int64)), 2, 2, P(out)) == sg.ERR_INVALID_ARG
+    assert lib.sgdkv_segment_offsets(P(np.array([1, 1], dtype=np.int64)), 0, 2, P(out)) == sg.ERR_INVALID_ARG
+    assert lib.sgdkv_segment_offsets(P(np.array([1, 1], dtype=np.int64)), 2, 0, P(out)) == sg.ERR_INVALID_ARG
+    assert lib.sgdkv_segment_offsets(None, 2, 2, P(out)) == sg.ERR_INVALID_ARG
+    assert lib.sgdkv_segment_offsets(P(np.array([1 << 61, 1 << 61], dtype=np.int64)), 2, 2, P(out)) \
+        == sg.ERR_INVALID_ARG
+    assert np.all(out == -7)
 
 
 @pytest.mark.skipif(_gpu(), reason="checks the no-device path")

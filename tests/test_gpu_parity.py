@@ -584,7 +584,7 @@ def test_gather_stream(dtype, d):
 
 def test_lse_exact_redo_paths():
     """Pass 1 fixes each row's reference at its largest logit among the chunk's first 16 keys and
-    redoes a chunk exactly when a sum leaves [0, 2^126] (fp32 overflow included). Every 16th key
+    redoes a chunk exactly when a sum leaves [0, 2^122] (fp32 overflow included). Every 16th key
     is strongly anti-aligned with the window queries (logit about -120) and three keys inside
     later chunks are strongly aligned (logit about +100, i.e. ~144 in base 2, far above any
     chunk-start reference), which forces the exact redo of their chunks."""
@@ -604,6 +604,34 @@ def test_lse_exact_redo_paths():
     res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=7, s=s, W=W)
     _check_scores(res["scores"].cpu().numpy(), orc["pooled"], "redo", rtol=_score_rtol(t["q_win"]))
     _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "redo", rtol=_score_rtol(t["q_win"]))
+
+
+def test_lse_redo_when_lane_sums_add_up_to_overflow():
+    """Several lanes of a row each below the old per-lane bound (2^126) but above 2^122: the 16
+    lanes of a row share the chunk's reference and are added as they are, so their sum would
+    overflow fp32. All keys are zero (logit 0, so every chunk's reference is 0) except eight keys
+    in eight different lanes (key index mod 16) of one chunk, with base-2 logits 125.5 - 0.1*i:
+    each of those lanes sums to about 2^125, the eight together to about 2^128. The chunk must be
+    redone exactly, and the scores must match the oracle."""
+    B, Hq, Hkv, d, C, w, s, W = 1, 4, 2, 64, 3000, 32, 4, 32
+    u = np.zeros(d)
+    u[0] = 1.0
+    q_win = np.broadcast_to(8.0 * u, (B, Hq, w, d)).copy()  # <q, k>/sqrt(d) = k[0] for every window row
+    k = np.zeros((B, Hkv, C, d))
+    spikes = [560 + 17 * i for i in range(8)]  # chunk of keys [512, 768): lanes 0..7 of its subtiles
+    for i, pos in enumerate(spikes):
+        k[:, :, pos, 0] = (125.5 - 0.1 * i) * math.log(2.0)  # natural-log logit of the key
+    v = np.random.Generator(np.random.PCG64(44)).standard_normal((B, Hkv, C, d))
+    t = {n: torch.from_numpy(x.astype(np.float32)).to(DEV) for n, x in dict(q_win=q_win, k=k, v=v).items()}
+    budgets = np.array([s + W + 30, s + W + 20])  # the spikes' pooling neighbourhoods hold the kept middle
+    _announce("pass-1 redo when lane sums overflow together")
+    res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=7, s=s, W=W)
+    g = res["scores"].cpu().numpy()
+    assert np.isfinite(g).all()
+    assert np.all(g[:, :, spikes] > 0.0)
+    _check_scores(g, orc["pooled"], "lane-sum overflow")
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, "lane-sum overflow")
+    _check_gather(res, t["k"], t["v"], budgets)
 
 
 @pytest.mark.parametrize("w,W", [(100, 128), (200, 200)])

@@ -6,6 +6,7 @@ binary variants) and exact-arithmetic identities (a mix of a vector with
 itself is the plain allocation of the normalised vector).
 """
 import json
+import math
 import os
 from fractions import Fraction
 
@@ -64,12 +65,13 @@ def test_thr_zeroes_below_mean(p):
     sc = np.array(sc)
     b = oracle.allocate_variant(sc, L, H, C, s, W, total, oracle.ALLOC_THR, mode=mode)
     assert int(b.sum()) == total and np.all(b >= s + W) and np.all(b <= C)
-    # the threshold is the fp64 mean (sum in flat order, then / n), as the allocation defines it
-    tot64 = 0.0
-    for x in sc.tolist():
-        tot64 += x
-    mean = tot64 / n
-    kept = [x >= mean for x in sc.tolist()]
+    # the threshold is the mean of all L*H scores, here in exact rational arithmetic; a score
+    # within an ulp of it may fall on either side of the fp64 mean, so such draws pin nothing
+    mean = sum(Fraction(x) for x in sc.tolist()) / n
+    ulp = Fraction(math.ulp(float(mean))) if mean > 0 else Fraction(0)
+    if any(abs(Fraction(x) - mean) <= ulp for x in sc.tolist()) and len(set(sc.tolist())) > 1:
+        return
+    kept = [Fraction(x) >= mean for x in sc.tolist()]
     # without caps, the shares of the surviving heads are exact rationals and a zeroed head gets nothing
     T = total - n * (s + W)
     tot = sum(Fraction(x) for x, k in zip(sc.tolist(), kept) if k)
