@@ -337,6 +337,25 @@ sgdkv_status sgdkv_decode_attention_ex(const sgdkv_decode_desc* desc, const void
                                        const sgdkv_decode_tail* tail, void* out, float* lse_out, void* workspace,
                                        size_t workspace_bytes, void* stream);
 
+/* sgdkv_decode_attention_ex without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation). The split partials go to a static
+ * device array of the library, 64 MiB per GPU, which every GPU the library
+ * runs on holds from its first use until the process ends; the call allocates
+ * nothing itself. The caller still passes q, the cache, the offsets, out and
+ * lse_out as for sgdkv_decode_attention_ex, with the same results.
+ * Calls on one GPU share that GPU's array: calls that overlap in time on one
+ * GPU (on different streams, or from several threads) race and give
+ * undefined results; calls ordered on one stream are safe. Nothing in the
+ * array needs to persist or be cleared between calls.
+ * Errors: those of sgdkv_decode_attention_ex except WORKSPACE; a decode whose
+ * partials (sgdkv_decode_workspace_size_ex for the same arguments) exceed
+ * 64 MiB (UNSUPPORTED, nothing enqueued). */
+sgdkv_status sgdkv_decode_attention_noalloc(const sgdkv_decode_desc* desc, const void* q, const void* k_c,
+                                            const void* v_c, const int64_t* offsets, const int64_t* offsets_host,
+                                            const sgdkv_decode_tail* tail, void* out, float* lse_out,
+                                            void* stream);
+
 /* ------------------------------------------------------------------ */
 /* Kernel timing for benchmarks (not part of the method).             */
 

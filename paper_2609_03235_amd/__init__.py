@@ -29,7 +29,7 @@ SYMBOLS = ("sgdkv_last_error", "sgdkv_version", "sgdkv_reduce_query_head_scores"
            "sgdkv_compress_workspace_size",
            "sgdkv_compress_layer", "sgdkv_compress_layer_ex",
            "sgdkv_decode_workspace_size", "sgdkv_decode_attention", "sgdkv_decode_workspace_size_ex",
-           "sgdkv_decode_attention_ex", "sgdkv_append_kv", "sgdkv_profile_enable",
+           "sgdkv_decode_attention_ex", "sgdkv_decode_attention_noalloc", "sgdkv_append_kv", "sgdkv_profile_enable",
            "sgdkv_profile_reset", "sgdkv_profile_read")
 
 
@@ -92,6 +92,7 @@ def load_library():
         "sgdkv_decode_attention": [P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
         "sgdkv_decode_workspace_size_ex": [P, P, i64, P],
         "sgdkv_decode_attention_ex": [P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
+        "sgdkv_decode_attention_noalloc": [P, P, P, P, P, P, P, P, P, P],
         "sgdkv_append_kv": [P, P, P, P, P, i64, i64, P],
         "sgdkv_profile_enable": [i32],
         "sgdkv_profile_reset": [],
@@ -297,9 +298,12 @@ class DecodeTail(ctypes.Structure):
 
 def decode_attention(q, k_c, v_c, offsets, offsets_host, num_kv_heads: int, *, out_dtype=None,
                      scale: float = 0.0, with_lse: bool = True, k_new=None, v_new=None, n_new: int = 0,
-                     workspace=None, out=None, lse=None, stream=None):
+                     workspace=None, out=None, lse=None, stream=None, no_alloc: bool = False):
     """One decode step over the ragged cache (sgdkv_decode_attention_ex). k_new/v_new [B, Hkv, capacity, d]
-    hold the rows appended since compression, of which the first n_new are attended. Returns (out, lse)."""
+    hold the rows appended since compression, of which the first n_new are attended. no_alloc: call
+    sgdkv_decode_attention_noalloc instead, which takes no workspace (its split partials go to the
+    library's static device scratch; pass out, and lse if wanted, to allocate nothing here either).
+    Returns (out, lse)."""
     import torch
     desc = decode_desc(q, num_kv_heads, out_dtype, scale)
     oh = np.ascontiguousarray(np.asarray(offsets_host, dtype=np.int64))
@@ -310,9 +314,14 @@ def decode_attention(q, k_c, v_c, offsets, offsets_host, num_kv_heads: int, *, o
                           device=q.device)
     if with_lse and lse is None:
         lse = torch.empty((B, Hq), dtype=torch.float32, device=q.device)
+    tail = DecodeTail(_ptr(k_new), _ptr(v_new), cap, int(n_new))
+    if no_alloc:
+        _check(load_library().sgdkv_decode_attention_noalloc(
+            ctypes.byref(desc), _ptr(q), _ptr(k_c), _ptr(v_c), _ptr(offsets), _np_ptr(oh), ctypes.byref(tail),
+            _ptr(out), _ptr(lse) if with_lse else None, _stream(stream)))
+        return out, (lse if with_lse else None)
     if workspace is None:
         workspace = alloc_workspace(decode_workspace_size(desc, oh, cap), q.device)
-    tail = DecodeTail(_ptr(k_new), _ptr(v_new), cap, int(n_new))
     st = load_library().sgdkv_decode_attention_ex(
         ctypes.byref(desc), _ptr(q), _ptr(k_c), _ptr(v_c), _ptr(offsets), _np_ptr(oh), ctypes.byref(tail), _ptr(out),
         _ptr(lse) if with_lse else None, _ptr(workspace), workspace.numel(), _stream(stream))

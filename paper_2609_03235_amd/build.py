@@ -22,7 +22,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-command-line-argument"]
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
-KERNEL_SOURCES = ["score_kernels.hip", "select_kernels.hip", "decode_kernels.hip"]
+KERNEL_SOURCES = ["score_kernels.hip", "select_kernels.hip", "decode_kernels.hip", "decode_scratch.hip"]
 HOST_SOURCES = ["sgdkv_host.cpp", "profile.cpp"]
 
 

@@ -712,10 +712,17 @@ sgdkv_status sgdkv_decode_attention(const sgdkv_decode_desc* desc, const void* q
                                    workspace_bytes, stream);
 }
 
-sgdkv_status sgdkv_decode_attention_ex(const sgdkv_decode_desc* desc, const void* q, const void* k_c,
-                                       const void* v_c, const int64_t* offsets, const int64_t* offsets_host,
-                                       const sgdkv_decode_tail* tail, void* out, float* lse_out, void* workspace,
-                                       size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Validation and launch of one decode step, shared by the decode entry points. With
+// static_scratch the split partials go to the library's static device scratch (no workspace
+// argument); otherwise to the caller's workspace.
+sgdkv_status decode_step(const sgdkv_decode_desc* desc, const void* q, const void* k_c, const void* v_c,
+                         const int64_t* offsets, const int64_t* offsets_host, const sgdkv_decode_tail* tail,
+                         void* out, float* lse_out, void* workspace, size_t workspace_bytes, bool static_scratch,
+                         void* stream) {
   const sgdkv_decode_tail none{nullptr, nullptr, 0, 0};
   const sgdkv_decode_tail& t = tail ? *tail : none;
   DecodePlan p;
@@ -731,7 +738,13 @@ sgdkv_status sgdkv_decode_attention_ex(const sgdkv_decode_desc* desc, const void
   const char* names[] = {"q", "k_c", "v_c", "offsets", "out", "lse_out", "k_new", "v_new"};
   for (int i = 0; i < 8; ++i)
     if (ptrs[i] && !aligned16(ptrs[i])) return fail(SGDKV_ERR_INVALID_ARG, "%s is not 16-byte aligned", names[i]);
-  if (p.bytes > 0) {
+  if (static_scratch) {
+    if (p.bytes > sgdkv::kDecodeScratchBytes)
+      return fail(SGDKV_ERR_UNSUPPORTED,
+                  "this decode needs %zu bytes of split partials; the static scratch holds %zu (use "
+                  "sgdkv_decode_attention_ex with a workspace)",
+                  p.bytes, sgdkv::kDecodeScratchBytes);
+  } else if (p.bytes > 0) {
     if (!workspace) return fail(SGDKV_ERR_WORKSPACE, "NULL workspace (%zu bytes needed)", p.bytes);
     if (reinterpret_cast<uintptr_t>(workspace) & 255u)
       return fail(SGDKV_ERR_WORKSPACE, "workspace is not 256-byte aligned");
@@ -739,6 +752,10 @@ sgdkv_status sgdkv_decode_attention_ex(const sgdkv_decode_desc* desc, const void
       return fail(SGDKV_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, p.bytes);
   }
   if (sgdkv_status st = check_device()) return st;
+  if (static_scratch) {
+    hipError_t e = sgdkv::decode_scratch(&workspace);
+    if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "static decode scratch: %s", hipGetErrorString(e));
+  }
   a.q = q;
   a.k_c = k_c;
   a.v_c = v_c;
@@ -756,6 +773,25 @@ sgdkv_status sgdkv_decode_attention_ex(const sgdkv_decode_desc* desc, const void
   e = sgdkv::launch_decode(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SGDKV_ERR_HIP, "decode kernels: %s", hipGetErrorString(e));
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+sgdkv_status sgdkv_decode_attention_ex(const sgdkv_decode_desc* desc, const void* q, const void* k_c,
+                                       const void* v_c, const int64_t* offsets, const int64_t* offsets_host,
+                                       const sgdkv_decode_tail* tail, void* out, float* lse_out, void* workspace,
+                                       size_t workspace_bytes, void* stream) {
+  return decode_step(desc, q, k_c, v_c, offsets, offsets_host, tail, out, lse_out, workspace, workspace_bytes,
+                     false, stream);
+}
+
+sgdkv_status sgdkv_decode_attention_noalloc(const sgdkv_decode_desc* desc, const void* q, const void* k_c,
+                                            const void* v_c, const int64_t* offsets, const int64_t* offsets_host,
+                                            const sgdkv_decode_tail* tail, void* out, float* lse_out,
+                                            void* stream) {
+  return decode_step(desc, q, k_c, v_c, offsets, offsets_host, tail, out, lse_out, nullptr, 0, true, stream);
 }
 
 sgdkv_status sgdkv_append_kv(const sgdkv_decode_desc* desc, const void* k_step, const void* v_step, void* k_new,

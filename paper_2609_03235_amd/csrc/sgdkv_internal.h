@@ -112,6 +112,11 @@ struct DecodeArgs {
 };
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);
+
+// Static device scratch of the decode entry point that allocates nothing: its size, and the
+// current device's address of it (looked up once per device).
+constexpr size_t kDecodeScratchBytes = size_t(64) << 20;
+hipError_t decode_scratch(void** ptr);
 hipError_t launch_append(const DecodeArgs& a, const void* k_step, const void* v_step, void* k_new, void* v_new,
                          int64_t slot, hipStream_t stream);
 

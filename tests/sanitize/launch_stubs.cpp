@@ -13,4 +13,5 @@ hipError_t launch_decode(const DecodeArgs&, hipStream_t) { return hipErrorNoDevi
 hipError_t launch_append(const DecodeArgs&, const void*, const void*, void*, void*, int64_t, hipStream_t) {
   return hipErrorNoDevice;
 }
+hipError_t decode_scratch(void**) { return hipErrorNoDevice; }
 }  // namespace sgdkv

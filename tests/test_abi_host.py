@@ -369,6 +369,28 @@ def test_segment_offsets_errors():
     assert np.all(out == -7)
 
 
+def test_noalloc_decode_rejects_partials_beyond_the_static_scratch():
+    """The static scratch holds 64 MiB of split partials; a decode that needs more is refused
+    before anything is enqueued (validation precedes the device check, so no GPU is needed)."""
+    lib = sg.load_library()
+    desc = sg.DecodeDesc(64, 64, 8, 128, sg.DTYPE_BF16, sg.DTYPE_F32, 0.0)
+    oh = np.full(64 * 8 + 1, 1 << 23, dtype=np.int64)
+    oh[0] = 0  # one segment of 2^23 rows, the others empty
+    assert sg.decode_workspace_size(desc, oh) > 64 << 20
+    P = sg._np_ptr
+    st = lib.sgdkv_decode_attention_noalloc(ctypes.byref(desc), FAKE, FAKE, FAKE, FAKE, P(oh), None, FAKE, None,
+                                            None)
+    assert st == sg.ERR_UNSUPPORTED
+    assert b"static scratch" in lib.sgdkv_last_error()
+    small = np.array([0, 10, 10, 30, 31], dtype=np.int64)
+    d2 = sg.DecodeDesc(2, 4, 2, 64, 1, 0, 0.0)
+    assert lib.sgdkv_decode_attention_noalloc(ctypes.byref(d2), FAKE, FAKE, FAKE, FAKE, P(np.array([0, 10, 9, 30, 31])),
+                                              None, FAKE, None, None) == sg.ERR_INVALID_ARG
+    if not _gpu():
+        assert lib.sgdkv_decode_attention_noalloc(ctypes.byref(d2), FAKE, FAKE, FAKE, FAKE, P(small), None, FAKE,
+                                                  None, None) == sg.ERR_HIP
+
+
 @pytest.mark.skipif(_gpu(), reason="checks the no-device path")
 def test_no_device_fails_after_validation():
     assert _compress(_desc(), [512, 512]) == sg.ERR_HIP
