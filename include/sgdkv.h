@@ -201,7 +201,7 @@ sgdkv_status sgdkv_compress_workspace_size(const sgdkv_compress_desc* desc, size
  *   the selection used); required in scores-only mode.
  * workspace: device, 256-byte aligned, >= sgdkv_compress_workspace_size.
  * Errors (nothing enqueued): sizes < 1; Hq % Hkv; Hkv > 64; d not 64/128
- *   (UNSUPPORTED); G*w > 512 (UNSUPPORTED); k_p even; s+W > C; W < w;
+ *   (UNSUPPORTED); G*w > 4096 (UNSUPPORTED); k_p even; s+W > C; W < w;
  *   a budget outside [s+W, C]; C > 2^31-1; misaligned or missing pointers;
  *   small workspace (WORKSPACE); no usable device (HIP). */
 sgdkv_status sgdkv_compress_layer(const sgdkv_compress_desc* desc, const int64_t* layer_budgets,
@@ -246,7 +246,7 @@ sgdkv_status sgdkv_compress_layer(const sgdkv_compress_desc* desc, const int64_t
  * Errors: those of sgdkv_compress_layer (with b_window >= C - P0 in place of
  *   b_window >= w); group_agg not 0..3; NULL or invalid qhead_scores for an
  *   Ipt. mode; Hq > 256 with an Ipt. mode (UNSUPPORTED); IPT_MAX with
- *   obs_window not a multiple of 16 (UNSUPPORTED); window_pos outside
+ *   obs_window not a multiple of 16 or above 512 (UNSUPPORTED); window_pos outside
  *   [-1, C]; reserved not 0. */
 #define SGDKV_GROUP_MEAN 0
 #define SGDKV_GROUP_IPT_MAX 1

@@ -19,7 +19,12 @@
 //
 // Work split: workgroup = 8 waves; wave v holds row blocks v, v+8, v+16, ...
 // (16 rows each) as MFMA A-fragments in registers, so a SIMD (waves v and
-// v+4) covers a quarter of the rows. Each key tile (128 keys; 64 in pass 2
+// v+4) covers a quarter of the rows. A workgroup holds at most 512 rows; a
+// KV head with more window rows (G*w > 512, e.g. the 128-token window of the
+// paper's main setting with GQA groups of 7 or 8) splits them over several
+// workgroups per key chunk (grid z = row split). Pass 1 partials are per row
+// anyway; pass 2 then leaves one column-sum partial per split, which the
+// pooling pass adds (or, for Ipt. max, maximises) in split order. Each key tile (128 keys; 64 in pass 2
 // for fp32 keys) is staged once in LDS and read by all eight waves as B-fragments;
 // blocks past the last row are skipped. MFMA 16x16x32 bf16 (or 8 x 16x16x4
 // f32 for fp32 inputs) accumulates in fp32.
@@ -30,9 +35,9 @@
 #include "sgdkv_internal.h"
 #include "segment_init.h"
 
-// Row blocks per wave the dispatch instantiates: at most 512 rows over all waves.
-#define SGDKV_SCORE_WAVES_MAX_RBW (kMaxGroupRowsMacro / (16 * SGDKV_SCORE_WAVES))
-#define kMaxGroupRowsMacro 512
+// Row blocks per wave the dispatch instantiates: at most 512 rows (one row split) over all waves.
+#define SGDKV_SCORE_WAVES_MAX_RBW (kMaxSplitRowsMacro / (16 * SGDKV_SCORE_WAVES))
+#define kMaxSplitRowsMacro 512
 
 namespace sgdkv {
 
@@ -83,16 +88,17 @@ struct KeyStage {
   }
 };
 
+// Window rows [r0, r0 + nrows) of KV head h (one row split) as A fragments.
 template <typename T, int D, int RBW>
-__device__ __forceinline__ void load_group_queries(const CompressArgs& a, int b, int h, int wid,
+__device__ __forceinline__ void load_group_queries(const CompressArgs& a, int b, int h, int r0, int nrows, int wid,
                                                    int lane, Frag<T> (&qa)[RBW][D / 32]) {
   using G = TileGeom<T, D>;
-  const T* qbase = static_cast<const T*>(a.q_win) + ((int64_t)(b * a.Hq + h * a.G) * a.w) * D;
-  const rsrc_t qr = make_rsrc(qbase, (uint64_t)a.R * G::RB);
+  const T* qbase = static_cast<const T*>(a.q_win) + ((int64_t)(b * a.Hq + h * a.G) * a.w + r0) * D;
+  const rsrc_t qr = make_rsrc(qbase, (uint64_t)nrows * G::RB);
   const int lr = lane & 15, lg = lane >> 4;
 #pragma unroll
   for (int j = 0; j < RBW; ++j) {
-    const int row = (wid + kScoreWaves * j) * 16 + lr;  // rows >= R read as zeros
+    const int row = (wid + kScoreWaves * j) * 16 + lr;  // rows >= nrows read as zeros
 #pragma unroll
     for (int c = 0; c < G::NC; ++c)
       qa[j][c] = gload_frag<T>(qr, (uint32_t)(row * G::RB + (32 * c + 8 * lg) * G::EB));
@@ -200,7 +206,7 @@ __device__ __forceinline__ void chunk_pipeline(char* kbuf, const rsrc_t& kr, int
 // pass the end of the head always take that exact path. Padded rows (past R)
 // keep m = 0.
 template <typename T, int D, int NB, int TILE>
-__device__ __forceinline__ void lse_exact_tile(const rsrc_t& kr, int lr, int lg, int wid, int w, int64_t tile0,
+__device__ __forceinline__ void lse_exact_tile(const rsrc_t& kr, int lr, int lg, int wid, int r0, int w, int64_t tile0,
                                             int64_t vis0, int64_t C, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
                                             float c2, float (&m)[NB > 0 ? NB : 1][4],
                                             float (&s)[NB > 0 ? NB : 1][4]) {
@@ -229,7 +235,7 @@ __device__ __forceinline__ void lse_exact_tile(const rsrc_t& kr, int lr, int lg,
     for (int j = 0; j < NB; ++j)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int wi = ((wid + kScoreWaves * j) * 16 + 4 * lg + i) % w;  // window index of the row
+        const int wi = (r0 + (wid + kScoreWaves * j) * 16 + 4 * lg + i) % w;  // window index of the row
         const float y = (masked && dk > wi) ? -INFINITY : acc[j][i] * c2;
         const float mn = fmaxf(m[j][i], y);
         if (mn != -INFINITY) {
@@ -241,8 +247,8 @@ __device__ __forceinline__ void lse_exact_tile(const rsrc_t& kr, int lr, int lg,
 }
 
 template <typename T, int D, int NB>
-__device__ void lse_chunk(const CompressArgs& a, char* kbuf, int seg, int chunk, int wid, int lane,
-                          const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], const rsrc_t& kr, int64_t key0,
+__device__ void lse_chunk(const CompressArgs& a, char* kbuf, int seg, int chunk, int r0, int nrows, int wid,
+                          int lane, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], const rsrc_t& kr, int64_t key0,
                           int64_t key_end) {
   constexpr int NBX = NB > 0 ? NB : 1;
   constexpr int TILE = kLseTile;
@@ -263,7 +269,7 @@ __device__ void lse_chunk(const CompressArgs& a, char* kbuf, int seg, int chunk,
 #pragma unroll
   for (int j = 0; j < NBX; ++j)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) real[j][i] = (wid + kScoreWaves * j) * 16 + 4 * lg + i < a.R;
+    for (int i = 0; i < 4; ++i) real[j][i] = (wid + kScoreWaves * j) * 16 + 4 * lg + i < nrows;
   reset();
   // whole tiles every row sees (keys below both the window block and the end of the head)
   const int64_t open_end = vis0 < a.C ? vis0 : a.C;
@@ -297,11 +303,11 @@ __device__ void lse_chunk(const CompressArgs& a, char* kbuf, int seg, int chunk,
     if (__any(bad)) {
       reset();
       for (int64_t t = 0; t < nfast; ++t)
-        lse_exact_tile<T, D, NB, TILE>(kr, lr, lg, wid, a.w, key0 + t * TILE, vis0, a.C, qa, c2, m, s);
+        lse_exact_tile<T, D, NB, TILE>(kr, lr, lg, wid, r0, a.w, key0 + t * TILE, vis0, a.C, qa, c2, m, s);
     }
   }
   for (int64_t t = nfast; t < ntiles; ++t)
-    lse_exact_tile<T, D, NB, TILE>(kr, lr, lg, wid, a.w, key0 + t * TILE, vis0, a.C, qa, c2, m, s);
+    lse_exact_tile<T, D, NB, TILE>(kr, lr, lg, wid, r0, a.w, key0 + t * TILE, vis0, a.C, qa, c2, m, s);
   // Combine the 16 lanes (keys) of each row, then store (m, s) for the row.
   float* part = a.lse_part + ((int64_t)seg * a.n_lse_chunks + chunk) * a.R * 2;
   const rsrc_t pr = make_rsrc(part, (uint64_t)a.R * 2 * sizeof(float));
@@ -321,9 +327,9 @@ __device__ void lse_chunk(const CompressArgs& a, char* kbuf, int seg, int chunk,
         mm = mn;
       }
       const int row = (wid + kScoreWaves * j) * 16 + 4 * lg + i;
-      if (lr == 0 && row < a.R) {
-        stf(pr, (uint32_t)(row * 8), mm);
-        stf(pr, (uint32_t)(row * 8 + 4), ss);
+      if (lr == 0 && row < nrows) {
+        stf(pr, (uint32_t)((r0 + row) * 8), mm);
+        stf(pr, (uint32_t)((r0 + row) * 8 + 4), ss);
       }
     }
 }
@@ -342,20 +348,22 @@ __global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
   if (key0 >= vis_end) return;
   const int64_t key_end = key0 + a.score_chunk < vis_end ? key0 + a.score_chunk : vis_end;
   const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
+  const int r0 = (int)blockIdx.z * a.rs_rows;
+  const int nrows = a.R - r0 < a.rs_rows ? a.R - r0 : a.rs_rows;
   const rsrc_t kr = make_rsrc(static_cast<const T*>(a.k) + (int64_t)seg * a.C * D, (uint64_t)a.C * G::RB);
   Frag<T> qa[RBW][G::NC];
-  load_group_queries<T, D, RBW>(a, b, h, wid, lane, qa);
+  load_group_queries<T, D, RBW>(a, b, h, r0, nrows, wid, lane, qa);
   // blocks this wave owns: RBW or RBW-1 (uniform per wave)
-  const int nrb = (a.R + 15) / 16;
+  const int nrb = (nrows + 15) / 16;
   if (wid + kScoreWaves * (RBW - 1) < nrb) {
-    lse_chunk<T, D, RBW>(a, ktile, seg, chunk, wid, lane, qa, kr, key0, key_end);
+    lse_chunk<T, D, RBW>(a, ktile, seg, chunk, r0, nrows, wid, lane, qa, kr, key0, key_end);
   } else {
     Frag<T> qb[RBW > 1 ? RBW - 1 : 1][G::NC];
 #pragma unroll
     for (int j = 0; j < RBW - 1; ++j)
 #pragma unroll
       for (int c = 0; c < G::NC; ++c) qb[j][c] = qa[j][c];
-    lse_chunk<T, D, RBW - 1>(a, ktile, seg, chunk, wid, lane, qb, kr, key0, key_end);
+    lse_chunk<T, D, RBW - 1>(a, ktile, seg, chunk, r0, nrows, wid, lane, qb, kr, key0, key_end);
   }
 }
 
@@ -399,8 +407,9 @@ __global__ __launch_bounds__(kBlock) void lse_merge_kernel(CompressArgs a) {
 template <typename T, int D, int NB, int RBW, bool MAXG>
 __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
                              float (*red)[kScoreWaves][MAXG ? RBW : 4][col_tile<T>()],
-                             int seg, int wid, int lane, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
-                             const rsrc_t& kr, int64_t key0, int64_t key_end) {
+                             int seg, int r0, int nrows, int wid, int lane,
+                             const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], const rsrc_t& kr, int64_t key0,
+                             int64_t key_end) {
   constexpr int NBX = NB > 0 ? NB : 1;
   constexpr int TILE = col_tile<T>();
   const int lr = lane & 15, lg = lane >> 4;
@@ -415,14 +424,15 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
   for (int j = 0; j < NBX; ++j)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int row = (wid + kScoreWaves * j) * 16 + 4 * lg + i;
-      float l = ldf(lr2, (uint32_t)(((int64_t)seg * a.R + row) * 4));
+      const int row = (wid + kScoreWaves * j) * 16 + 4 * lg + i;  // within the split
+      float l = ldf(lr2, (uint32_t)(((int64_t)seg * a.R + r0 + row) * 4));
       if (natural) l *= 1.44269504088896340736f;
-      const float lw = weighted && row < a.R ? a.qweight[h * a.G + row / a.w] : 0.f;
-      nlse[j][i] = row < a.R ? lw - l : -INFINITY;
+      const float lw = weighted && row < nrows ? a.qweight[h * a.G + (r0 + row) / a.w] : 0.f;
+      nlse[j][i] = row < nrows ? lw - l : -INFINITY;
     }
   const float c2 = a.c2;
-  const rsrc_t cr = make_rsrc(a.colsum + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
+  const int nseg = a.B * a.Hkv;
+  const rsrc_t cr = make_rsrc(a.colsum + ((int64_t)blockIdx.z * nseg + seg) * a.n_scored, (uint64_t)a.n_scored * 4);
   // Partials of tile t sit in red[t % 3]: written during tile t, complete at the barrier of
   // tile t+1, summed right after it, rewritten only after the barrier of tile t+2. Each
   // wave sums CPW columns: the LPC lanes of a column read the partials of PPL waves each
@@ -436,13 +446,13 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
     const float(*r)[MAXG ? RBW : 4][TILE] = red[(t + 3) % 3];
     float v = 0.f;
     if constexpr (MAXG) {
-      // the LPC lanes of a column take the group's heads in turn: sum a head's w/16 blocks
+      // the LPC lanes of a column take the split's heads in turn: sum a head's w/16 blocks
       // (block b sits with wave b % 8, slot b / 8), weight it, keep the maximum
-      const int bph = a.w / 16;
-      for (int g = rgrp; g < a.G; g += LPC) {
+      const int bph = a.w / 16, g0 = r0 / a.w, ng = nrows / a.w;
+      for (int g = rgrp; g < ng; g += LPC) {
         float sum = 0.f;
         for (int bb = g * bph; bb < (g + 1) * bph; ++bb) sum += r[bb % kScoreWaves][bb / kScoreWaves][rcol];
-        v = fmaxf(v, a.qweight[h * a.G + g] * sum);
+        v = fmaxf(v, a.qweight[h * a.G + g0 + g] * sum);
       }
 #pragma unroll
       for (int o = CPW; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
@@ -501,24 +511,26 @@ __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) 
   __shared__ float red[3][kScoreWaves][MAXG ? RBW : 4][col_tile<T>()];
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
-  if (blockIdx.x == 0) init_segment(a, seg);  // histograms and offsets for the selection that follows
+  if (blockIdx.x == 0 && blockIdx.z == 0) init_segment(a, seg);  // histograms, offsets for the selection
   const int64_t key0 = (int64_t)blockIdx.x * a.score_chunk;
   if (key0 >= a.n_scored) return;
   const int64_t key_end = key0 + a.score_chunk < a.n_scored ? key0 + a.score_chunk : a.n_scored;
   const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
+  const int r0 = (int)blockIdx.z * a.rs_rows;
+  const int nrows = a.R - r0 < a.rs_rows ? a.R - r0 : a.rs_rows;
   const rsrc_t kr = make_rsrc(static_cast<const T*>(a.k) + (int64_t)seg * a.C * D, (uint64_t)a.C * G::RB);
   Frag<T> qa[RBW][G::NC];
-  load_group_queries<T, D, RBW>(a, b, h, wid, lane, qa);
-  const int nrb = (a.R + 15) / 16;
+  load_group_queries<T, D, RBW>(a, b, h, r0, nrows, wid, lane, qa);
+  const int nrb = (nrows + 15) / 16;
   if (wid + kScoreWaves * (RBW - 1) < nrb) {
-    colsum_chunk<T, D, RBW, RBW, MAXG>(a, ktile, red, seg, wid, lane, qa, kr, key0, key_end);
+    colsum_chunk<T, D, RBW, RBW, MAXG>(a, ktile, red, seg, r0, nrows, wid, lane, qa, kr, key0, key_end);
   } else {
     Frag<T> qb[RBW > 1 ? RBW - 1 : 1][G::NC];
 #pragma unroll
     for (int j = 0; j < RBW - 1; ++j)
 #pragma unroll
       for (int c = 0; c < G::NC; ++c) qb[j][c] = qa[j][c];
-    colsum_chunk<T, D, RBW - 1, RBW, MAXG>(a, ktile, red, seg, wid, lane, qb, kr, key0, key_end);
+    colsum_chunk<T, D, RBW - 1, RBW, MAXG>(a, ktile, red, seg, r0, nrows, wid, lane, qb, kr, key0, key_end);
   }
 }
 
@@ -527,22 +539,24 @@ template <typename T, int D, int RBW>
 static hipError_t launch_scores_t(const CompressArgs& a, hipStream_t st) {
   const dim3 sblk(kScoreBlock);
   if (a.window_lse == nullptr) {
-    SGDKV_LAUNCH("score_lse", (lse_kernel<T, D, RBW>), dim3(a.n_lse_chunks, a.B * a.Hkv), sblk, st, a);
+    SGDKV_LAUNCH("score_lse", (lse_kernel<T, D, RBW>), dim3(a.n_lse_chunks, a.B * a.Hkv, a.n_rsplit), sblk, st, a);
     SGDKV_LAUNCH("lse_merge", lse_merge_kernel, dim3((unsigned)((a.R + kBlock - 1) / kBlock), a.B * a.Hkv),
                  dim3(kBlock), st, a);
   }
   if (a.n_col_chunks > 0) {
     if (a.agg == 1)
-      SGDKV_LAUNCH("score_colsum", (colsum_kernel<T, D, RBW, true>), dim3(a.n_col_chunks, a.B * a.Hkv), sblk, st, a);
+      SGDKV_LAUNCH("score_colsum", (colsum_kernel<T, D, RBW, true>), dim3(a.n_col_chunks, a.B * a.Hkv, a.n_rsplit),
+                   sblk, st, a);
     else
-      SGDKV_LAUNCH("score_colsum", (colsum_kernel<T, D, RBW, false>), dim3(a.n_col_chunks, a.B * a.Hkv), sblk, st, a);
+      SGDKV_LAUNCH("score_colsum", (colsum_kernel<T, D, RBW, false>), dim3(a.n_col_chunks, a.B * a.Hkv, a.n_rsplit),
+                   sblk, st, a);
   }
   return hipGetLastError();
 }
 
 template <typename T, int D>
 static hipError_t launch_scores_d(const CompressArgs& a, hipStream_t st) {
-  const int nrb = (a.R + 15) / 16;
+  const int nrb = (a.rs_rows + 15) / 16;  // blocks of the largest row split
   const int rbw = (nrb + kScoreWaves - 1) / kScoreWaves;
   switch (rbw) {
     case 1: return launch_scores_t<T, D, 1>(a, st);

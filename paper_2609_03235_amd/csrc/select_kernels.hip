@@ -20,7 +20,10 @@
 //   radix_pass<p>  digit-p histogram of candidates matching the digits
 //                  before it (each workgroup picks those from the earlier
 //                  histograms itself); pass 0 also pools:
-//                  pooled_j = (1/k_p) sum_{|t-j|<=r} a_t (zero outside)
+//                  pooled_j = (1/k_p) sum_{|t-j|<=r} a_t (zero outside), where
+//                  a_t combines the column-sum partials of the score pass's
+//                  row splits in split order (their sum; their maximum for
+//                  the Ipt. max aggregation)
 //   sel_count      picks the last digit (tau and q complete); per chunk:
 //                  sink/window rows, candidates > tau, == tau
 //   compact        ordered ballot/prefix compaction of a chunk -> kept_pos
@@ -172,7 +175,21 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(CompressArgs a) {
   // range read whatever the descriptor gives (zero past its end) and are not used.
   constexpr int U = 8;
   if constexpr (POOL) {
-    const rsrc_t cr = make_rsrc(a.colsum + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
+    const int nseg = a.B * a.Hkv;
+    const bool maxg = a.agg == 1;
+    auto split_rsrc = [&](int p) {
+      return make_rsrc(a.colsum + ((int64_t)p * nseg + seg) * a.n_scored, (uint64_t)a.n_scored * 4);
+    };
+    const rsrc_t cr = split_rsrc(0);
+    // a_t at byte offset off: the partials of all row splits, combined in split order
+    auto colsum_at = [&](uint32_t off) {
+      float x = ldf(cr, off);
+      for (int p = 1; p < a.n_rsplit; ++p) {
+        const float y = ldf(split_rsrc(p), off);
+        x = maxg ? fmaxf(x, y) : x + y;
+      }
+      return x;
+    };
     const int r = (a.kp - 1) / 2;
     const float fk = (float)a.kp;
     const bool staged = r <= kPoolHalo;
@@ -183,6 +200,14 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(CompressArgs a) {
         float x[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) x[u] = ldf(cr, (uint32_t)((j0 - r + i0 + tid + u * kBlock) * 4));
+        for (int p = 1; p < a.n_rsplit; ++p) {  // the other row splits' partials, in split order
+          const rsrc_t cp = split_rsrc(p);
+          float y[U];
+#pragma unroll
+          for (int u = 0; u < U; ++u) y[u] = ldf(cp, (uint32_t)((j0 - r + i0 + tid + u * kBlock) * 4));
+#pragma unroll
+          for (int u = 0; u < U; ++u) x[u] = maxg ? fmaxf(x[u], y[u]) : x[u] + y[u];
+        }
 #pragma unroll
         for (int u = 0; u < U; ++u)
           if (i0 + tid + u * kBlock < n) win[i0 + tid + u * kBlock] = x[u];
@@ -246,7 +271,7 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(CompressArgs a) {
             const float* wp = win + (j - j0);
             for (int t = 0; t <= 2 * r; ++t) sum += wp[t];
           } else {
-            for (int t = -r; t <= r; ++t) sum += ldf(cr, (uint32_t)((j + t) * 4));
+            for (int t = -r; t <= r; ++t) sum += colsum_at((uint32_t)((j + t) * 4));
           }
           v = sum / fk;
           stf(pr, (uint32_t)(j * 4), v);

@@ -297,7 +297,23 @@ namespace {
 struct CompressPlan {
   sgdkv::CompressArgs a;
   size_t off_lse_part, off_lse2, off_colsum, off_pooled, off_hist, off_state, off_counts, bytes;
+  int colsum_splits;  // row splits the column-sum region has room for
 };
+
+// Row splits of a KV head's R = G*w window rows over score workgroups of at most kMaxSplitRows
+// rows. Group mean and the weighted Ipt. modes: as even as whole 16-row blocks allow. Ipt. max:
+// whole query heads per split (w % 16 == 0 and w <= kMaxSplitRows, checked by the caller).
+void row_splits(int R, int w, bool whole_heads, int& n, int& rows) {
+  if (whole_heads) {
+    const int heads = sgdkv::kMaxSplitRows / w;
+    rows = heads * w;
+    n = (int)ceil_div(R, rows);
+  } else {
+    n = (int)ceil_div(R, sgdkv::kMaxSplitRows);
+    rows = (int)round_up(ceil_div(R, n), 16);
+  }
+  if (n == 1) rows = R;
+}
 
 // win0 = position of the first window row (seq_len - obs_window for the default window); the
 // workspace is sized for any win0 (scores for up to seq_len keys), so its size depends on d only.
@@ -361,13 +377,22 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, int64_t win0, CompressP
   const double scale = d->scale > 0.f ? (double)d->scale : 1.0 / std::sqrt((double)d->head_dim);
   a.c2 = (float)(scale * 1.4426950408889634074);
   a.out_scale = 1.0f / (float)G;
+  row_splits(a.R, a.w, false, a.n_rsplit, a.rs_rows);
+  // the column-sum region also fits the (possibly more) splits of the Ipt. max aggregation
+  p.colsum_splits = a.n_rsplit;
+  if (a.w % 16 == 0 && a.w <= sgdkv::kMaxSplitRows) {
+    int n_heads_split = 0, rows = 0;
+    row_splits(a.R, a.w, true, n_heads_split, rows);
+    p.colsum_splits = std::max(p.colsum_splits, n_heads_split);
+  }
 
   const int64_t nseg = (int64_t)a.B * a.Hkv;
   // score workgroups: about 512 in total (two per CU, one resident at a time: fewer, longer
-  // workgroups measured faster than more, shorter ones); a chunk is a whole number of key tiles, so no
-  // tile of pass 1 reaches into the next chunk (which would count those keys twice)
+  // workgroups measured faster than more, shorter ones), counting each row split; a chunk is a
+  // whole number of key tiles, so no tile of pass 1 reaches into the next chunk (which would count
+  // those keys twice). The chunk does not depend on the aggregation, so neither does the workspace.
   a.score_chunk = std::min<int64_t>(
-      std::max<int64_t>(round_up(ceil_div(nseg * a.C, 512), sgdkv::kScoreChunkQuantum),
+      std::max<int64_t>(round_up(ceil_div(nseg * a.n_rsplit * a.C, 512), sgdkv::kScoreChunkQuantum),
                         2 * sgdkv::kScoreChunkQuantum),
       1 << 16);
   // pass 1 covers the keys some window row sees: [0, min(C, win0 + w))
@@ -387,7 +412,7 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, int64_t win0, CompressP
   p.off_lse2 = off;
   off += align256((size_t)nseg * R * sizeof(float));
   p.off_colsum = off;
-  off += align256((size_t)nseg * a.C * sizeof(float));
+  off += align256((size_t)p.colsum_splits * nseg * a.C * sizeof(float));
   p.off_pooled = off;
   off += align256((size_t)nseg * a.C * sizeof(float));
   p.off_hist = off;
@@ -509,8 +534,10 @@ sgdkv_status sgdkv_compress_layer_ex(const sgdkv_compress_desc* desc, const sgdk
     if (!qhead_scores) return fail(SGDKV_ERR_INVALID_ARG, "group_agg %d needs qhead_scores", group_agg);
     if (a.Hq > sgdkv::kMaxIptQHeads)
       return fail(SGDKV_ERR_UNSUPPORTED, "num_q_heads %d > %d with an Ipt. aggregation", a.Hq, sgdkv::kMaxIptQHeads);
-    if (group_agg == SGDKV_GROUP_IPT_MAX && a.w % 16 != 0)
-      return fail(SGDKV_ERR_UNSUPPORTED, "Ipt. max needs obs_window %% 16 == 0 (got %d)", a.w);
+    if (group_agg == SGDKV_GROUP_IPT_MAX && (a.w % 16 != 0 || a.w > sgdkv::kMaxSplitRows))
+      return fail(SGDKV_ERR_UNSUPPORTED, "Ipt. max needs obs_window %% 16 == 0 and <= %d (got %d)",
+                  sgdkv::kMaxSplitRows, a.w);
+    if (group_agg == SGDKV_GROUP_IPT_MAX) row_splits(a.R, a.w, true, a.n_rsplit, a.rs_rows);
     for (int q = 0; q < a.Hq; ++q)
       if (!(qhead_scores[q] >= 0.0) || std::isinf(qhead_scores[q]))
         return fail(SGDKV_ERR_INVALID_ARG, "qhead_scores[%d] is %g", q, qhead_scores[q]);

@@ -9,7 +9,8 @@
 namespace sgdkv {
 
 constexpr int kMaxKvHeads = 64;    // per-head tables travel by value in kernel arguments
-constexpr int kMaxGroupRows = 512; // G*w rows of one KV head's window queries
+constexpr int kMaxSplitRows = 512; // window rows one score workgroup holds (a row split)
+constexpr int kMaxGroupRows = 4096; // G*w rows of one KV head's window queries, over all row splits
 constexpr int kMaxDecodeGroup = 16;
 constexpr int kMaxIptQHeads = 256;  // query heads per layer the Ipt. aggregations accept
 constexpr int kBlock = 256;        // threads per workgroup in every kernel
@@ -63,10 +64,15 @@ struct CompressArgs {
   // workspace regions
   float* lse_part;  // [B*Hkv][n_lse_chunks][R][2]  (m, s) in base-2 units
   float* lse2;      // [B*Hkv][R]                   base-2 LSE of each window row
-  float* colsum;    // [B*Hkv][n_scored]
+  float* colsum;    // [n_rsplit][B*Hkv][n_scored]: one column-sum partial per row split
   uint32_t* hist;   // [B*Hkv][4][256]: histogram of each radix digit
   uint32_t* state;  // [B*Hkv][4]: tau, its mask, q (rows equal to tau to keep), unused
   uint32_t* counts; // [B*Hkv][n_sel_chunks][4]: fixed, greater, equal, unused
+  // row splits: the R window rows of a KV head are split over n_rsplit score workgroups per key
+  // chunk (grid z), split p holding rows [p*rs_rows, min(R, (p+1)*rs_rows)); rs_rows is a
+  // multiple of 16 (of w for the Ipt. max aggregation, so that no query head straddles two)
+  int n_rsplit;
+  int rs_rows;
   // chunking
   int64_t score_chunk;  // keys per score workgroup (multiple of kScoreChunkQuantum)
   int n_lse_chunks;     // ceil(min(C, win0 + w) / score_chunk): keys some window row sees

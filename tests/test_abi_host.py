@@ -201,7 +201,8 @@ def test_compress_validation():
         (_desc(pool_kernel=4), good, None, None, sg.ERR_INVALID_ARG),
         (_desc(b_window=16), good, None, None, sg.ERR_INVALID_ARG),          # W < w
         (_desc(b_sink=2000, b_window=100), good, None, None, sg.ERR_INVALID_ARG),
-        (_desc(num_q_heads=64, num_kv_heads=2, obs_window=32), good, None, None, sg.ERR_UNSUPPORTED),  # G*w
+        (_desc(num_q_heads=64, num_kv_heads=2, obs_window=160, b_window=160), good, None, None,
+         sg.ERR_UNSUPPORTED),                                                  # G*w = 5120 > 4096
         (_desc(num_kv_heads=65, num_q_heads=65), [512] * 65, None, None, sg.ERR_UNSUPPORTED),
         (_desc(dtype=5), good, None, None, sg.ERR_INVALID_ARG),
         (_desc(scale=-1.0), good, None, None, sg.ERR_INVALID_ARG),
@@ -243,6 +244,8 @@ def test_compress_options_validation():
         (_desc(), sg.GROUP_IPT_MEAN, [0.5, -0.2, 0.1, 0.9], -1, sg.ERR_INVALID_ARG, "qhead"),
         (_desc(), sg.GROUP_IPT_ONLY, [0.5, np.nan, 0.1, 0.9], -1, sg.ERR_INVALID_ARG, "qhead"),
         (_desc(obs_window=20), sg.GROUP_IPT_MAX, four, -1, sg.ERR_UNSUPPORTED, "Ipt"),  # w % 16
+        (_desc(num_q_heads=2, obs_window=528, b_window=528), sg.GROUP_IPT_MAX, [0.5, 0.2], -1,
+         sg.ERR_UNSUPPORTED, "Ipt"),                                           # one head beyond a split
         (_desc(num_q_heads=320, num_kv_heads=64, obs_window=32), sg.GROUP_IPT_MEAN, [0.1] * 320, -1,
          sg.ERR_UNSUPPORTED, "num_q_heads"),                                   # too many query heads
         (_desc(), 0, None, -2, sg.ERR_INVALID_ARG, "window_pos"),
@@ -270,6 +273,19 @@ def test_workspace_size_independent_of_budgets():
     n = sg.compress_workspace_size(_desc())
     assert n > 0 and n % 256 == 0
     assert sg.compress_workspace_size(_desc(batch=2)) > n
+
+
+def test_window_rows_beyond_one_workgroup():
+    """G*w up to 4096 window rows per KV head: the rows are split over several score workgroups,
+    each leaving its own column-sum partial, so the workspace grows with the number of splits."""
+    one = sg.compress_workspace_size(_desc(num_q_heads=16, num_kv_heads=2, obs_window=64, b_window=64))  # 512 rows
+    two = sg.compress_workspace_size(_desc(num_q_heads=16, num_kv_heads=2, obs_window=128, b_window=128))
+    assert two - one >= 2 * 2048 * 4  # a second [B*Hkv][C] fp32 partial, and a larger LSE region
+    big = _desc(num_q_heads=64, num_kv_heads=2, obs_window=128, b_window=128)  # 4096 rows: 8 splits
+    assert sg.compress_workspace_size(big) > two
+    if not _gpu():  # validation passes, then no device
+        assert _compress(big, [512, 512]) == sg.ERR_HIP
+        assert _compress_ex(big, sg.GROUP_IPT_MAX, [0.5] * 64) == sg.ERR_HIP
 
 
 def _decode(desc, offsets_host, ptrs=None, ws_bytes=None, ws=FAKE):

@@ -13,6 +13,7 @@ compares with the oracle on the same seeded inputs:
 * decode: the oracle's compressed cache fed to the GPU decode, within 1e-5
   absolute for fp32 inputs and 2e-2 absolute (fp32 output) for bf16 inputs.
 """
+import dataclasses
 import math
 
 import numpy as np
@@ -241,6 +242,69 @@ def test_ipt_group_aggregation(agg, B, C, Hq, Hkv, d, w):
         plain = sg.compress_layer(t["q_win"], t["k"], t["v"], budgets, pool_kernel=7, b_sink=s, b_window=W)
         torch.cuda.synchronize()
         assert torch.equal(one["scores"], plain["scores"]) and torch.equal(one["kept_pos"], plain["kept_pos"])
+
+
+# ---------------------------------------------------------------------- window rows over several workgroups
+# A KV head's G*w window rows beyond 512 are split over several score workgroups per key chunk
+# (the paper's Query-Aware window is the last 128 tokens, Sec. 5: 896 rows for GQA groups of 7,
+# 1024 for groups of 8).
+@pytest.mark.parametrize("key,dtype", [("qwen25_32k", torch.bfloat16), ("qwen25_32k", torch.float32),
+                                       ("qwen3_256k", torch.bfloat16), ("qwen3_256k", torch.float32)],
+                         ids=["g7-bf16", "g7-f32", "g8-bf16", "g8-f32"])
+def test_window_128_at_32k(key, dtype):
+    """The 128-token window at a 32K prompt with the Qwen2.5-7B (28/4) and Qwen3-32B (64/8) head
+    layouts, against the oracle end to end, decode included. bf16 inputs are drawn like the bf16
+    workloads (heavy-hitter and sink rows); fp32 inputs like the fp32 workload, N(0,1), to which
+    the fp32 decode tolerance applies."""
+    wl = dataclasses.replace(workloads.WORKLOADS[key], obs_window=128)
+    C, w, kp, s, W = 32768, 128, wl.pool_kernel, wl.b_sink, wl.b_window
+    Hq, Hkv = wl.num_q_heads, wl.num_kv_heads
+    if dtype == torch.bfloat16:
+        t = workloads.torch_layer_tensors(wl, 0, DEV, batch=1, seq_len=C, dtype=dtype)
+    else:
+        t = {n: torch.from_numpy(x).to(DEV) for n, x in workloads.numpy_tensors(wl, batch=1, seq_len=C).items()}
+    sc = workloads.head_scores(wl)[:Hkv]
+    total = sg.total_from_ratio(0.25, 1, Hkv, C, s, W)
+    budgets = sg.allocate_budgets(sc, 1, Hkv, C, s, W, total)
+    _announce(f"window 128 {key} {dtype}: Hq={Hq} Hkv={Hkv} rows={Hq // Hkv * w} budgets={budgets.tolist()}")
+    rtol = _score_rtol(t["q_win"])
+    res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=kp, s=s, W=W)
+    worst = _check_scores(res["scores"].cpu().numpy(), orc["pooled"], f"w128 {key}", rtol=rtol)
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, f"w128 {key}", rtol=rtol)
+    _check_gather(res, t["k"], t["v"], budgets)
+    atol = 2e-2 if dtype == torch.bfloat16 else 1e-5
+    _decode_on_oracle_cache(orc, t["q"], Hkv, dtype, atol, f"w128 {key}")
+    _announce(f"window 128 {key} {dtype}: worst score rel err {worst:.3e}")
+
+
+@pytest.mark.parametrize("agg", [sg.GROUP_MEAN, sg.GROUP_IPT_MAX, sg.GROUP_IPT_MEAN, sg.GROUP_IPT_ONLY])
+@pytest.mark.parametrize("Hq,Hkv,w,dtype", [(28, 4, 128, torch.bfloat16), (10, 2, 208, torch.float32),
+                                            (18, 2, 100, torch.bfloat16)], ids=["g7w128", "g5w208", "g9w100"])
+def test_row_splits_with_every_aggregation(agg, Hq, Hkv, w, dtype):
+    """Row splits that are uneven or cut through query heads: 896 rows as 448 + 448 (Ipt. max: heads
+    0-3 and 4-6), 1040 rows as 352 + 352 + 336 (Ipt. max: 416 + 416 + 208), 900 rows as 464 + 436
+    (Ipt. max is not built for a window that is not a multiple of 16). Each against the oracle,
+    with a zero score and a tie for the top of a group among the Ipt. weights."""
+    if agg == sg.GROUP_IPT_MAX and w % 16:
+        pytest.skip("Ipt. max needs obs_window % 16 == 0")
+    B, C, d = 2, 3000, 128 if dtype == torch.bfloat16 else 64
+    wl, t = _qwen_small(B, C, Hq=Hq, Hkv=Hkv, d=d, w=w)
+    if dtype != torch.bfloat16:
+        t = {k: x.float() for k, x in t.items()}
+    s, W = wl.b_sink, max(wl.b_window, w)
+    rng = np.random.Generator(np.random.PCG64(77 + agg))
+    qs = rng.beta(0.5, 2.0, size=Hq)
+    qs[1] = 0.0
+    G = Hq // Hkv
+    qs[G] = qs[G + 1] = qs.max() + 0.05
+    budgets = np.maximum(np.array([int(C * f) for f in (0.3, 0.45, 0.25, 0.4)[:Hkv]]), s + W)
+    _announce(f"row splits agg={agg} Hq={Hq} Hkv={Hkv} w={w} rows={G * w} {dtype}")
+    res, orc = _compress_both(t["q_win"], t["k"], t["v"], budgets, kp=7, s=s, W=W, agg=agg,
+                              qhead_scores=None if agg == sg.GROUP_MEAN else qs)
+    rtol = _score_rtol(t["q_win"])
+    _check_scores(res["scores"].cpu().numpy(), orc["pooled"], f"splits agg={agg}", rtol=rtol)
+    _check_kept(res, orc, t["q_win"].shape, C, w, s, W, budgets, f"splits agg={agg}", rtol=rtol)
+    _check_gather(res, t["k"], t["v"], budgets)
 
 
 @pytest.mark.parametrize("case", ["unaware", "proxy", "unaware_ipt_max", "tiny_proxy", "tiny_unaware"])
@@ -651,30 +715,83 @@ def test_long_window_spans_masked_tiles(w, W):
 
 # ---------------------------------------------------------------------- full workload sizes
 # Each workload at its full shape and batch, with the launch configuration the benchmark times
-# (layer 0 of the workload's stack, budgets from the 25 % allocation over every layer's heads).
-# Every sequence is checked by what holds at any size: offsets, the kept set equal to the top-k
-# of the GPU's own scores, the gathered rows equal to the input rows. The oracle then runs the
-# whole layer on the listed sequences: scores, kept sets and decode are compared element by
-# element there.
-FULL_CASES = [("qwen25_32k", (0,)), ("qwen25_128k", (0, 7)), ("qwen3_256k", (15,)), ("qwen25_1m", (31,))]
-
-
-@pytest.mark.parametrize("key,oracle_seqs", FULL_CASES, ids=[c[0] for c in FULL_CASES])
-def test_full_size(key, oracle_seqs):
+# (budgets from the allocation over every layer's heads at the given ratio). Every sequence is
+# checked by what holds at any size: offsets, the kept set equal to the top-k of the GPU's own
+# scores, the gathered rows equal to the input rows. The oracle then runs the whole layer on the
+# listed sequences: scores, kept sets and decode are compared element by element there.
+#
+# The 128K stack (28 layers x 4 KV heads, batch 8) at its three budgets: at 50 % Algorithm 1 caps
+# the heads whose share exceeds the middle (Appendix A.1), and the layer with the most capped
+# heads is checked too. Variants at 128K x 8: Ipt. max group aggregation (Appendix A.7), the
+# Query-Unaware window before a 256-token question (Sec. 5), 64 rows appended after compression,
+# and the paper's 128-token window (896 rows per KV head, two row splits).
+def _capped_layer(key, ratio):
     wl = workloads.WORKLOADS[key]
+    L, Hkv, C, s, W = wl.layers, wl.num_kv_heads, wl.seq_len, wl.b_sink, wl.b_window
+    total = sg.total_from_ratio(ratio, L, Hkv, C, s, W)
+    full = (sg.allocate_budgets(workloads.head_scores(wl), L, Hkv, C, s, W, total).reshape(L, Hkv) == C).sum(axis=1)
+    return int(np.argmax(full))  # the first layer with the most heads kept in full
+
+
+FULL_CASES = [
+    ("qwen25_32k", 0.25, 0, "plain", (0,)),
+    ("qwen25_128k", 0.25, 0, "plain", (0, 7)),
+    ("qwen25_128k", 0.25, 13, "plain", (3,)),
+    ("qwen25_128k", 0.25, 27, "plain", (5,)),
+    ("qwen25_128k", 0.10, 0, "plain", (2,)),
+    ("qwen25_128k", 0.50, 0, "plain", (6,)),
+    ("qwen25_128k", 0.50, "capped", "plain", (1,)),
+    ("qwen25_128k", 0.25, 0, "ipt_max", (4,)),
+    ("qwen25_128k", 0.25, 0, "unaware", (1,)),
+    ("qwen25_128k", 0.25, 0, "append64", (0,)),
+    ("qwen25_128k", 0.25, 0, "w128", (7,)),
+    ("qwen3_256k", 0.25, 0, "plain", (15,)),
+    ("qwen25_1m", 0.25, 0, "plain", (31,)),
+]
+
+
+@pytest.mark.parametrize("key,ratio,layer,variant,oracle_seqs", FULL_CASES,
+                         ids=[f"{c[0]}-r{int(c[1] * 100)}-L{c[2]}-{c[3]}" for c in FULL_CASES])
+def test_full_size(key, ratio, layer, variant, oracle_seqs):
+    wl = workloads.WORKLOADS[key]
+    if variant == "w128":
+        wl = dataclasses.replace(wl, obs_window=128)
+    if layer == "capped":
+        layer = _capped_layer(key, ratio)
     L, B, Hq, Hkv, d, C = wl.layers, wl.batch, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.seq_len
     w, kp, s, W = wl.obs_window, wl.pool_kernel, wl.b_sink, wl.b_window
     sc = workloads.head_scores(wl)
-    total = sg.total_from_ratio(0.25, L, Hkv, C, s, W)
+    agg, qs = 0, None
+    if variant == "ipt_max":
+        # per-attention-head scores as the benchmark draws them; the allocation takes their group maxima
+        qall = np.random.Generator(np.random.PCG64(wl.seed + 200)).beta(0.5, 2.0, size=(L, Hq))
+        sc = sg.reduce_query_head_scores(qall, Hkv).reshape(-1)
+        assert np.array_equal(sc, oracle.reduce_group_max(qall, Hkv).reshape(-1))
+        agg, qs = sg.GROUP_IPT_MAX, qall[layer]
+    win0 = C - 256 - w if variant == "unaware" else None
+    total = sg.total_from_ratio(ratio, L, Hkv, C, s, W)
     budgets_all = sg.allocate_budgets(sc, L, Hkv, C, s, W, total)
     assert np.array_equal(budgets_all, oracle.allocate_budgets(sc, L, Hkv, C, s, W, total))
-    budgets = budgets_all.reshape(L, Hkv)[0]
-    _announce(f"full size {wl.name}: B={B} C={C} Hq={Hq} Hkv={Hkv} budgets={budgets.tolist()}")
-    t = workloads.torch_layer_tensors(wl, 0, DEV)
+    budgets = budgets_all.reshape(L, Hkv)[layer]
+    n_full = int((budgets == C).sum())
+    _announce(f"full size {wl.name} ratio {ratio} layer {layer} {variant}: B={B} C={C} Hq={Hq} Hkv={Hkv} "
+              f"budgets={budgets.tolist()} ({n_full} heads kept in full)")
+    if layer == 0 and ratio == 0.50 and key == "qwen25_128k":
+        assert (budgets_all == C).sum() > 0, "the 50 % stack caps some heads"
+    t = workloads.torch_layer_tensors(wl, layer, DEV)
     rtol = _score_rtol(t["q_win"])
-    res = sg.compress_layer(t["q_win"], t["k"], t["v"], budgets, pool_kernel=kp, b_sink=s, b_window=W)
+    res = sg.compress_layer(t["q_win"], t["k"], t["v"], budgets, pool_kernel=kp, b_sink=s, b_window=W,
+                            group_agg=agg, qhead_scores=qs, window_pos=-1 if win0 is None else win0)
+    tail, n_new = {}, 0
+    if variant == "append64":
+        n_new = 64
+        gen = torch.Generator(device=DEV)
+        gen.manual_seed(wl.seed + 300)
+        k_new = torch.randn((B, Hkv, n_new, d), generator=gen, device=DEV).to(t["k"].dtype)
+        v_new = torch.randn((B, Hkv, n_new, d), generator=gen, device=DEV).to(t["k"].dtype)
+        tail = dict(k_new=k_new, v_new=v_new, n_new=n_new)
     out, lse = sg.decode_attention(t["q"], res["k_c"], res["v_c"], res["offsets"], res["offsets_host"], Hkv,
-                                   out_dtype=torch.float32)
+                                   out_dtype=torch.float32, **tail)
     torch.cuda.synchronize()
     offs = res["offsets"].cpu().numpy()
     assert np.array_equal(offs, res["offsets_host"])
@@ -687,30 +804,37 @@ def test_full_size(key, oracle_seqs):
     for b in range(B):
         for h in range(Hkv):
             seg = kept[offs[b * Hkv + h]:offs[b * Hkv + h + 1]]
-            ref = oracle.select(scores[b, h].astype(np.float64), C, w, s, W, int(budgets[h]) - s - W)
+            ref = oracle.select(scores[b, h].astype(np.float64), C, w, s, W, int(budgets[h]) - s - W, win0=win0)
             assert np.array_equal(seg, ref), f"b={b} h={h}: kept set differs from top-k of GPU scores"
     _check_gather(res, t["k"], t["v"], budgets)
-    _announce(f"full size {wl.name}: properties hold for all {B} sequences; oracle on {list(oracle_seqs)}")
+    _announce(f"full size {wl.name} {variant}: properties hold for all {B} sequences; oracle on {list(oracle_seqs)}")
     for b in oracle_seqs:
         orc = oracle.compress(_f64(t["q_win"][b:b + 1]), _f64(t["k"][b:b + 1]), _f64(t["v"][b:b + 1]), budgets,
-                              w=w, kp=kp, s=s, W=W)
+                              w=w, kp=kp, s=s, W=W, agg=agg, qhead_scores=qs, win0=win0)
         worst = _check_scores(scores[b:b + 1], orc["pooled"], f"full {key} b={b}", rtol=rtol)
+        cend = C - W
         for h in range(Hkv):
             seg = kept[offs[b * Hkv + h]:offs[b * Hkv + h + 1]]
             ref = orc["kept_pos"][orc["offsets"][h]:orc["offsets"][h + 1]]
             if not np.array_equal(seg, ref):
                 po = orc["pooled"][0, h]
-                tau = np.sort(po[s:C - W])[::-1][int(budgets[h]) - s - W - 1]
+                tau = np.sort(po[s:cend])[::-1][int(budgets[h]) - s - W - 1]
                 diff = np.setxor1d(seg, ref)
                 assert np.all(np.abs(po[diff] - tau) <= rtol * tau), \
                     f"full {key} b={b} h={h}: kept sets differ outside the near-tie band"
         del orc
         # decode of this sequence over the GPU's compressed cache (shown above to be the input rows)
         lo, hi = offs[b * Hkv], offs[(b + 1) * Hkv]
-        ref_out, ref_lse = oracle.decode(_f64(t["q"][b:b + 1]), _f64(res["k_c"][lo:hi]), _f64(res["v_c"][lo:hi]),
-                                         offs[b * Hkv:(b + 1) * Hkv + 1] - lo, Hkv)
+        seg_offs = offs[b * Hkv:(b + 1) * Hkv + 1] - lo
+        if n_new:
+            ref_out, ref_lse = oracle.decode_append(_f64(t["q"][b:b + 1]), _f64(res["k_c"][lo:hi]),
+                                                    _f64(res["v_c"][lo:hi]), seg_offs, _f64(k_new[b:b + 1]),
+                                                    _f64(v_new[b:b + 1]), n_new, Hkv)
+        else:
+            ref_out, ref_lse = oracle.decode(_f64(t["q"][b:b + 1]), _f64(res["k_c"][lo:hi]), _f64(res["v_c"][lo:hi]),
+                                             seg_offs, Hkv)
         err = np.abs(out[b:b + 1].cpu().numpy() - ref_out).max()
         assert err <= 2e-2, f"full {key} b={b}: decode max abs err {err:.3e}"
         assert np.abs(lse[b:b + 1].cpu().numpy() - ref_lse).max() <= 2e-2
-        _announce(f"full size {wl.name}: sequence {b} matches the oracle (worst score rel err {worst:.3e}, "
+        _announce(f"full size {wl.name} {variant}: sequence {b} matches the oracle (worst score rel err {worst:.3e}, "
                   f"decode err {err:.2e})")
