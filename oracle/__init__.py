@@ -96,6 +96,12 @@ def num_threads() -> int:
     return int(_load().orc_num_threads())
 
 
+def set_num_threads(n: int) -> None:
+    """OpenMP threads of the oracle's later calls from this thread (its libgomp is the process's)."""
+    _load()
+    ctypes.CDLL("libgomp.so.1").omp_set_num_threads(int(n))
+
+
 # --------------------------------------------------------------- allocation
 def reduce_group_max(per_q, num_kv_heads: int) -> np.ndarray:
     """[L, Hq] per-query-head scores -> [L, Hkv], max over each group (Appendix A.7)."""

@@ -1,6 +1,6 @@
 """Host-side logic of bench.py (no GPU): the one-GPU guard, the issue-bound peak of the score
-passes, the source hash that ties stored counters to the code, and the traffic summary's
-calibration arithmetic."""
+passes, the compression roofline, the source hash that ties stored counters to the code, and the
+traffic summary's calibration arithmetic."""
 import json
 import os
 import shutil
@@ -28,6 +28,21 @@ def test_score_issue_peak():
     lanes = 256 * 4 * 32 * 2.4e9
     assert t == pytest.approx(256 / 2.5e15 + 4 / lanes + 2 / lanes, rel=1e-12)
     assert 2 * 128 / t / 1e12 == pytest.approx(1432.6, abs=0.1)
+
+
+def test_compression_roof_of_the_128k_layer():
+    # 128K prompt, batch 8, 28/4 heads, d 128, w 64, bf16, a 25 % layer (T = 4 * 32768 rows):
+    # MFMA 2*28*64*128*131072*8 flops = 481 GFLOP at 2.5 PFLOP/s = 192 us; HBM per sequence
+    # 2*(4*131072*128 + 4*131072*128) + 4*131072 + 2*28*64*128 bytes = 269.4 MB over 8 TB/s
+    roof, roof2 = bench.compress_roof_seconds(8, 131072, 28, 4, 128, 64, 2, 131072.0, "bf16")
+    hbm = 8 * (2 * (4 * 131072 * 128 + 4 * 131072 * 128) + 4 * 131072 + 2 * 28 * 64 * 128)
+    assert roof == pytest.approx(hbm / 8e12, rel=1e-12)
+    assert roof * 1e6 == pytest.approx(269.4, abs=0.1)
+    # computing the window LSE too: the GEMM twice (384.8 us) against K read twice (403.6 us)
+    k = 8 * 2 * 4 * 131072 * 128
+    assert roof2 == pytest.approx(max(2 * 8 * 2 * 28 * 64 * 128 * 131072 / 2.5e15, (hbm + k) / 8e12), rel=1e-12)
+    assert roof / roof2 == pytest.approx(0.6675, abs=1e-4)
+    assert bench.percentile([5, 1, 4, 2, 3], 0.5) == 3 and bench.percentile([1, 2], 0.1) == pytest.approx(1.1)
 
 
 def test_source_hash_ignores_comments_but_not_code(tmp_path, monkeypatch):
@@ -66,8 +81,8 @@ def test_traffic_summary_scales_by_the_copy(tmp_path, monkeypatch):
     _csv(tmp_path / "w.csv", "WRITE_SIZE", [(fill, kib), (copy, kib), (copy, kib), (copy, kib),
                                             (copy, 9 * kib), (fill, 4 * kib), (gather, 50.0), (gather, 50.0)])
     out = tmp_path / "traffic.json"
-    monkeypatch.setattr(bench, "traffic_path", lambda w, r: str(out))
-    args = type("A", (), dict(calibrate_copy_mib=mib, workload="toy", ratio=0.25))()
+    monkeypatch.setattr(bench, "traffic_path", lambda wl, r, w: str(out))
+    args = type("A", (), dict(calibrate_copy_mib=mib, workload="tiny", ratio=0.25, obs_window=0))()
     bench.summarize_traffic(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), args)
     d = json.loads(out.read_text())
     ff = kib / (kib / 2 + 2)  # median of the three copies' fetch
