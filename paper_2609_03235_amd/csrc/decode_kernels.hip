@@ -6,15 +6,16 @@
 //
 //   decode_split: each wave owns one split of a segment's rows: the splits of
 //     a segment take its 16-row steps in turn, so together they sweep the
-//     segment front to back (a wave keeps its own partial). Logits of the
-//     G heads against 16 keys at a time are one 16x16 MFMA (the G query rows
-//     padded to 16 form the A operand). The wave keeps an online softmax
-//     (running max m and sum s per head, base-2 units) and accumulates P.V in
-//     fp32 on the vector ALU (bf16 V rows are widened exactly); the next
-//     step's K and V are already in flight. One partial (m, s, o[d]) per head
-//     and chunk is written; waves never synchronise with each other.
+//     segment front to back. Logits of the G heads against 16 keys at a time
+//     are one 16x16 MFMA (the G query rows padded to 16 form the A operand).
+//     The wave keeps an online softmax (running max m and sum s per head,
+//     base-2 units) and accumulates P.V in fp32 on the vector ALU (bf16 V
+//     rows are widened exactly); the next step's K and V are already in
+//     flight. The four waves of a workgroup are four neighbouring splits of
+//     one segment: at the end they merge their partials through LDS, in wave
+//     order, and the workgroup writes one partial (m, s, o[d]) per head.
 //   decode_combine: per (sequence, query head), a fixed-order log-sum-exp
-//     merge of the chunk partials; out = o/s, lse = (m + log2 s) * ln 2.
+//     merge of the workgroup partials; out = o/s, lse = (m + log2 s) * ln 2.
 //
 // Work is a flattened (chunk, segment) grid, so unequal budgets (one head
 // with most of the rows, others with few) still spread over the whole chip.
@@ -220,12 +221,15 @@ __device__ __forceinline__ void decode_chunk(const DecodeArgs& a, float (*pls)[1
 // CPL = value columns per lane; GM = compile-time bound on the group size (8
 // or 16); PF = steps of K/V in flight ahead of the one being computed; OCC =
 // workgroups per CU the registers are sized for. Each wave owns one split of
-// a segment: split index = 4*blockIdx.x + wave.
+// a segment: split index = 4*x + wave within the workgroup's region (the
+// segment's compressed rows for x < n_cwg, its appended rows after them).
 template <typename T, int D, int CPL, int GM, int PF, int OCC>
 __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a) {
   using S = DecodeStep<T, D, CPL>;
   __shared__ __attribute__((aligned(16))) float pls[kWaves][2][16][16];  // probabilities [key][head]
   __shared__ __attribute__((aligned(16))) float als[kWaves][2][16];      // per-head rescale (exact pass)
+  __shared__ float mws[kWaves][16], sws[kWaves][16];                     // each wave's (m, s) per head
+  __shared__ __attribute__((aligned(16))) float ows[kWaves][GM][D];      // each wave's o per head
 
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
@@ -233,31 +237,35 @@ __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a)
   int64_t r0, r1;
   clamp_segment(a, seg, r0, r1);
   const int64_t len = r1 - r0;
-  // splits 0 .. n_chunk_max-1 cover the segment's compressed rows, the next ones the rows
-  // appended since compression; a wave whose split is empty leaves (waves never synchronise)
-  const int64_t chunk = (int64_t)blockIdx.x * kWaves + wid;
-  const bool appended = chunk >= a.n_chunk_max;
+  // workgroups 0 .. n_cwg-1 cover the segment's compressed rows, the next ones the rows appended
+  // since compression. A workgroup whose first split is empty leaves (uniform over the
+  // workgroup); a wave whose own split is empty joins the merge with an empty partial.
+  const bool appended = (int)blockIdx.x >= a.n_cwg;
+  const int64_t wg = appended ? (int64_t)blockIdx.x - a.n_cwg : (int64_t)blockIdx.x;
+  const int64_t chunk = wg * kWaves + wid;  // split index within the region
   const int64_t rows = appended ? a.n_new : len;
   // The compressed rows of a segment are dealt to its nck splits 16 rows at a time (split w
   // takes steps w, w + nck, ...), so the splits of a segment sweep it together from front to
   // back; appended rows form contiguous splits.
-  int64_t c0, stride, c1;
-  int nsteps;
+  int64_t c0 = 0, stride = 16, c1 = 0;
+  int nsteps = 0;
+  bool active;
   if (appended) {
-    c0 = (chunk - a.n_chunk_max) * a.chunk;
-    if (c0 >= rows) return;
-    stride = 16;
+    if (wg * kWaves * a.chunk >= rows) return;
+    c0 = chunk * a.chunk;
+    active = c0 < rows;
     c1 = c0 + a.chunk < rows ? c0 + a.chunk : rows;
-    nsteps = (int)((c1 - c0 + 15) / 16);
+    nsteps = active ? (int)((c1 - c0 + 15) / 16) : 0;
   } else {
     int64_t nck = (rows + a.chunk - 1) / a.chunk;
     if (nck > a.n_chunk_max) nck = a.n_chunk_max;  // device offsets beyond the host's: fewer, longer splits
     const int64_t total_steps = (rows + 15) / 16;
-    if (chunk >= nck) return;
+    if (wg * kWaves >= nck) return;
+    active = chunk < nck;
     c0 = chunk * 16;
     stride = nck * 16;
     c1 = rows;
-    nsteps = (int)((total_steps - chunk + nck - 1) / nck);
+    nsteps = active ? (int)((total_steps - chunk + nck - 1) / nck) : 0;
   }
 
   const int lr = lane & 15, lgp = lane >> 4;
@@ -275,18 +283,30 @@ __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a)
   for (int c = 0; c < S::NC; ++c) qa[c] = gload_frag<T>(qr, (uint32_t)(lr * S::RB + (32 * c + 8 * lgp) * S::EB));
 
   float m[4], s[4], o[GM][CPL];
-  decode_chunk<T, D, CPL, GM, PF, false>(a, pls[wid], als[wid], kr, vr, c0, stride, c1, nsteps, qa, lane, m, s, o);
-  // 2^64 bounds every probability, so s and o stay finite unless V is huge or the
-  // first step's maximum sat far below a later logit: then redo with rescaling
-  bool bad = false;
+  if (active) {
+    decode_chunk<T, D, CPL, GM, PF, false>(a, pls[wid], als[wid], kr, vr, c0, stride, c1, nsteps, qa, lane, m, s, o);
+    // 2^64 bounds every probability, so s and o stay finite unless V is huge or the
+    // first step's maximum sat far below a later logit: then redo with rescaling
+    bool bad = false;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) bad |= !(s[i] <= 1.8446744073709552e19f);
+    for (int i = 0; i < 4; ++i) bad |= !(s[i] <= 1.8446744073709552e19f);
 #pragma unroll
-  for (int g = 0; g < GM; ++g)
+    for (int g = 0; g < GM; ++g)
 #pragma unroll
-    for (int e = 0; e < CPL; ++e) bad |= !(fabsf(o[g][e]) < INFINITY);
-  if (__any(bad))
-    decode_chunk<T, D, CPL, GM, PF, true>(a, pls[wid], als[wid], kr, vr, c0, stride, c1, nsteps, qa, lane, m, s, o);
+      for (int e = 0; e < CPL; ++e) bad |= !(fabsf(o[g][e]) < INFINITY);
+    if (__any(bad))
+      decode_chunk<T, D, CPL, GM, PF, true>(a, pls[wid], als[wid], kr, vr, c0, stride, c1, nsteps, qa, lane, m, s, o);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      m[i] = -INFINITY;
+      s[i] = 0.f;
+    }
+#pragma unroll
+    for (int g = 0; g < GM; ++g)
+#pragma unroll
+      for (int e = 0; e < CPL; ++e) o[g][e] = 0.f;
+  }
 
   // Reduce within the wave: the 16 lanes of each head's sum, the KG key groups of o.
 #pragma unroll
@@ -300,109 +320,145 @@ __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a)
       for (int sft = S::LPR; sft < 64; sft <<= 1) x += __shfl_xor(x, sft, 64);
       o[g][e] = x;
     }
-  // write this chunk's partial for each of the G heads: (m, s) and o[D] in two arrays, one
-  // descriptor each for the whole group (per-lane descriptors would cost waterfall loops)
-  const int64_t bq0 = (int64_t)b * a.Hq + (int64_t)h * G;
-  const int64_t ncm = a.n_part;
+  // Merge the workgroup's splits: each wave leaves its (m, s) and o per head in LDS; then the
+  // workgroup's threads merge them in wave order and write one partial per head at slot x:
+  // (m, s) and o[D] in two arrays, one descriptor each for the whole group (per-lane descriptors
+  // would cost waterfall loops).
   if (lr == 0) {
-    const rsrc_t mr = make_rsrc(a.part_ms + bq0 * ncm * 2, (uint64_t)G * ncm * 8);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int hd = 4 * lgp + i;
-      if (hd < G)
-        st64(mr, (uint32_t)(((int64_t)hd * ncm + chunk) * 8),
-             (uint64_t)__float_as_uint(m[i]) | ((uint64_t)__float_as_uint(s[i]) << 32));
+      mws[wid][4 * lgp + i] = m[i];
+      sws[wid][4 * lgp + i] = s[i];
     }
   }
   const int kg = lane / S::LPR, col0 = CPL * (lane % S::LPR);
   if (kg == 0) {
-    const rsrc_t orr = make_rsrc(a.part + bq0 * ncm * D, (uint64_t)G * ncm * D * 4);
 #pragma unroll
-    for (int g = 0; g < GM; ++g) {
-      if (g < G) {
+    for (int g = 0; g < GM; ++g)
 #pragma unroll
-        for (int e = 0; e < CPL; e += 4)
-          st128(orr, (uint32_t)((((int64_t)g * ncm + chunk) * D + col0 + e) * 4),
-                u32x4{__float_as_uint(o[g][e]), __float_as_uint(o[g][e + 1]), __float_as_uint(o[g][e + 2]),
-                      __float_as_uint(o[g][e + 3])});
-      }
+      for (int e = 0; e < CPL; e += 4)
+        *reinterpret_cast<f32x4*>(&ows[wid][g][col0 + e]) = f32x4{o[g][e], o[g][e + 1], o[g][e + 2], o[g][e + 3]};
+  }
+  __syncthreads();
+  const int64_t bq0 = (int64_t)b * a.Hq + (int64_t)h * G;
+  const int64_t ncm = a.n_part;
+  const uint32_t slot = blockIdx.x;
+  const rsrc_t mr = make_rsrc(a.part_ms + bq0 * ncm * 2, (uint64_t)G * ncm * 8);
+  const rsrc_t orr = make_rsrc(a.part + bq0 * ncm * D, (uint64_t)G * ncm * D * 4);
+  for (int idx = tid; idx < G * D; idx += kBlock) {
+    const int g = idx / D, col = idx % D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, mws[w][g]);
+    float O = 0.f, Ssum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float mw = mws[w][g];
+      const float e = mw == -INFINITY ? 0.f : fast_exp2(mw - M);
+      O += ows[w][g][col] * e;
+      Ssum += sws[w][g] * e;
     }
+    stf(orr, (uint32_t)((((int64_t)g * ncm + slot) * D + col) * 4), O);
+    if (col == 0)
+      st64(mr, (uint32_t)(((int64_t)g * ncm + slot) * 8),
+           (uint64_t)__float_as_uint(M) | ((uint64_t)__float_as_uint(Ssum) << 32));
   }
 }
 
-// One 1024-thread workgroup per (sequence, query head). The global maximum of
-// the chunk references comes first; then thread (group, c4) sums the chunks
-// group, group + NG, ... (eight independent loads in flight) for columns
-// 4*c4 .. 4*c4+3, and the NG group sums are added in group order.
+// One 256-thread workgroup per (sequence, query head), one pass over the slots: thread (group,
+// c4) loads the slots group, group + NG, ... (eight at a time, all in flight together) for
+// columns 4*c4 .. 4*c4+3 and merges them with a running reference (the maximum m seen, with the
+// sums rescaled when it moves); then the NG group results are merged in group order.
 template <int D>
-__global__ __launch_bounds__(1024) void decode_combine_kernel(DecodeArgs a) {
-  constexpr int NT = 1024, TPR = D / 4, NG = NT / TPR, U = 8;
-  __shared__ float red_m[NT / 64];
+__global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
+  constexpr int NT = 256, TPR = D / 4, NG = NT / TPR, U = 8;
+  __shared__ float red_m[NG], red_s[NG];
   __shared__ __attribute__((aligned(16))) float red_o[NG][D];
-  __shared__ float red_s[NG];
   const int bq = blockIdx.x;
   const int b = bq / a.Hq, qh = bq % a.Hq, h = qh / a.G;
   const int seg = b * a.Hkv + h;
-  int64_t r0, r1;
-  clamp_segment(a, seg, r0, r1);
-  const int64_t len = r1 - r0;
-  // valid splits: the segment's first nseg ones, then n_new_chunks from index n_chunk_max on;
-  // dense index c maps to split c (c < nseg) or n_chunk_max + c - nseg
   const int64_t ncm = a.n_part;
-  int64_t nseg = (len + a.chunk - 1) / a.chunk;
-  if (nseg > a.n_chunk_max) nseg = a.n_chunk_max;
-  const int64_t nch = nseg + a.n_new_chunks;
-  auto slot = [&](int64_t c) { return c < nseg ? c : a.n_chunk_max + (c - nseg); };
   const int tid = threadIdx.x, c4 = tid % TPR, grp = tid / TPR;
   const rsrc_t mr = make_rsrc(a.part_ms + (int64_t)bq * ncm * 2, (uint64_t)ncm * 8);
   const rsrc_t orr = make_rsrc(a.part + (int64_t)bq * ncm * D, (uint64_t)ncm * D * 4);
-  float M = -INFINITY;
-  for (int64_t c = tid; c < nch; c += NT) M = fmaxf(M, ldf(mr, (uint32_t)(slot(c) * 8)));
-  M = wave_max(M);
-  if ((tid & 63) == 0) red_m[tid >> 6] = M;
-  __syncthreads();
-  M = red_m[0];
+  // The first batch of slots is loaded before the segment's length is known, as if every
+  // compressed slot were valid (slots past n_part read as zeros), so that its loads travel
+  // together with the offsets' instead of after them; slots that turn out invalid are not used.
+  uint64_t ms[U];
+  u32x4 ov[U];
+  auto load_batch = [&](int64_t c, auto&& slot_of) {
 #pragma unroll
-  for (int u = 1; u < NT / 64; ++u) M = fmaxf(M, red_m[u]);
-  float S = 0.f, O[4] = {0.f, 0.f, 0.f, 0.f};
-  if (M != -INFINITY) {
-    for (int64_t c = grp; c < nch; c += U * NG) {
-      uint64_t ms[U];
-      u32x4 ov[U];
+    for (int u = 0; u < U; ++u) {
+      const int64_t sl = slot_of(c + u * NG);
+      ms[u] = ld64(mr, (uint32_t)(sl * 8));
+      ov[u] = ld128(orr, (uint32_t)((sl * D + 4 * c4) * 4));
+    }
+  };
+  load_batch(grp, [&](int64_t c) { return c < ncm ? c : ncm; });
+  int64_t r0, r1;
+  clamp_segment(a, seg, r0, r1);
+  const int64_t len = r1 - r0;
+  // valid slots: the workgroups of the segment's nseg splits, then those of its appended splits
+  // from slot n_cwg on; dense index c maps to slot c (c < ncs) or n_cwg + c - ncs (past nch:
+  // the offset past the buffer, which reads as zeros)
+  int64_t nseg = (len + a.chunk - 1) / a.chunk;
+  if (nseg > a.n_chunk_max) nseg = a.n_chunk_max;
+  const int64_t ncs = (nseg + kWaves - 1) / kWaves;
+  const int64_t nch = ncs + (a.n_new_chunks + kWaves - 1) / kWaves;
+  auto slot = [&](int64_t c) { return c >= nch ? ncm : (c < ncs ? c : a.n_cwg + (c - ncs)); };
+  if (a.n_new_chunks > 0) load_batch(grp, slot);  // appended slots do not follow the compressed ones
+  float M = -INFINITY, S = 0.f, O[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int64_t c = grp; c < nch; c += U * NG) {
+    if (c != grp) load_batch(c, slot);
 #pragma unroll
-      for (int u = 0; u < U; ++u) {  // chunks past nch read as zeros (offset past the buffer)
-        const int64_t cc = c + u * NG;
-        const bool ok = cc < nch;
-        const int64_t sl = slot(cc);
-        ms[u] = ld64(mr, ok ? (uint32_t)(sl * 8) : (uint32_t)(ncm * 8));
-        ov[u] = ld128(orr, ok ? (uint32_t)((sl * D + 4 * c4) * 4) : (uint32_t)(ncm * D * 4));
+    for (int u = 0; u < U; ++u)
+      if (!(c + u * NG < nch)) {  // a slot past the segment's (possibly stale memory): m = -inf, s = o = 0
+        ms[u] = 0xFF800000ull;
+        ov[u] = u32x4{0u, 0u, 0u, 0u};
       }
+    float Mn = M;
+#pragma unroll
+    for (int u = 0; u < U; ++u) Mn = fmaxf(Mn, __uint_as_float((uint32_t)ms[u]));
+    if (Mn != -INFINITY) {
+      const float r = M == -INFINITY ? 0.f : fast_exp2(M - Mn);
+      S *= r;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) O[k] *= r;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const float mc = __uint_as_float((uint32_t)ms[u]), sc = __uint_as_float((uint32_t)(ms[u] >> 32));
-        const float e = (c + u * NG < nch && mc != -INFINITY) ? fast_exp2(mc - M) : 0.f;
+        const float e = mc != -INFINITY ? fast_exp2(mc - Mn) : 0.f;
         S += sc * e;
         O[0] += __uint_as_float(ov[u].x) * e;
         O[1] += __uint_as_float(ov[u].y) * e;
         O[2] += __uint_as_float(ov[u].z) * e;
         O[3] += __uint_as_float(ov[u].w) * e;
       }
+      M = Mn;
     }
   }
   *reinterpret_cast<f32x4*>(&red_o[grp][4 * c4]) = f32x4{O[0], O[1], O[2], O[3]};
-  if (c4 == 0) red_s[grp] = S;
+  if (c4 == 0) {
+    red_m[grp] = M;
+    red_s[grp] = S;
+  }
   __syncthreads();
   if (tid >= D) return;
   const int col = tid;
-  S = red_s[0];
-  float Oc = red_o[0][col];
+  float Mf = red_m[0];
 #pragma unroll
-  for (int g = 1; g < NG; ++g) {
-    S += red_s[g];
-    Oc += red_o[g][col];
+  for (int g = 1; g < NG; ++g) Mf = fmaxf(Mf, red_m[g]);
+  float Sf = 0.f, Oc = 0.f;
+  if (Mf != -INFINITY) {
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const float e = red_m[g] == -INFINITY ? 0.f : fast_exp2(red_m[g] - Mf);
+      Sf += red_s[g] * e;
+      Oc += red_o[g][col] * e;
+    }
   }
-  const bool empty = !(S > 0.f);
-  const float res = empty ? 0.f : Oc / S;
+  const bool empty = !(Sf > 0.f);
+  const float res = empty ? 0.f : Oc / Sf;
   if (a.out_dtype == 1) {
     const rsrc_t outr = make_rsrc(static_cast<char*>(a.out) + (int64_t)bq * D * 2, (uint64_t)D * 2);
     const float other = __shfl_xor(res, 1, 64);  // two columns per 32-bit store
@@ -413,7 +469,7 @@ __global__ __launch_bounds__(1024) void decode_combine_kernel(DecodeArgs a) {
   }
   if (a.lse_out != nullptr && col == 0) {
     const rsrc_t lr = make_rsrc(a.lse_out, (uint64_t)a.B * a.Hq * 4);
-    const float lse = empty ? -INFINITY : (M + fast_log2(S)) * 0.69314718055994530942f;
+    const float lse = empty ? -INFINITY : (Mf + fast_log2(Sf)) * 0.69314718055994530942f;
     stf(lr, (uint32_t)bq * 4, lse);
   }
 }
@@ -431,7 +487,7 @@ __global__ __launch_bounds__(1024) void decode_combine_kernel(DecodeArgs a) {
 // One step of K/V in flight ahead of the one being computed (more measured no faster).
 template <typename T, int D>
 static void launch_decode_t(const DecodeArgs& a, hipStream_t st) {
-  const dim3 grid((a.n_chunk_max + a.n_new_chunks + kWaves - 1) / kWaves, a.B * a.Hkv);
+  const dim3 grid(a.n_cwg + (a.n_new_chunks + kWaves - 1) / kWaves, a.B * a.Hkv);
   constexpr bool wide = sizeof(T) == 2;
   constexpr int PF = wide ? SGDKV_DECODE_PF : 1;
   constexpr int CPL = wide ? SGDKV_DECODE_CPL : 8;
@@ -477,9 +533,9 @@ hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {
     }
   }
   if (a.D == 128)
-    SGDKV_LAUNCH("decode_combine", decode_combine_kernel<128>, dim3(a.B * a.Hq), dim3(1024), st, a);
+    SGDKV_LAUNCH("decode_combine", decode_combine_kernel<128>, dim3(a.B * a.Hq), dim3(256), st, a);
   else
-    SGDKV_LAUNCH("decode_combine", decode_combine_kernel<64>, dim3(a.B * a.Hq), dim3(1024), st, a);
+    SGDKV_LAUNCH("decode_combine", decode_combine_kernel<64>, dim3(a.B * a.Hq), dim3(256), st, a);
   return hipGetLastError();
 }
 

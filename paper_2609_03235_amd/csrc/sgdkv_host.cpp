@@ -654,6 +654,15 @@ sgdkv_status sgdkv_compress_layer_ex(const sgdkv_compress_desc* desc, const sgdk
 // -------------------------------------------------------------- decode plan
 namespace {
 
+#ifndef SGDKV_DECODE_SPLITS
+#define SGDKV_DECODE_SPLITS 8192
+#endif
+#ifndef SGDKV_DECODE_MIN_CHUNK
+#define SGDKV_DECODE_MIN_CHUNK 128
+#endif
+constexpr int64_t kDecodeSplits = SGDKV_DECODE_SPLITS;
+constexpr int64_t kDecodeMinChunk = SGDKV_DECODE_MIN_CHUNK;
+
 struct DecodePlan {
   sgdkv::DecodeArgs a;
   size_t bytes;
@@ -701,14 +710,17 @@ sgdkv_status plan_decode(const sgdkv_decode_desc* d, const int64_t* offsets_host
   const double scale = d->scale > 0.f ? (double)d->scale : 1.0 / std::sqrt((double)d->head_dim);
   a.c2 = (float)(scale * 1.4426950408889634074);
   a.total_rows = total;
-  // rows per wave-sized split: about 8192 splits over the whole batch (four rounds of the
-  // 2048 resident waves), at least 256 rows; one round of longer splits measured slower
-  a.chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(total - offsets_host[0], 8192), 64), 256), 1 << 24);
+  // rows per wave-sized split: about kDecodeSplits splits over the whole batch, at least
+  // kDecodeMinChunk rows; one round of longer splits measured slower
+  a.chunk = std::min<int64_t>(
+      std::max<int64_t>(round_up(ceil_div(total - offsets_host[0], kDecodeSplits), 64), kDecodeMinChunk), 1 << 24);
   a.n_chunk_max = (int)ceil_div(longest, a.chunk);
   if ((int64_t)a.B * a.Hkv * capacity * rb > 0xFFFFFFFFll)
     return fail(SGDKV_ERR_UNSUPPORTED, "appended regions of %lld rows per head exceed 4 GiB", (long long)capacity);
   a.cap = capacity;
-  a.n_part = a.n_chunk_max + (int)ceil_div(capacity, a.chunk);
+  const int wpw = sgdkv::kBlock / 64;  // splits (waves) per decode workgroup
+  a.n_cwg = (int)ceil_div(a.n_chunk_max, wpw);
+  a.n_part = a.n_cwg + (int)ceil_div(ceil_div(capacity, a.chunk), wpw);
   p.bytes = align256((size_t)a.B * a.Hq * a.n_part * (a.D + 2) * sizeof(float));
   return SGDKV_OK;
 }

@@ -104,17 +104,20 @@ struct DecodeArgs {
   int64_t total_rows;  // offsets_host[B*Hkv]: device offsets are clamped to it
   void* out;
   float* lse_out;
-  float* part;        // [B*Hq][n_part][D]: o per split (16-byte aligned rows)
-  float* part_ms;     // [B*Hq][n_part][2]: (m, s) per split
-  int64_t chunk;      // rows per split (multiple of 64, at least 256)
+  // The splits of a segment are grouped by workgroup (kBlock / 64 splits each), and a workgroup
+  // merges its splits into one partial per query head: slot = the workgroup's index in x.
+  float* part;        // [B*Hq][n_part][D]: o per workgroup slot (16-byte aligned rows)
+  float* part_ms;     // [B*Hq][n_part][2]: (m, s) per workgroup slot
+  int64_t chunk;      // rows per split (multiple of 64, at least 128)
   int n_chunk_max;    // max over segments of ceil(len / chunk): splits of the compressed rows
+  int n_cwg;          // ceil(n_chunk_max / waves per workgroup): workgroups (slots) of the compressed rows
   // rows appended after compression: (b, h) owns rows [0, n_new) of k_new/v_new + (b*Hkv+h)*cap rows;
-  // their splits come after the compressed ones, at index n_chunk_max + j
+  // their workgroups come after the compressed ones, at slot n_cwg + j
   const void* k_new;
   const void* v_new;
   int64_t cap, n_new;
   int n_new_chunks;   // ceil(n_new / chunk)
-  int n_part;         // split slots per (b, q): n_chunk_max + ceil(capacity / chunk)
+  int n_part;         // slots per (b, q): n_cwg + ceil(ceil(capacity / chunk) / waves per workgroup)
 };
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);

@@ -504,15 +504,18 @@ def test_decode_fixed_reference_redo():
     overflows while s does not. Both must match the oracle."""
     rng = np.random.Generator(np.random.PCG64(21))
     d, Hq, Hkv = 128, 8, 4
-    lens = [600, 300, 900, 40]  # B=1; 256-row chunks: every planted key is past its first step
+    # B=1. The segments' 16-row steps are dealt to their splits in turn (split w takes steps w,
+    # w + n, ...), n = 5, 3, 8, 1 splits with 128-row splits (3, 2, 4, 1 with 256-row ones): every
+    # planted key sits at step >= n, so it is past the first step of its split
+    lens = [600, 300, 900, 40]
     offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
     q = rng.standard_normal((1, Hq, d))
     kc = rng.standard_normal((offs[-1], d))
     vc = rng.standard_normal((offs[-1], d))
-    for seg, pos, f in ((0, 20, 6.0), (0, 356, 6.0), (2, 700, 9.0)):
-        kc[offs[seg] + pos] = f * q[0, 2 * seg]  # far above the first step of its chunk
-    kc[offs[1] + 40] = 3.0 * q[0, 2]  # ~38 above the first step's maximum: s stays below 2^64 ...
-    vc[offs[1] + 40] = 1e30  # ... but 2^38 * 1e30 overflows o
+    for seg, pos, f in ((0, 120, 6.0), (0, 356, 6.0), (2, 700, 9.0)):
+        kc[offs[seg] + pos] = f * q[0, 2 * seg]  # far above the first step of its split
+    kc[offs[1] + 100] = 3.0 * q[0, 2]  # ~38 above the first step's maximum: s stays below 2^64 ...
+    vc[offs[1] + 100] = 1e30  # ... but 2^38 * 1e30 overflows o
     qt = torch.from_numpy(q).to(torch.bfloat16).to(DEV)
     kt = torch.from_numpy(kc).to(torch.bfloat16).to(DEV)
     vt = torch.from_numpy(vc).to(torch.bfloat16).to(DEV)
@@ -530,7 +533,7 @@ def test_decode_fixed_reference_redo():
 def test_decode_with_appended_rows(dtype, cap):
     """Generation after compression: each step appends one K/V row per KV head (sgdkv_append_kv)
     and decodes over the compressed segment plus the rows appended so far, against the oracle.
-    A capacity of 300 rows spans two 256-row splits of the appended region; one segment kept
+    A capacity of 300 rows spans three 128-row splits of the appended region; one segment kept
     no rows at all, so it attends to its appended rows alone."""
     rng = np.random.Generator(np.random.PCG64(77))
     B, Hq, Hkv, d = 2, 8, 4, 128 if dtype == torch.bfloat16 else 64
