@@ -40,6 +40,29 @@ __device__ __forceinline__ int64_t uniform64(int64_t v) {
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
+// A decode workgroup's segment and its index in the segment's workgroup layout (x < n_cwg: its
+// compressed rows; n_cwg + j: its appended rows), and how many workgroups were launched for the
+// segment's compressed rows (ncw): from the compact table, or the (x, segment) grid.
+__device__ __forceinline__ void decode_workgroup(const DecodeArgs& a, int& seg, int& x, int& ncw) {
+  if (a.compact) {
+    const int flat = blockIdx.x;
+    int lo = 0, hi = a.B * a.Hkv;  // the last segment lo with wg_start[lo] <= flat (uniform)
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (a.wg_start[mid] <= flat) lo = mid;
+      else hi = mid;
+    }
+    seg = lo;
+    ncw = a.wg_start[seg + 1] - a.wg_start[seg] - a.n_new_wg;
+    const int local = flat - a.wg_start[seg];
+    x = local < ncw ? local : a.n_cwg + (local - ncw);
+  } else {
+    seg = blockIdx.y;
+    x = blockIdx.x;
+    ncw = a.n_cwg;
+  }
+}
+
 __device__ __forceinline__ void clamp_segment(const DecodeArgs& a, int seg, int64_t& r0, int64_t& r1) {
   const int nseg = a.B * a.Hkv;
   const rsrc_t orr = make_rsrc(a.offsets, (uint64_t)(nseg + 1) * 8);
@@ -231,7 +254,8 @@ __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a)
   __shared__ float mws[kWaves][16], sws[kWaves][16];                     // each wave's (m, s) per head
   __shared__ __attribute__((aligned(16))) float ows[kWaves][GM][D];      // each wave's o per head
 
-  const int seg = blockIdx.y;
+  int seg, x, ncw;
+  decode_workgroup(a, seg, x, ncw);
   const int b = seg / a.Hkv, h = seg % a.Hkv;
   const int tid = threadIdx.x, wid = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   int64_t r0, r1;
@@ -240,8 +264,8 @@ __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a)
   // workgroups 0 .. n_cwg-1 cover the segment's compressed rows, the next ones the rows appended
   // since compression. A workgroup whose first split is empty leaves (uniform over the
   // workgroup); a wave whose own split is empty joins the merge with an empty partial.
-  const bool appended = (int)blockIdx.x >= a.n_cwg;
-  const int64_t wg = appended ? (int64_t)blockIdx.x - a.n_cwg : (int64_t)blockIdx.x;
+  const bool appended = x >= a.n_cwg;
+  const int64_t wg = appended ? (int64_t)x - a.n_cwg : (int64_t)x;
   const int64_t chunk = wg * kWaves + wid;  // split index within the region
   const int64_t rows = appended ? a.n_new : len;
   // The compressed rows of a segment are dealt to its nck splits 16 rows at a time (split w
@@ -258,7 +282,9 @@ __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a)
     nsteps = active ? (int)((c1 - c0 + 15) / 16) : 0;
   } else {
     int64_t nck = (rows + a.chunk - 1) / a.chunk;
-    if (nck > a.n_chunk_max) nck = a.n_chunk_max;  // device offsets beyond the host's: fewer, longer splits
+    // device offsets beyond the host's: fewer, longer splits (as many as were launched)
+    if (nck > a.n_chunk_max) nck = a.n_chunk_max;
+    if (nck > (int64_t)ncw * kWaves) nck = (int64_t)ncw * kWaves;
     const int64_t total_steps = (rows + 15) / 16;
     if (wg * kWaves >= nck) return;
     active = chunk < nck;
@@ -342,7 +368,7 @@ __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a)
   __syncthreads();
   const int64_t bq0 = (int64_t)b * a.Hq + (int64_t)h * G;
   const int64_t ncm = a.n_part;
-  const uint32_t slot = blockIdx.x;
+  const uint32_t slot = x;
   const rsrc_t mr = make_rsrc(a.part_ms + bq0 * ncm * 2, (uint64_t)G * ncm * 8);
   const rsrc_t orr = make_rsrc(a.part + bq0 * ncm * D, (uint64_t)G * ncm * D * 4);
   for (int idx = tid; idx < G * D; idx += kBlock) {
@@ -378,6 +404,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
   const int b = bq / a.Hq, qh = bq % a.Hq, h = qh / a.G;
   const int seg = b * a.Hkv + h;
   const int64_t ncm = a.n_part;
+  const int ncw = a.compact ? a.wg_start[seg + 1] - a.wg_start[seg] - a.n_new_wg : a.n_cwg;
   const int tid = threadIdx.x, c4 = tid % TPR, grp = tid / TPR;
   const rsrc_t mr = make_rsrc(a.part_ms + (int64_t)bq * ncm * 2, (uint64_t)ncm * 8);
   const rsrc_t orr = make_rsrc(a.part + (int64_t)bq * ncm * D, (uint64_t)ncm * D * 4);
@@ -403,6 +430,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
   // the offset past the buffer, which reads as zeros)
   int64_t nseg = (len + a.chunk - 1) / a.chunk;
   if (nseg > a.n_chunk_max) nseg = a.n_chunk_max;
+  if (nseg > (int64_t)ncw * kWaves) nseg = (int64_t)ncw * kWaves;  // as the split kernel clamps
   const int64_t ncs = (nseg + kWaves - 1) / kWaves;
   const int64_t nch = ncs + (a.n_new_chunks + kWaves - 1) / kWaves;
   auto slot = [&](int64_t c) { return c >= nch ? ncm : (c < ncs ? c : a.n_cwg + (c - ncs)); };
@@ -487,7 +515,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
 // One step of K/V in flight ahead of the one being computed (more measured no faster).
 template <typename T, int D>
 static void launch_decode_t(const DecodeArgs& a, hipStream_t st) {
-  const dim3 grid(a.n_cwg + (a.n_new_chunks + kWaves - 1) / kWaves, a.B * a.Hkv);
+  const dim3 grid = a.compact ? dim3((unsigned)a.wg_start[a.B * a.Hkv]) : dim3(a.n_cwg + a.n_new_wg, a.B * a.Hkv);
   constexpr bool wide = sizeof(T) == 2;
   constexpr int PF = wide ? SGDKV_DECODE_PF : 1;
   constexpr int CPL = wide ? SGDKV_DECODE_CPL : 8;
@@ -523,7 +551,7 @@ hipError_t launch_append(const DecodeArgs& a, const void* k_step, const void* v_
 }
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {
-  if (a.n_chunk_max + a.n_new_chunks > 0) {
+  if (a.compact ? a.wg_start[a.B * a.Hkv] > 0 : a.n_chunk_max + a.n_new_chunks > 0) {
     if (a.kv_dtype == 1) {
       if (a.D == 128) launch_decode_t<__bf16, 128>(a, st);
       else launch_decode_t<__bf16, 64>(a, st);

@@ -805,6 +805,19 @@ sgdkv_status decode_step(const sgdkv_decode_desc* desc, const void* q, const voi
   a.v_new = t.v_new;
   a.n_new = t.n_new;
   a.n_new_chunks = (int)ceil_div(t.n_new, a.chunk);
+  a.n_new_wg = (int)ceil_div(a.n_new_chunks, sgdkv::kBlock / 64);
+  // compact decode grid: the workgroups each segment needs, from the host copy of the offsets
+  const int64_t nseg = (int64_t)a.B * a.Hkv;
+  a.compact = nseg <= sgdkv::kMaxCompactSegs ? 1 : 0;
+  if (a.compact) {
+    int64_t run = 0;
+    a.wg_start[0] = 0;
+    for (int64_t i = 0; i < nseg; ++i) {
+      const int64_t splits = std::min<int64_t>(ceil_div(offsets_host[i + 1] - offsets_host[i], a.chunk), a.n_chunk_max);
+      run += ceil_div(splits, sgdkv::kBlock / 64) + a.n_new_wg;
+      a.wg_start[i + 1] = (int32_t)run;  // at most nseg * (n_cwg + n_new_wg) workgroups
+    }
+  }
   a.part = static_cast<float*>(workspace);
   a.part_ms = a.part + (size_t)a.B * a.Hq * a.n_part * a.D;
   hipError_t e = hipGetLastError();

@@ -12,6 +12,7 @@ constexpr int kMaxKvHeads = 64;    // per-head tables travel by value in kernel 
 constexpr int kMaxSplitRows = 512; // window rows one score workgroup holds (a row split)
 constexpr int kMaxGroupRows = 4096; // G*w rows of one KV head's window queries, over all row splits
 constexpr int kMaxDecodeGroup = 16;
+constexpr int kMaxCompactSegs = 512;  // decode segments whose workgroup table travels in the kernel arguments
 constexpr int kMaxIptQHeads = 256;  // query heads per layer the Ipt. aggregations accept
 constexpr int kBlock = 256;        // threads per workgroup in every kernel
 constexpr int kLseTile = 128;      // keys staged in LDS per step of score pass 1
@@ -118,6 +119,13 @@ struct DecodeArgs {
   int64_t cap, n_new;
   int n_new_chunks;   // ceil(n_new / chunk)
   int n_part;         // slots per (b, q): n_cwg + ceil(ceil(capacity / chunk) / waves per workgroup)
+  // Compact grid (B*Hkv <= kMaxCompactSegs): only workgroups with work are launched, segment
+  // after segment (from the host copy of the offsets); segment s owns workgroups
+  // [wg_start[s], wg_start[s+1]), its compressed rows' first, then n_new_wg for its appended rows.
+  // Otherwise (compact = 0) the grid is (n_cwg + n_new_wg) x segments.
+  int compact;
+  int n_new_wg;       // ceil(n_new_chunks / waves per workgroup)
+  int32_t wg_start[kMaxCompactSegs + 1];
 };
 
 hipError_t launch_decode(const DecodeArgs& a, hipStream_t stream);

@@ -457,6 +457,63 @@ def test_decode_edge_segments_and_bf16_output():
     assert np.all(np.abs(ob - ref) <= 2e-2 + ulp)
 
 
+@pytest.mark.parametrize("B,n_new", [(64, 0), (66, 0), (66, 37)], ids=["512-seg-compact", "528-seg-grid", "528-seg-grid-append"])
+def test_decode_many_segments(B, n_new):
+    """Decode launches only the workgroups with work (a per-segment table in the kernel arguments)
+    for up to 512 (sequence, KV head) segments, and an (x, segment) grid beyond that; both against
+    the oracle, with empty, single-row and multi-split segments, and rows appended after
+    compression on the grid path."""
+    rng = np.random.Generator(np.random.PCG64(B + n_new))
+    d, Hq, Hkv = 64, 16, 8
+    lens = rng.integers(0, 400, size=B * Hkv)
+    lens[::7] = 0
+    lens[3::11] = 1
+    lens[5] = 3000  # several workgroups of splits
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    mk = lambda *shape: torch.from_numpy(rng.standard_normal(shape).astype(np.float32)).to(DEV)
+    kc, vc, q = mk(offs[-1], d), mk(offs[-1], d), mk(B, Hq, d)
+    tail = {}
+    if n_new:
+        cap = 64
+        tail = dict(k_new=mk(B, Hkv, cap, d), v_new=mk(B, Hkv, cap, d), n_new=n_new)
+    _announce(f"decode over {B * Hkv} segments, {n_new} appended rows")
+    out, lse = sg.decode_attention(q, kc, vc, torch.from_numpy(offs).to(DEV), offs, Hkv, out_dtype=torch.float32,
+                                   **tail)
+    torch.cuda.synchronize()
+    if n_new:
+        ref, ref_lse = oracle.decode_append(_f64(q), _f64(kc), _f64(vc), offs, _f64(tail["k_new"]),
+                                            _f64(tail["v_new"]), n_new, Hkv)
+    else:
+        ref, ref_lse = oracle.decode(_f64(q), _f64(kc), _f64(vc), offs, Hkv)
+    assert np.abs(out.cpu().numpy() - ref).max() <= 1e-5
+    fin = np.isfinite(ref_lse)
+    assert np.array_equal(np.isfinite(lse.cpu().numpy()), fin)
+    assert np.abs(lse.cpu().numpy()[fin] - ref_lse[fin]).max() <= 1e-5
+
+
+def test_decode_device_offsets_beyond_the_plan():
+    """The device offsets decide the rows; the host copy only plans the launch. A device table whose
+    segments are longer than the host copy's (its last segment takes rows the plan gave to none)
+    still attends to every device row: the launched splits take longer strides."""
+    rng = np.random.Generator(np.random.PCG64(12))
+    d, Hq, Hkv = 64, 4, 2
+    host = np.array([0, 200, 300, 300, 500], dtype=np.int64)  # B=2 x 2 heads
+    dev = np.array([0, 250, 500, 700, 1400], dtype=np.int64)
+    mk = lambda *shape: torch.from_numpy(rng.standard_normal(shape).astype(np.float32)).to(DEV)
+    kc, vc, q = mk(int(dev[-1]), d), mk(int(dev[-1]), d), mk(2, Hq, d)
+    desc = sg.decode_desc(q, Hkv, torch.float32)
+    ws = sg.alloc_workspace(sg.decode_workspace_size(desc, dev), DEV)  # room for the device table's splits
+    _announce("decode with device offsets beyond the host plan")
+    out, lse = sg.decode_attention(q, kc, vc, torch.from_numpy(dev).to(DEV), host, Hkv, out_dtype=torch.float32,
+                                   workspace=ws)
+    torch.cuda.synchronize()
+    ref, ref_lse = oracle.decode(_f64(q), _f64(kc[:int(host[-1])]), _f64(vc[:int(host[-1])]),
+                                 np.minimum(dev, host[-1]), Hkv)
+    assert np.abs(out.cpu().numpy() - ref).max() <= 1e-5
+    fin = np.isfinite(ref_lse)
+    assert np.abs(lse.cpu().numpy()[fin] - ref_lse[fin]).max() <= 1e-5
+
+
 @pytest.mark.parametrize("dtype,G", [(torch.bfloat16, 16), (torch.bfloat16, 12), (torch.float32, 16),
                                      (torch.float32, 9)])
 def test_decode_large_groups(dtype, G):
