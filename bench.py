@@ -501,8 +501,9 @@ def main():
     log(f"[bench] inputs ready in {time.perf_counter() - t0:.1f}s: {wl.name}, total budget {total} rows "
         f"({args.ratio:.0%}), {L} layers x {B} sequences")
 
-    def step(gs=gstream):
-        # S0 on the host, then every layer's compression, then every layer's decode
+    def step(gs=gstream, dec_ev=None):
+        # S0 on the host, then every layer's compression, then every layer's decode; dec_ev (a pair
+        # of events) brackets the decode phase on the launch stream
         allocate()
         for l in range(L):
             t = layers[l]
@@ -512,6 +513,8 @@ def main():
                               gather_stream=gs if l < L - 1 else None)  # nothing follows the last
         if gs is not None and L > 1:
             stream.wait_stream(gs)  # every layer's compressed cache is complete before decode
+        if dec_ev is not None:
+            dec_ev[0].record(stream)
         for l in range(L):
             o = outs[l]
             kn = vn = None
@@ -522,6 +525,8 @@ def main():
             sg.decode_attention(layers[l]["q"], o["k_c"], o["v_c"], o["offsets"], offsets_host[l], Hkv,
                                 out_dtype=torch.float32, k_new=kn, v_new=vn, n_new=n_new, workspace=ws_d,
                                 out=dec_out[l], lse=dec_lse[l], stream=stream)
+        if dec_ev is not None:
+            dec_ev[1].record(stream)
 
     for _ in range(args.warmup):
         step()
@@ -532,17 +537,20 @@ def main():
     # an event after every step on the launch stream gives the spread of the step times (recording
     # an event adds no synchronisation)
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    # two more per step bracket its decode phase (all layers' decode kernels, launch gaps included)
+    dec_evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     ev0.record(stream)
     t_wall0 = time.perf_counter()
     for i in range(args.steps):
-        step()
+        step(dec_ev=dec_evs[i])
         evs[i].record(stream)
     ev1.record(stream)
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t_wall0) * 1e3 / args.steps
     ms_per_step = ev0.elapsed_time(ev1) / args.steps
     step_ms = [ev0.elapsed_time(evs[0])] + [evs[i - 1].elapsed_time(evs[i]) for i in range(1, args.steps)]
+    dec_phase_ms = statistics.mean(a.elapsed_time(b) for a, b in dec_evs)
 
     # ------------------------------------------------------------ timed region with kernel events
     sg.profile_reset()
@@ -615,10 +623,14 @@ def main():
     decode = roof("decode_split") if "decode_split" in kern else None
     other_roofs = {n: roof(n) for n in ("score_lse", "score_colsum", "gather", "pool_radix_hist")
                    if n in kern and n != dominant}
-    dec_ms = (kern.get("decode_split", (0, 0))[1] + kern.get("decode_combine", (0, 0))[1]) / args.steps
+    # decode time: the decode phase of the timed steps (two events around it on the launch stream:
+    # every layer's split and combine kernels with the launch gaps between them, and no per-kernel
+    # events); the per-kernel event durations of the profiled run are kept beside it
+    dec_ms = dec_phase_ms
+    dec_kernel_ms = sum(kern.get(n, (0, 0))[1] for n in ("decode_split", "decode_combine", "append")) / args.steps
     dec_bytes = work["decode_split"][1] * L
-    # compression time: the step minus its decode kernels (the gathers overlap other kernels, so
-    # a sum of kernel durations would count them twice)
+    # compression time: the step minus its decode phase (the gathers overlap other kernels, so a
+    # sum of kernel durations would count them twice)
     comp_ms = ms_per_step - dec_ms
     roofs = [compress_roof_seconds(B, C, Hq, Hkv, d, w, eb, float(T_layers[l]), wl.dtype) for l in range(L)]
     roof_s, roof2_s = sum(r[0] for r in roofs), sum(r[1] for r in roofs)
@@ -714,7 +726,11 @@ def main():
         compress_roof=compress_roof,
         decode=dict(gbps=round(dec_bytes / (dec_ms / 1e3) / 1e9, 1) if dec_ms > 0 else None,
                     frac_of_peak=round(dec_bytes / (dec_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4) if dec_ms > 0 else None,
-                    ms_per_step=round(dec_ms, 4), split_kernel=decode),
+                    ms_per_step=round(dec_ms, 4), kernel_events_ms_per_step=round(dec_kernel_ms, 4),
+                    note="ms_per_step: the decode phase of the timed steps (events around it); "
+                         "kernel_events_ms_per_step: the sum of its kernels' own event durations in the "
+                         "profiled run (each bracketed by two events)",
+                    split_kernel=decode),
         roofline=roofline, roofline_serial=roofline_serial, other_rooflines=other_roofs, kernels=kernels,
         profiled_ms_per_step=round(prof_ms_per_step, 4),
         wall_ms_per_step=round(wall_ms, 4), cpu_baseline=cpu,
