@@ -376,8 +376,8 @@ def summarize_kernel_trace(path, args):
                                                                             else "") + ".", "",
              "| kernel | calls | avg us (timed) | avg us (serial) | min us | max us |", "|---|---:|---:|---:|---:|---:|"]
     for _, name, n, timed, ser, lo, hi in rows:
-        lines.append(f"| `{name}` | {n} | {statistics.mean(timed):.2f} | "
-                     f"{statistics.mean(ser) if ser else float('nan'):.2f} | {lo:.2f} | {hi:.2f} |")
+        ser_s = f"{statistics.mean(ser):.2f}" if ser else "—"  # no serial steps in this run
+        lines.append(f"| `{name}` | {n} | {statistics.mean(timed):.2f} | {ser_s} | {lo:.2f} | {hi:.2f} |")
     out = os.path.join(ROOT, "profiles", f"kernels_{tag}.md")
     with open(out, "w") as fh:
         fh.write("\n".join(lines) + "\n")
