@@ -795,18 +795,18 @@ def _capped_layer(key, ratio):
 
 FULL_CASES = [
     ("qwen25_32k", 0.25, 0, "plain", (0,)),
-    ("qwen25_128k", 0.25, 0, "plain", (0, 7)),
+    ("qwen25_128k", 0.25, 0, "plain", (0, 1, 2, 3, 4, 5, 6, 7)),
     ("qwen25_128k", 0.25, 13, "plain", (3,)),
     ("qwen25_128k", 0.25, 27, "plain", (5,)),
     ("qwen25_128k", 0.10, 0, "plain", (2,)),
-    ("qwen25_128k", 0.50, 0, "plain", (6,)),
+    ("qwen25_128k", 0.50, 0, "plain", (0, 3, 6)),
     ("qwen25_128k", 0.50, "capped", "plain", (1,)),
     ("qwen25_128k", 0.25, 0, "ipt_max", (4,)),
     ("qwen25_128k", 0.25, 0, "unaware", (1,)),
     ("qwen25_128k", 0.25, 0, "append64", (0,)),
     ("qwen25_128k", 0.25, 0, "w128", (7,)),
-    ("qwen3_256k", 0.25, 0, "plain", (15,)),
-    ("qwen25_1m", 0.25, 0, "plain", (31,)),
+    ("qwen3_256k", 0.25, 0, "plain", (0, 15)),
+    ("qwen25_1m", 0.25, 0, "plain", (0, 31)),
 ]
 
 
