@@ -88,8 +88,16 @@ struct KeyStage {
   }
 };
 
+// Row block of slot j of wave wid: blocks wid, wid+8, ... (interleaved), or, with HW (head
+// waves), blocks wid*RBW .. wid*RBW+RBW-1, so that the rows of a wave belong to one query head
+// when w is a multiple of 16*RBW.
+template <int RBW, bool HW>
+__device__ __forceinline__ int row_block(int wid, int j) {
+  return HW ? wid * RBW + j : wid + kScoreWaves * j;
+}
+
 // Window rows [r0, r0 + nrows) of KV head h (one row split) as A fragments.
-template <typename T, int D, int RBW>
+template <typename T, int D, int RBW, bool HW = false>
 __device__ __forceinline__ void load_group_queries(const CompressArgs& a, int b, int h, int r0, int nrows, int wid,
                                                    int lane, Frag<T> (&qa)[RBW][D / 32]) {
   using G = TileGeom<T, D>;
@@ -98,7 +106,7 @@ __device__ __forceinline__ void load_group_queries(const CompressArgs& a, int b,
   const int lr = lane & 15, lg = lane >> 4;
 #pragma unroll
   for (int j = 0; j < RBW; ++j) {
-    const int row = (wid + kScoreWaves * j) * 16 + lr;  // rows >= nrows read as zeros
+    const int row = row_block<RBW, HW>(wid, j) * 16 + lr;  // rows >= nrows read as zeros
 #pragma unroll
     for (int c = 0; c < G::NC; ++c)
       qa[j][c] = gload_frag<T>(qr, (uint32_t)(row * G::RB + (32 * c + 8 * lg) * G::EB));
@@ -400,13 +408,21 @@ __global__ __launch_bounds__(kBlock) void lse_merge_kernel(CompressArgs a) {
 // g = r / w of the group. The group mean, Ipt. mean and Ipt. only sum every
 // row with a weight (1, sigma_g, or 1 for the top-scored head and 0 for the
 // others), folded into the exp2 argument as log2 of the weight, so they cost
-// nothing extra. Ipt. max (MAXG) needs each query head's own column sum: the
-// waves keep one partial per row block (16 rows of a single head when w is a
-// multiple of 16), and the reduction adds each head's blocks, weights them
-// and takes the maximum.
-template <typename T, int D, int NB, int RBW, bool MAXG>
+// nothing extra. Ipt. max (MAXG) needs each query head's own column sum. With
+// head waves (HW: a wave's row blocks are consecutive and lie in one query
+// head, which needs w to be a multiple of 16*RBW) the waves sum their rows as
+// for the group mean and the reduction adds the partials of each head's
+// waves, weights them and takes the maximum. Otherwise the waves keep one
+// partial per row block (16 rows of a single head when w is a multiple of
+// 16), and the reduction adds each head's blocks the same way.
+template <bool MAXG, bool HW>
+constexpr bool block_partials() {
+  return MAXG && !HW;
+}
+
+template <typename T, int D, int NB, int RBW, bool MAXG, bool HW>
 __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
-                             float (*red)[kScoreWaves][MAXG ? RBW : 4][col_tile<T>()],
+                             float (*red)[kScoreWaves][block_partials<MAXG, HW>() ? RBW : 4][col_tile<T>()],
                              int seg, int r0, int nrows, int wid, int lane,
                              const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], const rsrc_t& kr, int64_t key0,
                              int64_t key_end) {
@@ -424,7 +440,7 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
   for (int j = 0; j < NBX; ++j)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int row = (wid + kScoreWaves * j) * 16 + 4 * lg + i;  // within the split
+      const int row = row_block<RBW, HW>(wid, j) * 16 + 4 * lg + i;  // within the split
       float l = ldf(lr2, (uint32_t)(((int64_t)seg * a.R + r0 + row) * 4));
       if (natural) l *= 1.44269504088896340736f;
       const float lw = weighted && row < nrows ? a.qweight[h * a.G + (r0 + row) / a.w] : 0.f;
@@ -442,10 +458,25 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
   constexpr int CPW = TILE / kScoreWaves, LPC = 64 / CPW, PPL = kScoreWaves / LPC;
   static_assert(CPW <= 16 && 64 % CPW == 0 && PPL >= 1 && PPL * LPC == kScoreWaves, "reduction layout");
   const int rcol = CPW * wid + lane % CPW, rgrp = lane / CPW;
+  constexpr bool BP = block_partials<MAXG, HW>();
   auto reduce = [&](int64_t t) {  // t may be -1: nothing is stored
-    const float(*r)[MAXG ? RBW : 4][TILE] = red[(t + 3) % 3];
+    const float(*r)[BP ? RBW : 4][TILE] = red[(t + 3) % 3];
     float v = 0.f;
-    if constexpr (MAXG) {
+    if constexpr (MAXG && HW) {
+      // the LPC lanes of a column take the split's heads in turn: add the four lane-group
+      // partials of each of a head's w/(16*RBW) waves in wave order, weight, keep the maximum
+      const int wph = a.w / (16 * RBW), g0 = r0 / a.w, ng = nrows / a.w;
+      for (int g = rgrp; g < ng; g += LPC) {
+        float sum = 0.f;
+        for (int wv = g * wph; wv < (g + 1) * wph; ++wv)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) sum += r[wv][q][rcol];
+        v = fmaxf(v, a.qweight[h * a.G + g0 + g] * sum);
+      }
+#pragma unroll
+      for (int o = CPW; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+      v = max_lane_groups(v);
+    } else if constexpr (MAXG) {
       // the LPC lanes of a column take the split's heads in turn: sum a head's w/16 blocks
       // (block b sits with wave b % 8, slot b / 8), weight it, keep the maximum
       const int bph = a.w / 16, g0 = r0 / a.w, ng = nrows / a.w;
@@ -475,7 +506,7 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
   chunk_pipeline<T, D, NB, TILE>(
       kbuf, kr, key0, a.C, ntiles, lr, lg, qa, [](const f32x4(&)[NBX]) {},
       [&](int64_t t, int sub, const f32x4(&acc)[NBX]) {
-        if constexpr (MAXG) {
+        if constexpr (BP) {
           // one column partial per row block (a single query head's rows)
 #pragma unroll
           for (int j = 0; j < NB; ++j) {
@@ -504,11 +535,11 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
   reduce(ntiles - 1);
 }
 
-template <typename T, int D, int RBW, bool MAXG>
+template <typename T, int D, int RBW, bool MAXG, bool HW>
 __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) {
   using G = TileGeom<T, D>;
   __shared__ __attribute__((aligned(16))) char ktile[2 * col_tile<T>() * G::LDS_STRIDE];
-  __shared__ float red[3][kScoreWaves][MAXG ? RBW : 4][col_tile<T>()];
+  __shared__ float red[3][kScoreWaves][block_partials<MAXG, HW>() ? RBW : 4][col_tile<T>()];
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
   if (blockIdx.x == 0 && blockIdx.z == 0) init_segment(a, seg);  // histograms, offsets for the selection
@@ -520,17 +551,28 @@ __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) 
   const int nrows = a.R - r0 < a.rs_rows ? a.R - r0 : a.rs_rows;
   const rsrc_t kr = make_rsrc(static_cast<const T*>(a.k) + (int64_t)seg * a.C * D, (uint64_t)a.C * G::RB);
   Frag<T> qa[RBW][G::NC];
-  load_group_queries<T, D, RBW>(a, b, h, r0, nrows, wid, lane, qa);
+  load_group_queries<T, D, RBW, HW>(a, b, h, r0, nrows, wid, lane, qa);
   const int nrb = (nrows + 15) / 16;
-  if (wid + kScoreWaves * (RBW - 1) < nrb) {
-    colsum_chunk<T, D, RBW, RBW, MAXG>(a, ktile, red, seg, r0, nrows, wid, lane, qa, kr, key0, key_end);
+  if constexpr (HW) {
+    // a row split holds whole heads of w/16 blocks, a multiple of RBW: each wave has all
+    // RBW of its blocks or none (a wave without rows still stages keys and meets every barrier)
+    if (row_block<RBW, HW>(wid, 0) < nrb) {
+      colsum_chunk<T, D, RBW, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qa, kr, key0, key_end);
+    } else {
+      Frag<T> qz[1][G::NC];  // never read: the wave has no row blocks
+#pragma unroll
+      for (int c = 0; c < G::NC; ++c) qz[0][c] = qa[0][c];
+      colsum_chunk<T, D, 0, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qz, kr, key0, key_end);
+    }
+  } else if (wid + kScoreWaves * (RBW - 1) < nrb) {
+    colsum_chunk<T, D, RBW, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qa, kr, key0, key_end);
   } else {
     Frag<T> qb[RBW > 1 ? RBW - 1 : 1][G::NC];
 #pragma unroll
     for (int j = 0; j < RBW - 1; ++j)
 #pragma unroll
       for (int c = 0; c < G::NC; ++c) qb[j][c] = qa[j][c];
-    colsum_chunk<T, D, RBW - 1, RBW, MAXG>(a, ktile, red, seg, r0, nrows, wid, lane, qb, kr, key0, key_end);
+    colsum_chunk<T, D, RBW - 1, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qb, kr, key0, key_end);
   }
 }
 
@@ -544,12 +586,13 @@ static hipError_t launch_scores_t(const CompressArgs& a, hipStream_t st) {
                  dim3(kBlock), st, a);
   }
   if (a.n_col_chunks > 0) {
-    if (a.agg == 1)
-      SGDKV_LAUNCH("score_colsum", (colsum_kernel<T, D, RBW, true>), dim3(a.n_col_chunks, a.B * a.Hkv, a.n_rsplit),
-                   sblk, st, a);
+    const dim3 cgrid(a.n_col_chunks, a.B * a.Hkv, a.n_rsplit);
+    if (a.agg == 1 && a.w % (16 * RBW) == 0)
+      SGDKV_LAUNCH("score_colsum", (colsum_kernel<T, D, RBW, true, true>), cgrid, sblk, st, a);
+    else if (a.agg == 1)
+      SGDKV_LAUNCH("score_colsum", (colsum_kernel<T, D, RBW, true, false>), cgrid, sblk, st, a);
     else
-      SGDKV_LAUNCH("score_colsum", (colsum_kernel<T, D, RBW, false>), dim3(a.n_col_chunks, a.B * a.Hkv, a.n_rsplit),
-                   sblk, st, a);
+      SGDKV_LAUNCH("score_colsum", (colsum_kernel<T, D, RBW, false, false>), cgrid, sblk, st, a);
   }
   return hipGetLastError();
 }

@@ -217,12 +217,18 @@ def test_bf16_qwen_shaped(B, C, Hq, Hkv, d):
 
 
 @pytest.mark.parametrize("agg", [sg.GROUP_IPT_MAX, sg.GROUP_IPT_MEAN, sg.GROUP_IPT_ONLY])
-@pytest.mark.parametrize("B,C,Hq,Hkv,d,w", [(2, 2600, 28, 4, 128, 64), (1, 1500, 16, 2, 64, 32)])
-def test_ipt_group_aggregation(agg, B, C, Hq, Hkv, d, w):
+@pytest.mark.parametrize("B,C,Hq,Hkv,d,w,dtype", [(2, 2600, 28, 4, 128, 64, torch.bfloat16),
+                                                  (1, 1500, 16, 2, 64, 32, torch.bfloat16),
+                                                  (2, 2100, 14, 2, 64, 64, torch.float32)],
+                         ids=["g7w64-bf16", "g8w32-bf16", "g7w64-f32"])
+def test_ipt_group_aggregation(agg, B, C, Hq, Hkv, d, w, dtype):
     """Ipt. max / mean / only (Appendix A.7): per-query-head window attention weighted by the
     summarization score, then max or mean over the group, or the top head's alone. The scores
-    include a zero, a tie for the top of a group and a spread of magnitudes."""
+    include a zero, a tie for the top of a group and a spread of magnitudes. In these shapes each
+    score wave of Ipt. max holds the rows of one query head."""
     wl, t = _qwen_small(B, C, Hq=Hq, Hkv=Hkv, d=d, w=w)
+    if dtype != torch.bfloat16:
+        t = {k: x.float() for k, x in t.items()}
     s, W = wl.b_sink, wl.b_window
     rng = np.random.Generator(np.random.PCG64(31 + agg))
     qs = rng.beta(0.5, 2.0, size=Hq)
