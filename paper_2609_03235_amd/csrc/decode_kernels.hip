@@ -29,7 +29,7 @@
 namespace sgdkv {
 
 namespace {
-constexpr int kWaves = kBlock / 64;
+constexpr int kWaves = kDecodeWaves;
 
 // The segment bounds are the same for every lane: taking them from lane 0 lets the
 // compiler keep them, and every buffer descriptor built from them, in scalar
@@ -243,11 +243,12 @@ __device__ __forceinline__ void decode_chunk(const DecodeArgs& a, float (*pls)[1
 
 // CPL = value columns per lane; GM = compile-time bound on the group size (8
 // or 16); PF = steps of K/V in flight ahead of the one being computed; OCC =
-// workgroups per CU the registers are sized for. Each wave owns one split of
-// a segment: split index = 4*x + wave within the workgroup's region (the
+// waves per SIMD the registers are sized for (launch bounds: at least OCC
+// waves per execution unit). Each wave owns one split of a segment: split
+// index = kWaves*x + wave within the workgroup's region (the
 // segment's compressed rows for x < n_cwg, its appended rows after them).
 template <typename T, int D, int CPL, int GM, int PF, int OCC>
-__global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kDecodeBlock, OCC) void decode_split_kernel(DecodeArgs a) {
   using S = DecodeStep<T, D, CPL>;
   __shared__ __attribute__((aligned(16))) float pls[kWaves][2][16][16];  // probabilities [key][head]
   __shared__ __attribute__((aligned(16))) float als[kWaves][2][16];      // per-head rescale (exact pass)
@@ -371,7 +372,7 @@ __global__ __launch_bounds__(kBlock, OCC) void decode_split_kernel(DecodeArgs a)
   const uint32_t slot = x;
   const rsrc_t mr = make_rsrc(a.part_ms + bq0 * ncm * 2, (uint64_t)G * ncm * 8);
   const rsrc_t orr = make_rsrc(a.part + bq0 * ncm * D, (uint64_t)G * ncm * D * 4);
-  for (int idx = tid; idx < G * D; idx += kBlock) {
+  for (int idx = tid; idx < G * D; idx += kDecodeBlock) {
     const int g = idx / D, col = idx % D;
     float M = -INFINITY;
 #pragma unroll
@@ -521,9 +522,9 @@ static void launch_decode_t(const DecodeArgs& a, hipStream_t st) {
   constexpr int CPL = wide ? SGDKV_DECODE_CPL : 8;
   constexpr int OCC = wide ? SGDKV_DECODE_OCC : 2;
   if (a.G <= 8)
-    SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, CPL, 8, PF, OCC>), grid, dim3(kBlock), st, a);
+    SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, CPL, 8, PF, OCC>), grid, dim3(kDecodeBlock), st, a);
   else
-    SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, 8, 16, 1, 2>), grid, dim3(kBlock), st, a);
+    SGDKV_LAUNCH("decode_split", (decode_split_kernel<T, D, 8, 16, 1, 2>), grid, dim3(kDecodeBlock), st, a);
 }
 
 // Copies one token's K rows (blockIdx.y = 0) or V rows (1), [B*Hkv][d] each, into row `slot`

@@ -718,7 +718,7 @@ sgdkv_status plan_decode(const sgdkv_decode_desc* d, const int64_t* offsets_host
   if ((int64_t)a.B * a.Hkv * capacity * rb > 0xFFFFFFFFll)
     return fail(SGDKV_ERR_UNSUPPORTED, "appended regions of %lld rows per head exceed 4 GiB", (long long)capacity);
   a.cap = capacity;
-  const int wpw = sgdkv::kBlock / 64;  // splits (waves) per decode workgroup
+  const int wpw = sgdkv::kDecodeWaves;  // splits (waves) per decode workgroup
   a.n_cwg = (int)ceil_div(a.n_chunk_max, wpw);
   a.n_part = a.n_cwg + (int)ceil_div(ceil_div(capacity, a.chunk), wpw);
   p.bytes = align256((size_t)a.B * a.Hq * a.n_part * (a.D + 2) * sizeof(float));
@@ -805,7 +805,7 @@ sgdkv_status decode_step(const sgdkv_decode_desc* desc, const void* q, const voi
   a.v_new = t.v_new;
   a.n_new = t.n_new;
   a.n_new_chunks = (int)ceil_div(t.n_new, a.chunk);
-  a.n_new_wg = (int)ceil_div(a.n_new_chunks, sgdkv::kBlock / 64);
+  a.n_new_wg = (int)ceil_div(a.n_new_chunks, sgdkv::kDecodeWaves);
   // compact decode grid: the workgroups each segment needs, from the host copy of the offsets
   const int64_t nseg = (int64_t)a.B * a.Hkv;
   a.compact = nseg <= sgdkv::kMaxCompactSegs ? 1 : 0;
@@ -814,7 +814,7 @@ sgdkv_status decode_step(const sgdkv_decode_desc* desc, const void* q, const voi
     a.wg_start[0] = 0;
     for (int64_t i = 0; i < nseg; ++i) {
       const int64_t splits = std::min<int64_t>(ceil_div(offsets_host[i + 1] - offsets_host[i], a.chunk), a.n_chunk_max);
-      run += ceil_div(splits, sgdkv::kBlock / 64) + a.n_new_wg;
+      run += ceil_div(splits, sgdkv::kDecodeWaves) + a.n_new_wg;
       a.wg_start[i + 1] = (int32_t)run;  // at most nseg * (n_cwg + n_new_wg) workgroups
     }
   }

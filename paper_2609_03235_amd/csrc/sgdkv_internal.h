@@ -14,7 +14,12 @@ constexpr int kMaxGroupRows = 4096; // G*w rows of one KV head's window queries,
 constexpr int kMaxDecodeGroup = 16;
 constexpr int kMaxCompactSegs = 512;  // decode segments whose workgroup table travels in the kernel arguments
 constexpr int kMaxIptQHeads = 256;  // query heads per layer the Ipt. aggregations accept
-constexpr int kBlock = 256;        // threads per workgroup in every kernel
+constexpr int kBlock = 256;        // threads per workgroup in every kernel but the decode split
+#ifndef SGDKV_DECODE_BLOCK
+#define SGDKV_DECODE_BLOCK 256
+#endif
+constexpr int kDecodeBlock = SGDKV_DECODE_BLOCK;  // threads per decode-split workgroup: one split per wave
+constexpr int kDecodeWaves = kDecodeBlock / 64;   // splits a decode workgroup merges into one partial
 constexpr int kLseTile = 128;      // keys staged in LDS per step of score pass 1
 constexpr int kColTileBf16 = 128;  // keys staged in LDS per step of score pass 2 (bf16 keys)
 constexpr int kColTileF32 = 64;    // the same for fp32 keys (LDS holds half as many)
@@ -105,7 +110,7 @@ struct DecodeArgs {
   int64_t total_rows;  // offsets_host[B*Hkv]: device offsets are clamped to it
   void* out;
   float* lse_out;
-  // The splits of a segment are grouped by workgroup (kBlock / 64 splits each), and a workgroup
+  // The splits of a segment are grouped by workgroup (kDecodeWaves splits each), and a workgroup
   // merges its splits into one partial per query head: slot = the workgroup's index in x.
   float* part;        // [B*Hq][n_part][D]: o per workgroup slot (16-byte aligned rows)
   float* part_ms;     // [B*Hq][n_part][2]: (m, s) per workgroup slot
