@@ -219,13 +219,16 @@ def test_bf16_qwen_shaped(B, C, Hq, Hkv, d):
 @pytest.mark.parametrize("agg", [sg.GROUP_IPT_MAX, sg.GROUP_IPT_MEAN, sg.GROUP_IPT_ONLY])
 @pytest.mark.parametrize("B,C,Hq,Hkv,d,w,dtype", [(2, 2600, 28, 4, 128, 64, torch.bfloat16),
                                                   (1, 1500, 16, 2, 64, 32, torch.bfloat16),
-                                                  (2, 2100, 14, 2, 64, 64, torch.float32)],
-                         ids=["g7w64-bf16", "g8w32-bf16", "g7w64-f32"])
+                                                  (2, 2100, 14, 2, 64, 64, torch.float32),
+                                                  (1, 1800, 14, 2, 128, 48, torch.bfloat16),
+                                                  (1, 1200, 14, 2, 64, 16, torch.bfloat16)],
+                         ids=["g7w64-bf16", "g8w32-bf16", "g7w64-f32", "g7w48-bf16", "g7w16-bf16"])
 def test_ipt_group_aggregation(agg, B, C, Hq, Hkv, d, w, dtype):
     """Ipt. max / mean / only (Appendix A.7): per-query-head window attention weighted by the
     summarization score, then max or mean over the group, or the top head's alone. The scores
     include a zero, a tie for the top of a group and a spread of magnitudes. In these shapes each
-    score wave of Ipt. max holds the rows of one query head."""
+    score wave of Ipt. max holds the rows of one query head (4, 2, 4, 3 and 1 row blocks per wave),
+    and with groups of 7 one wave holds none."""
     wl, t = _qwen_small(B, C, Hq=Hq, Hkv=Hkv, d=d, w=w)
     if dtype != torch.bfloat16:
         t = {k: x.float() for k, x in t.items()}
