@@ -634,6 +634,56 @@ def test_decode_with_appended_rows(dtype, cap):
     assert torch.equal(a, b) and torch.equal(la, lb)
 
 
+def _random_decode_case(rng):
+    """One seeded decode configuration: batch, heads, group, head dim, dtype, ragged segment lengths
+    (empty, short, split-sized and long ones) and, sometimes, rows appended after compression."""
+    B = int(rng.integers(1, 5))
+    Hkv = int(rng.choice([1, 2, 4, 8]))
+    G = int(rng.integers(1, 9))
+    d = int(rng.choice([64, 128]))
+    dtype = [torch.bfloat16, torch.float32][int(rng.integers(0, 2))]
+    kind = rng.choice(["empty", "short", "mid", "long"], size=B * Hkv, p=[0.15, 0.25, 0.45, 0.15])
+    hi = {"empty": 1, "short": 24, "mid": 2500, "long": 20000}
+    lo = {"empty": 0, "short": 1, "mid": 100, "long": 5000}
+    lens = [int(rng.integers(lo[k], hi[k])) if hi[k] > 1 else 0 for k in kind]
+    cap = int(rng.choice([0, 0, 64, 300]))
+    n_new = int(rng.integers(0, cap + 1)) if cap else 0
+    return B, Hkv, G, d, dtype, lens, cap, n_new
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_decode_random_shapes(seed):
+    """Decode over ragged caches of seeded random shapes (group sizes 1-8, head dims 64 and 128,
+    bf16 and fp32, empty to 20000-row segments, appended rows or none) against the oracle: output
+    within the dtype's tolerance, log-sum-exp likewise, empty segments give 0 and -inf."""
+    rng = np.random.Generator(np.random.PCG64(1000 + seed))
+    B, Hkv, G, d, dtype, lens, cap, n_new = _random_decode_case(rng)
+    Hq = G * Hkv
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    mk = lambda *shape: torch.from_numpy(rng.standard_normal(shape)).to(dtype).to(DEV)
+    kc, vc = mk(max(int(offs[-1]), 1), d), mk(max(int(offs[-1]), 1), d)
+    q = mk(B, Hq, d)
+    tail = {}
+    if cap:
+        k_new, v_new = mk(B, Hkv, cap, d), mk(B, Hkv, cap, d)
+        tail = dict(k_new=k_new, v_new=v_new, n_new=n_new)
+    _announce(f"random decode seed {seed}: B={B} Hkv={Hkv} G={G} d={d} {dtype} rows={int(offs[-1])} "
+              f"longest={max(lens)} empty={lens.count(0)} cap={cap} n_new={n_new}")
+    out, lse = sg.decode_attention(q, kc, vc, torch.from_numpy(offs).to(DEV), offs, Hkv, out_dtype=torch.float32,
+                                   **tail)
+    torch.cuda.synchronize()
+    if cap:
+        ref, ref_lse = oracle.decode_append(_f64(q), _f64(kc), _f64(vc), offs, _f64(k_new), _f64(v_new), n_new, Hkv)
+    else:
+        ref, ref_lse = oracle.decode(_f64(q), _f64(kc), _f64(vc), offs, Hkv)
+    atol = 2e-2 if dtype == torch.bfloat16 else 1e-5
+    o, l = out.cpu().numpy(), lse.cpu().numpy()
+    assert np.abs(o - ref).max() <= atol
+    fin = np.isfinite(ref_lse)
+    assert np.array_equal(np.isfinite(l), fin) and np.abs(l[fin] - ref_lse[fin]).max(initial=0.0) <= max(atol, 1e-5)
+    assert np.all(o[~fin] == 0)
+
+
 def test_run_twice_bitwise():
     wl, t = _qwen_small(2, 2222)
     budgets = np.array([700, 500, 1500, 400])
