@@ -684,6 +684,62 @@ def test_decode_random_shapes(seed):
     assert np.all(o[~fin] == 0)
 
 
+def test_graph_capture_replays():
+    """A serving loop can capture compression and decode in a HIP graph: on these paths the library
+    only launches kernels (no allocation, memset or synchronisation). One layer's compress + decode
+    is captured once, then replayed on new inputs written in place, with eager calls and
+    synchronisations between the replays; every replay must equal the eager calls bit for bit."""
+    B, C = 2, 3000
+    wl, t = _qwen_small(B, C)
+    s, W, kp, Hkv = wl.b_sink, wl.b_window, wl.pool_kernel, wl.num_kv_heads
+    budgets = np.array([700, 500, 1500, 400])
+    T = int(budgets.sum())
+    Hq, d = t["q"].shape[1], t["q"].shape[2]
+    ws = sg.alloc_workspace(sg.compress_workspace_size(
+        sg.compress_desc(t["q_win"], t["k"], pool_kernel=kp, b_sink=s, b_window=W)), DEV)
+    outs = dict(k_c=torch.empty((B * T, d), dtype=t["k"].dtype, device=DEV),
+                v_c=torch.empty((B * T, d), dtype=t["k"].dtype, device=DEV),
+                kept_pos=torch.empty(B * T, dtype=torch.int32, device=DEV),
+                offsets=torch.empty(B * Hkv + 1, dtype=torch.int64, device=DEV),
+                scores=torch.empty((B, Hkv, C - wl.obs_window), dtype=torch.float32, device=DEV))
+    offs_host = sg.segment_offsets(budgets, B)
+    dws = sg.alloc_workspace(sg.decode_workspace_size(sg.decode_desc(t["q"], Hkv, torch.float32), offs_host), DEV)
+    dout = torch.empty((B, Hq, d), dtype=torch.float32, device=DEV)
+    dlse = torch.empty((B, Hq), dtype=torch.float32, device=DEV)
+
+    def layer():
+        sg.compress_layer(t["q_win"], t["k"], t["v"], budgets, pool_kernel=kp, b_sink=s, b_window=W,
+                          workspace=ws, out=outs)
+        sg.decode_attention(t["q"], outs["k_c"], outs["v_c"], outs["offsets"], offs_host, Hkv,
+                            out_dtype=torch.float32, workspace=dws, out=dout, lse=dlse)
+
+    layer()  # eager once: device checks and plans are cached before the capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        layer()
+    torch.cuda.synchronize()
+    for r in range(3):
+        _, fresh = _qwen_small(B, C, seed_layer=r + 1)
+        for name in ("q_win", "k", "v", "q"):
+            t[name].copy_(fresh[name])
+        _announce(f"graph replay {r}")
+        g.replay()
+        torch.cuda.synchronize()
+        got = {n: x.clone() for n, x in outs.items()}
+        got_out, got_lse = dout.clone(), dlse.clone()
+        ref = sg.compress_layer(t["q_win"], t["k"], t["v"], budgets, pool_kernel=kp, b_sink=s, b_window=W)
+        ref_out, ref_lse = sg.decode_attention(t["q"], ref["k_c"], ref["v_c"], ref["offsets"], ref["offsets_host"],
+                                               Hkv, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        for n in outs:
+            assert torch.equal(got[n], ref[n]), f"replay {r}: {n} differs from the eager call"
+        assert torch.equal(got_out, ref_out) and torch.equal(got_lse, ref_lse), f"replay {r}: decode differs"
+        if r:
+            assert not torch.equal(got["scores"], prev), "the replay read the new inputs"
+        prev = got["scores"]
+
+
 def test_run_twice_bitwise():
     wl, t = _qwen_small(2, 2222)
     budgets = np.array([700, 500, 1500, 400])
