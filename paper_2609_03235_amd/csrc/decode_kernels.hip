@@ -63,6 +63,18 @@ __device__ __forceinline__ void decode_workgroup(const DecodeArgs& a, int& seg, 
   }
 }
 
+// A segment's partial slots: the first one and how many (its launched workgroups, compressed
+// rows' first, appended rows' after them).
+__device__ __forceinline__ void segment_slots(const DecodeArgs& a, int seg, int64_t& base, int& n) {
+  if (a.compact) {
+    base = a.wg_start[seg];
+    n = a.wg_start[seg + 1] - a.wg_start[seg];
+  } else {
+    n = a.n_cwg + a.n_new_wg;
+    base = (int64_t)seg * n;
+  }
+}
+
 __device__ __forceinline__ void clamp_segment(const DecodeArgs& a, int seg, int64_t& r0, int64_t& r1) {
   const int nseg = a.B * a.Hkv;
   const rsrc_t orr = make_rsrc(a.offsets, (uint64_t)(nseg + 1) * 8);
@@ -348,9 +360,9 @@ __global__ __launch_bounds__(kDecodeBlock, OCC) void decode_split_kernel(DecodeA
       o[g][e] = x;
     }
   // Merge the workgroup's splits: each wave leaves its (m, s) and o per head in LDS; then the
-  // workgroup's threads merge them in wave order and write one partial per head at slot x:
-  // (m, s) and o[D] in two arrays, one descriptor each for the whole group (per-lane descriptors
-  // would cost waterfall loops).
+  // workgroup's threads merge them in wave order and write one partial per head in the
+  // workgroup's slot: (m, s) and o[D] in two arrays, one descriptor each over the segment's slots
+  // (per-lane descriptors would cost waterfall loops).
   if (lr == 0) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -367,11 +379,12 @@ __global__ __launch_bounds__(kDecodeBlock, OCC) void decode_split_kernel(DecodeA
         *reinterpret_cast<f32x4*>(&ows[wid][g][col0 + e]) = f32x4{o[g][e], o[g][e + 1], o[g][e + 2], o[g][e + 3]};
   }
   __syncthreads();
-  const int64_t bq0 = (int64_t)b * a.Hq + (int64_t)h * G;
-  const int64_t ncm = a.n_part;
-  const uint32_t slot = x;
-  const rsrc_t mr = make_rsrc(a.part_ms + bq0 * ncm * 2, (uint64_t)G * ncm * 8);
-  const rsrc_t orr = make_rsrc(a.part + bq0 * ncm * D, (uint64_t)G * ncm * D * 4);
+  int64_t sbase;
+  int nsl;
+  segment_slots(a, seg, sbase, nsl);
+  const int64_t slot = a.compact ? (int64_t)blockIdx.x - sbase : x;  // within the segment's slots
+  const rsrc_t mr = make_rsrc(a.part_ms + sbase * G * 2, (uint64_t)nsl * G * 8);
+  const rsrc_t orr = make_rsrc(a.part + sbase * G * D, (uint64_t)nsl * G * D * 4);
   for (int idx = tid; idx < G * D; idx += kDecodeBlock) {
     const int g = idx / D, col = idx % D;
     float M = -INFINITY;
@@ -385,9 +398,9 @@ __global__ __launch_bounds__(kDecodeBlock, OCC) void decode_split_kernel(DecodeA
       O += ows[w][g][col] * e;
       Ssum += sws[w][g] * e;
     }
-    stf(orr, (uint32_t)((((int64_t)g * ncm + slot) * D + col) * 4), O);
+    stf(orr, (uint32_t)(((slot * G + g) * D + col) * 4), O);
     if (col == 0)
-      st64(mr, (uint32_t)(((int64_t)g * ncm + slot) * 8),
+      st64(mr, (uint32_t)((slot * G + g) * 8),
            (uint64_t)__float_as_uint(M) | ((uint64_t)__float_as_uint(Ssum) << 32));
   }
 }
@@ -402,24 +415,28 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
   __shared__ float red_m[NG], red_s[NG];
   __shared__ __attribute__((aligned(16))) float red_o[NG][D];
   const int bq = blockIdx.x;
-  const int b = bq / a.Hq, qh = bq % a.Hq, h = qh / a.G;
+  const int b = bq / a.Hq, qh = bq % a.Hq, h = qh / a.G, g = qh % a.G;
   const int seg = b * a.Hkv + h;
-  const int64_t ncm = a.n_part;
-  const int ncw = a.compact ? a.wg_start[seg + 1] - a.wg_start[seg] - a.n_new_wg : a.n_cwg;
+  int64_t sbase;
+  int nsl;
+  segment_slots(a, seg, sbase, nsl);
+  const int64_t ncm = nsl;  // the segment's slots; slot ncm (past the descriptor) reads as zeros
+  const int ncw = nsl - a.n_new_wg;  // launched workgroups of the compressed rows
+  const int G = a.G;
   const int tid = threadIdx.x, c4 = tid % TPR, grp = tid / TPR;
-  const rsrc_t mr = make_rsrc(a.part_ms + (int64_t)bq * ncm * 2, (uint64_t)ncm * 8);
-  const rsrc_t orr = make_rsrc(a.part + (int64_t)bq * ncm * D, (uint64_t)ncm * D * 4);
+  const rsrc_t mr = make_rsrc(a.part_ms + sbase * G * 2, (uint64_t)nsl * G * 8);
+  const rsrc_t orr = make_rsrc(a.part + sbase * G * D, (uint64_t)nsl * G * D * 4);
   // The first batch of slots is loaded before the segment's length is known, as if every
-  // compressed slot were valid (slots past n_part read as zeros), so that its loads travel
-  // together with the offsets' instead of after them; slots that turn out invalid are not used.
+  // compressed slot were valid, so that its loads travel together with the offsets' instead of
+  // after them; slots that turn out invalid are not used.
   uint64_t ms[U];
   u32x4 ov[U];
   auto load_batch = [&](int64_t c, auto&& slot_of) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t sl = slot_of(c + u * NG);
-      ms[u] = ld64(mr, (uint32_t)(sl * 8));
-      ov[u] = ld128(orr, (uint32_t)((sl * D + 4 * c4) * 4));
+      ms[u] = ld64(mr, (uint32_t)((sl * G + g) * 8));
+      ov[u] = ld128(orr, (uint32_t)(((sl * G + g) * D + 4 * c4) * 4));
     }
   };
   load_batch(grp, [&](int64_t c) { return c < ncm ? c : ncm; });
@@ -427,14 +444,14 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
   clamp_segment(a, seg, r0, r1);
   const int64_t len = r1 - r0;
   // valid slots: the workgroups of the segment's nseg splits, then those of its appended splits
-  // from slot n_cwg on; dense index c maps to slot c (c < ncs) or n_cwg + c - ncs (past nch:
-  // the offset past the buffer, which reads as zeros)
+  // from slot ncw on; dense index c maps to slot c (c < ncs) or ncw + c - ncs (past nch: the
+  // slot past the descriptor, which reads as zeros)
   int64_t nseg = (len + a.chunk - 1) / a.chunk;
   if (nseg > a.n_chunk_max) nseg = a.n_chunk_max;
   if (nseg > (int64_t)ncw * kWaves) nseg = (int64_t)ncw * kWaves;  // as the split kernel clamps
   const int64_t ncs = (nseg + kWaves - 1) / kWaves;
   const int64_t nch = ncs + (a.n_new_chunks + kWaves - 1) / kWaves;
-  auto slot = [&](int64_t c) { return c >= nch ? ncm : (c < ncs ? c : a.n_cwg + (c - ncs)); };
+  auto slot = [&](int64_t c) { return c >= nch ? ncm : (c < ncs ? c : ncw + (c - ncs)); };
   if (a.n_new_chunks > 0) load_batch(grp, slot);  // appended slots do not follow the compressed ones
   float M = -INFINITY, S = 0.f, O[4] = {0.f, 0.f, 0.f, 0.f};
   for (int64_t c = grp; c < nch; c += U * NG) {

@@ -720,8 +720,20 @@ sgdkv_status plan_decode(const sgdkv_decode_desc* d, const int64_t* offsets_host
   a.cap = capacity;
   const int wpw = sgdkv::kDecodeWaves;  // splits (waves) per decode workgroup
   a.n_cwg = (int)ceil_div(a.n_chunk_max, wpw);
-  a.n_part = a.n_cwg + (int)ceil_div(ceil_div(capacity, a.chunk), wpw);
-  p.bytes = align256((size_t)a.B * a.Hq * a.n_part * (a.D + 2) * sizeof(float));
+  // one partial slot per launched workgroup: with the compact grid each segment's own
+  // workgroups (so the workspace follows the total of the splits, not the longest segment),
+  // otherwise n_cwg per segment; plus the workgroups of a full appended region
+  const int64_t new_wg_cap = ceil_div(ceil_div(capacity, a.chunk), wpw);
+  if (nseg <= sgdkv::kMaxCompactSegs) {
+    int64_t slots = 0;
+    for (int64_t i = 0; i < nseg; ++i)
+      slots += ceil_div(std::min<int64_t>(ceil_div(offsets_host[i + 1] - offsets_host[i], a.chunk), a.n_chunk_max),
+                        wpw) + new_wg_cap;
+    a.n_slots = slots;
+  } else {
+    a.n_slots = nseg * (a.n_cwg + new_wg_cap);
+  }
+  p.bytes = align256((size_t)a.n_slots * G * (a.D + 2) * sizeof(float));
   return SGDKV_OK;
 }
 
@@ -819,7 +831,7 @@ sgdkv_status decode_step(const sgdkv_decode_desc* desc, const void* q, const voi
     }
   }
   a.part = static_cast<float*>(workspace);
-  a.part_ms = a.part + (size_t)a.B * a.Hq * a.n_part * a.D;
+  a.part_ms = a.part + (size_t)a.n_slots * a.G * a.D;
   hipError_t e = hipGetLastError();
   (void)e;
   e = sgdkv::launch_decode(a, static_cast<hipStream_t>(stream));

@@ -111,9 +111,11 @@ struct DecodeArgs {
   void* out;
   float* lse_out;
   // The splits of a segment are grouped by workgroup (kDecodeWaves splits each), and a workgroup
-  // merges its splits into one partial per query head: slot = the workgroup's index in x.
-  float* part;        // [B*Hq][n_part][D]: o per workgroup slot (16-byte aligned rows)
-  float* part_ms;     // [B*Hq][n_part][2]: (m, s) per workgroup slot
+  // merges its splits into one partial per query head of the group, in its own slot: its flat
+  // index in the compact grid, seg * (n_cwg + n_new_wg) + x in the (x, segment) grid. A segment's
+  // slots are contiguous (its compressed rows' workgroups, then its appended rows').
+  float* part;        // [n_slots][G][D]: o per slot and query head (16-byte aligned rows)
+  float* part_ms;     // [n_slots][G][2]: (m, s) per slot and query head
   int64_t chunk;      // rows per split (multiple of 64, at least 128)
   int n_chunk_max;    // max over segments of ceil(len / chunk): splits of the compressed rows
   int n_cwg;          // ceil(n_chunk_max / waves per workgroup): workgroups (slots) of the compressed rows
@@ -123,7 +125,7 @@ struct DecodeArgs {
   const void* v_new;
   int64_t cap, n_new;
   int n_new_chunks;   // ceil(n_new / chunk)
-  int n_part;         // slots per (b, q): n_cwg + ceil(ceil(capacity / chunk) / waves per workgroup)
+  int64_t n_slots;    // slots the workspace holds (planned for the appended region's capacity)
   // Compact grid (B*Hkv <= kMaxCompactSegs): only workgroups with work are launched, segment
   // after segment (from the host copy of the offsets); segment s owns workgroups
   // [wg_start[s], wg_start[s+1]), its compressed rows' first, then n_new_wg for its appended rows.

@@ -387,10 +387,12 @@ def test_segment_offsets_errors():
 
 def test_noalloc_decode_rejects_partials_beyond_the_static_scratch():
     """The static scratch holds 64 MiB of split partials; a decode that needs more is refused
-    before anything is enqueued (validation precedes the device check, so no GPU is needed)."""
+    before anything is enqueued (validation precedes the device check, so no GPU is needed).
+    Beyond 512 segments every segment holds the slots of the longest one: 1024 segments with one
+    of 2^23 rows need gigabytes."""
     lib = sg.load_library()
-    desc = sg.DecodeDesc(64, 64, 8, 128, sg.DTYPE_BF16, sg.DTYPE_F32, 0.0)
-    oh = np.full(64 * 8 + 1, 1 << 23, dtype=np.int64)
+    desc = sg.DecodeDesc(128, 64, 8, 128, sg.DTYPE_BF16, sg.DTYPE_F32, 0.0)
+    oh = np.full(128 * 8 + 1, 1 << 23, dtype=np.int64)
     oh[0] = 0  # one segment of 2^23 rows, the others empty
     assert sg.decode_workspace_size(desc, oh) > 64 << 20
     P = sg._np_ptr
@@ -405,6 +407,28 @@ def test_noalloc_decode_rejects_partials_beyond_the_static_scratch():
     if not _gpu():
         assert lib.sgdkv_decode_attention_noalloc(ctypes.byref(d2), FAKE, FAKE, FAKE, FAKE, P(small), None, FAKE,
                                                   None, None) == sg.ERR_HIP
+
+
+def test_decode_workspace_follows_the_splits_not_the_longest_segment():
+    """With up to 512 segments the split partials are one slot per launched decode workgroup
+    (G*(d+2) floats): about 16384 splits over the batch, four per workgroup, plus at most one
+    part-filled workgroup per segment, however unequal the segments. One segment of 2^23 rows
+    among 511 empty ones needs the same few megabytes as equal segments of the same total, and
+    both fit the 64 MiB static scratch."""
+    G, d = 8, 128
+    per_wg = G * (d + 2) * 4
+    for lens in ([1 << 23] + [0] * 511, [(1 << 23) // 512] * 512, [1 << 14] * 7 + [1 << 22]):
+        n = len(lens)
+        desc = sg.DecodeDesc(n // 8, 8 * G, 8, d, sg.DTYPE_BF16, sg.DTYPE_F32, 0.0)
+        oh = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+        need = sg.decode_workspace_size(desc, oh)
+        wgs = need // per_wg
+        assert need <= 64 << 20 and wgs <= 16384 // 4 + n + 1, (lens[:3], need)
+        assert wgs >= sum(lens) // (1 << 16)  # at least one workgroup per 4 splits of at most 16384 rows
+    # appended regions add their workgroups per segment
+    desc = sg.DecodeDesc(2, 16, 2, d, sg.DTYPE_BF16, sg.DTYPE_F32, 0.0)
+    oh = np.array([0, 1000, 1000, 5000, 5000], dtype=np.int64)
+    assert sg.decode_workspace_size(desc, oh, 4096) > sg.decode_workspace_size(desc, oh)
 
 
 @pytest.mark.skipif(_gpu(), reason="checks the no-device path")
