@@ -375,28 +375,35 @@ __global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
   }
 }
 
-// Merge the per-chunk partials of every window row: one thread per row of segment
-// blockIdx.y takes the maximum of the chunk references, then adds the rescaled sums in
-// chunk order, in fp64. Neighbouring threads read neighbouring rows, so the loads coalesce.
+// Merge the per-chunk partials of every window row in fp64: 16 lanes per row (16 rows per
+// workgroup of segment blockIdx.y), lane l taking chunks l, l+16, ...; the maximum of the chunk
+// references over the 16 lanes, then each lane's rescaled sums in chunk order, and the 16 lane
+// sums added in a fixed butterfly order. A row's lanes read neighbouring chunks' partials.
+constexpr int kMergeLanes = 16;
 __global__ __launch_bounds__(kBlock) void lse_merge_kernel(CompressArgs a) {
   const int64_t seg = blockIdx.y;
-  const int row = blockIdx.x * kBlock + threadIdx.x;
-  if (row >= a.R) return;
+  const int lane = threadIdx.x % kMergeLanes;
+  const int row = blockIdx.x * (kBlock / kMergeLanes) + threadIdx.x / kMergeLanes;
+  const bool live = row < a.R;  // every lane takes part in the shuffles
   const int n = a.n_lse_chunks;
   const rsrc_t pr = make_rsrc(a.lse_part + seg * n * a.R * 2, (uint64_t)n * a.R * 2 * sizeof(float));
   auto off = [&](int c) { return (uint32_t)(((int64_t)c * a.R + row) * 8); };
   float mx = -INFINITY;
-#pragma unroll 8
-  for (int c = 0; c < n; ++c) mx = fmaxf(mx, ldf(pr, off(c)));
+  if (live)
+    for (int c = lane; c < n; c += kMergeLanes) mx = fmaxf(mx, ldf(pr, off(c)));
+#pragma unroll
+  for (int o = 1; o < kMergeLanes; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
   double sum = 0.0;
-  if (mx != -INFINITY) {
-#pragma unroll 8
-    for (int c = 0; c < n; ++c) {
+  if (live && mx != -INFINITY) {
+    for (int c = lane; c < n; c += kMergeLanes) {
       const uint64_t ms = ld64(pr, off(c));
       const float mc = __uint_as_float((uint32_t)ms), sc = __uint_as_float((uint32_t)(ms >> 32));
       if (mc != -INFINITY) sum += (double)sc * exp2((double)mc - (double)mx);
     }
   }
+#pragma unroll
+  for (int o = 1; o < kMergeLanes; o <<= 1) sum += __shfl_xor(sum, o, 64);
+  if (!live || lane != 0) return;
   const float lse2 = (mx == -INFINITY || !(sum > 0.0)) ? -INFINITY : (float)((double)mx + log2(sum));
   const rsrc_t lr = make_rsrc(a.lse2 + seg * a.R, (uint64_t)a.R * sizeof(float));
   stf(lr, (uint32_t)row * 4u, lse2);
@@ -582,7 +589,8 @@ static hipError_t launch_scores_t(const CompressArgs& a, hipStream_t st) {
   const dim3 sblk(kScoreBlock);
   if (a.window_lse == nullptr) {
     SGDKV_LAUNCH("score_lse", (lse_kernel<T, D, RBW>), dim3(a.n_lse_chunks, a.B * a.Hkv, a.n_rsplit), sblk, st, a);
-    SGDKV_LAUNCH("lse_merge", lse_merge_kernel, dim3((unsigned)((a.R + kBlock - 1) / kBlock), a.B * a.Hkv),
+    constexpr int rows_per_wg = kBlock / kMergeLanes;
+    SGDKV_LAUNCH("lse_merge", lse_merge_kernel, dim3((unsigned)((a.R + rows_per_wg - 1) / rows_per_wg), a.B * a.Hkv),
                  dim3(kBlock), st, a);
   }
   if (a.n_col_chunks > 0) {
