@@ -387,12 +387,13 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, int64_t win0, CompressP
   }
 
   const int64_t nseg = (int64_t)a.B * a.Hkv;
-  // score workgroups: about 512 in total (two per CU, one resident at a time: fewer, longer
-  // workgroups measured faster than more, shorter ones), counting each row split; a chunk is a
-  // whole number of key tiles, so no tile of pass 1 reaches into the next chunk (which would count
-  // those keys twice). The chunk does not depend on the aggregation, so neither does the workspace.
+  // score workgroups: about one per compute unit in total (one round of one resident workgroup per
+  // CU: fewer, longer workgroups measured faster than two rounds, and 1.5 rounds leave the second
+  // half empty), counting each row split; a chunk is a whole number of key tiles, so no tile of
+  // pass 1 reaches into the next chunk (which would count those keys twice). The chunk does not
+  // depend on the aggregation, so neither does the workspace.
   a.score_chunk = std::min<int64_t>(
-      std::max<int64_t>(round_up(ceil_div(nseg * a.n_rsplit * a.C, 512), sgdkv::kScoreChunkQuantum),
+      std::max<int64_t>(round_up(ceil_div(nseg * a.n_rsplit * a.C, sgdkv::kScoreWorkgroups), sgdkv::kScoreChunkQuantum),
                         2 * sgdkv::kScoreChunkQuantum),
       1 << 16);
   // pass 1 covers the keys some window row sees: [0, min(C, win0 + w))

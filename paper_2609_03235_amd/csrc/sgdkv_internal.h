@@ -24,6 +24,7 @@ constexpr int kLseTile = 128;      // keys staged in LDS per step of score pass 
 constexpr int kColTileBf16 = 128;  // keys staged in LDS per step of score pass 2 (bf16 keys)
 constexpr int kColTileF32 = 64;    // the same for fp32 keys (LDS holds half as many)
 constexpr int kScoreChunkQuantum = 128;  // score chunks are whole tiles of both passes
+constexpr int kScoreWorkgroups = 256;   // score workgroups a launch aims at: the MI355X's compute units
 constexpr int kHistChunkMax = 8192;      // positions per pooling / radix-pass workgroup, at most
 constexpr int kPoolHalo = 64;            // pooling radii up to this are staged in LDS
 constexpr int kCopyRows = 64;            // output rows per work item of the row gather
