@@ -10,7 +10,7 @@
 //
 //   pass 1 (lse_kernel + lse_merge_kernel): base-2 log-sum-exp of every
 //     window row over its causal keys. Each workgroup covers one chunk of
-//     keys (about 512 workgroups per launch) and leaves per-row partials
+//     keys (about one workgroup per CU per launch) and leaves per-row partials
 //     (m, s); the merge combines the chunks in a fixed order, in fp64.
 //   pass 2 (colsum_kernel): for every scored key j < P0,
 //     a_j = (1/G) sum_rows exp2(l_rj*log2(e) - lse2_r) (group mean; the Ipt.
