@@ -715,11 +715,19 @@ sgdkv_status plan_decode(const sgdkv_decode_desc* d, const int64_t* offsets_host
   // kDecodeMinChunk rows; one round of longer splits measured slower
   a.chunk = std::min<int64_t>(
       std::max<int64_t>(round_up(ceil_div(total - offsets_host[0], kDecodeSplits), 64), kDecodeMinChunk), 1 << 24);
+  // a batch whose minimum-size splits would launch fewer workgroups than the device has compute
+  // units gets splits half as long (64 rows measured best at 32K x B 1: shorter ones add more
+  // partials to combine than they save)
+  const int wpw = sgdkv::kDecodeWaves;  // splits (waves) per decode workgroup
+  if (a.chunk == kDecodeMinChunk) {
+    int64_t wgs = 0;
+    for (int64_t i = 0; i < nseg; ++i) wgs += ceil_div(ceil_div(offsets_host[i + 1] - offsets_host[i], a.chunk), wpw);
+    if (wgs < sgdkv::kScoreWorkgroups) a.chunk = kDecodeMinChunk / 2;
+  }
   a.n_chunk_max = (int)ceil_div(longest, a.chunk);
   if ((int64_t)a.B * a.Hkv * capacity * rb > 0xFFFFFFFFll)
     return fail(SGDKV_ERR_UNSUPPORTED, "appended regions of %lld rows per head exceed 4 GiB", (long long)capacity);
   a.cap = capacity;
-  const int wpw = sgdkv::kDecodeWaves;  // splits (waves) per decode workgroup
   a.n_cwg = (int)ceil_div(a.n_chunk_max, wpw);
   // one partial slot per launched workgroup: with the compact grid each segment's own
   // workgroups (so the workspace follows the total of the splits, not the longest segment),

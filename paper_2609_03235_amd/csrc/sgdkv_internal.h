@@ -24,7 +24,7 @@ constexpr int kLseTile = 128;      // keys staged in LDS per step of score pass 
 constexpr int kColTileBf16 = 128;  // keys staged in LDS per step of score pass 2 (bf16 keys)
 constexpr int kColTileF32 = 64;    // the same for fp32 keys (LDS holds half as many)
 constexpr int kScoreChunkQuantum = 128;  // score chunks are whole tiles of both passes
-constexpr int kScoreWorkgroups = 256;   // score workgroups a launch aims at: the MI355X's compute units
+constexpr int kScoreWorkgroups = 256;   // workgroups that fill the MI355X (its compute units): score launches aim at it
 constexpr int kHistChunkMax = 8192;      // positions per pooling / radix-pass workgroup, at most
 constexpr int kPoolHalo = 64;            // pooling radii up to this are staged in LDS
 constexpr int kCopyRows = 64;            // output rows per work item of the row gather
@@ -117,7 +117,7 @@ struct DecodeArgs {
   // slots are contiguous (its compressed rows' workgroups, then its appended rows').
   float* part;        // [n_slots][G][D]: o per slot and query head (16-byte aligned rows)
   float* part_ms;     // [n_slots][G][2]: (m, s) per slot and query head
-  int64_t chunk;      // rows per split (multiple of 64, at least 128)
+  int64_t chunk;      // rows per split (multiple of 64, at least 128, or 64 for a batch too small to fill the chip)
   int n_chunk_max;    // max over segments of ceil(len / chunk): splits of the compressed rows
   int n_cwg;          // ceil(n_chunk_max / waves per workgroup): workgroups (slots) of the compressed rows
   // rows appended after compression: (b, h) owns rows [0, n_new) of k_new/v_new + (b*Hkv+h)*cap rows;

@@ -571,14 +571,14 @@ def test_decode_fixed_reference_redo():
     rng = np.random.Generator(np.random.PCG64(21))
     d, Hq, Hkv = 128, 8, 4
     # B=1. The segments' 16-row steps are dealt to their splits in turn (split w takes steps w,
-    # w + n, ...), n = 5, 3, 8, 1 splits with 128-row splits (3, 2, 4, 1 with 256-row ones): every
-    # planted key sits at step >= n, so it is past the first step of its split
+    # w + n, ...), n = 10, 5, 15, 1 splits with the 64-row splits a batch this small gets (5, 3, 8, 1
+    # with 128-row ones): every planted key sits at step >= n, so it is past the first step of its split
     lens = [600, 300, 900, 40]
     offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
     q = rng.standard_normal((1, Hq, d))
     kc = rng.standard_normal((offs[-1], d))
     vc = rng.standard_normal((offs[-1], d))
-    for seg, pos, f in ((0, 120, 6.0), (0, 356, 6.0), (2, 700, 9.0)):
+    for seg, pos, f in ((0, 200, 6.0), (0, 356, 6.0), (2, 700, 9.0)):
         kc[offs[seg] + pos] = f * q[0, 2 * seg]  # far above the first step of its split
     kc[offs[1] + 100] = 3.0 * q[0, 2]  # ~38 above the first step's maximum: s stays below 2^64 ...
     vc[offs[1] + 100] = 1e30  # ... but 2^38 * 1e30 overflows o
