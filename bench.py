@@ -150,10 +150,10 @@ KERNEL_OF = {  # demangled ("sgdkv::name<...") or mangled ("_ZN5sgdkv<len>name..
     "decode_split": r"sgdkv(::|\d+)decode_split_kernel", "decode_combine": r"sgdkv(::|\d+)decode_combine_kernel",
     "pool_radix_hist": r"sgdkv(::|\d+)radix_pass_kernel(<0, true, true|ILi0ELb1ELb1E)",
     "radix_hist": r"sgdkv(::|\d+)radix_pass_kernel(<[123], false, true|ILi[123]ELb0ELb1E)",
-    "sel_count": r"sgdkv(::|\d+)sel_count_kernel", "compact": r"sgdkv(::|\d+)compact_kernel"}
+    "compact": r"sgdkv(::|\d+)compact_kernel"}
 SOURCE_OF = {"score_lse": "score_kernels.hip", "score_colsum": "score_kernels.hip", "lse_merge": "score_kernels.hip",
              "gather": "select_kernels.hip", "pool_radix_hist": "select_kernels.hip", "radix_hist": "select_kernels.hip",
-             "sel_count": "select_kernels.hip", "compact": "select_kernels.hip",
+             "compact": "select_kernels.hip",
              "decode_split": "decode_kernels.hip", "decode_combine": "decode_kernels.hip"}
 SHARED_SOURCES = ("device_common.h", "mfma_frag.h", "sgdkv_internal.h", "segment_init.h")
 
@@ -302,7 +302,7 @@ def summarize_counters(paths, args):
              "per XCD); VALU issue = 4 x SQ_ACTIVE_INST_VALU / (SIMDs x cycles) (wave-cycles, so it can pass 1 "
              "with several waves per SIMD); dual issue = 4 x SQ_ACTIVE_INST_VALU2 / (SIMDs x cycles); "
              "co-execution = SQ_VALU_MFMA_COEXEC_CYCLES / SQ_VALU_MFMA_BUSY_CYCLES.", ""]
-    for name in ("score_lse", "score_colsum", "pool_radix_hist", "radix_hist", "sel_count", "compact", "gather",
+    for name in ("score_lse", "score_colsum", "pool_radix_hist", "radix_hist", "compact", "gather",
                  "decode_split", "decode_combine"):
         if name not in vals:
             continue

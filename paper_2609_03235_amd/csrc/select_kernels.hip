@@ -19,14 +19,15 @@
 //                  which otherwise does it, does not run)
 //   radix_pass<p>  digit-p histogram of candidates matching the digits
 //                  before it (each workgroup picks those from the earlier
-//                  histograms itself); pass 0 also pools:
+//                  histograms itself); the last pass also keeps each chunk's
+//                  histogram and its count above the prefix; pass 0 also pools:
 //                  pooled_j = (1/k_p) sum_{|t-j|<=r} a_t (zero outside), where
 //                  a_t combines the column-sum partials of the score pass's
 //                  row splits in split order (their sum; their maximum for
 //                  the Ipt. max aggregation)
-//   sel_count      picks the last digit (tau and q complete); per chunk:
-//                  sink/window rows, candidates > tau, == tau
-//   compact        ordered ballot/prefix compaction of a chunk -> kept_pos
+//   compact        picks tau and q from the four histograms, then the ordered
+//                  ballot/prefix compaction of a chunk -> kept_pos (the rows kept
+//                  before the chunk from the last radix pass's chunk histograms)
 //   copy_rows      K and V rows of the kept positions -> the ragged cache
 #include <algorithm>
 
@@ -40,19 +41,10 @@ namespace {
 
 // Radix-select state of a segment: the digits of tau found so far (prefix,
 // under mask) and how many rows are still to place among the candidates that
-// match them. sel_count stores the final one (tau, q) for the compaction.
+// match them; after the fourth digit, prefix = tau and rem = q.
 struct SegState {
   uint32_t prefix, mask, rem;
 };
-
-__device__ __forceinline__ SegState load_state(const CompressArgs& a, int seg) {
-  const rsrc_t r = make_rsrc(a.state + (int64_t)seg * 4, 16);
-  SegState st;
-  st.prefix = ld32(r, 0);
-  st.mask = ld32(r, 4);
-  st.rem = ld32(r, 8);
-  return st;
-}
 
 // Adds one to bin `bin` of an LDS histogram for every lane with `valid` (call
 // with the whole wave). Scores crowd into a few bins, where one atomic per
@@ -285,14 +277,29 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(CompressArgs a) {
   } else {
     __syncthreads();
     const int64_t c0 = j0 > cbeg ? j0 : cbeg, c1 = j1 < cend ? j1 : cend;
+    uint32_t above = 0;  // the last pass: candidates above the 24-bit prefix (all of them above tau)
     for (int64_t jb = c0; jb < c1; jb += U * kBlock) {
       uint32_t x[U];
 #pragma unroll
       for (int u = 0; u < U; ++u) x[u] = ld32(pr, (uint32_t)((jb + tid + u * kBlock) * 4));
       // few candidates still match the prefix here, spread over more bins: one atomic per lane
 #pragma unroll
-      for (int u = 0; u < U; ++u)
-        if (jb + tid + u * kBlock < c1 && (x[u] & st.mask) == st.prefix) atomicAdd(&lh[(x[u] >> shift) & 255u], 1u);
+      for (int u = 0; u < U; ++u) {
+        const bool in = jb + tid + u * kBlock < c1;
+        if (in && (x[u] & st.mask) == st.prefix) atomicAdd(&lh[(x[u] >> shift) & 255u], 1u);
+        if (PASS == 3) above += in && (x[u] & st.mask) > st.prefix;
+      }
+    }
+    if constexpr (PASS == 3) {
+      // the chunk's histogram and its count above, for the compaction's running totals
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) above += __shfl_xor(above, o, 64);
+      if ((tid & 63) == 0) lh[256 + (tid >> 6)] = above;
+      __syncthreads();
+      const rsrc_t chr = make_rsrc(a.chunk_hist + ((int64_t)seg * a.n_hist_chunks + blockIdx.x) * kChunkHistWords,
+                                   kChunkHistWords * 4);
+      st32(chr, (uint32_t)tid * 4u, lh[tid]);
+      if (tid == 0) st32(chr, 256u * 4u, lh[256] + lh[257] + lh[258] + lh[259]);
     }
   }
   if (!hist) return;
@@ -301,110 +308,64 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(CompressArgs a) {
   if (v) atomicAdd(a.hist + ((int64_t)seg * 4 + PASS) * 256 + tid, v);
 }
 
-__global__ __launch_bounds__(kBlock) void sel_count_kernel(CompressArgs a) {
-  __shared__ uint32_t red[3][kBlock / 64];
-  __shared__ uint32_t sh[256 + 8];
-  const int seg = blockIdx.y, h = seg % a.Hkv;
-  const SegState st = derive_state<4>(a, seg, sh);
-  if (blockIdx.x == 0 && threadIdx.x == 0) {  // tau and q for the compaction
-    const rsrc_t sr = make_rsrc(a.state + (int64_t)seg * 4, 16);
-    st32(sr, 0, st.prefix);
-    st32(sr, 4, st.mask);
-    st32(sr, 8, st.rem);
-  }
-  const bool active = a.m[h] > 0;
-  const uint32_t tau = st.prefix;
-  const int64_t j0 = (int64_t)blockIdx.x * a.sel_chunk;
-  const int64_t j1 = j0 + a.sel_chunk < a.C ? j0 + a.sel_chunk : a.C;
-  const int64_t cend = a.C - a.W;
-  const rsrc_t pr = make_rsrc(a.pooled + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
-  uint32_t nf = 0, ng = 0, ne = 0;
-  // U loads per thread in flight before any is used; positions past the scored range read 0
-  // (outside the descriptor) and are window rows anyway
-  constexpr int U = 8;
-  for (int64_t base = j0; base < j1; base += U * kBlock) {
-    uint32_t x[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) x[u] = ld32(pr, (uint32_t)((base + u * kBlock + threadIdx.x) * 4));
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int64_t j = base + u * kBlock + threadIdx.x;
-      if (j >= j1) continue;
-      if (j < a.s || j >= cend) {
-        ++nf;
-      } else if (active) {
-        ng += x[u] > tau;
-        ne += x[u] == tau;
-      }
-    }
-  }
-  // fixed-order block reduction
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    nf += __shfl_xor(nf, o, 64);
-    ng += __shfl_xor(ng, o, 64);
-    ne += __shfl_xor(ne, o, 64);
-  }
-  const int wid = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) {
-    red[0][wid] = nf;
-    red[1][wid] = ng;
-    red[2][wid] = ne;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t f = 0, g = 0, e = 0;
-    for (int u = 0; u < kBlock / 64; ++u) {
-      f += red[0][u];
-      g += red[1][u];
-      e += red[2][u];
-    }
-    const rsrc_t cr = make_rsrc(a.counts + (int64_t)seg * a.n_sel_chunks * 4,
-                                (uint64_t)a.n_sel_chunks * 16);
-    const uint32_t base = blockIdx.x * 16u;
-    st32(cr, base + 0, f);
-    st32(cr, base + 4, g);
-    st32(cr, base + 8, e);
-  }
-}
-
-// Ordered compaction of one chunk of positions: writes the prompt positions of
-// the kept rows (ascending) into the segment's slice of kept_pos.
+// Ordered compaction of one chunk of positions (the chunks of the radix passes, then chunks of
+// window rows): writes the prompt positions of the kept rows (ascending) into the segment's
+// slice of kept_pos. tau and q come from the segment's four digit histograms; the rows the
+// chunks before this one keep, from their positions (sink and window rows) and, for their
+// candidates, the last pass's chunk histograms: those above tau's top 24 bits, those matching
+// them with a last digit above tau's, and those equal to tau (of which the first q are kept).
 __global__ __launch_bounds__(kBlock) void compact_kernel(CompressArgs a) {
   __shared__ uint32_t wt0[kBlock / 64], wt1[kBlock / 64];
   __shared__ uint32_t pre[3][kBlock / 64];
+  __shared__ uint32_t sh[256 + 8];
   const int seg = blockIdx.y, b = seg / a.Hkv, h = seg % a.Hkv;
   const int chunk = blockIdx.x;
   const int tid = threadIdx.x;
-  const SegState st = load_state(a, seg);
+  const SegState st = derive_state<4>(a, seg, sh);
   const bool active = a.m[h] > 0;
   const uint32_t tau = st.prefix;
   const uint32_t q = active ? st.rem : 0u;
+  const int64_t j0 = (int64_t)chunk * a.hist_chunk;
+  const int64_t j1 = j0 + a.hist_chunk < a.C ? j0 + a.hist_chunk : a.C;
+  const int64_t cend = a.C - a.W;
 
   // totals of the chunks before this one: sink/window rows, > tau, == tau
-  const rsrc_t cr = make_rsrc(a.counts + (int64_t)seg * a.n_sel_chunks * 4, (uint64_t)a.n_sel_chunks * 16);
-  uint32_t f = 0, g = 0, e = 0;
-  for (int c = tid; c < chunk; c += kBlock) {
-    f += ld32(cr, c * 16u + 0);
-    g += ld32(cr, c * 16u + 4);
-    e += ld32(cr, c * 16u + 8);
+  const uint32_t F = (uint32_t)((j0 < a.s ? j0 : a.s) + (j0 > cend ? j0 - cend : 0));
+  uint32_t g = 0, e = 0;
+  if (active) {
+    const int nc = chunk < a.n_hist_chunks ? chunk : a.n_hist_chunks;
+    const rsrc_t chr = make_rsrc(a.chunk_hist + (int64_t)seg * a.n_hist_chunks * kChunkHistWords,
+                                 (uint64_t)a.n_hist_chunks * kChunkHistWords * 4);
+    const uint32_t dt = tau & 255u;
+    constexpr int U = 32;  // loads in flight per thread
+    uint32_t bin = 0, above = 0;
+    for (int c0 = 0; c0 < nc; c0 += U) {
+      uint32_t x[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c = c0 + u < nc ? c0 + u : nc;  // past the chunks before this one: read, not used
+        x[u] = ld32(chr, (uint32_t)(c * kChunkHistWords + tid) * 4u);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) bin += c0 + u < nc ? x[u] : 0u;
+    }
+    for (int c = tid; c < nc; c += kBlock) above += ld32(chr, (uint32_t)(c * kChunkHistWords + 256) * 4u);
+    g = above + (tid > (int)dt ? bin : 0u);
+    e = tid == (int)dt ? bin : 0u;
   }
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
-    f += __shfl_xor(f, o, 64);
     g += __shfl_xor(g, o, 64);
     e += __shfl_xor(e, o, 64);
   }
   if ((tid & 63) == 0) {
-    pre[0][tid >> 6] = f;
     pre[1][tid >> 6] = g;
     pre[2][tid >> 6] = e;
   }
   __syncthreads();
-  uint32_t F = 0, Gt = 0, E = 0;
+  uint32_t Gt = 0, E = 0;
 #pragma unroll
   for (int u = 0; u < kBlock / 64; ++u) {
-    F += pre[0][u];
     Gt += pre[1][u];
     E += pre[2][u];
   }
@@ -416,9 +377,6 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(CompressArgs a) {
   const rsrc_t kp = make_rsrc(a.kept_pos + seg_off, (uint64_t)seg_len * 4);
   const rsrc_t pr = make_rsrc(a.pooled + (int64_t)seg * a.n_scored, (uint64_t)a.n_scored * 4);
 
-  const int64_t j0 = (int64_t)chunk * a.sel_chunk;
-  const int64_t j1 = j0 + a.sel_chunk < a.C ? j0 + a.sel_chunk : a.C;
-  const int64_t cend = a.C - a.W;
   // positions in order, 256 at a time; the scores of the next U*256 are loaded together first
   constexpr int U = 8;
   for (int64_t ubase = j0; ubase < j1; ubase += U * kBlock) {
@@ -524,8 +482,7 @@ hipError_t launch_select(const CompressArgs& a, bool scores_only, hipStream_t st
     SGDKV_LAUNCH("radix_hist", (radix_pass_kernel<2, false, true>), hgrid, blk, st, a);
     SGDKV_LAUNCH("radix_hist", (radix_pass_kernel<3, false, true>), hgrid, blk, st, a);
   }
-  SGDKV_LAUNCH("sel_count", sel_count_kernel, dim3(a.n_sel_chunks, nseg), blk, st, a);
-  SGDKV_LAUNCH("compact", compact_kernel, dim3(a.n_sel_chunks, nseg), blk, st, a);
+  SGDKV_LAUNCH("compact", compact_kernel, dim3(a.n_cmp_chunks, nseg), blk, st, a);
   return hipGetLastError();
 }
 

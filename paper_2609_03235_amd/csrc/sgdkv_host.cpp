@@ -296,7 +296,7 @@ namespace {
 
 struct CompressPlan {
   sgdkv::CompressArgs a;
-  size_t off_lse_part, off_lse2, off_colsum, off_pooled, off_hist, off_state, off_counts, bytes;
+  size_t off_lse_part, off_lse2, off_colsum, off_pooled, off_hist, off_chunk_hist, bytes;
   int colsum_splits;  // row splits the column-sum region has room for
 };
 
@@ -399,13 +399,12 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, int64_t win0, CompressP
   // pass 1 covers the keys some window row sees: [0, min(C, win0 + w))
   a.n_lse_chunks = (int)ceil_div(std::min<int64_t>(a.C, win0 + a.w), a.score_chunk);
   a.n_col_chunks = (int)ceil_div(a.n_scored, a.score_chunk);
-  // selection workgroups: about 2048 in total
-  a.sel_chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(nseg * a.C, 2048), 256), 1024), 1 << 20);
-  // pooling and radix passes: about 1024 workgroups, at most kHistChunkMax positions each
-  a.hist_chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(nseg * a.n_scored, 1024), 256), 256),
+  // pooling, radix and compaction passes: about 1024 workgroups, of 1024 to kHistChunkMax positions
+  // (fewer, longer chunks at small sizes: the compaction adds up the chunks before its own)
+  a.hist_chunk = std::min<int64_t>(std::max<int64_t>(round_up(ceil_div(nseg * a.n_scored, 1024), 256), 1024),
                                    sgdkv::kHistChunkMax);
   a.n_hist_chunks = (int)ceil_div(a.n_scored, a.hist_chunk);
-  a.n_sel_chunks = (int)ceil_div(a.C, a.sel_chunk);
+  a.n_cmp_chunks = (int)ceil_div(a.C, a.hist_chunk);
 
   size_t off = 0;
   p.off_lse_part = off;
@@ -418,10 +417,8 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, int64_t win0, CompressP
   off += align256((size_t)nseg * a.C * sizeof(float));
   p.off_hist = off;
   off += align256((size_t)nseg * 4 * 256 * sizeof(uint32_t));  // one 256-bin histogram per radix digit
-  p.off_state = off;
-  off += align256((size_t)nseg * 4 * sizeof(uint32_t));
-  p.off_counts = off;
-  off += align256((size_t)nseg * a.n_sel_chunks * 4 * sizeof(uint32_t));
+  p.off_chunk_hist = off;
+  off += align256((size_t)nseg * a.n_hist_chunks * sgdkv::kChunkHistWords * sizeof(uint32_t));
   p.bytes = off;
   return SGDKV_OK;
 }
@@ -611,8 +608,7 @@ sgdkv_status sgdkv_compress_layer_ex(const sgdkv_compress_desc* desc, const sgdk
   a.lse2 = reinterpret_cast<float*>(ws + p.off_lse2);
   a.colsum = reinterpret_cast<float*>(ws + p.off_colsum);
   a.hist = reinterpret_cast<uint32_t*>(ws + p.off_hist);
-  a.state = reinterpret_cast<uint32_t*>(ws + p.off_state);
-  a.counts = reinterpret_cast<uint32_t*>(ws + p.off_counts);
+  a.chunk_hist = reinterpret_cast<uint32_t*>(ws + p.off_chunk_hist);
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = hipGetLastError();  // clear a stale error left by earlier, unrelated work

@@ -27,6 +27,7 @@ constexpr int kScoreChunkQuantum = 128;  // score chunks are whole tiles of both
 constexpr int kScoreWorkgroups = 256;   // workgroups that fill the MI355X (its compute units): score launches aim at it
 constexpr int kHistChunkMax = 8192;      // positions per pooling / radix-pass workgroup, at most
 constexpr int kPoolHalo = 64;            // pooling radii up to this are staged in LDS
+constexpr int kChunkHistWords = 260;     // a scored chunk's last-digit histogram and count above (16-byte rows)
 constexpr int kCopyRows = 64;            // output rows per work item of the row gather
 #ifndef SGDKV_SCORE_WAVES
 #define SGDKV_SCORE_WAVES 8
@@ -73,8 +74,9 @@ struct CompressArgs {
   float* lse2;      // [B*Hkv][R]                   base-2 LSE of each window row
   float* colsum;    // [n_rsplit][B*Hkv][n_scored]: one column-sum partial per row split
   uint32_t* hist;   // [B*Hkv][4][256]: histogram of each radix digit
-  uint32_t* state;  // [B*Hkv][4]: tau, its mask, q (rows equal to tau to keep), unused
-  uint32_t* counts; // [B*Hkv][n_sel_chunks][4]: fixed, greater, equal, unused
+  // [B*Hkv][n_hist_chunks][kChunkHistWords]: per scored chunk, the last digit's histogram of its
+  // candidates that match tau's top 24 bits (256 bins), then how many candidates lie above them
+  uint32_t* chunk_hist;
   // row splits: the R window rows of a KV head are split over n_rsplit score workgroups per key
   // chunk (grid z), split p holding rows [p*rs_rows, min(R, (p+1)*rs_rows)); rs_rows is a
   // multiple of 16 (of w for the Ipt. max aggregation, so that no query head straddles two)
@@ -84,10 +86,9 @@ struct CompressArgs {
   int64_t score_chunk;  // keys per score workgroup (multiple of kScoreChunkQuantum)
   int n_lse_chunks;     // ceil(min(C, win0 + w) / score_chunk): keys some window row sees
   int n_col_chunks;     // ceil(n_scored / score_chunk)
-  int64_t sel_chunk;    // positions per selection workgroup
-  int64_t hist_chunk;   // scored positions per pooling / radix-pass workgroup (multiple of 256)
-  int n_hist_chunks;    // ceil(n_scored / hist_chunk)
-  int n_sel_chunks;     // ceil(C / sel_chunk)
+  int64_t hist_chunk;   // positions per pooling / radix-pass / compaction workgroup (multiple of 256)
+  int n_hist_chunks;    // ceil(n_scored / hist_chunk): scored chunks
+  int n_cmp_chunks;     // ceil(C / hist_chunk): compaction chunks (the last ones hold window rows only)
   // per KV head of this layer (shared by every sequence)
   int64_t T_layer;
   int64_t m[kMaxKvHeads];           // middle rows kept per head
