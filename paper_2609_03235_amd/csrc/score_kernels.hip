@@ -348,13 +348,19 @@ __global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
   __shared__ __attribute__((aligned(16))) char ktile[2 * kLseTile * G::LDS_STRIDE];
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
-  // the last chunks go first: the one with the window block ends with its exact (masked) tiles
+  // the tail chunk (the causally masked tiles, on the exact path) goes first, then the uniform
+  // chunks of keys every row sees; keys past the last window row's position are seen by no row
   const int chunk = (int)(gridDim.x - 1 - blockIdx.x);
-  const int64_t key0 = (int64_t)chunk * a.score_chunk;
-  // keys past the last window row's position are seen by no row
   const int64_t vis_end = a.win0 + a.w < a.C ? a.win0 + a.w : a.C;
-  if (key0 >= vis_end) return;
-  const int64_t key_end = key0 + a.score_chunk < vis_end ? key0 + a.score_chunk : vis_end;
+  int64_t key0, key_end;
+  if (chunk < a.n_lse_head) {
+    key0 = (int64_t)chunk * a.lse_chunk;
+    key_end = key0 + a.lse_chunk < a.lse_tail0 ? key0 + a.lse_chunk : a.lse_tail0;
+  } else {
+    key0 = a.lse_tail0;
+    key_end = vis_end;
+  }
+  if (key0 >= key_end) return;
   const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
   const int r0 = (int)blockIdx.z * a.rs_rows;
   const int nrows = a.R - r0 < a.rs_rows ? a.R - r0 : a.rs_rows;

@@ -297,6 +297,7 @@ namespace {
 struct CompressPlan {
   sgdkv::CompressArgs a;
   size_t off_lse_part, off_lse2, off_colsum, off_pooled, off_hist, off_chunk_hist, bytes;
+  int lse_chunks_max;  // pass-1 chunks any window position gives (sizes their partials)
   int colsum_splits;  // row splits the column-sum region has room for
 };
 
@@ -396,8 +397,37 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, int64_t win0, CompressP
       std::max<int64_t>(round_up(ceil_div(nseg * a.n_rsplit * a.C, sgdkv::kScoreWorkgroups), sgdkv::kScoreChunkQuantum),
                         2 * sgdkv::kScoreChunkQuantum),
       1 << 16);
-  // pass 1 covers the keys some window row sees: [0, min(C, win0 + w))
-  a.n_lse_chunks = (int)ceil_div(std::min<int64_t>(a.C, win0 + a.w), a.score_chunk);
+  // pass 1 covers the keys some window row sees, [0, min(C, win0 + w)), in uniform chunks (about
+  // one workgroup per CU). The chunk holding the causally masked tiles runs them on the exact
+  // path, which then ends the launch. Where that costs more than what splitting those tiles off
+  // into a short chunk of their own costs -- its workgroups (one per segment and row split, on
+  // the exact path, dispatched first) leave their CUs idle for the rest of the launch, about
+  // tiles-per-chunk x tails / (256 CUs) tile times, against about two for the exact tiles --
+  // the masked tiles get that chunk, and the uniform chunks aim at the CUs the tails leave. The
+  // chunk sizes depend on C only, so the workspace does not depend on win0.
+  {
+    const int64_t tails = nseg * a.n_rsplit;
+    const int64_t vis_end = std::min<int64_t>(a.C, win0 + a.w);
+    const int64_t open_end = std::min<int64_t>(a.C, win0);
+    auto chunk_for = [&](int64_t target) {
+      return std::min<int64_t>(
+          std::max<int64_t>(round_up(ceil_div(tails * a.C, target), sgdkv::kScoreChunkQuantum),
+                            2 * sgdkv::kScoreChunkQuantum),
+          1 << 16);
+    };
+    a.lse_chunk = chunk_for(sgdkv::kScoreWorkgroups);
+    const bool split_tail = (a.lse_chunk / sgdkv::kLseTile) * tails < 2 * sgdkv::kScoreWorkgroups &&
+                            tails < sgdkv::kScoreWorkgroups;
+    if (split_tail) {
+      a.lse_chunk = chunk_for(sgdkv::kScoreWorkgroups - tails);
+      a.lse_tail0 = open_end / sgdkv::kLseTile * sgdkv::kLseTile;
+    } else {
+      a.lse_tail0 = vis_end;  // no tail chunk: the last uniform chunk holds the masked tiles
+    }
+    a.n_lse_head = (int)ceil_div(a.lse_tail0, a.lse_chunk);
+    a.n_lse_chunks = a.n_lse_head + (vis_end > a.lse_tail0 ? 1 : 0);
+    p.lse_chunks_max = (int)ceil_div(a.C, a.lse_chunk) + 1;
+  }
   a.n_col_chunks = (int)ceil_div(a.n_scored, a.score_chunk);
   // pooling, radix and compaction passes: about 1024 workgroups, of 1024 to kHistChunkMax positions
   // (fewer, longer chunks at small sizes: the compaction adds up the chunks before its own)
@@ -408,7 +438,7 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, int64_t win0, CompressP
 
   size_t off = 0;
   p.off_lse_part = off;
-  off += align256((size_t)nseg * a.n_lse_chunks * R * 2 * sizeof(float));
+  off += align256((size_t)nseg * p.lse_chunks_max * R * 2 * sizeof(float));
   p.off_lse2 = off;
   off += align256((size_t)nseg * R * sizeof(float));
   p.off_colsum = off;

@@ -83,8 +83,14 @@ struct CompressArgs {
   int n_rsplit;
   int rs_rows;
   // chunking
-  int64_t score_chunk;  // keys per score workgroup (multiple of kScoreChunkQuantum)
-  int n_lse_chunks;     // ceil(min(C, win0 + w) / score_chunk): keys some window row sees
+  int64_t score_chunk;  // keys per pass-2 workgroup (multiple of kScoreChunkQuantum)
+  // pass 1: n_lse_head chunks of lse_chunk keys over [0, lse_tail0), the keys every window row sees
+  // in whole tiles, then (if any key remains that some row sees) one chunk [lse_tail0, min(C, win0 + w))
+  // holding the causally masked tiles, which take the exact path
+  int64_t lse_chunk;
+  int64_t lse_tail0;
+  int n_lse_head;
+  int n_lse_chunks;     // n_lse_head + the tail chunk
   int n_col_chunks;     // ceil(n_scored / score_chunk)
   int64_t hist_chunk;   // positions per pooling / radix-pass / compaction workgroup (multiple of 256)
   int n_hist_chunks;    // ceil(n_scored / hist_chunk): scored chunks
