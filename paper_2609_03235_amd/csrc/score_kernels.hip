@@ -124,10 +124,11 @@ __device__ __forceinline__ void load_group_queries(const CompressArgs& a, int b,
 // before its end, makes that buffer readable; the buffer written at the start
 // of tile t was last read before the barrier of tile t-1. The MFMAs of the
 // subtile after the chunk's last one run on whatever keys follow (zeros past
-// the head) and are discarded. On gfx950 a wave's own MFMAs and vector
-// instructions issue one after the other, and exp2 overlaps little with the
-// MFMAs of the SIMD's other wave; the two waves of a SIMD mainly hide each
-// other's latencies.
+// the head) and are discarded. REV streams the chunk's tiles last to first
+// (step t covers tile ntiles-1-t; the steps after the last read zeros). On
+// gfx950 a wave's own MFMAs and vector instructions issue one after the other,
+// and exp2 overlaps little with the MFMAs of the SIMD's other wave; the two
+// waves of a SIMD mainly hide each other's latencies.
 template <typename T, int D, int NB>
 __device__ __forceinline__ void subtile_mfma(const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
                                              const Frag<T> (&kb)[D / 32], f32x4 (&acc)[NB > 0 ? NB : 1]) {
@@ -148,7 +149,8 @@ __device__ __forceinline__ void subtile_frags(const char* ktile, int t, int lr, 
 // Hooks: begin(acc) once with the logits of the chunk's first subtile (before
 // any sub call); sub(t, s, acc) per subtile; at_barrier(t) right after tile t's
 // barrier; end_tile(t) after tile t's last subtile.
-template <typename T, int D, int NB, int TILE, typename Begin, typename Sub, typename AtBarrier, typename EndTile>
+template <typename T, int D, int NB, int TILE, bool REV = false, typename Begin, typename Sub, typename AtBarrier,
+          typename EndTile>
 __device__ __forceinline__ void chunk_pipeline(char* kbuf, const rsrc_t& kr, int64_t key0, int64_t C, int64_t ntiles,
                                                int lr, int lg, const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32],
                                                Begin&& begin, Sub&& sub, AtBarrier&& at_barrier, EndTile&& end_tile) {
@@ -159,7 +161,7 @@ __device__ __forceinline__ void chunk_pipeline(char* kbuf, const rsrc_t& kr, int
   static_assert(S >= 4 && S % 2 == 0, "tile geometry");
   // keys past the head read as zeros; the clamp keeps byte offsets below 4 GiB
   auto tile_key = [&](int64_t t) {
-    const int64_t k = key0 + t * TILE;
+    const int64_t k = REV ? (t < ntiles ? key0 + (ntiles - 1 - t) * TILE : C) : key0 + t * TILE;
     return k < C ? k : C;
   };
   KeyStage<T, D, TILE> stage;
@@ -462,6 +464,10 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
   const float c2 = a.c2;
   const int nseg = a.B * a.Hkv;
   const rsrc_t cr = make_rsrc(a.colsum + ((int64_t)blockIdx.z * nseg + seg) * a.n_scored, (uint64_t)a.n_scored * 4);
+  // The chunk's tiles go last to first: pass 1 streams about the same chunks first to last, so
+  // the keys it read last, the ends of the chunks, are partly still in the last-level cache.
+  // Each key's sum does not depend on the order, so neither does the result.
+  const int64_t ntiles = (key_end - key0 + TILE - 1) / TILE;
   // Partials of tile t sit in red[t % 3]: written during tile t, complete at the barrier of
   // tile t+1, summed right after it, rewritten only after the barrier of tile t+2. Each
   // wave sums CPW columns: the LPC lanes of a column read the partials of PPL waves each
@@ -511,12 +517,11 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
       for (int o = CPW; o < 16; o <<= 1) v += __shfl_xor(v, o, 64);
       v = sum_lane_groups(v);
     }
-    const int64_t key = key0 + t * TILE + rcol;
+    const int64_t key = key0 + (ntiles - 1 - t) * TILE + rcol;  // step t holds tile ntiles-1-t
     const bool store = t >= 0 && lane < CPW && key < key_end;
     stf(cr, store ? (uint32_t)(key * 4) : (uint32_t)(a.n_scored * 4), v * a.out_scale);
   };
-  const int64_t ntiles = (key_end - key0 + TILE - 1) / TILE;
-  chunk_pipeline<T, D, NB, TILE>(
+  chunk_pipeline<T, D, NB, TILE, true>(
       kbuf, kr, key0, a.C, ntiles, lr, lg, qa, [](const f32x4(&)[NBX]) {},
       [&](int64_t t, int sub, const f32x4(&acc)[NBX]) {
         if constexpr (BP) {
