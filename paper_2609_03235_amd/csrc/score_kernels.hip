@@ -435,10 +435,22 @@ constexpr bool block_partials() {
   return MAXG && !HW;
 }
 
+// LDS layout of pass 2's column partials: three tiles in flight, each with RW partial rows of
+// TILE columns per wave. A partial row is 16 banks further than the one before it and a wave's
+// rows 16 banks further again, so that neither the four lane groups of a wave storing a subtile
+// nor the four waves whose partials the reduction reads together meet in one bank.
+template <typename T, int RW>
+struct ColPartials {
+  static constexpr int TILE = col_tile<T>();
+  static constexpr int SL = TILE + 16;         // floats per partial row
+  static constexpr int SW = RW * SL + 16;      // floats per wave
+  static constexpr int ST = kScoreWaves * SW;  // floats per tile
+  static constexpr int WORDS = 3 * ST;
+  __device__ static constexpr int at(int t3, int wave, int r, int col) { return t3 * ST + wave * SW + r * SL + col; }
+};
+
 template <typename T, int D, int NB, int RBW, bool MAXG, bool HW>
-__device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
-                             float (*red)[kScoreWaves][block_partials<MAXG, HW>() ? RBW : 4][col_tile<T>()],
-                             int seg, int r0, int nrows, int wid, int lane,
+__device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float* red, int seg, int r0, int nrows, int wid, int lane,
                              const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], const rsrc_t& kr, int64_t key0,
                              int64_t key_end) {
   constexpr int NBX = NB > 0 ? NB : 1;
@@ -478,8 +490,9 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
   static_assert(CPW <= 16 && 64 % CPW == 0 && PPL >= 1 && PPL * LPC == kScoreWaves, "reduction layout");
   const int rcol = CPW * wid + lane % CPW, rgrp = lane / CPW;
   constexpr bool BP = block_partials<MAXG, HW>();
+  using CP = ColPartials<T, BP ? RBW : 4>;
   auto reduce = [&](int64_t t) {  // t may be -1: nothing is stored
-    const float(*r)[BP ? RBW : 4][TILE] = red[(t + 3) % 3];
+    const float* r = red + CP::at((int)((uint32_t)(t + 3) % 3u), 0, 0, 0);
     float v = 0.f;
     if constexpr (MAXG && HW) {
       // the LPC lanes of a column take the split's heads in turn: add the four lane-group
@@ -489,7 +502,7 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
         float sum = 0.f;
         for (int wv = g * wph; wv < (g + 1) * wph; ++wv)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) sum += r[wv][q][rcol];
+          for (int q = 0; q < 4; ++q) sum += r[wv * CP::SW + q * CP::SL + rcol];
         v = fmaxf(v, a.qweight[h * a.G + g0 + g] * sum);
       }
 #pragma unroll
@@ -501,7 +514,8 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
       const int bph = a.w / 16, g0 = r0 / a.w, ng = nrows / a.w;
       for (int g = rgrp; g < ng; g += LPC) {
         float sum = 0.f;
-        for (int bb = g * bph; bb < (g + 1) * bph; ++bb) sum += r[bb % kScoreWaves][bb / kScoreWaves][rcol];
+        for (int bb = g * bph; bb < (g + 1) * bph; ++bb)
+          sum += r[(bb % kScoreWaves) * CP::SW + (bb / kScoreWaves) * CP::SL + rcol];
         v = fmaxf(v, a.qweight[h * a.G + g0 + g] * sum);
       }
 #pragma unroll
@@ -512,7 +526,7 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
 #pragma unroll
       for (int k = 0; k < PPL; ++k)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) v += r[rgrp + LPC * k][g][rcol];
+        for (int g = 0; g < 4; ++g) v += r[(rgrp + LPC * k) * CP::SW + g * CP::SL + rcol];
 #pragma unroll
       for (int o = CPW; o < 16; o <<= 1) v += __shfl_xor(v, o, 64);
       v = sum_lane_groups(v);
@@ -524,13 +538,14 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
   chunk_pipeline<T, D, NB, TILE, true>(
       kbuf, kr, key0, a.C, ntiles, lr, lg, qa, [](const f32x4(&)[NBX]) {},
       [&](int64_t t, int sub, const f32x4(&acc)[NBX]) {
+        const int t3 = (int)((uint32_t)t % 3u);  // tiles of a chunk: far fewer than 2^32
         if constexpr (BP) {
           // one column partial per row block (a single query head's rows)
 #pragma unroll
           for (int j = 0; j < NB; ++j) {
             const float p = (fast_exp2(fmaf(acc[j][0], c2, nlse[j][0])) + fast_exp2(fmaf(acc[j][1], c2, nlse[j][1]))) +
                             (fast_exp2(fmaf(acc[j][2], c2, nlse[j][2])) + fast_exp2(fmaf(acc[j][3], c2, nlse[j][3])));
-            red[t % 3][wid][j][16 * sub + lr] = sum_lane_groups(p);
+            red[CP::at(t3, wid, j, 16 * sub + lr)] = sum_lane_groups(p);
           }
         } else {
           float p = 0.f;
@@ -545,7 +560,7 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf,
               for (int i = 0; i < 4; ++i) pp[i] += fast_exp2(fmaf(acc[j][i], c2, nlse[j][i]));
             p = (pp[0] + pp[1]) + (pp[2] + pp[3]);
           }
-          red[t % 3][wid][lg][16 * sub + lr] = p;  // one partial per lane group; the reduction adds them
+          red[CP::at(t3, wid, lg, 16 * sub + lr)] = p;  // one partial per lane group; the reduction adds them
         }
       },
       [&](int64_t t) { reduce(t - 1); }, [](int64_t) {});
@@ -557,7 +572,7 @@ template <typename T, int D, int RBW, bool MAXG, bool HW>
 __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) {
   using G = TileGeom<T, D>;
   __shared__ __attribute__((aligned(16))) char ktile[2 * col_tile<T>() * G::LDS_STRIDE];
-  __shared__ float red[3][kScoreWaves][block_partials<MAXG, HW>() ? RBW : 4][col_tile<T>()];
+  __shared__ __attribute__((aligned(16))) float red[ColPartials<T, block_partials<MAXG, HW>() ? RBW : 4>::WORDS];
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
   if (blockIdx.x == 0 && blockIdx.z == 0) init_segment(a, seg);  // histograms, offsets for the selection
