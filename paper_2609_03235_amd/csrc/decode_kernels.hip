@@ -275,8 +275,9 @@ __global__ __launch_bounds__(kDecodeBlock, OCC) void decode_split_kernel(DecodeA
   clamp_segment(a, seg, r0, r1);
   const int64_t len = r1 - r0;
   // workgroups 0 .. n_cwg-1 cover the segment's compressed rows, the next ones the rows appended
-  // since compression. A workgroup whose first split is empty leaves (uniform over the
-  // workgroup); a wave whose own split is empty joins the merge with an empty partial.
+  // since compression. Compact grid: every launched workgroup writes its slot (an empty partial
+  // if it has no rows). (x, segment) grid: a workgroup whose first split is empty leaves (uniform
+  // over the workgroup). A wave whose own split is empty joins the merge with an empty partial.
   const bool appended = x >= a.n_cwg;
   const int64_t wg = appended ? (int64_t)x - a.n_cwg : (int64_t)x;
   const int64_t chunk = wg * kWaves + wid;  // split index within the region
@@ -288,18 +289,24 @@ __global__ __launch_bounds__(kDecodeBlock, OCC) void decode_split_kernel(DecodeA
   int nsteps = 0;
   bool active;
   if (appended) {
-    if (wg * kWaves * a.chunk >= rows) return;
+    if (!a.compact && wg * kWaves * a.chunk >= rows) return;
     c0 = chunk * a.chunk;
     active = c0 < rows;
     c1 = c0 + a.chunk < rows ? c0 + a.chunk : rows;
     nsteps = active ? (int)((c1 - c0 + 15) / 16) : 0;
   } else {
-    int64_t nck = (rows + a.chunk - 1) / a.chunk;
-    // device offsets beyond the host's: fewer, longer splits (as many as were launched)
-    if (nck > a.n_chunk_max) nck = a.n_chunk_max;
-    if (nck > (int64_t)ncw * kWaves) nck = (int64_t)ncw * kWaves;
+    // compact grid: four splits per launched workgroup (at most one per step); (x, segment) grid:
+    // splits of about a.chunk rows, and device offsets beyond the host's give fewer, longer
+    // splits (as many as were launched)
     const int64_t total_steps = (rows + 15) / 16;
-    if (wg * kWaves >= nck) return;
+    int64_t nck = a.compact ? (int64_t)ncw * kWaves : (rows + a.chunk - 1) / a.chunk;
+    if (a.compact) {
+      if (nck > total_steps) nck = total_steps;
+    } else {
+      if (nck > a.n_chunk_max) nck = a.n_chunk_max;
+      if (nck > (int64_t)ncw * kWaves) nck = (int64_t)ncw * kWaves;
+      if (wg * kWaves >= nck) return;
+    }
     active = chunk < nck;
     c0 = chunk * 16;
     stride = nck * 16;
@@ -440,19 +447,23 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeArgs a) {
     }
   };
   load_batch(grp, [&](int64_t c) { return c < ncm ? c : ncm; });
-  int64_t r0, r1;
-  clamp_segment(a, seg, r0, r1);
-  const int64_t len = r1 - r0;
-  // valid slots: the workgroups of the segment's nseg splits, then those of its appended splits
-  // from slot ncw on; dense index c maps to slot c (c < ncs) or ncw + c - ncs (past nch: the
-  // slot past the descriptor, which reads as zeros)
-  int64_t nseg = (len + a.chunk - 1) / a.chunk;
-  if (nseg > a.n_chunk_max) nseg = a.n_chunk_max;
-  if (nseg > (int64_t)ncw * kWaves) nseg = (int64_t)ncw * kWaves;  // as the split kernel clamps
-  const int64_t ncs = (nseg + kWaves - 1) / kWaves;
-  const int64_t nch = ncs + (a.n_new_chunks + kWaves - 1) / kWaves;
+  // Valid slots. Compact grid: all of the segment's (every launched workgroup writes its slot).
+  // (x, segment) grid: the workgroups of the segment's nsp splits, then those of its appended
+  // splits from slot ncw on; dense index c maps to slot c (c < ncs) or ncw + c - ncs (past nch:
+  // the slot past the descriptor, which reads as zeros).
+  int64_t ncs = ncm, nch = ncm;
+  if (!a.compact) {
+    int64_t r0, r1;
+    clamp_segment(a, seg, r0, r1);
+    const int64_t len = r1 - r0;
+    int64_t nsp = (len + a.chunk - 1) / a.chunk;
+    if (nsp > a.n_chunk_max) nsp = a.n_chunk_max;
+    if (nsp > (int64_t)ncw * kWaves) nsp = (int64_t)ncw * kWaves;  // as the split kernel clamps
+    ncs = (nsp + kWaves - 1) / kWaves;
+    nch = ncs + (a.n_new_chunks + kWaves - 1) / kWaves;
+    if (a.n_new_chunks > 0) load_batch(grp, [&](int64_t c) { return c >= nch ? ncm : (c < ncs ? c : ncw + (c - ncs)); });
+  }
   auto slot = [&](int64_t c) { return c >= nch ? ncm : (c < ncs ? c : ncw + (c - ncs)); };
-  if (a.n_new_chunks > 0) load_batch(grp, slot);  // appended slots do not follow the compressed ones
   float M = -INFINITY, S = 0.f, O[4] = {0.f, 0.f, 0.f, 0.f};
   for (int64_t c = grp; c < nch; c += U * NG) {
     if (c != grp) load_batch(c, slot);

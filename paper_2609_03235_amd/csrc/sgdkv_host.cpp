@@ -13,6 +13,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -687,8 +688,54 @@ namespace {
 #ifndef SGDKV_DECODE_MIN_CHUNK
 #define SGDKV_DECODE_MIN_CHUNK 128
 #endif
+#ifndef SGDKV_DECODE_WHOLE_ROUNDS
+#define SGDKV_DECODE_WHOLE_ROUNDS 1
+#endif
 constexpr int64_t kDecodeSplits = SGDKV_DECODE_SPLITS;
 constexpr int64_t kDecodeMinChunk = SGDKV_DECODE_MIN_CHUNK;
+constexpr bool kDecodeWholeRounds = SGDKV_DECODE_WHOLE_ROUNDS != 0;
+// decode workgroups the MI355X runs at once: two per compute unit (their registers), 256 units
+constexpr int64_t kDecodeResident = 2 * sgdkv::kScoreWorkgroups;
+
+// Workgroups of each segment's compressed rows on the compact grid. Each workgroup's four waves
+// are four splits of about chunk rows, which gives w0 workgroups in all. The device runs
+// kDecodeResident of them at once and starts the next one where one ends, so a grid of, say,
+// 3.7 rounds leaves a quarter of the device idle for a workgroup's length at its end. With more
+// than one round, the workgroups are therefore shared out over the segments in proportion to
+// their 16-row steps (largest remainder, ties to the lower segment; a non-empty segment left
+// with none gets one from the largest) so that they fill the nearest whole number of rounds; the
+// kernel deals a segment's steps to four splits per launched workgroup.
+std::vector<int64_t> compact_workgroups(const int64_t* offsets_host, int64_t nseg, int64_t chunk) {
+  const int64_t wpw = sgdkv::kDecodeWaves;
+  std::vector<int64_t> n((size_t)nseg);
+  int64_t w0 = 0, steps = 0;
+  for (int64_t i = 0; i < nseg; ++i) {
+    const int64_t len = offsets_host[i + 1] - offsets_host[i];
+    n[i] = ceil_div(ceil_div(len, chunk), wpw);
+    w0 += n[i];
+    steps += ceil_div(len, 16);
+  }
+  if (!kDecodeWholeRounds || w0 <= kDecodeResident) return n;
+  const int64_t target = (w0 + kDecodeResident / 2) / kDecodeResident * kDecodeResident;
+  std::vector<std::pair<int64_t, int64_t>> rem;  // (fractional part scaled by steps, -segment)
+  int64_t given = 0;
+  for (int64_t i = 0; i < nseg; ++i) {
+    const int64_t st = ceil_div(offsets_host[i + 1] - offsets_host[i], 16);
+    n[i] = target * st / steps;
+    rem.emplace_back(target * st % steps, -i);
+    given += n[i];
+  }
+  std::sort(rem.begin(), rem.end(), std::greater<>());
+  for (int64_t j = 0; j < target - given; ++j) n[(size_t)-rem[(size_t)j].second] += 1;
+  // a non-empty segment whose share rounded to none gets one, taken from the largest segment
+  for (int64_t i = 0; i < nseg; ++i) {
+    if (n[i] != 0 || offsets_host[i + 1] == offsets_host[i]) continue;
+    n[i] = 1;
+    const int64_t big = std::max_element(n.begin(), n.end()) - n.begin();
+    if (n[big] > 1) n[big] -= 1;
+  }
+  return n;
+}
 
 struct DecodePlan {
   sgdkv::DecodeArgs a;
@@ -760,11 +807,15 @@ sgdkv_status plan_decode(const sgdkv_decode_desc* d, const int64_t* offsets_host
   // otherwise n_cwg per segment; plus the workgroups of a full appended region
   const int64_t new_wg_cap = ceil_div(ceil_div(capacity, a.chunk), wpw);
   if (nseg <= sgdkv::kMaxCompactSegs) {
-    int64_t slots = 0;
-    for (int64_t i = 0; i < nseg; ++i)
-      slots += ceil_div(std::min<int64_t>(ceil_div(offsets_host[i + 1] - offsets_host[i], a.chunk), a.n_chunk_max),
-                        wpw) + new_wg_cap;
+    int64_t slots = 0, most = 0;
+    for (const int64_t n : compact_workgroups(offsets_host, nseg, a.chunk)) {
+      slots += n + new_wg_cap;
+      most = std::max(most, n);
+    }
     a.n_slots = slots;
+    // a segment's appended-row workgroups are numbered from n_cwg on: past its compressed-row
+    // workgroups, also where whole rounds gave a segment more of them than its splits need
+    a.n_cwg = (int)std::max<int64_t>(a.n_cwg, most);
   } else {
     a.n_slots = nseg * (a.n_cwg + new_wg_cap);
   }
@@ -857,12 +908,12 @@ sgdkv_status decode_step(const sgdkv_decode_desc* desc, const void* q, const voi
   const int64_t nseg = (int64_t)a.B * a.Hkv;
   a.compact = nseg <= sgdkv::kMaxCompactSegs ? 1 : 0;
   if (a.compact) {
+    const std::vector<int64_t> wgs = compact_workgroups(offsets_host, nseg, a.chunk);
     int64_t run = 0;
     a.wg_start[0] = 0;
     for (int64_t i = 0; i < nseg; ++i) {
-      const int64_t splits = std::min<int64_t>(ceil_div(offsets_host[i + 1] - offsets_host[i], a.chunk), a.n_chunk_max);
-      run += ceil_div(splits, sgdkv::kDecodeWaves) + a.n_new_wg;
-      a.wg_start[i + 1] = (int32_t)run;  // at most nseg * (n_cwg + n_new_wg) workgroups
+      run += wgs[(size_t)i] + a.n_new_wg;
+      a.wg_start[i + 1] = (int32_t)run;
     }
   }
   a.part = static_cast<float*>(workspace);

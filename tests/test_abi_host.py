@@ -431,6 +431,28 @@ def test_decode_workspace_follows_the_splits_not_the_longest_segment():
     assert sg.decode_workspace_size(desc, oh, 4096) > sg.decode_workspace_size(desc, oh)
 
 
+def test_decode_workgroups_fill_whole_rounds():
+    """Beyond one round of decode workgroups (the 512 an MI355X runs at once), the compact grid's
+    workgroups are shared out over the segments so that they fill a whole number of rounds:
+    one workgroup slot each, so the workspace holds a multiple of 512 slots. One round or less
+    keeps a workgroup per four splits of the planned length."""
+    G, d = 7, 128
+    per_wg = G * (d + 2) * 4
+    rng = np.random.Generator(np.random.PCG64(5))
+    for n, hi in [(32, 70000), (128, 140000), (512, 3000), (37, 50000)]:
+        lens = rng.integers(0, hi, size=n)
+        lens[::9] = 0
+        lens[1::13] = 1
+        desc = sg.DecodeDesc(1, n * G, n, d, sg.DTYPE_BF16, sg.DTYPE_F32, 0.0)
+        oh = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+        wgs = sg.decode_workspace_size(desc, oh) // per_wg
+        assert wgs % 512 == 0 and wgs >= int(np.count_nonzero(lens)), (n, hi, wgs)
+    lens = [300, 0, 1000, 5]  # under one round: four splits per workgroup (64 rows each, a batch this small)
+    desc = sg.DecodeDesc(1, 4 * G, 4, d, sg.DTYPE_BF16, sg.DTYPE_F32, 0.0)
+    oh = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    assert sg.decode_workspace_size(desc, oh) // per_wg == 2 + 0 + 4 + 1
+
+
 @pytest.mark.skipif(_gpu(), reason="checks the no-device path")
 def test_no_device_fails_after_validation():
     assert _compress(_desc(), [512, 512]) == sg.ERR_HIP

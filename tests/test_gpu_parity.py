@@ -466,15 +466,19 @@ def test_decode_edge_segments_and_bf16_output():
     assert np.all(np.abs(ob - ref) <= 2e-2 + ulp)
 
 
-@pytest.mark.parametrize("B,n_new", [(64, 0), (66, 0), (66, 37)], ids=["512-seg-compact", "528-seg-grid", "528-seg-grid-append"])
-def test_decode_many_segments(B, n_new):
+@pytest.mark.parametrize("B,n_new,maxlen", [(64, 0, 400), (64, 0, 3000), (64, 21, 3000), (66, 0, 400), (66, 37, 400)],
+                         ids=["512-seg-compact", "512-seg-whole-rounds", "512-seg-whole-rounds-append", "528-seg-grid",
+                              "528-seg-grid-append"])
+def test_decode_many_segments(B, n_new, maxlen):
     """Decode launches only the workgroups with work (a per-segment table in the kernel arguments)
     for up to 512 (sequence, KV head) segments, and an (x, segment) grid beyond that; both against
     the oracle, with empty, single-row and multi-split segments, and rows appended after
-    compression on the grid path."""
-    rng = np.random.Generator(np.random.PCG64(B + n_new))
+    compression. With segments up to 3000 rows the compact grid holds more than one round of
+    workgroups, which are then shared out over the segments by their lengths (tiny segments
+    keep one)."""
+    rng = np.random.Generator(np.random.PCG64(B + n_new + maxlen))
     d, Hq, Hkv = 64, 16, 8
-    lens = rng.integers(0, 400, size=B * Hkv)
+    lens = rng.integers(0, maxlen, size=B * Hkv)
     lens[::7] = 0
     lens[3::11] = 1
     lens[5] = 3000  # several workgroups of splits
