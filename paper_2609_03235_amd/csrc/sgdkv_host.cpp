@@ -790,12 +790,16 @@ sgdkv_status plan_decode(const sgdkv_decode_desc* d, const int64_t* offsets_host
       std::max<int64_t>(round_up(ceil_div(total - offsets_host[0], kDecodeSplits), 64), kDecodeMinChunk), 1 << 24);
   // a batch whose minimum-size splits would launch fewer workgroups than the device has compute
   // units gets splits half as long (64 rows measured best at 32K x B 1: shorter ones add more
-  // partials to combine than they save)
+  // partials to combine than they save); one that would launch more than two rounds of them gets
+  // splits twice as long (fewer workgroups, each with less of its fixed cost per row, and fewer
+  // partials to combine: decode per 128K x B 8 layer -3.7 %; the 256K x B 16 and 1M x B 32 caches
+  // already have splits of 512 rows and more)
   const int wpw = sgdkv::kDecodeWaves;  // splits (waves) per decode workgroup
   if (a.chunk == kDecodeMinChunk) {
     int64_t wgs = 0;
     for (int64_t i = 0; i < nseg; ++i) wgs += ceil_div(ceil_div(offsets_host[i + 1] - offsets_host[i], a.chunk), wpw);
     if (wgs < sgdkv::kScoreWorkgroups) a.chunk = kDecodeMinChunk / 2;
+    else if (wgs > 2 * kDecodeResident) a.chunk = kDecodeMinChunk * 2;
   }
   a.n_chunk_max = (int)ceil_div(longest, a.chunk);
   if ((int64_t)a.B * a.Hkv * capacity * rb > 0xFFFFFFFFll)

@@ -124,7 +124,8 @@ struct DecodeArgs {
   // slots are contiguous (its compressed rows' workgroups, then its appended rows').
   float* part;        // [n_slots][G][D]: o per slot and query head (16-byte aligned rows)
   float* part_ms;     // [n_slots][G][2]: (m, s) per slot and query head
-  int64_t chunk;      // rows per split (multiple of 64, at least 128, or 64 for a batch too small to fill the chip);
+  int64_t chunk;      // rows per split (multiple of 64: at least 128, 256 for batches past two rounds of
+                      // 128-row workgroups, or 64 for a batch too small to fill the chip);
                       // on the compact grid it only sizes the workgroups and the appended rows' splits
   int n_chunk_max;    // max over segments of ceil(len / chunk): splits of the compressed rows
   int n_cwg;          // ceil(n_chunk_max / waves per workgroup): workgroups (slots) of the compressed rows; on the
