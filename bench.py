@@ -97,8 +97,8 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="qwen25_128k",
                     help="qwen25_128k (default), qwen25_32k, qwen3_256k, qwen25_1m, tiny")
     ap.add_argument("--ratio", type=float, default=0.25, help="budget as a fraction of all rows")

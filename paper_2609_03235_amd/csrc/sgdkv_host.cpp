@@ -15,6 +15,7 @@
 #include <cstring>
 #include <functional>
 #include <mutex>
+#include <queue>
 #include <string>
 #include <vector>
 
@@ -728,11 +729,16 @@ std::vector<int64_t> compact_workgroups(const int64_t* offsets_host, int64_t nse
   std::sort(rem.begin(), rem.end(), std::greater<>());
   for (int64_t j = 0; j < target - given; ++j) n[(size_t)-rem[(size_t)j].second] += 1;
   // a non-empty segment whose share rounded to none gets one, taken from the largest segment
+  // (ties: the lower one)
+  std::priority_queue<std::pair<int64_t, int64_t>> big;  // (workgroups, -segment)
+  for (int64_t i = 0; i < nseg; ++i) big.emplace(n[i], -i);
   for (int64_t i = 0; i < nseg; ++i) {
     if (n[i] != 0 || offsets_host[i + 1] == offsets_host[i]) continue;
     n[i] = 1;
-    const int64_t big = std::max_element(n.begin(), n.end()) - n.begin();
-    if (n[big] > 1) n[big] -= 1;
+    const int64_t b = -big.top().second;
+    big.pop();
+    if (n[b] > 1) n[b] -= 1;
+    big.emplace(n[b], -b);
   }
   return n;
 }
