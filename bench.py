@@ -450,46 +450,69 @@ def main():
                                            full_fraction=args.full_fraction)
 
     budgets = allocate().reshape(L, Hkv)
-    layers = [workloads.torch_layer_tensors(wl, l, dev) for l in range(L)]
-    lse_in = [None] * L
-    if args.caller_lse:
-        # Stand-in for the LSE prefill attention already produced: fp32 logits of each window
-        # row over its causal keys, one (sequence, KV head) block at a time, outside the timed region.
-        G = Hq // Hkv
-        scale = 1.0 / math.sqrt(d)
-        pos = torch.arange(win0, win0 + w, device=dev)[:, None]
-        for l in range(L):
-            out = torch.empty((B, Hq, w), dtype=torch.float32, device=dev)
-            for b in range(B):
-                for h in range(Hkv):
-                    qg = layers[l]["q_win"][b, h * G:(h + 1) * G].float().reshape(G * w, d)
-                    kt = layers[l]["k"][b, h].float().t().contiguous()
-                    lg = (qg @ kt) * scale
-                    lg = lg.reshape(G, w, C).masked_fill(torch.arange(C, device=dev)[None, :] > pos, float("-inf"))
-                    out[b, h * G:(h + 1) * G] = torch.logsumexp(lg, dim=-1)
-                    del lg, kt
-            lse_in[l] = out
-    outs = []
-    for l in range(L):
-        T = int(budgets[l].sum())
-        outs.append(dict(k_c=torch.empty((B * T, d), dtype=layers[l]["k"].dtype, device=dev),
-                         v_c=torch.empty((B * T, d), dtype=layers[l]["k"].dtype, device=dev),
-                         kept_pos=torch.empty(B * T, dtype=torch.int32, device=dev),
-                         offsets=torch.empty(B * Hkv + 1, dtype=torch.int64, device=dev),
-                         scores=torch.empty((B, Hkv, n_scored), dtype=torch.float32, device=dev)))
-    dec_out = [torch.empty((B, Hq, d), dtype=torch.float32, device=dev) for _ in range(L)]
     n_new = args.decode_new
-    tails = [None] * L
-    if n_new > 0:
-        # rows appended since compression (one generated token per row), drawn like the cache
-        gen = torch.Generator(device=dev)
-        gen.manual_seed(wl.seed + 300)
+
+    def make_set(r):
+        """One copy of every layer's inputs and outputs (copy r draws its inputs as layers L*r ..)."""
+        layers = [workloads.torch_layer_tensors(wl, l + L * r, dev) for l in range(L)]
+        lse_in = [None] * L
+        if args.caller_lse:
+            # Stand-in for the LSE prefill attention already produced: fp32 logits of each window
+            # row over its causal keys, one (sequence, KV head) block at a time, outside the timed region.
+            G = Hq // Hkv
+            scale = 1.0 / math.sqrt(d)
+            pos = torch.arange(win0, win0 + w, device=dev)[:, None]
+            for l in range(L):
+                out = torch.empty((B, Hq, w), dtype=torch.float32, device=dev)
+                for b in range(B):
+                    for h in range(Hkv):
+                        qg = layers[l]["q_win"][b, h * G:(h + 1) * G].float().reshape(G * w, d)
+                        kt = layers[l]["k"][b, h].float().t().contiguous()
+                        lg = (qg @ kt) * scale
+                        lg = lg.reshape(G, w, C).masked_fill(torch.arange(C, device=dev)[None, :] > pos,
+                                                             float("-inf"))
+                        out[b, h * G:(h + 1) * G] = torch.logsumexp(lg, dim=-1)
+                        del lg, kt
+                lse_in[l] = out
+        outs = []
         for l in range(L):
-            kn = torch.randn((B, Hkv, n_new, d), generator=gen, device=dev).to(layers[l]["k"].dtype)
-            vn = torch.randn((B, Hkv, n_new, d), generator=gen, device=dev).to(layers[l]["k"].dtype)
-            step_kv = torch.randn((2, B, Hkv, d), generator=gen, device=dev).to(layers[l]["k"].dtype)
-            tails[l] = (kn, vn, step_kv)
-    dec_lse = [torch.empty((B, Hq), dtype=torch.float32, device=dev) for _ in range(L)]
+            T = int(budgets[l].sum())
+            outs.append(dict(k_c=torch.empty((B * T, d), dtype=layers[l]["k"].dtype, device=dev),
+                             v_c=torch.empty((B * T, d), dtype=layers[l]["k"].dtype, device=dev),
+                             kept_pos=torch.empty(B * T, dtype=torch.int32, device=dev),
+                             offsets=torch.empty(B * Hkv + 1, dtype=torch.int64, device=dev),
+                             scores=torch.empty((B, Hkv, n_scored), dtype=torch.float32, device=dev)))
+        tails = [None] * L
+        if n_new > 0:
+            # rows appended since compression (one generated token per row), drawn like the cache
+            gen = torch.Generator(device=dev)
+            gen.manual_seed(wl.seed + 300 + r)
+            for l in range(L):
+                kn = torch.randn((B, Hkv, n_new, d), generator=gen, device=dev).to(layers[l]["k"].dtype)
+                vn = torch.randn((B, Hkv, n_new, d), generator=gen, device=dev).to(layers[l]["k"].dtype)
+                step_kv = torch.randn((2, B, Hkv, d), generator=gen, device=dev).to(layers[l]["k"].dtype)
+                tails[l] = (kn, vn, step_kv)
+        return dict(layers=layers, lse_in=lse_in, outs=outs, tails=tails,
+                    dec_out=[torch.empty((B, Hq, d), dtype=torch.float32, device=dev) for _ in range(L)],
+                    dec_lse=[torch.empty((B, Hq), dtype=torch.float32, device=dev) for _ in range(L)])
+
+    # A step whose inputs and outputs fit the last-level caches would time cached reads: below
+    # 1 GiB per step, the steps rotate over enough distinct copies to make 1 GiB.
+    def tensor_bytes(x):
+        if isinstance(x, torch.Tensor):
+            return x.numel() * x.element_size()
+        if isinstance(x, dict):
+            return sum(tensor_bytes(v) for v in x.values())
+        if isinstance(x, (list, tuple)):
+            return sum(tensor_bytes(v) for v in x)
+        return 0
+
+    sets = [make_set(0)]
+    step_bytes = tensor_bytes(sets[0])
+    n_copies = max(1, -(-(1 << 30) // max(step_bytes, 1)))
+    sets += [make_set(r) for r in range(1, n_copies)]
+    layers, tails = sets[0]["layers"], sets[0]["tails"]
+    step_count = [0]
     cdesc = sg.compress_desc(layers[0]["q_win"], layers[0]["k"], pool_kernel=kp, b_sink=s, b_window=W)
     # the gathers' stream keeps torch's default priority; the gather does not use the workspace
     gstream = None if args.no_gather_stream else torch.cuda.Stream(device=dev)
@@ -504,6 +527,10 @@ def main():
     def step(gs=gstream, dec_ev=None):
         # S0 on the host, then every layer's compression, then every layer's decode; dec_ev (a pair
         # of events) brackets the decode phase on the launch stream
+        cur = sets[step_count[0] % n_copies]
+        step_count[0] += 1
+        layers, lse_in, outs, tails = cur["layers"], cur["lse_in"], cur["outs"], cur["tails"]
+        dec_out, dec_lse = cur["dec_out"], cur["dec_lse"]
         allocate()
         for l in range(L):
             t = layers[l]
@@ -719,7 +746,8 @@ def main():
                     obs_window=w, pool_kernel=kp, b_sink=s, b_window=W, budget_ratio=args.ratio,
                     total_budget_rows=int(budgets.sum()), window_lse="caller" if args.caller_lse else "computed",
                     alloc_variant=args.alloc_variant, group_agg=args.group_agg, window_start=win0,
-                    decode_appended_rows=n_new, gather_stream=not args.no_gather_stream),
+                    decode_appended_rows=n_new, gather_stream=not args.no_gather_stream,
+                    input_copies=n_copies),
         step_ms=dict(median=round(statistics.median(step_ms), 4), p10=round(percentile(step_ms, 0.1), 4),
                      p90=round(percentile(step_ms, 0.9), 4), mean=round(ms_per_step, 4)),
         compress_tokens_per_s=round(tokens / (comp_ms / 1e3), 1) if comp_ms > 0 else None,
