@@ -922,6 +922,7 @@ FULL_CASES = [
     ("qwen25_128k", 0.50, "capped", "plain", (1,)),
     ("qwen25_128k", 0.25, 0, "ipt_max", (4,)),
     ("qwen25_128k", 0.25, 0, "unaware", (1,)),
+    ("qwen25_128k", 0.25, 0, "proxy", (2,)),
     ("qwen25_128k", 0.25, 0, "append64", (0,)),
     ("qwen25_128k", 0.25, 0, "w128", (7,)),
     ("qwen3_256k", 0.25, 0, "plain", (0, 15)),
@@ -947,7 +948,7 @@ def test_full_size(key, ratio, layer, variant, oracle_seqs):
         sc = sg.reduce_query_head_scores(qall, Hkv).reshape(-1)
         assert np.array_equal(sc, oracle.reduce_group_max(qall, Hkv).reshape(-1))
         agg, qs = sg.GROUP_IPT_MAX, qall[layer]
-    win0 = C - 256 - w if variant == "unaware" else None
+    win0 = C - 256 - w if variant == "unaware" else (C if variant == "proxy" else None)
     total = sg.total_from_ratio(ratio, L, Hkv, C, s, W)
     budgets_all = sg.allocate_budgets(sc, L, Hkv, C, s, W, total)
     assert np.array_equal(budgets_all, oracle.allocate_budgets(sc, L, Hkv, C, s, W, total))
