@@ -410,9 +410,14 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(CompressArgs a) {
 // workgroups take items in a grid-stride loop, so the grid may be smaller
 // than the item count (the library shrinks it when the copy runs beside
 // other work). Every thread keeps several 16-byte loads in flight before
-// storing. RB = bytes per row.
-template <int RB>
+// storing. RB = bytes per row. BESIDE: the copy runs beside the next layer's window scoring,
+// whose second pass re-reads the ends of the first pass's key chunks from the last-level cache;
+// its loads and stores then carry the non-temporal hint, so that they do not push those keys out
+// (the 28-layer 128K x B 8 step 1 % faster, the score passes and the copy itself faster beside
+// each other; alone, the copy was slower with it).
+template <int RB, bool BESIDE>
 __global__ __launch_bounds__(kBlock) void copy_rows_kernel(CompressArgs a) {
+  constexpr int NT = BESIDE ? 2 : 0;  // buffer cache policy: the non-temporal bit
   constexpr int V16 = RB / 16;                        // 16-byte pieces per row
   constexpr int PER = kCopyRows * V16 / kBlock;       // pieces per thread per tensor
   static_assert(PER >= 1 && (kCopyRows * V16) % kBlock == 0, "copy tile must split evenly");
@@ -438,13 +443,13 @@ __global__ __launch_bounds__(kBlock) void copy_rows_kernel(CompressArgs a) {
       const uint32_t pos = ld32(kp, (uint32_t)(row * 4));
       const uint32_t src = pos * RB + c16 * 16;
       dst[u] = (uint32_t)(row * RB + c16 * 16);
-      kx[u] = ld128(ki, src);
-      vx[u] = ld128(vi, src);
+      kx[u] = __builtin_amdgcn_raw_buffer_load_b128(ki, (int)src, 0, NT);
+      vx[u] = __builtin_amdgcn_raw_buffer_load_b128(vi, (int)src, 0, NT);
     }
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
-      st128(ko, dst[u], kx[u]);
-      st128(vo, dst[u], vx[u]);
+      __builtin_amdgcn_raw_buffer_store_b128(kx[u], ko, (int)dst[u], 0, NT);
+      __builtin_amdgcn_raw_buffer_store_b128(vx[u], vo, (int)dst[u], 0, NT);
     }
   }
 }
@@ -492,10 +497,20 @@ hipError_t launch_gather(const CompressArgs& a, int max_blocks, hipStream_t st) 
   // a full grid is capped too (the loop covers the rest), keeping blocks x threads below 2^32
   const unsigned grid = (unsigned)std::min<int64_t>(items, max_blocks > 0 ? max_blocks : (1 << 20));
   const dim3 blk(kBlock);
+  const bool beside = max_blocks > 0;
   switch (a.D * (a.dtype == 1 ? 2 : 4)) {
-    case 128: SGDKV_LAUNCH("gather", copy_rows_kernel<128>, dim3(grid), blk, st, a); break;
-    case 256: SGDKV_LAUNCH("gather", copy_rows_kernel<256>, dim3(grid), blk, st, a); break;
-    case 512: SGDKV_LAUNCH("gather", copy_rows_kernel<512>, dim3(grid), blk, st, a); break;
+    case 128:
+      if (beside) SGDKV_LAUNCH("gather", (copy_rows_kernel<128, true>), dim3(grid), blk, st, a);
+      else SGDKV_LAUNCH("gather", (copy_rows_kernel<128, false>), dim3(grid), blk, st, a);
+      break;
+    case 256:
+      if (beside) SGDKV_LAUNCH("gather", (copy_rows_kernel<256, true>), dim3(grid), blk, st, a);
+      else SGDKV_LAUNCH("gather", (copy_rows_kernel<256, false>), dim3(grid), blk, st, a);
+      break;
+    case 512:
+      if (beside) SGDKV_LAUNCH("gather", (copy_rows_kernel<512, true>), dim3(grid), blk, st, a);
+      else SGDKV_LAUNCH("gather", (copy_rows_kernel<512, false>), dim3(grid), blk, st, a);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
