@@ -86,7 +86,9 @@ __device__ __forceinline__ void clamp_segment(const DecodeArgs& a, int seg, int6
 }  // namespace
 
 // Loads of one 16-key step: the K fragments of the MFMA (key lr, k = 32c + 8*lg)
-// and this lane's V rows (keys kg + KG*u, columns col0 .. col0+CPL-1).
+// and this lane's V rows (keys kg + KG*u, columns col0 .. col0+CPL-1). A decode reads each cached
+// row once, so the loads carry the non-temporal hint: at 128K x B 8, 256K x B 16 and 1M x B 32
+// the split kernel streams 5-6 % faster with it.
 template <typename T, int D, int CPL>
 struct DecodeStep {
   static constexpr int EB = sizeof(T);
@@ -102,18 +104,18 @@ struct DecodeStep {
   __device__ __forceinline__ void load(const rsrc_t& kr, const rsrc_t& vr, int64_t k0, int lr, int lgp, int kg,
                                        int col0) {
 #pragma unroll
-    for (int c = 0; c < NC; ++c) kb[c] = gload_frag<T>(kr, (uint32_t)((k0 + lr) * RB + (32 * c + 8 * lgp) * EB));
+    for (int c = 0; c < NC; ++c) kb[c] = gload_frag_nt<T>(kr, (uint32_t)((k0 + lr) * RB + (32 * c + 8 * lgp) * EB));
 #pragma unroll
     for (int u = 0; u < VPL; ++u) {
       const uint32_t off = (uint32_t)((k0 + kg + KG * u) * RB + col0 * EB);
       if constexpr (NW == 2) {
-        const uint64_t x = ld64(vr, off);
+        const uint64_t x = ld64_nt(vr, off);
         vv[u][0] = (uint32_t)x;
         vv[u][1] = (uint32_t)(x >> 32);
       } else {
 #pragma unroll
         for (int x = 0; x < NW / 4; ++x) {
-          const u32x4 y = ld128(vr, off + 16 * x);
+          const u32x4 y = ld128_nt(vr, off + 16 * x);
           vv[u][4 * x] = y.x;
           vv[u][4 * x + 1] = y.y;
           vv[u][4 * x + 2] = y.z;

@@ -59,6 +59,20 @@ __device__ __forceinline__ uint64_t ld64(rsrc_t r, uint32_t byte_off) {
   return (uint64_t)w.x | ((uint64_t)w.y << 32);
 }
 
+// Non-temporal accesses (the cache-policy nt bit): for data streamed once, so that it does not
+// displace what the caches hold for others.
+constexpr int kNonTemporal = 2;
+__device__ __forceinline__ u32x4 ld128_nt(rsrc_t r, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, kNonTemporal);
+}
+__device__ __forceinline__ uint64_t ld64_nt(rsrc_t r, uint32_t byte_off) {
+  u32x2 w = __builtin_amdgcn_raw_buffer_load_b64(r, (int)byte_off, 0, kNonTemporal);
+  return (uint64_t)w.x | ((uint64_t)w.y << 32);
+}
+__device__ __forceinline__ void st128_nt(rsrc_t r, uint32_t byte_off, u32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)byte_off, 0, kNonTemporal);
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 

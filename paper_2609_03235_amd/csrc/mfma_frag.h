@@ -43,6 +43,22 @@ __device__ __forceinline__ Frag<float> gload_frag<float>(rsrc_t r, uint32_t off)
   f.v1 = ld128(r, off + 16);
   return f;
 }
+// The same with the non-temporal hint (keys streamed once).
+template <typename T>
+__device__ __forceinline__ Frag<T> gload_frag_nt(rsrc_t r, uint32_t off);
+template <>
+__device__ __forceinline__ Frag<__bf16> gload_frag_nt<__bf16>(rsrc_t r, uint32_t off) {
+  Frag<__bf16> f;
+  f.v = ld128_nt(r, off);
+  return f;
+}
+template <>
+__device__ __forceinline__ Frag<float> gload_frag_nt<float>(rsrc_t r, uint32_t off) {
+  Frag<float> f;
+  f.v0 = ld128_nt(r, off);
+  f.v1 = ld128_nt(r, off + 16);
+  return f;
+}
 
 template <typename T>
 __device__ __forceinline__ Frag<T> lds_frag(const char* base, uint32_t off);

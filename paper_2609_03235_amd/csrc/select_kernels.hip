@@ -417,7 +417,7 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(CompressArgs a) {
 // each other; alone, the copy was slower with it).
 template <int RB, bool BESIDE>
 __global__ __launch_bounds__(kBlock) void copy_rows_kernel(CompressArgs a) {
-  constexpr int NT = BESIDE ? 2 : 0;  // buffer cache policy: the non-temporal bit
+  constexpr int NT = BESIDE ? kNonTemporal : 0;  // buffer cache policy
   constexpr int V16 = RB / 16;                        // 16-byte pieces per row
   constexpr int PER = kCopyRows * V16 / kBlock;       // pieces per thread per tensor
   static_assert(PER >= 1 && (kCopyRows * V16) % kBlock == 0, "copy tile must split evenly");
