@@ -282,8 +282,9 @@ typedef struct sgdkv_decode_desc {
  * lengths (offsets_host: host [B*Hkv+1] int64, non-decreasing from 0): the
  * split partials, G*(d+2) floats per decode workgroup. With up to 512
  * segments (B*Hkv) these are the segments' own workgroups, about one per
- * 4 splits of about 16384 over the batch, however unequal the segments; with
- * more segments every segment holds as many as the longest one needs. */
+ * 4 splits of about 12288 over the batch (past 512 workgroups, rounded to a
+ * multiple of 512), however unequal the segments; with more segments every
+ * segment holds as many as the longest one needs. */
 sgdkv_status sgdkv_decode_workspace_size(const sgdkv_decode_desc* desc, const int64_t* offsets_host,
                                          size_t* bytes);
 

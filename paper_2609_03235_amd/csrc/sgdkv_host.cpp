@@ -684,7 +684,7 @@ sgdkv_status sgdkv_compress_layer_ex(const sgdkv_compress_desc* desc, const sgdk
 namespace {
 
 #ifndef SGDKV_DECODE_SPLITS
-#define SGDKV_DECODE_SPLITS 16384
+#define SGDKV_DECODE_SPLITS 12288
 #endif
 #ifndef SGDKV_DECODE_MIN_CHUNK
 #define SGDKV_DECODE_MIN_CHUNK 128
