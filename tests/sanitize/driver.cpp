@@ -189,6 +189,30 @@ void device_validation() {
   expect(sgdkv_append_kv(&dd, F, F, F, F, 10, 10, nullptr) == SGDKV_ERR_INVALID_ARG, "slot == capacity");
 }
 
+// Decode planning over ragged segment sets: empty, one-row and long segments, past one round of
+// decode workgroups (their share-out over the segments) and within it, with appended regions.
+void decode_plans(int rounds) {
+  for (int r = 0; r < rounds; ++r) {
+    const int Hkv = (int)randint(1, 8), B = (int)randint(1, 512 / Hkv), G = (int)randint(1, 16);
+    const int64_t nseg = (int64_t)B * Hkv;
+    std::vector<int64_t> oh((size_t)nseg + 1, 0);
+    const int64_t top = randint(0, 3) == 0 ? 3000 : (int64_t)1 << randint(10, 20);
+    for (int64_t i = 0; i < nseg; ++i) {
+      const int kind = (int)randint(0, 9);
+      const int64_t len = kind == 0 ? 0 : kind == 1 ? 1 : kind == 2 ? randint(2, 40) : randint(0, top);
+      oh[(size_t)i + 1] = oh[(size_t)i] + len;
+    }
+    sgdkv_decode_desc dd{B, Hkv * G, Hkv, randint(0, 1) ? 128 : 64, (int)randint(0, 1), 0, 0.f};
+    size_t bytes = 0;
+    const int64_t cap = randint(0, 2) == 0 ? randint(1, 300) : 0;
+    expect(sgdkv_decode_workspace_size_ex(&dd, oh.data(), cap, &bytes) == SGDKV_OK, "decode plan", r);
+    int64_t nonempty = 0;
+    for (int64_t i = 0; i < nseg; ++i) nonempty += oh[(size_t)i + 1] > oh[(size_t)i];
+    const size_t per_wg = (size_t)G * (dd.head_dim + 2) * sizeof(float);
+    expect(bytes >= (size_t)nonempty * per_wg, "a workgroup slot per non-empty segment", r);
+  }
+}
+
 void oracle_compress_decode(int rounds) {
   for (int r = 0; r < rounds; ++r) {
     const int B = (int)randint(1, 2), Hkv = (int)randint(1, 3), G = (int)randint(1, 3), Hq = Hkv * G;
@@ -250,6 +274,7 @@ int main() {
   allocation_against_oracle(400);
   offsets_cases(100);
   device_validation();
+  decode_plans(300);
   oracle_compress_decode(40);
   if (g_failures) {
     std::fprintf(stderr, "%d failures\n", g_failures);
