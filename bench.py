@@ -46,10 +46,12 @@ PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 # A second, composed figure for the score passes, reported beside the MFMA roofline as
 # issue_peak / issue_frac: the chip-wide issue time of one logit when its MFMA share (2*d flops
-# at the MFMA peak), its exp2 (a quarter of the plain fp32 vector rate, 256 CUs x 4 SIMDs x 32
-# lanes at 2.4 GHz) and its two plain vector ops (fma, add) are counted one after the other.
-VALU_OPS = 256 * 4 * 32 * 2.4e9
-EXP2_OPS = VALU_OPS / 4
+# at the MFMA peak), its exp2 and its two plain vector ops (fma, add) are counted one after the
+# other, at the vector-port costs the issue counters give on gfx950: 4 cycles for a 64-lane plain
+# fp32 op (16 lanes per cycle) and 8 for a 64-lane exp2 (8 lanes per cycle), on 256 CUs x 4 SIMDs
+# at 2.4 GHz. At d = 128 that is 16 + 16 cycles per 16x16x32 bf16 MFMA: half the MFMA peak.
+VALU_OPS = 256 * 4 * 16 * 2.4e9
+EXP2_OPS = 256 * 4 * 8 * 2.4e9
 
 
 def score_logit_seconds(d, dtype):

@@ -22,12 +22,14 @@ def test_more_than_one_gpu_is_refused():
 
 
 def test_score_issue_peak():
-    # MFMA 2d flops at 2.5 PFLOP/s, one exp2 at a quarter of the fp32 lane rate, fma + add at
-    # the full rate (256 CUs x 4 SIMDs x 32 lanes x 2.4 GHz): 1.79e-13 s per logit at d = 128
+    # MFMA 2d flops at 2.5 PFLOP/s, then one exp2 (8 lanes per SIMD cycle) and fma + add (16 lanes
+    # per SIMD cycle each) on 256 CUs x 4 SIMDs at 2.4 GHz: 2.04e-13 s per logit at d = 128, so
+    # the vector work of a 16x16x32 MFMA's 64 logits (16 cycles) equals the MFMA's own 16 cycles
     t = bench.score_logit_seconds(128, "bf16")
-    lanes = 256 * 4 * 32 * 2.4e9
-    assert t == pytest.approx(256 / 2.5e15 + 4 / lanes + 2 / lanes, rel=1e-12)
-    assert 2 * 128 / t / 1e12 == pytest.approx(1432.6, abs=0.1)
+    simd_hz = 256 * 4 * 2.4e9
+    assert t == pytest.approx(256 / 2.5e15 + 1 / (8 * simd_hz) + 2 / (16 * simd_hz), rel=1e-12)
+    assert 2 * 128 / t / 1e12 == pytest.approx(1254.1, abs=0.1)
+    assert 2.5e15 / (2 * 128 / t) == pytest.approx(2.0, rel=0.01)
 
 
 def test_compression_roof_of_the_128k_layer():
