@@ -90,23 +90,28 @@ struct KeyStage {
 
 // Row block of slot j of wave wid: blocks wid, wid+8, ... (interleaved), or, with HW (head
 // waves), blocks wid*RBW .. wid*RBW+RBW-1, so that the rows of a wave belong to one query head
-// when w is a multiple of 16*RBW.
+// when w is a multiple of 16*RBW. Balanced head waves (bal: seven heads of one wave each, the
+// group size of a 28/4-head model): the last wave, which would hold no rows, takes the last
+// block of the heads of waves 4-6 (slots 0-2), so that each SIMD (waves s and s+4) carries
+// 2*RBW - 1 blocks instead of 2*RBW on three SIMDs and RBW on the fourth.
+constexpr int kBalFirstWave = kScoreWaves / 2;  // heads of waves 4-6 lend their last block
 template <int RBW, bool HW>
-__device__ __forceinline__ int row_block(int wid, int j) {
+__device__ __forceinline__ int row_block(int wid, int j, bool bal = false) {
+  if (HW && bal && wid == kScoreWaves - 1) return (kBalFirstWave + j) * RBW + RBW - 1;
   return HW ? wid * RBW + j : wid + kScoreWaves * j;
 }
 
 // Window rows [r0, r0 + nrows) of KV head h (one row split) as A fragments.
 template <typename T, int D, int RBW, bool HW = false>
 __device__ __forceinline__ void load_group_queries(const CompressArgs& a, int b, int h, int r0, int nrows, int wid,
-                                                   int lane, Frag<T> (&qa)[RBW][D / 32]) {
+                                                   int lane, Frag<T> (&qa)[RBW][D / 32], bool bal = false) {
   using G = TileGeom<T, D>;
   const T* qbase = static_cast<const T*>(a.q_win) + ((int64_t)(b * a.Hq + h * a.G) * a.w + r0) * D;
   const rsrc_t qr = make_rsrc(qbase, (uint64_t)nrows * G::RB);
   const int lr = lane & 15, lg = lane >> 4;
 #pragma unroll
   for (int j = 0; j < RBW; ++j) {
-    const int row = row_block<RBW, HW>(wid, j) * 16 + lr;  // rows >= nrows read as zeros
+    const int row = row_block<RBW, HW>(wid, j, bal) * 16 + lr;  // rows >= nrows read as zeros
 #pragma unroll
     for (int c = 0; c < G::NC; ++c)
       qa[j][c] = gload_frag<T>(qr, (uint32_t)(row * G::RB + (32 * c + 8 * lg) * G::EB));
@@ -434,25 +439,33 @@ template <bool MAXG, bool HW>
 constexpr bool block_partials() {
   return MAXG && !HW;
 }
+// Balanced head waves: the last wave keeps four lane-group partials for each of its three blocks,
+// 12 rows instead of 4.
+template <bool MAXG, bool HW, int RBW>
+constexpr int bal_extra_rows() {
+  return MAXG && HW && RBW == 4 ? 8 : 0;
+}
 
 // LDS layout of pass 2's column partials: three tiles in flight, each with RW partial rows of
 // TILE columns per wave. A partial row is 16 banks further than the one before it and a wave's
 // rows 16 banks further again, so that neither the four lane groups of a wave storing a subtile
 // nor the four waves whose partials the reduction reads together meet in one bank.
-template <typename T, int RW>
+template <typename T, int RW, int EXTRA = 0>
 struct ColPartials {
   static constexpr int TILE = col_tile<T>();
   static constexpr int SL = TILE + 16;         // floats per partial row
   static constexpr int SW = RW * SL + 16;      // floats per wave
-  static constexpr int ST = kScoreWaves * SW;  // floats per tile
+  static constexpr int ST = kScoreWaves * SW + EXTRA * SL;  // floats per tile (EXTRA more rows for the last wave)
   static constexpr int WORDS = 3 * ST;
   __device__ static constexpr int at(int t3, int wave, int r, int col) { return t3 * ST + wave * SW + r * SL + col; }
 };
 
-template <typename T, int D, int NB, int RBW, bool MAXG, bool HW>
+// MIXED: the wave's blocks belong to different heads (the last wave of the balanced head-wave
+// layout): it leaves four lane-group partials per block, in rows 4j .. 4j+3 of its region.
+template <typename T, int D, int NB, int RBW, bool MAXG, bool HW, bool MIXED = false>
 __device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float* red, int seg, int r0, int nrows, int wid, int lane,
                              const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], const rsrc_t& kr, int64_t key0,
-                             int64_t key_end) {
+                             int64_t key_end, bool bal = false) {
   constexpr int NBX = NB > 0 ? NB : 1;
   constexpr int TILE = col_tile<T>();
   const int lr = lane & 15, lg = lane >> 4;
@@ -467,7 +480,7 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float* red, int 
   for (int j = 0; j < NBX; ++j)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int row = row_block<RBW, HW>(wid, j) * 16 + 4 * lg + i;  // within the split
+      const int row = row_block<RBW, HW>(wid, j, bal) * 16 + 4 * lg + i;  // within the split
       float l = ldf(lr2, (uint32_t)(((int64_t)seg * a.R + r0 + row) * 4));
       if (natural) l *= 1.44269504088896340736f;
       const float lw = weighted && row < nrows ? a.qweight[h * a.G + (r0 + row) / a.w] : 0.f;
@@ -490,19 +503,23 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float* red, int 
   static_assert(CPW <= 16 && 64 % CPW == 0 && PPL >= 1 && PPL * LPC == kScoreWaves, "reduction layout");
   const int rcol = CPW * wid + lane % CPW, rgrp = lane / CPW;
   constexpr bool BP = block_partials<MAXG, HW>();
-  using CP = ColPartials<T, BP ? RBW : 4>;
+  using CP = ColPartials<T, BP ? RBW : 4, bal_extra_rows<MAXG, HW, RBW>()>;
   auto reduce = [&](int64_t t) {  // t may be -1: nothing is stored
     const float* r = red + CP::at((int)((uint32_t)(t + 3) % 3u), 0, 0, 0);
     float v = 0.f;
     if constexpr (MAXG && HW) {
       // the LPC lanes of a column take the split's heads in turn: add the four lane-group
       // partials of each of a head's w/(16*RBW) waves in wave order, weight, keep the maximum
+      // (balanced layout: heads 4-6 then add the block partial they lent to the last wave)
       const int wph = a.w / (16 * RBW), g0 = r0 / a.w, ng = nrows / a.w;
       for (int g = rgrp; g < ng; g += LPC) {
         float sum = 0.f;
         for (int wv = g * wph; wv < (g + 1) * wph; ++wv)
 #pragma unroll
           for (int q = 0; q < 4; ++q) sum += r[wv * CP::SW + q * CP::SL + rcol];
+        if (bal && g >= kBalFirstWave)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) sum += r[(kScoreWaves - 1) * CP::SW + (4 * (g - kBalFirstWave) + q) * CP::SL + rcol];
         v = fmaxf(v, a.qweight[h * a.G + g0 + g] * sum);
       }
 #pragma unroll
@@ -547,6 +564,14 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float* red, int 
                             (fast_exp2(fmaf(acc[j][2], c2, nlse[j][2])) + fast_exp2(fmaf(acc[j][3], c2, nlse[j][3])));
             red[CP::at(t3, wid, j, 16 * sub + lr)] = sum_lane_groups(p);
           }
+        } else if constexpr (MIXED) {
+          // four lane-group partials per block (each block a different head's rows)
+#pragma unroll
+          for (int j = 0; j < NB; ++j) {
+            const float p = (fast_exp2(fmaf(acc[j][0], c2, nlse[j][0])) + fast_exp2(fmaf(acc[j][1], c2, nlse[j][1]))) +
+                            (fast_exp2(fmaf(acc[j][2], c2, nlse[j][2])) + fast_exp2(fmaf(acc[j][3], c2, nlse[j][3])));
+            red[CP::at(t3, wid, 4 * j + lg, 16 * sub + lr)] = p;
+          }
         } else {
           float p = 0.f;
           if constexpr (NB > 0) {
@@ -572,7 +597,8 @@ template <typename T, int D, int RBW, bool MAXG, bool HW>
 __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) {
   using G = TileGeom<T, D>;
   __shared__ __attribute__((aligned(16))) char ktile[2 * col_tile<T>() * G::LDS_STRIDE];
-  __shared__ __attribute__((aligned(16))) float red[ColPartials<T, block_partials<MAXG, HW>() ? RBW : 4>::WORDS];
+  __shared__ __attribute__((aligned(16)))
+  float red[ColPartials<T, block_partials<MAXG, HW>() ? RBW : 4, bal_extra_rows<MAXG, HW, RBW>()>::WORDS];
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
   if (blockIdx.x == 0 && blockIdx.z == 0) init_segment(a, seg);  // histograms, offsets for the selection
@@ -583,19 +609,39 @@ __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) 
   const int r0 = (int)blockIdx.z * a.rs_rows;
   const int nrows = a.R - r0 < a.rs_rows ? a.R - r0 : a.rs_rows;
   const rsrc_t kr = make_rsrc(static_cast<const T*>(a.k) + (int64_t)seg * a.C * D, (uint64_t)a.C * G::RB);
+  // balanced head waves: a split of seven heads of one wave each, four blocks per head (with
+  // three blocks per head the busiest SIMD would carry six blocks either way)
+  constexpr bool can_bal = MAXG && HW && RBW == 4;
+  const bool bal = can_bal && nrows == 7 * a.w && a.w == 16 * RBW;
   Frag<T> qa[RBW][G::NC];
-  load_group_queries<T, D, RBW, HW>(a, b, h, r0, nrows, wid, lane, qa);
+  load_group_queries<T, D, RBW, HW>(a, b, h, r0, nrows, wid, lane, qa, bal);
   const int nrb = (nrows + 15) / 16;
   if constexpr (HW) {
     // a row split holds whole heads of w/16 blocks, a multiple of RBW: each wave has all
     // RBW of its blocks or none (a wave without rows still stages keys and meets every barrier)
+    if constexpr (can_bal) {
+      if (bal && wid >= kBalFirstWave) {
+        Frag<T> qb[3][G::NC];  // waves 4-6: their first three blocks; wave 7: the three lent blocks
+#pragma unroll
+        for (int j = 0; j < 3; ++j)
+#pragma unroll
+          for (int c = 0; c < G::NC; ++c) qb[j][c] = qa[j][c];
+        if (wid == kScoreWaves - 1)
+          colsum_chunk<T, D, 3, RBW, MAXG, HW, true>(a, ktile, red, seg, r0, nrows, wid, lane, qb, kr, key0, key_end,
+                                                     bal);
+        else
+          colsum_chunk<T, D, 3, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qb, kr, key0, key_end, bal);
+        return;
+      }
+    }
+    // (every wave reduces some columns, so each needs to know the layout: bal goes to all)
     if (row_block<RBW, HW>(wid, 0) < nrb) {
-      colsum_chunk<T, D, RBW, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qa, kr, key0, key_end);
+      colsum_chunk<T, D, RBW, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qa, kr, key0, key_end, bal);
     } else {
       Frag<T> qz[1][G::NC];  // never read: the wave has no row blocks
 #pragma unroll
       for (int c = 0; c < G::NC; ++c) qz[0][c] = qa[0][c];
-      colsum_chunk<T, D, 0, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qz, kr, key0, key_end);
+      colsum_chunk<T, D, 0, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qz, kr, key0, key_end, bal);
     }
   } else if (wid + kScoreWaves * (RBW - 1) < nrb) {
     colsum_chunk<T, D, RBW, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qa, kr, key0, key_end);
