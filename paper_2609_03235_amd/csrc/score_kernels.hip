@@ -510,7 +510,8 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float* red, int 
     if constexpr (MAXG && HW) {
       // the LPC lanes of a column take the split's heads in turn: add the four lane-group
       // partials of each of a head's w/(16*RBW) waves in wave order, weight, keep the maximum
-      // (balanced layout: heads 4-6 then add the block partial they lent to the last wave)
+      // (balanced layout: heads 4-6 then add the four lane-group partials of the block they lent
+      // to the last wave)
       const int wph = a.w / (16 * RBW), g0 = r0 / a.w, ng = nrows / a.w;
       for (int g = rgrp; g < ng; g += LPC) {
         float sum = 0.f;
