@@ -227,8 +227,9 @@ def test_ipt_group_aggregation(agg, B, C, Hq, Hkv, d, w, dtype):
     """Ipt. max / mean / only (Appendix A.7): per-query-head window attention weighted by the
     summarization score, then max or mean over the group, or the top head's alone. The scores
     include a zero, a tie for the top of a group and a spread of magnitudes. In these shapes each
-    score wave of Ipt. max holds the rows of one query head (4, 2, 4, 3 and 1 row blocks per wave),
-    and with groups of 7 one wave holds none."""
+    score wave of Ipt. max holds the rows of one query head (4, 2, 4, 3 and 1 row blocks per wave);
+    with groups of 7 one wave would hold none: with four blocks per head (w = 64, bf16 and fp32) it
+    takes the last block of three heads (the balanced layout), with three or one it stays empty."""
     wl, t = _qwen_small(B, C, Hq=Hq, Hkv=Hkv, d=d, w=w)
     if dtype != torch.bfloat16:
         t = {k: x.float() for k, x in t.items()}
