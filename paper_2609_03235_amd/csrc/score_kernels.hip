@@ -463,7 +463,8 @@ struct ColPartials {
 // MIXED: the wave's blocks belong to different heads (the last wave of the balanced head-wave
 // layout): it leaves four lane-group partials per block, in rows 4j .. 4j+3 of its region.
 template <typename T, int D, int NB, int RBW, bool MAXG, bool HW, bool MIXED = false>
-__device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float* red, int seg, int r0, int nrows, int wid, int lane,
+__device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float* red, float* qws, int seg, int r0, int nrows,
+                             int wid, int lane,
                              const Frag<T> (&qa)[NB > 0 ? NB : 1][D / 32], const rsrc_t& kr, int64_t key0,
                              int64_t key_end, bool bal = false) {
   constexpr int NBX = NB > 0 ? NB : 1;
@@ -504,6 +505,13 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float* red, int 
   const int rcol = CPW * wid + lane % CPW, rgrp = lane / CPW;
   constexpr bool BP = block_partials<MAXG, HW>();
   using CP = ColPartials<T, BP ? RBW : 4, bal_extra_rows<MAXG, HW, RBW>()>;
+  // Ipt. max: the split's head weights go to LDS once (a global load in the per-tile reduction
+  // would wait behind the key tiles in flight)
+  if constexpr (MAXG) {
+    const int g0 = r0 / a.w, ng = nrows / a.w;  // at most kMaxSplitRows / 16 heads
+    if (wid == 0 && lane < ng) qws[lane] = a.qweight[h * a.G + g0 + lane];
+    __syncthreads();
+  }
   auto reduce = [&](int64_t t) {  // t may be -1: nothing is stored
     const float* r = red + CP::at((int)((uint32_t)(t + 3) % 3u), 0, 0, 0);
     float v = 0.f;
@@ -512,7 +520,7 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float* red, int 
       // partials of each of a head's w/(16*RBW) waves in wave order, weight, keep the maximum
       // (balanced layout: heads 4-6 then add the four lane-group partials of the block they lent
       // to the last wave)
-      const int wph = a.w / (16 * RBW), g0 = r0 / a.w, ng = nrows / a.w;
+      const int wph = a.w / (16 * RBW), ng = nrows / a.w;
       for (int g = rgrp; g < ng; g += LPC) {
         float sum = 0.f;
         for (int wv = g * wph; wv < (g + 1) * wph; ++wv)
@@ -521,7 +529,7 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float* red, int 
         if (bal && g >= kBalFirstWave)
 #pragma unroll
           for (int q = 0; q < 4; ++q) sum += r[(kScoreWaves - 1) * CP::SW + (4 * (g - kBalFirstWave) + q) * CP::SL + rcol];
-        v = fmaxf(v, a.qweight[h * a.G + g0 + g] * sum);
+        v = fmaxf(v, qws[g] * sum);
       }
 #pragma unroll
       for (int o = CPW; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
@@ -529,12 +537,12 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float* red, int 
     } else if constexpr (MAXG) {
       // the LPC lanes of a column take the split's heads in turn: sum a head's w/16 blocks
       // (block b sits with wave b % 8, slot b / 8), weight it, keep the maximum
-      const int bph = a.w / 16, g0 = r0 / a.w, ng = nrows / a.w;
+      const int bph = a.w / 16, ng = nrows / a.w;
       for (int g = rgrp; g < ng; g += LPC) {
         float sum = 0.f;
         for (int bb = g * bph; bb < (g + 1) * bph; ++bb)
           sum += r[(bb % kScoreWaves) * CP::SW + (bb / kScoreWaves) * CP::SL + rcol];
-        v = fmaxf(v, a.qweight[h * a.G + g0 + g] * sum);
+        v = fmaxf(v, qws[g] * sum);
       }
 #pragma unroll
       for (int o = CPW; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
@@ -600,6 +608,7 @@ __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) 
   __shared__ __attribute__((aligned(16))) char ktile[2 * col_tile<T>() * G::LDS_STRIDE];
   __shared__ __attribute__((aligned(16)))
   float red[ColPartials<T, block_partials<MAXG, HW>() ? RBW : 4, bal_extra_rows<MAXG, HW, RBW>()>::WORDS];
+  __shared__ float qws[MAXG ? kMaxSplitRows / 16 : 1];  // Ipt. max: the row split's head weights
   const int seg = blockIdx.y;
   const int b = seg / a.Hkv, h = seg % a.Hkv;
   if (blockIdx.x == 0 && blockIdx.z == 0) init_segment(a, seg);  // histograms, offsets for the selection
@@ -628,31 +637,32 @@ __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) 
 #pragma unroll
           for (int c = 0; c < G::NC; ++c) qb[j][c] = qa[j][c];
         if (wid == kScoreWaves - 1)
-          colsum_chunk<T, D, 3, RBW, MAXG, HW, true>(a, ktile, red, seg, r0, nrows, wid, lane, qb, kr, key0, key_end,
-                                                     bal);
+          colsum_chunk<T, D, 3, RBW, MAXG, HW, true>(a, ktile, red, qws, seg, r0, nrows, wid, lane, qb, kr, key0,
+                                                     key_end, bal);
         else
-          colsum_chunk<T, D, 3, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qb, kr, key0, key_end, bal);
+          colsum_chunk<T, D, 3, RBW, MAXG, HW>(a, ktile, red, qws, seg, r0, nrows, wid, lane, qb, kr, key0, key_end,
+                                               bal);
         return;
       }
     }
     // (every wave reduces some columns, so each needs to know the layout: bal goes to all)
     if (row_block<RBW, HW>(wid, 0) < nrb) {
-      colsum_chunk<T, D, RBW, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qa, kr, key0, key_end, bal);
+      colsum_chunk<T, D, RBW, RBW, MAXG, HW>(a, ktile, red, qws, seg, r0, nrows, wid, lane, qa, kr, key0, key_end, bal);
     } else {
       Frag<T> qz[1][G::NC];  // never read: the wave has no row blocks
 #pragma unroll
       for (int c = 0; c < G::NC; ++c) qz[0][c] = qa[0][c];
-      colsum_chunk<T, D, 0, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qz, kr, key0, key_end, bal);
+      colsum_chunk<T, D, 0, RBW, MAXG, HW>(a, ktile, red, qws, seg, r0, nrows, wid, lane, qz, kr, key0, key_end, bal);
     }
   } else if (wid + kScoreWaves * (RBW - 1) < nrb) {
-    colsum_chunk<T, D, RBW, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qa, kr, key0, key_end);
+    colsum_chunk<T, D, RBW, RBW, MAXG, HW>(a, ktile, red, qws, seg, r0, nrows, wid, lane, qa, kr, key0, key_end);
   } else {
     Frag<T> qb[RBW > 1 ? RBW - 1 : 1][G::NC];
 #pragma unroll
     for (int j = 0; j < RBW - 1; ++j)
 #pragma unroll
       for (int c = 0; c < G::NC; ++c) qb[j][c] = qa[j][c];
-    colsum_chunk<T, D, RBW - 1, RBW, MAXG, HW>(a, ktile, red, seg, r0, nrows, wid, lane, qb, kr, key0, key_end);
+    colsum_chunk<T, D, RBW - 1, RBW, MAXG, HW>(a, ktile, red, qws, seg, r0, nrows, wid, lane, qb, kr, key0, key_end);
   }
 }
 
