@@ -526,9 +526,11 @@ __device__ void colsum_chunk(const CompressArgs& a, char* kbuf, float* red, floa
         for (int wv = g * wph; wv < (g + 1) * wph; ++wv)
 #pragma unroll
           for (int q = 0; q < 4; ++q) sum += r[wv * CP::SW + q * CP::SL + rcol];
-        if (bal && g >= kBalFirstWave)
+        if (bal && g >= kBalFirstWave) {
+          const float* lent = r + (kScoreWaves - 1) * CP::SW + 4 * (g - kBalFirstWave) * CP::SL + rcol;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) sum += r[(kScoreWaves - 1) * CP::SW + (4 * (g - kBalFirstWave) + q) * CP::SL + rcol];
+          for (int q = 0; q < 4; ++q) sum += lent[q * CP::SL];
+        }
         v = fmaxf(v, qws[g] * sum);
       }
 #pragma unroll
