@@ -369,8 +369,8 @@ __global__ __launch_bounds__(kScoreBlock, 1) void lse_kernel(CompressArgs a) {
   }
   if (key0 >= key_end) return;
   const int tid = threadIdx.x, wid = tid >> 6, lane = tid & 63;
-  const int r0 = (int)blockIdx.z * a.rs_rows;
-  const int nrows = a.R - r0 < a.rs_rows ? a.R - r0 : a.rs_rows;
+  const int r0 = (int)blockIdx.z * a.lse_rs_rows;
+  const int nrows = a.R - r0 < a.lse_rs_rows ? a.R - r0 : a.lse_rs_rows;
   const rsrc_t kr = make_rsrc(static_cast<const T*>(a.k) + (int64_t)seg * a.C * D, (uint64_t)a.C * G::RB);
   Frag<T> qa[RBW][G::NC];
   load_group_queries<T, D, RBW>(a, b, h, r0, nrows, wid, lane, qa);
@@ -669,15 +669,21 @@ __global__ __launch_bounds__(kScoreBlock, 1) void colsum_kernel(CompressArgs a) 
 }
 
 // Host-side dispatch ----------------------------------------------------------
+// Pass 1 (and its merge) with RBW row blocks per wave for its row split.
 template <typename T, int D, int RBW>
-static hipError_t launch_scores_t(const CompressArgs& a, hipStream_t st) {
+static hipError_t launch_lse_t(const CompressArgs& a, hipStream_t st) {
   const dim3 sblk(kScoreBlock);
-  if (a.window_lse == nullptr) {
-    SGDKV_LAUNCH("score_lse", (lse_kernel<T, D, RBW>), dim3(a.n_lse_chunks, a.B * a.Hkv, a.n_rsplit), sblk, st, a);
-    constexpr int rows_per_wg = kBlock / kMergeLanes;
-    SGDKV_LAUNCH("lse_merge", lse_merge_kernel, dim3((unsigned)((a.R + rows_per_wg - 1) / rows_per_wg), a.B * a.Hkv),
-                 dim3(kBlock), st, a);
-  }
+  SGDKV_LAUNCH("score_lse", (lse_kernel<T, D, RBW>), dim3(a.n_lse_chunks, a.B * a.Hkv, a.lse_n_rsplit), sblk, st, a);
+  constexpr int rows_per_wg = kBlock / kMergeLanes;
+  SGDKV_LAUNCH("lse_merge", lse_merge_kernel, dim3((unsigned)((a.R + rows_per_wg - 1) / rows_per_wg), a.B * a.Hkv),
+               dim3(kBlock), st, a);
+  return hipGetLastError();
+}
+
+// Pass 2 with RBW row blocks per wave for its row split.
+template <typename T, int D, int RBW>
+static hipError_t launch_colsum_t(const CompressArgs& a, hipStream_t st) {
+  const dim3 sblk(kScoreBlock);
   if (a.n_col_chunks > 0) {
     const dim3 cgrid(a.n_col_chunks, a.B * a.Hkv, a.n_rsplit);
     if (a.agg == 1 && a.w % (16 * RBW) == 0)
@@ -690,23 +696,40 @@ static hipError_t launch_scores_t(const CompressArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <typename T, int D>
-static hipError_t launch_scores_d(const CompressArgs& a, hipStream_t st) {
-  const int nrb = (a.rs_rows + 15) / 16;  // blocks of the largest row split
-  const int rbw = (nrb + kScoreWaves - 1) / kScoreWaves;
-  switch (rbw) {
-    case 1: return launch_scores_t<T, D, 1>(a, st);
-    case 2: return launch_scores_t<T, D, 2>(a, st);
-    case 3: return launch_scores_t<T, D, 3>(a, st);
-    case 4: return launch_scores_t<T, D, 4>(a, st);
+// Row blocks per wave for a row split of `rows` rows (its largest split), as a template argument.
+template <typename T, int D, template <typename, int, int> class L>
+static hipError_t dispatch_rbw(int rows, const CompressArgs& a, hipStream_t st) {
+  const int nrb = (rows + 15) / 16;
+  switch ((nrb + kScoreWaves - 1) / kScoreWaves) {
+    case 1: return L<T, D, 1>::run(a, st);
+    case 2: return L<T, D, 2>::run(a, st);
+    case 3: return L<T, D, 3>::run(a, st);
+    case 4: return L<T, D, 4>::run(a, st);
 #if SGDKV_SCORE_WAVES_MAX_RBW > 4
-    case 5: return launch_scores_t<T, D, 5>(a, st);
-    case 6: return launch_scores_t<T, D, 6>(a, st);
-    case 7: return launch_scores_t<T, D, 7>(a, st);
-    case 8: return launch_scores_t<T, D, 8>(a, st);
+    case 5: return L<T, D, 5>::run(a, st);
+    case 6: return L<T, D, 6>::run(a, st);
+    case 7: return L<T, D, 7>::run(a, st);
+    case 8: return L<T, D, 8>::run(a, st);
 #endif
     default: return hipErrorInvalidValue;
   }
+}
+template <typename T, int D, int RBW>
+struct LseLaunch {
+  static hipError_t run(const CompressArgs& a, hipStream_t st) { return launch_lse_t<T, D, RBW>(a, st); }
+};
+template <typename T, int D, int RBW>
+struct ColsumLaunch {
+  static hipError_t run(const CompressArgs& a, hipStream_t st) { return launch_colsum_t<T, D, RBW>(a, st); }
+};
+
+template <typename T, int D>
+static hipError_t launch_scores_d(const CompressArgs& a, hipStream_t st) {
+  if (a.window_lse == nullptr) {
+    const hipError_t e = dispatch_rbw<T, D, LseLaunch>(a.lse_rs_rows, a, st);
+    if (e != hipSuccess) return e;
+  }
+  return dispatch_rbw<T, D, ColsumLaunch>(a.rs_rows, a, st);
 }
 
 hipError_t launch_scores(const CompressArgs& a, hipStream_t st) {

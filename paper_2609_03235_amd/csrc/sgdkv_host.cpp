@@ -381,6 +381,8 @@ sgdkv_status plan_compress(const sgdkv_compress_desc* d, int64_t win0, CompressP
   a.c2 = (float)(scale * 1.4426950408889634074);
   a.out_scale = 1.0f / (float)G;
   row_splits(a.R, a.w, false, a.n_rsplit, a.rs_rows);
+  a.lse_n_rsplit = a.n_rsplit;  // pass 1 keeps the even split (Ipt. max changes pass 2's only)
+  a.lse_rs_rows = a.rs_rows;
   // the column-sum region also fits the (possibly more) splits of the Ipt. max aggregation
   p.colsum_splits = a.n_rsplit;
   if (a.w % 16 == 0 && a.w <= sgdkv::kMaxSplitRows) {

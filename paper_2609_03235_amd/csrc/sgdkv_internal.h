@@ -82,6 +82,10 @@ struct CompressArgs {
   // multiple of 16 (of w for the Ipt. max aggregation, so that no query head straddles two)
   int n_rsplit;
   int rs_rows;
+  // pass 1's row split: the even one also under Ipt. max (a row's LSE needs no other row, and
+  // whole heads would give one split more rows than the others)
+  int lse_n_rsplit;
+  int lse_rs_rows;
   // chunking
   int64_t score_chunk;  // keys per pass-2 workgroup (multiple of kScoreChunkQuantum)
   // pass 1: n_lse_head chunks of lse_chunk keys over [0, lse_tail0), the keys every window row sees
