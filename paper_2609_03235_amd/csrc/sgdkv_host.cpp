@@ -707,8 +707,11 @@ constexpr int64_t kDecodeResident = 2 * sgdkv::kScoreWorkgroups;
 // than one round, the workgroups are therefore shared out over the segments in proportion to
 // their 16-row steps (largest remainder, ties to the lower segment; a non-empty segment left
 // with none gets one from the largest) so that they fill the nearest whole number of rounds; the
-// kernel deals a segment's steps to four splits per launched workgroup.
-std::vector<int64_t> compact_workgroups(const int64_t* offsets_host, int64_t nseg, int64_t chunk) {
+// kernel deals a segment's steps to four splits per launched workgroup. The new_wg workgroups of
+// each segment's appended rows count toward the rounds when they come to at most half a round, so
+// that they fill the last one instead of starting another.
+std::vector<int64_t> compact_workgroups(const int64_t* offsets_host, int64_t nseg, int64_t chunk,
+                                        int64_t new_wg = 0) {
   const int64_t wpw = sgdkv::kDecodeWaves;
   std::vector<int64_t> n((size_t)nseg);
   int64_t w0 = 0, steps = 0;
@@ -719,7 +722,8 @@ std::vector<int64_t> compact_workgroups(const int64_t* offsets_host, int64_t nse
     steps += ceil_div(len, 16);
   }
   if (!kDecodeWholeRounds || w0 <= kDecodeResident) return n;
-  const int64_t target = (w0 + kDecodeResident / 2) / kDecodeResident * kDecodeResident;
+  const int64_t extra = nseg * new_wg <= kDecodeResident / 2 ? nseg * new_wg : 0;
+  const int64_t target = (w0 + extra + kDecodeResident / 2) / kDecodeResident * kDecodeResident - extra;
   std::vector<std::pair<int64_t, int64_t>> rem;  // (fractional part scaled by steps, -segment)
   int64_t given = 0;
   for (int64_t i = 0; i < nseg; ++i) {
@@ -819,10 +823,19 @@ sgdkv_status plan_decode(const sgdkv_decode_desc* d, const int64_t* offsets_host
   // otherwise n_cwg per segment; plus the workgroups of a full appended region
   const int64_t new_wg_cap = ceil_div(ceil_div(capacity, a.chunk), wpw);
   if (nseg <= sgdkv::kMaxCompactSegs) {
+    // the most slots and compressed-row workgroups of any call with up to new_wg_cap appended
+    // workgroups per segment (appended ones count toward the rounds only while they fit in half
+    // a round: past that the plan is the one without them)
     int64_t slots = 0, most = 0;
-    for (const int64_t n : compact_workgroups(offsets_host, nseg, a.chunk)) {
-      slots += n + new_wg_cap;
-      most = std::max(most, n);
+    const int64_t k_fold = std::min<int64_t>(new_wg_cap, kDecodeResident / 2 / nseg);
+    for (int64_t k = 0; k <= k_fold + 1 && k <= new_wg_cap; ++k) {
+      const int64_t kk = k <= k_fold ? k : new_wg_cap;
+      int64_t s = 0;
+      for (const int64_t n : compact_workgroups(offsets_host, nseg, a.chunk, kk)) {
+        s += n + kk;
+        most = std::max(most, n);
+      }
+      slots = std::max(slots, s);
     }
     a.n_slots = slots;
     // a segment's appended-row workgroups are numbered from n_cwg on: past its compressed-row
@@ -920,7 +933,7 @@ sgdkv_status decode_step(const sgdkv_decode_desc* desc, const void* q, const voi
   const int64_t nseg = (int64_t)a.B * a.Hkv;
   a.compact = nseg <= sgdkv::kMaxCompactSegs ? 1 : 0;
   if (a.compact) {
-    const std::vector<int64_t> wgs = compact_workgroups(offsets_host, nseg, a.chunk);
+    const std::vector<int64_t> wgs = compact_workgroups(offsets_host, nseg, a.chunk, a.n_new_wg);
     int64_t run = 0;
     a.wg_start[0] = 0;
     for (int64_t i = 0; i < nseg; ++i) {
