@@ -454,6 +454,22 @@ def test_decode_workgroups_fill_whole_rounds():
     assert sg.decode_workspace_size(desc, oh) // per_wg == 2 + 0 + 4 + 1
 
 
+def test_decode_workspace_with_appended_rows():
+    """Appended-row workgroups (one per segment for up to 4 x 256 rows at this size) count toward the
+    whole rounds while they come to at most half a round, so a capacity of 64 rows needs no more
+    slots than none: 32 segments of 32768 rows plan 1024 workgroups, and with one appended each 992
+    + 32. Past half a round the plan is the one without them, plus every appended slot."""
+    G, d = 7, 128
+    per_wg = G * (d + 2) * 4
+    desc = sg.DecodeDesc(8, 4 * G, 4, d, sg.DTYPE_BF16, sg.DTYPE_F32, 0.0)
+    oh = np.arange(33, dtype=np.int64) * 32768
+    assert sg.decode_workspace_size(desc, oh) // per_wg == 1024
+    assert sg.decode_workspace_size(desc, oh, 64) // per_wg == 1024
+    assert sg.decode_workspace_size(desc, oh, 1024) // per_wg == 1024
+    cap = 300000  # ceil(ceil(300000 / 256) / 4) = 293 appended workgroups per segment
+    assert sg.decode_workspace_size(desc, oh, cap) // per_wg == 1024 + 32 * 293
+
+
 @pytest.mark.skipif(_gpu(), reason="checks the no-device path")
 def test_no_device_fails_after_validation():
     assert _compress(_desc(), [512, 512]) == sg.ERR_HIP
